@@ -1,0 +1,57 @@
+/*
+ * vla_debug.h - test hooks of libvla.so: single kernels behind the C ABI, for
+ * per-kernel parity tests and for checking where CU-masked streams place
+ * work. Same conventions as vla.h (asynchronous, status + vla_last_error).
+ */
+#ifndef VLA_DEBUG_H
+#define VLA_DEBUG_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#include "vla.h"
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/*
+ * out[m][n] = act(sum_k A[m][k] * Wt[n][k] + bias[n]) for m < M, n < N, fp32
+ * out (leading dimension ldo). This is the projection kernel every dense
+ * layer of both stages uses (the layers are plain matrix products).
+ *  A   device [M][lda], a_type 0 = fp32, 1 = bf16 (fp32 A is rounded to bf16
+ *      on load when the weight is bf16).
+ *  Wt  device [N][ldw] weight, transposed (K contiguous), w_type 0/1.
+ *  bias device fp32 [N] or NULL. act: 0 none, 1 SiLU, 2 tanh-GELU.
+ * bf16 weights need K, lda, ldw multiples of 8; fp32 weights need fp32 A.
+ */
+vla_status vla_debug_gemm(int M, int N, int K, const void* A, int lda, int a_type, const void* Wt, int ldw,
+                          int w_type, const float* bias, int act, float* out, int ldo, hipStream_t stream);
+
+/*
+ * o = softmax(q k^T / sqrt(hd)) v over the keys [k0 ; k1] (segment 1 may be
+ * empty), grouped KV heads (query head h uses KV head h / (Hq / Hkv)).
+ *  q  device [B][Hq][Lq][hd]; k0, v0 [B][Hkv][len0][hd]; k1, v1 [B][Hkv][len1][hd];
+ *  o  device [B][Lq][Hq * hd]. et 0 = fp32, 1 = bf16 for every tensor.
+ * hd a multiple of 8 up to 256; len0 >= 1.
+ */
+vla_status vla_debug_attention(int B, int Hq, int Hkv, int Lq, int hd, int et, const void* q, const void* k0,
+                               const void* v0, int len0, const void* k1, const void* v1, int len1, void* o,
+                               hipStream_t stream);
+
+/*
+ * Launch `blocks` one-wave workgroups on the pool stream restricted to
+ * `cu_count` compute units (the VLM-side mask of vla_step, or the action-side
+ * mask counted from the top when from_top != 0). Each workgroup sleeps
+ * `spin` x 64 cycles-ish and writes out[2*i] = HW_ID, out[2*i+1] = XCC_ID
+ * hardware register words. out: device uint32 [2 * blocks]. The join stream
+ * waits for the probe.
+ */
+vla_status vla_debug_cu_probe(int device, int cu_count, int from_top, int blocks, int spin, uint32_t* out,
+                              hipStream_t join);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* VLA_DEBUG_H */

@@ -1,0 +1,300 @@
+// C ABI of libvla: argument validation, error reporting, and stage
+// co-execution on CU-masked streams (paper Section 4.1.2: the VLM stage's
+// stream is restricted to a subset of the compute units so the action stage
+// always finds free units; one lockstep = one VLM batch alongside one action
+// batch).
+#include <cstring>
+#include <map>
+#include <mutex>
+
+#include "../../include/vla.h"
+#include "../../include/vla_debug.h"
+#include "model.h"
+
+// ---------------------------------------------------------------- errors
+static thread_local std::string g_last_error;
+void vla_set_error(const std::string& m) { g_last_error = m; }
+void vla_clear_error() { g_last_error.clear(); }
+
+template <typename F>
+static vla_status guarded(F&& f) {
+  try {
+    vla_clear_error();
+    f();
+    return VLA_OK;
+  } catch (const VlaError& e) {
+    vla_set_error(e.msg);
+    return (vla_status)e.status;
+  } catch (const std::bad_alloc&) {
+    vla_set_error("host allocation failed");
+    return VLA_ENOMEM;
+  } catch (const std::exception& e) {
+    vla_set_error(e.what());
+    return VLA_EINVAL;
+  }
+}
+
+// ---------------------------------------------------------------- stream pool
+// Streams are created once per (device, mask) and live until the process
+// ends. Mask bit i selects one compute unit; the driver spreads consecutive
+// bits over the accelerator dies (XCDs) first, so the lowest k bits give
+// k/8 units on each of the 8 XCDs.
+namespace {
+
+struct DevicePool {
+  std::map<int, hipStream_t> vlm;     // key: cu count (256 = unrestricted)
+  std::map<int, hipStream_t> adit;    // key: cu count from the top of the mask
+  hipEvent_t ev_start = nullptr, ev_v = nullptr, ev_a = nullptr;
+};
+
+std::mutex g_pool_mu;
+std::map<int, DevicePool> g_pools;
+
+int device_cu_count(int dev) {
+  hipDeviceProp_t p;
+  VLA_HIP(hipGetDeviceProperties(&p, dev));
+  return p.multiProcessorCount;
+}
+
+hipStream_t make_masked(int dev, int count, bool from_top) {
+  const int total = device_cu_count(dev);
+  hipStream_t s = nullptr;
+  if (count >= total) {
+    VLA_HIP(hipStreamCreateWithFlags(&s, hipStreamNonBlocking));
+    return s;
+  }
+  const int words = (total + 31) / 32;
+  std::vector<uint32_t> mask(words, 0u);
+  for (int i = 0; i < count; ++i) {
+    const int bit = from_top ? total - 1 - i : i;
+    mask[bit / 32] |= 1u << (bit % 32);
+  }
+  VLA_HIP(hipExtStreamCreateWithCUMask(&s, (uint32_t)words, mask.data()));
+  return s;
+}
+
+DevicePool& pool(int dev) {
+  auto& p = g_pools[dev];
+  if (!p.ev_start) {
+    VLA_HIP(hipEventCreateWithFlags(&p.ev_start, hipEventDisableTiming));
+    VLA_HIP(hipEventCreateWithFlags(&p.ev_v, hipEventDisableTiming));
+    VLA_HIP(hipEventCreateWithFlags(&p.ev_a, hipEventDisableTiming));
+  }
+  return p;
+}
+
+hipStream_t vlm_stream(int dev, int count) {
+  auto& p = pool(dev);
+  auto it = p.vlm.find(count);
+  if (it != p.vlm.end()) return it->second;
+  hipStream_t s = make_masked(dev, count, false);
+  p.vlm[count] = s;
+  return s;
+}
+
+hipStream_t adit_stream(int dev, int count) {
+  auto& p = pool(dev);
+  if (count <= 0) count = 256;
+  auto it = p.adit.find(count);
+  if (it != p.adit.end()) return it->second;
+  hipStream_t s = make_masked(dev, count, true);
+  p.adit[count] = s;
+  return s;
+}
+
+void check_model(vla_model m) { VLA_REQUIRE(m != nullptr, "null model"); }
+
+void check_prefill(vla_model m, int B, const float* pix, const int32_t* ids, void* kv) {
+  check_model(m);
+  VLA_REQUIRE(B >= 1 && B <= m->cfg.max_batch,
+              "batch " + std::to_string(B) + " outside [1, " + std::to_string(m->cfg.max_batch) + "]");
+  VLA_REQUIRE(pix && ids && kv, "null pixels, text_ids or kv_out");
+}
+
+void check_denoise(vla_model m, int B, const void* kv, const float* noise, int steps, float* act) {
+  check_model(m);
+  VLA_REQUIRE(B >= 1 && B <= m->cfg.max_batch,
+              "batch " + std::to_string(B) + " outside [1, " + std::to_string(m->cfg.max_batch) + "]");
+  VLA_REQUIRE(steps >= 1 && steps <= 1000, "steps must be in [1, 1000]");
+  VLA_REQUIRE(kv && noise && act, "null kv, noise or actions_out");
+  VLA_REQUIRE((const void*)noise != (const void*)act, "actions_out may not alias noise");
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------- model API
+extern "C" {
+
+size_t vla_weight_count(const vla_config* cfg) {
+  if (!cfg) { vla_set_error("null config"); return 0; }
+  std::string why = vla_config_check(*cfg);
+  if (!why.empty()) { vla_set_error(why); return 0; }
+  return vla_weight_count_impl(*cfg);
+}
+
+vla_status vla_create_model(const vla_config* cfg, const float* weights_host, size_t n_floats, int device,
+                            vla_model* out) {
+  return guarded([&] {
+    VLA_REQUIRE(cfg && weights_host && out, "null config, weights or out");
+    *out = nullptr;
+    std::string why = vla_config_check(*cfg);
+    VLA_REQUIRE(why.empty(), why);
+    const size_t need = vla_weight_count_impl(*cfg);
+    VLA_REQUIRE(n_floats == need, "parameter buffer has " + std::to_string(n_floats) + " values, shape needs " +
+                                      std::to_string(need));
+    int ndev = 0;
+    VLA_HIP(hipGetDeviceCount(&ndev));
+    VLA_REQUIRE(device >= 0 && device < ndev, "device " + std::to_string(device) + " not present");
+    auto* m = new vla_model_s();
+    try {
+      m->init(*cfg, weights_host, n_floats, device);
+    } catch (...) {
+      try { m->destroy(); } catch (...) {}
+      delete m;
+      throw;
+    }
+    *out = m;
+  });
+}
+
+void vla_destroy_model(vla_model m) {
+  if (!m) return;
+  try { m->destroy(); } catch (...) {}
+  delete m;
+}
+
+vla_status vla_set_graphs(vla_model m, int enabled) {
+  return guarded([&] {
+    check_model(m);
+    m->graphs = enabled != 0;
+  });
+}
+
+size_t vla_kv_bytes(vla_model m, int batch) {
+  if (!m) { vla_set_error("null model"); return 0; }
+  if (batch < 1 || batch > m->cfg.max_batch) { vla_set_error("batch out of range"); return 0; }
+  return m->kv_bytes(batch);
+}
+
+vla_status vla_prefill_ex(vla_model m, int batch, const float* pixels, const int32_t* text_ids, const float* state,
+                          void* kv_out, hipStream_t stream) {
+  return guarded([&] {
+    check_prefill(m, batch, pixels, text_ids, kv_out);
+    DeviceGuard g(m->device);
+    m->prefill(batch, pixels, text_ids, m->cfg.head_kind == VLA_HEAD_DIT ? state : nullptr, kv_out, stream);
+  });
+}
+
+vla_status vla_prefill(vla_model m, int batch, const float* pixels, const int32_t* text_ids, void* kv_out,
+                       hipStream_t stream) {
+  return vla_prefill_ex(m, batch, pixels, text_ids, nullptr, kv_out, stream);
+}
+
+vla_status vla_denoise(vla_model m, int batch, const void* kv, const float* noise, int steps, float* actions_out,
+                       hipStream_t stream) {
+  return guarded([&] {
+    check_denoise(m, batch, kv, noise, steps, actions_out);
+    DeviceGuard g(m->device);
+    m->denoise(batch, kv, noise, steps, actions_out, stream);
+  });
+}
+
+vla_status vla_step(const vla_step_args* a, hipStream_t join) {
+  return guarded([&] {
+    VLA_REQUIRE(a != nullptr, "null step args");
+    const bool do_v = a->vlm_batch > 0, do_a = a->adit_batch > 0;
+    VLA_REQUIRE(a->vlm_batch >= 0 && a->adit_batch >= 0, "negative batch");
+    VLA_REQUIRE(do_v || do_a, "both halves empty");
+    if (do_v) check_prefill(a->vlm_model, a->vlm_batch, a->pixels, a->text_ids, a->kv_out);
+    if (do_a) check_denoise(a->adit_model, a->adit_batch, a->kv_in, a->noise, a->steps, a->actions_out);
+    VLA_REQUIRE(a->vlm_cu_count >= 8 && a->vlm_cu_count <= 256 && a->vlm_cu_count % 8 == 0,
+                "vlm_cu_count must be a multiple of 8 in [8, 256]");
+    VLA_REQUIRE(a->adit_cu_count == 0 || (a->adit_cu_count >= 8 && a->adit_cu_count <= 256 && a->adit_cu_count % 8 == 0),
+                "adit_cu_count must be 0 or a multiple of 8 in [8, 256]");
+    const int dev = do_v ? a->vlm_model->device : a->adit_model->device;
+    VLA_REQUIRE(!(do_v && do_a) || a->vlm_model->device == a->adit_model->device, "models on different devices");
+    if (do_v && do_a && a->vlm_model == a->adit_model)
+      VLA_REQUIRE(a->kv_out != a->kv_in, "kv_out and kv_in of one model must be different buffers");
+    DeviceGuard g(dev);
+    std::lock_guard<std::mutex> lk(g_pool_mu);
+    DevicePool& p = pool(dev);
+    const int total = device_cu_count(dev);
+    hipStream_t vs = vlm_stream(dev, a->vlm_cu_count >= total ? 256 : a->vlm_cu_count);
+    hipStream_t as = adit_stream(dev, a->adit_cu_count == 0 || a->adit_cu_count >= total ? 256 : a->adit_cu_count);
+    // both halves start after the work already queued on the join stream
+    VLA_HIP(hipEventRecord(p.ev_start, join));
+    if (do_v) VLA_HIP(hipStreamWaitEvent(vs, p.ev_start, 0));
+    if (do_a) VLA_HIP(hipStreamWaitEvent(as, p.ev_start, 0));
+    if (do_v) a->vlm_model->prefill(a->vlm_batch, a->pixels, a->text_ids,
+                                    a->vlm_model->cfg.head_kind == VLA_HEAD_DIT ? a->state : nullptr, a->kv_out, vs);
+    if (do_a) a->adit_model->denoise(a->adit_batch, a->kv_in, a->noise, a->steps, a->actions_out, as);
+    if (do_v) { VLA_HIP(hipEventRecord(p.ev_v, vs)); VLA_HIP(hipStreamWaitEvent(join, p.ev_v, 0)); }
+    if (do_a) { VLA_HIP(hipEventRecord(p.ev_a, as)); VLA_HIP(hipStreamWaitEvent(join, p.ev_a, 0)); }
+  });
+}
+
+const char* vla_last_error(void) { return g_last_error.c_str(); }
+
+// ---------------------------------------------------------------- test hooks
+vla_status vla_debug_gemm(int M, int N, int K, const void* A, int lda, int a_type, const void* Wt, int ldw, int w_type,
+                          const float* bias, int act, float* out, int ldo, hipStream_t s) {
+  return guarded([&] {
+    VLA_REQUIRE(M >= 0 && N >= 0 && K >= 0 && A && Wt && out, "bad gemm arguments");
+    VLA_REQUIRE(a_type == ET_F32 || a_type == ET_BF16, "bad a_type");
+    VLA_REQUIRE(w_type == ET_F32 || w_type == ET_BF16, "bad w_type");
+    VLA_REQUIRE(lda >= K && ldw >= K && ldo >= N, "leading dimensions too small");
+    if (w_type == ET_BF16) {
+      VLA_REQUIRE(K % 8 == 0 && lda % 8 == 0 && ldw % 8 == 0, "bf16 path needs K, lda, ldw % 8 == 0");
+    } else {
+      VLA_REQUIRE(a_type == ET_F32, "fp32 weights need fp32 activations");
+    }
+    VLA_REQUIRE(act >= ACT_NONE && act <= ACT_GELU, "bad act");
+    GemmArgs g{};
+    g.M = M; g.N = N; g.K = K; g.A = A; g.lda = lda; g.a_type = a_type; g.W = Wt; g.ldw = ldw; g.w_type = w_type;
+    g.mode = EPI_STORE; g.act = act; g.bias = bias; g.tab_period = 1; g.out = out; g.ldo = ldo; g.out_type = ET_F32;
+    launch_gemm(g, s);
+    VLA_HIP(hipGetLastError());
+  });
+}
+
+vla_status vla_debug_attention(int B, int Hq, int Hkv, int Lq, int hd, int et, const void* q, const void* k0,
+                               const void* v0, int len0, const void* k1, const void* v1, int len1, void* o,
+                               hipStream_t s) {
+  return guarded([&] {
+    VLA_REQUIRE(B >= 1 && Hq >= 1 && Hkv >= 1 && Hq % Hkv == 0 && Lq >= 1, "bad attention shape");
+    VLA_REQUIRE(hd >= 8 && hd <= 256 && hd % 8 == 0, "hd must be a multiple of 8 in [8, 256]");
+    VLA_REQUIRE(len0 >= 1 && len1 >= 0, "segment 0 needs a key");
+    VLA_REQUIRE(q && k0 && v0 && o && (len1 == 0 || (k1 && v1)), "null attention buffer");
+    VLA_REQUIRE(et == ET_F32 || et == ET_BF16, "bad element type");
+    AttnArgs a{};
+    a.B = B; a.Hq = Hq; a.Hkv = Hkv; a.Lq = Lq; a.hd = hd; a.et = et; a.scale = 1.0f / sqrtf((float)hd);
+    a.q = q; a.q_sb = (long)Hq * Lq * hd; a.q_sh = (long)Lq * hd; a.q_si = hd;
+    a.seg[0] = AttnSeg{k0, (long)Hkv * len0 * hd, (long)len0 * hd, hd, v0, (long)Hkv * len0 * hd, (long)len0 * hd, hd, len0};
+    a.seg[1] = AttnSeg{k1, (long)Hkv * len1 * hd, (long)len1 * hd, hd, v1, (long)Hkv * len1 * hd, (long)len1 * hd, hd, len1};
+    a.o = o; a.o_sb = (long)Lq * Hq * hd; a.o_sh = hd; a.o_si = (long)Hq * hd;   // [B][Lq][Hq*hd]
+    launch_attention(a, s);
+    VLA_HIP(hipGetLastError());
+  });
+}
+
+vla_status vla_debug_cu_probe(int device, int cu_count, int from_top, int blocks, int spin, uint32_t* out,
+                              hipStream_t join) {
+  return guarded([&] {
+    VLA_REQUIRE(blocks >= 1 && blocks <= 65536 && spin >= 0 && spin <= 100000 && out, "bad probe arguments");
+    VLA_REQUIRE(cu_count >= 8 && cu_count <= 256 && cu_count % 8 == 0, "cu_count must be a multiple of 8 in [8, 256]");
+    DeviceGuard g(device);
+    std::lock_guard<std::mutex> lk(g_pool_mu);
+    DevicePool& p = pool(device);
+    const int total = device_cu_count(device);
+    hipStream_t s = from_top ? adit_stream(device, cu_count >= total ? 256 : cu_count)
+                             : vlm_stream(device, cu_count >= total ? 256 : cu_count);
+    VLA_HIP(hipEventRecord(p.ev_start, join));
+    VLA_HIP(hipStreamWaitEvent(s, p.ev_start, 0));
+    launch_cu_probe(out, blocks, spin, s);
+    VLA_HIP(hipGetLastError());
+    VLA_HIP(hipEventRecord(p.ev_v, s));
+    VLA_HIP(hipStreamWaitEvent(join, p.ev_v, 0));
+  });
+}
+
+}  // extern "C"

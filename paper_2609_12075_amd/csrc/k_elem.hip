@@ -1,0 +1,237 @@
+// Row-wise and element-wise kernels of the VLA path on gfx950: RMSNorm /
+// LayerNorm / adaLN modulation (one wavefront per row, wave64 reductions),
+// patch extraction, token embedding, the flow-time sinusoid, RoPE tables,
+// parameter conversion and a placement probe for CU-masked streams.
+#include "common.h"
+
+namespace {
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+
+__device__ __forceinline__ float round_bf16(float x) { return (float)(bf16)x; }
+
+// ---------------------------------------------------------------- norms
+__global__ void __launch_bounds__(256) norm_kernel(NormArgs a) {
+  const int lane = threadIdx.x & 63;
+  const int r = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (r >= a.rows) return;
+  const int rin = a.skip > 0 ? r + (r / a.skip_group + 1) * a.skip : r;
+  const float* x = a.in + (long)rin * a.ld_in;
+  const int d = a.d;
+  float mean = 0.f, rstd;
+  if (a.kind == 0) {
+    float ss = 0.f;
+    for (int i = lane; i < d; i += 64) ss = fmaf(x[i], x[i], ss);
+    ss = wave_sum(ss);
+    rstd = rsqrtf(ss / d + a.eps);
+  } else {
+    float s = 0.f;
+    for (int i = lane; i < d; i += 64) s += x[i];
+    mean = wave_sum(s) / d;
+    float vs = 0.f;
+    for (int i = lane; i < d; i += 64) { const float t = x[i] - mean; vs = fmaf(t, t, vs); }
+    rstd = rsqrtf(wave_sum(vs) / d + a.eps);
+  }
+  bf16* ob = reinterpret_cast<bf16*>(a.out) + (long)r * a.ld_out;
+  float* of = reinterpret_cast<float*>(a.out) + (long)r * a.ld_out;
+  for (int i = lane; i < d; i += 64) {
+    float y = (x[i] - mean) * rstd;
+    if (a.kind == 2) y = y * (1.0f + a.g[i]) + a.b[i];
+    else {
+      if (a.g) y *= a.g[i];
+      if (a.b) y += a.b[i];
+    }
+    if (a.out_type == ET_BF16) ob[i] = (bf16)y; else of[i] = y;
+  }
+}
+
+// ---------------------------------------------------------------- staging
+// One thread per output element of [n_images * T][ldo].
+__global__ void im2col_kernel(const float* pix, int n_images, int hw, int p, void* out, int ldo, int out_type) {
+  const int gp = hw / p, T = gp * gp, kdim = 3 * p * p;
+  const long total = (long)n_images * T * ldo;
+  for (long e = blockIdx.x * (long)blockDim.x + threadIdx.x; e < total; e += (long)gridDim.x * blockDim.x) {
+    const int col = (int)(e % ldo);
+    const long row = e / ldo;
+    float v = 0.f;
+    if (col < kdim) {
+      const int img = (int)(row / T), t = (int)(row % T);
+      const int py = t / gp, px = t % gp;
+      const int c = col / (p * p), dy = (col / p) % p, dx = col % p;
+      v = pix[(((long)img * 3 + c) * hw + (py * p + dy)) * hw + px * p + dx];
+    }
+    if (out_type == ET_BF16) reinterpret_cast<bf16*>(out)[e] = (bf16)v;
+    else reinterpret_cast<float*>(out)[e] = v;
+  }
+}
+
+__global__ void embed_kernel(const int32_t* ids, int B, int n, int vocab, const void* table, int table_type,
+                             int d, float* h, long P, int first) {
+  const long total = (long)B * n * d;
+  for (long e = blockIdx.x * (long)blockDim.x + threadIdx.x; e < total; e += (long)gridDim.x * blockDim.x) {
+    const int i = (int)(e % d);
+    const long tok = e / d;
+    const int b = (int)(tok / n), j = (int)(tok % n);
+    int id = ids[(long)b * n + j];
+    id = id < 0 ? 0 : (id >= vocab ? vocab - 1 : id);
+    const float v = table_type == ET_BF16 ? (float)reinterpret_cast<const bf16*>(table)[(long)id * d + i]
+                                          : reinterpret_cast<const float*>(table)[(long)id * d + i];
+    h[((long)b * P + first + j) * d + i] = v;
+  }
+}
+
+// out[k][i], k < steps: angle = 1000 * t_k * 10000^(-i/half), in double.
+__global__ void time_embed_kernel(int steps, int dim, float* out) {
+  const int half = dim / 2;
+  const int k = blockIdx.x;
+  for (int i = threadIdx.x; i < half; i += blockDim.x) {
+    const double t = 1.0 - (double)k / steps;
+    const double w = pow(10000.0, -(double)i / half);
+    const double ang = 1000.0 * t * w;
+    out[(long)k * dim + i] = (float)sin(ang);
+    out[(long)k * dim + half + i] = (float)cos(ang);
+  }
+}
+
+__global__ void rope_table_kernel(int npos, int hd, double base, float* out) {
+  const int half = hd / 2;
+  const long total = (long)npos * half;
+  for (long e = blockIdx.x * (long)blockDim.x + threadIdx.x; e < total; e += (long)gridDim.x * blockDim.x) {
+    const int pos = (int)(e / half), i = (int)(e % half);
+    const double ang = pos * pow(base, -2.0 * i / hd);
+    out[e * 2 + 0] = (float)cos(ang);
+    out[e * 2 + 1] = (float)sin(ang);
+  }
+}
+
+__global__ void copy_f32_kernel(const float* src, float* dst, long n) {
+  for (long e = blockIdx.x * (long)blockDim.x + threadIdx.x; e < n; e += (long)gridDim.x * blockDim.x) dst[e] = src[e];
+}
+
+__global__ void silu_f32_kernel(const float* src, float* dst, long n) {
+  for (long e = blockIdx.x * (long)blockDim.x + threadIdx.x; e < n; e += (long)gridDim.x * blockDim.x) {
+    const float x = src[e];
+    dst[e] = x / (1.0f + __expf(-x));
+  }
+}
+
+__global__ void dit_state_rows_kernel(const void* st, int et, int B, int d, int seq, const float* pos, float* X) {
+  const long total = (long)B * d;
+  for (long e = blockIdx.x * (long)blockDim.x + threadIdx.x; e < total; e += (long)gridDim.x * blockDim.x) {
+    const int b = (int)(e / d), i = (int)(e % d);
+    const float v = et == ET_BF16 ? (float)reinterpret_cast<const bf16*>(st)[e] : reinterpret_cast<const float*>(st)[e];
+    X[(long)b * seq * d + i] = v + pos[i];
+  }
+}
+
+// ---------------------------------------------------------------- parameters
+// 32 x 32 tiles through LDS: src [K][N] -> dst[rowmap(n)][k] (ldk), zero k >= K.
+__global__ void transpose_convert_kernel(const float* src, int K, int N, void* dst, int ldk, int et, const int* rowmap) {
+  __shared__ float tile[32][33];
+  const int n0 = blockIdx.x * 32, k0 = blockIdx.y * 32;
+  const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;   // 256 threads: 32 x 8
+  for (int j = ty; j < 32; j += 8) {
+    const int k = k0 + j, n = n0 + tx;
+    tile[j][tx] = (k < K && n < N) ? src[(long)k * N + n] : 0.f;
+  }
+  __syncthreads();
+  for (int j = ty; j < 32; j += 8) {
+    const int n = n0 + j, k = k0 + tx;
+    if (n < N && k < ldk) {
+      const long row = rowmap ? rowmap[n] : n;
+      const float v = tile[tx][j];
+      if (et == ET_BF16) reinterpret_cast<bf16*>(dst)[row * ldk + k] = (bf16)v;
+      else reinterpret_cast<float*>(dst)[row * ldk + k] = v;
+    }
+  }
+}
+
+__global__ void convert_kernel(const float* src, long n, void* dst, int et) {
+  for (long e = blockIdx.x * (long)blockDim.x + threadIdx.x; e < n; e += (long)gridDim.x * blockDim.x) {
+    if (et == ET_BF16) reinterpret_cast<bf16*>(dst)[e] = (bf16)src[e];
+    else reinterpret_cast<float*>(dst)[e] = src[e];
+  }
+}
+
+__global__ void round_bf16_kernel(const float* src, long n, float* dst) {
+  for (long e = blockIdx.x * (long)blockDim.x + threadIdx.x; e < n; e += (long)gridDim.x * blockDim.x)
+    dst[e] = round_bf16(src[e]);
+}
+
+// ---------------------------------------------------------------- probe
+__global__ void cu_probe_kernel(uint32_t* out, int spin) {
+  // HW_ID (hwreg 4) and XCC_ID (hwreg 20), read whole (size 32, offset 0)
+  const uint32_t hw = __builtin_amdgcn_s_getreg((31 << 11) | (0 << 6) | 4);
+  const uint32_t xcc = __builtin_amdgcn_s_getreg((31 << 11) | (0 << 6) | 20);
+  for (int i = 0; i < spin; ++i) __builtin_amdgcn_s_sleep(64);
+  if (threadIdx.x == 0) {
+    out[2 * blockIdx.x + 0] = hw;
+    out[2 * blockIdx.x + 1] = xcc;
+  }
+}
+
+inline int grid_for(long n, int block = 256) {
+  long g = (n + block - 1) / block;
+  return (int)(g < 1 ? 1 : (g > 65536 ? 65536 : g));
+}
+
+}  // namespace
+
+void launch_norm(const NormArgs& a, hipStream_t s) {
+  if (a.rows <= 0) return;
+  hipLaunchKernelGGL(norm_kernel, dim3((a.rows + 3) / 4), dim3(256), 0, s, a);
+}
+
+void launch_im2col(const float* pix, int n_images, int hw, int p, void* out, int ldo, int out_type, hipStream_t s) {
+  const long total = (long)n_images * (hw / p) * (hw / p) * ldo;
+  hipLaunchKernelGGL(im2col_kernel, dim3(grid_for(total)), dim3(256), 0, s, pix, n_images, hw, p, out, ldo, out_type);
+}
+
+void launch_embed(const int32_t* ids, int B, int n, int vocab, const void* table, int table_type, int d, float* h,
+                  long P, int first, hipStream_t s) {
+  const long total = (long)B * n * d;
+  hipLaunchKernelGGL(embed_kernel, dim3(grid_for(total)), dim3(256), 0, s, ids, B, n, vocab, table, table_type, d, h, P,
+                     first);
+}
+
+void launch_time_embed(int steps, int dim, float* out, hipStream_t s) {
+  hipLaunchKernelGGL(time_embed_kernel, dim3(steps), dim3(128), 0, s, steps, dim, out);
+}
+
+void launch_rope_table(int npos, int hd, double base, float* out, hipStream_t s) {
+  hipLaunchKernelGGL(rope_table_kernel, dim3(grid_for((long)npos * hd / 2)), dim3(256), 0, s, npos, hd, base, out);
+}
+
+void launch_copy_f32(const float* src, float* dst, long n, hipStream_t s) {
+  hipLaunchKernelGGL(copy_f32_kernel, dim3(grid_for(n)), dim3(256), 0, s, src, dst, n);
+}
+
+void launch_silu_f32(const float* src, float* dst, long n, hipStream_t s) {
+  hipLaunchKernelGGL(silu_f32_kernel, dim3(grid_for(n)), dim3(256), 0, s, src, dst, n);
+}
+
+void launch_dit_state_rows(const void* st, int et, int B, int d, int seq, const float* pos, float* X, hipStream_t s) {
+  hipLaunchKernelGGL(dit_state_rows_kernel, dim3(grid_for((long)B * d)), dim3(256), 0, s, st, et, B, d, seq, pos, X);
+}
+
+void launch_transpose_convert(const float* src, int K, int N, void* dst, int ldk, int et, const int* rowmap,
+                              hipStream_t s) {
+  dim3 grid((N + 31) / 32, (ldk + 31) / 32);
+  hipLaunchKernelGGL(transpose_convert_kernel, grid, dim3(256), 0, s, src, K, N, dst, ldk, et, rowmap);
+}
+
+void launch_convert(const float* src, long n, void* dst, int et, hipStream_t s) {
+  hipLaunchKernelGGL(convert_kernel, dim3(grid_for(n)), dim3(256), 0, s, src, n, dst, et);
+}
+
+void launch_round_bf16_f32(const float* src, long n, float* dst, hipStream_t s) {
+  hipLaunchKernelGGL(round_bf16_kernel, dim3(grid_for(n)), dim3(256), 0, s, src, n, dst);
+}
+
+void launch_cu_probe(uint32_t* out, int blocks, int spin, hipStream_t s) {
+  hipLaunchKernelGGL(cu_probe_kernel, dim3(blocks), dim3(64), 0, s, out, spin);
+}

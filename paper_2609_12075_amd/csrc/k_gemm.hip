@@ -1,0 +1,301 @@
+// Matrix products of the VLA stages on gfx950.
+//
+// Every dense projection of both stages (QKV, attention output, MLP, patch
+// embedding, projector, action in/out, time and adaLN conditioning) is
+// D[m][n] = sum_k A[m][k] W[n][k] with the weight stored transposed (K
+// contiguous). bf16 models use the CDNA4 matrix cores
+// (v_mfma_f32_16x16x32_bf16, fp32 accumulation); fp32 models use a VALU FMA
+// kernel. The product is computed as D^T = W A^T so that each lane of the
+// matrix instruction ends up owning four consecutive output columns of one
+// row: that makes the fused epilogues (bias, residual add, GeGLU pairs, RoPE
+// pairs, head scatter, Euler update) lane-local and the stores contiguous.
+#include "common.h"
+
+typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
+typedef __attribute__((ext_vector_type(4))) __bf16 bf16x4;
+typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2;
+typedef __attribute__((ext_vector_type(4))) float f32x4;
+
+// ---------------------------------------------------------------- epilogue
+__device__ __forceinline__ float act_apply(float x, int act) {
+  if (act == ACT_SILU) return x / (1.0f + __expf(-x));
+  if (act == ACT_GELU) {
+    const float c = 0.7978845608028654f;   // sqrt(2/pi)
+    return 0.5f * x * (1.0f + tanhf(c * (x + 0.044715f * x * x * x)));
+  }
+  return x;
+}
+
+__device__ __forceinline__ void store_elem(void* base, long idx, int type, float v) {
+  if (type == ET_BF16) reinterpret_cast<bf16*>(base)[idx] = (bf16)v;
+  else reinterpret_cast<float*>(base)[idx] = v;
+}
+
+// Epilogue for output row m and the four columns n0..n0+3 (n0 % 4 == 0).
+__device__ __forceinline__ void epilogue4(const GemmArgs& a, int m, int n0, float v[4]) {
+  if (m >= a.M || n0 >= a.N) return;
+  const int nv = min(4, a.N - n0);
+  switch (a.mode) {
+    case EPI_STORE: {
+      long row = a.row_group > 0 ? (long)(m / a.row_group) * a.row_group_stride + (long)(m % a.row_group) * a.ldo
+                                 : (long)m * a.ldo;
+      float r[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        float x = v[j];
+        if (j < nv) {
+          if (a.bias) x += a.bias[n0 + j];
+          if (a.tab) x += a.tab[(long)(m % a.tab_period) * a.ldtab + n0 + j];
+        }
+        r[j] = act_apply(x, a.act);
+      }
+      if (a.out_type == ET_BF16) {
+        bf16* o = reinterpret_cast<bf16*>(a.out) + row + n0;
+        if (nv == 4 && ((reinterpret_cast<uintptr_t>(o) & 7) == 0)) {
+          bf16x4 w = {(bf16)r[0], (bf16)r[1], (bf16)r[2], (bf16)r[3]};
+          *reinterpret_cast<bf16x4*>(o) = w;
+        } else {
+          for (int j = 0; j < nv; ++j) o[j] = (bf16)r[j];
+        }
+      } else {
+        float* o = reinterpret_cast<float*>(a.out) + row + n0;
+        if (nv == 4 && ((reinterpret_cast<uintptr_t>(o) & 15) == 0)) {
+          *reinterpret_cast<f32x4*>(o) = f32x4{r[0], r[1], r[2], r[3]};
+        } else {
+          for (int j = 0; j < nv; ++j) o[j] = r[j];
+        }
+      }
+      break;
+    }
+    case EPI_RESID: {
+      long row = a.row_group > 0 ? (long)(m / a.row_group) * a.row_group_stride + (long)(m % a.row_group) * a.ldo
+                                 : (long)m * a.ldo;
+      float* o = reinterpret_cast<float*>(a.out) + row + n0;
+      for (int j = 0; j < nv; ++j) {
+        float x = v[j] + (a.bias ? a.bias[n0 + j] : 0.0f);
+        if (a.gate) x *= a.gate[n0 + j];
+        o[j] += x;
+      }
+      break;
+    }
+    case EPI_GEGLU: {
+      // weight rows interleaved: row 2f = gate f, row 2f + 1 = up f
+      bf16* ob = reinterpret_cast<bf16*>(a.out);
+      float* of = reinterpret_cast<float*>(a.out);
+      const int f0 = n0 >> 1;
+      for (int j = 0; j + 1 < nv; j += 2) {
+        float g = v[j], u = v[j + 1];
+        if (a.bias) { g += a.bias[n0 + j]; u += a.bias[n0 + j + 1]; }
+        float r = act_apply(g, ACT_GELU) * u;
+        long idx = (long)m * a.ldo + f0 + (j >> 1);
+        if (a.out_type == ET_BF16) ob[idx] = (bf16)r; else of[idx] = r;
+      }
+      break;
+    }
+    case EPI_QKV: {
+      const QkvEpi& q = a.qkv;
+      const int c0 = q.n_off + n0;            // logical column (multiple of 4)
+      const int hd = q.hd;
+      const int b = m / q.seq, i = m % q.seq;
+      int seg, head, j0;
+      if (c0 < q.n_q * hd) { seg = 0; head = c0 / hd; j0 = c0 % hd; }
+      else if (c0 < (q.n_q + q.n_kv) * hd) { seg = 1; head = (c0 - q.n_q * hd) / hd; j0 = (c0 - q.n_q * hd) % hd; }
+      else { seg = 2; head = (c0 - (q.n_q + q.n_kv) * hd) / hd; j0 = (c0 - (q.n_q + q.n_kv) * hd) % hd; }
+      float x[4];
+      for (int j = 0; j < 4; ++j) x[j] = v[j] + ((a.bias && j < nv) ? a.bias[n0 + j] : 0.0f);
+      void* dst; long idx;
+      if (seg == 0) { dst = q.q; idx = (long)b * q.q_sb + (long)head * q.q_sh + (long)i * q.q_si; }
+      else if (seg == 1) { dst = q.k; idx = (long)b * q.k_sb + (long)head * q.k_sh + (long)i * q.k_si; }
+      else { dst = q.v; idx = (long)b * q.v_sb + (long)head * q.v_sh + (long)i * q.v_si; }
+      if (seg < 2 && q.pos0 >= 0) {
+        // weight rows of q and k are stored pair-interleaved per head:
+        // row 2t holds dimension t and row 2t + 1 holds dimension t + hd/2
+        const int half = hd >> 1, pos = q.pos0 + i;
+        for (int j = 0; j < 4; j += 2) {
+          const int t = (j0 + j) >> 1;
+          const float cs = q.rope_cs[((long)pos * half + t) * 2 + 0];
+          const float sn = q.rope_cs[((long)pos * half + t) * 2 + 1];
+          const float x1 = x[j], x2 = x[j + 1];
+          store_elem(dst, idx + t, a.out_type, x1 * cs - x2 * sn);
+          store_elem(dst, idx + t + half, a.out_type, x2 * cs + x1 * sn);
+        }
+      } else {
+        for (int j = 0; j < nv; ++j) store_elem(dst, idx + j0 + j, a.out_type, x[j]);
+      }
+      break;
+    }
+    case EPI_EULER: {
+      float* o = reinterpret_cast<float*>(a.out) + (long)m * a.ldo + n0;
+      for (int j = 0; j < nv; ++j) o[j] += a.dt * (v[j] + (a.bias ? a.bias[n0 + j] : 0.0f));
+      break;
+    }
+  }
+}
+
+// ---------------------------------------------------------------- bf16 MFMA kernel
+// Block: 256 threads = 4 waves in a 2 x 2 grid over a BN (weight rows) x BM
+// (activation rows) tile; K advances in steps of 64 through a double-buffered
+// LDS tile whose rows are padded by 8 elements (conflict-free 16-byte reads).
+template <int BN, int BM, typename TA>
+__global__ void __launch_bounds__(256)
+gemm_mfma_kernel(GemmArgs a) {
+  constexpr int BK = 64, LDK = BK + 8;
+  constexpr int TN = BN / 32, TM = BM / 32;         // 16-wide subtiles per wave
+  constexpr int WCH = BN * 8 / 256, ACH = BM * 8 / 256;   // 8-element chunks per thread
+  constexpr int LDC = BN + 4;         // fp32 output tile row stride (epilogue)
+  constexpr int OPER_BYTES = 2 * (BN + BM) * LDK * 2, OUT_BYTES = BM * LDC * 4;
+  __shared__ __attribute__((aligned(16))) char smem[OPER_BYTES > OUT_BYTES ? OPER_BYTES : OUT_BYTES];
+  auto Ws = reinterpret_cast<bf16 (*)[BN][LDK]>(smem);
+  auto As = reinterpret_cast<bf16 (*)[BM][LDK]>(smem + 2 * BN * LDK * 2);
+  auto Cs = reinterpret_cast<float (*)[LDC]>(smem);
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wn0 = (wave >> 1) * (BN / 2), wm0 = (wave & 1) * (BM / 2);
+  const int n_blk = blockIdx.y * BN, m_blk = blockIdx.x * BM;
+  const int K = a.K;
+  const int nk = (K + BK - 1) / BK;
+  const bf16* W = reinterpret_cast<const bf16*>(a.W);
+  const TA* A = reinterpret_cast<const TA*>(a.A);
+
+  bf16x8 wreg[WCH], areg[ACH];
+  const int crow = tid >> 3, ccol = (tid & 7) * 8;
+
+  auto load_tile = [&](int kt) {
+    const int k = kt * BK + ccol;
+#pragma unroll
+    for (int j = 0; j < WCH; ++j) {
+      const int n = n_blk + crow + 32 * j;
+      if (n < a.N && k < K) wreg[j] = *reinterpret_cast<const bf16x8*>(W + (long)n * a.ldw + k);
+      else wreg[j] = bf16x8{};
+    }
+#pragma unroll
+    for (int j = 0; j < ACH; ++j) {
+      const int m = m_blk + crow + 32 * j;
+      if (m < a.M && k < K) {
+        if constexpr (sizeof(TA) == 2) {
+          areg[j] = *reinterpret_cast<const bf16x8*>(A + (long)m * a.lda + k);
+        } else {
+          const f32x4* p = reinterpret_cast<const f32x4*>(A + (long)m * a.lda + k);
+          f32x4 x0 = p[0], x1 = p[1];
+          areg[j] = bf16x8{(bf16)x0[0], (bf16)x0[1], (bf16)x0[2], (bf16)x0[3],
+                           (bf16)x1[0], (bf16)x1[1], (bf16)x1[2], (bf16)x1[3]};
+        }
+      } else {
+        areg[j] = bf16x8{};
+      }
+    }
+  };
+  auto store_tile = [&](int buf) {
+#pragma unroll
+    for (int j = 0; j < WCH; ++j) *reinterpret_cast<bf16x8*>(&Ws[buf][crow + 32 * j][ccol]) = wreg[j];
+#pragma unroll
+    for (int j = 0; j < ACH; ++j) *reinterpret_cast<bf16x8*>(&As[buf][crow + 32 * j][ccol]) = areg[j];
+  };
+
+  f32x4 acc[TN][TM];
+#pragma unroll
+  for (int i = 0; i < TN; ++i)
+#pragma unroll
+    for (int j = 0; j < TM; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  load_tile(0);
+  store_tile(0);
+  __syncthreads();
+  const int lr = lane & 15, lk = (lane >> 4) * 8;
+  for (int kt = 0; kt < nk; ++kt) {
+    const int buf = kt & 1;
+    if (kt + 1 < nk) load_tile(kt + 1);
+#pragma unroll
+    for (int kc = 0; kc < BK; kc += 32) {
+      bf16x8 wf[TN], af[TM];
+#pragma unroll
+      for (int i = 0; i < TN; ++i) wf[i] = *reinterpret_cast<const bf16x8*>(&Ws[buf][wn0 + 16 * i + lr][kc + lk]);
+#pragma unroll
+      for (int j = 0; j < TM; ++j) af[j] = *reinterpret_cast<const bf16x8*>(&As[buf][wm0 + 16 * j + lr][kc + lk]);
+#pragma unroll
+      for (int i = 0; i < TN; ++i)
+#pragma unroll
+        for (int j = 0; j < TM; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[i], af[j], acc[i][j], 0, 0, 0);
+    }
+    if (kt + 1 < nk) store_tile(buf ^ 1);
+    __syncthreads();
+  }
+
+  // lane owns D[n = 4*(lane/16) + r][m = lane % 16] of every 16 x 16 subtile;
+  // stage the tile through LDS (operand tiles are dead after the last
+  // barrier) so each thread then finishes four consecutive columns of a row.
+#pragma unroll
+  for (int i = 0; i < TN; ++i)
+#pragma unroll
+    for (int j = 0; j < TM; ++j)
+      *reinterpret_cast<f32x4*>(&Cs[wm0 + 16 * j + lr][wn0 + 16 * i + (lane >> 4) * 4]) = acc[i][j];
+  __syncthreads();
+#pragma unroll 1
+  for (int c = tid; c < BM * (BN / 4); c += 256) {
+    const int mr = c / (BN / 4), nc = (c % (BN / 4)) * 4;
+    f32x4 t = *reinterpret_cast<const f32x4*>(&Cs[mr][nc]);
+    float v[4] = {t[0], t[1], t[2], t[3]};
+    epilogue4(a, m_blk + mr, n_blk + nc, v);
+  }
+}
+
+// ---------------------------------------------------------------- fp32 VALU kernel
+// 64 x 64 tile, 256 threads, each thread 4 columns x 4 rows; K in steps of 16.
+__global__ void __launch_bounds__(256) gemm_f32_kernel(GemmArgs a) {
+  constexpr int BN = 64, BM = 64, BK = 16;
+  __shared__ float Ws[BK][BN + 4];
+  __shared__ float As[BK][BM + 4];
+  const int tid = threadIdx.x;
+  const int n_blk = blockIdx.y * BN, m_blk = blockIdx.x * BM;
+  const float* W = reinterpret_cast<const float*>(a.W);
+  const float* A = reinterpret_cast<const float*>(a.A);
+  const int tn = (tid & 15) * 4, tm = (tid >> 4) * 4;
+  float acc[4][4] = {};
+  for (int k0 = 0; k0 < a.K; k0 += BK) {
+    for (int e = tid; e < BN * BK; e += 256) {
+      const int r = e / BK, kk = e % BK;
+      const int n = n_blk + r, k = k0 + kk;
+      Ws[kk][r] = (n < a.N && k < a.K) ? W[(long)n * a.ldw + k] : 0.0f;
+      const int m = m_blk + r;
+      As[kk][r] = (m < a.M && k < a.K) ? A[(long)m * a.lda + k] : 0.0f;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int kk = 0; kk < BK; ++kk) {
+      float w[4], x[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) { w[i] = Ws[kk][tn + i]; x[i] = As[kk][tm + i]; }
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+#pragma unroll
+        for (int c = 0; c < 4; ++c) acc[r][c] = fmaf(x[r], w[c], acc[r][c]);
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int r = 0; r < 4; ++r) epilogue4(a, m_blk + tm + r, n_blk + tn, acc[r]);
+}
+
+// ---------------------------------------------------------------- dispatch
+template <int BN, int BM>
+static void launch_mfma(const GemmArgs& a, hipStream_t s) {
+  dim3 grid((a.M + BM - 1) / BM, (a.N + BN - 1) / BN);
+  if (a.a_type == ET_BF16) hipLaunchKernelGGL((gemm_mfma_kernel<BN, BM, bf16>), grid, dim3(256), 0, s, a);
+  else hipLaunchKernelGGL((gemm_mfma_kernel<BN, BM, float>), grid, dim3(256), 0, s, a);
+}
+
+void launch_gemm(const GemmArgs& a, hipStream_t s) {
+  if (a.M <= 0 || a.N <= 0) return;
+  if (a.w_type == ET_F32) {
+    dim3 grid((a.M + 63) / 64, (a.N + 63) / 64);
+    hipLaunchKernelGGL(gemm_f32_kernel, grid, dim3(256), 0, s, a);
+    return;
+  }
+  // Pick the largest tile that still gives the chip (256 CUs) enough blocks.
+  auto blocks = [&](int bn, int bm) { return (long)((a.M + bm - 1) / bm) * ((a.N + bn - 1) / bn); };
+  if (a.M >= 128 && blocks(128, 128) >= 256) launch_mfma<128, 128>(a, s);
+  else if (a.M >= 64 && blocks(128, 64) >= 256) launch_mfma<128, 64>(a, s);
+  else if (a.M > 32) launch_mfma<64, 64>(a, s);
+  else launch_mfma<64, 32>(a, s);
+}

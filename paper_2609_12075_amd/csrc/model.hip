@@ -1,0 +1,722 @@
+// Model runtime: parameter upload, workspaces and the two stages of one
+// batched VLA inference (paper Section 2.1: VLM -> per-layer prefix state ->
+// action diffusion transformer running a fixed number of denoising steps).
+// Stages are recorded once per (batch, steps, buffers) into a HIP graph and
+// replayed (Section 4.1.1 records one graph per stage and batch size).
+#include <algorithm>
+#include <cstring>
+#include <functional>
+
+#include "model.h"
+
+namespace {
+
+inline int round_up(int x, int m) { return (x + m - 1) / m * m; }
+
+// ---------------------------------------------------------------- shape walk
+// Walks the canonical parameter order; `take(n)` is called once per tensor
+// with its element count. The same walk sizes the buffer and loads it.
+template <typename Take>
+void walk_params(const vla_config& c, Take&& take) {
+  const int E = c.vit_layers > 0 ? c.vit_d : c.llm_d;
+  const int T = (c.img_hw / c.patch) * (c.img_hw / c.patch);
+  const long pd = 3L * c.patch * c.patch;
+  take(pd * E); take(E); take((long)T * E);
+  for (int l = 0; l < c.vit_layers; ++l) {
+    const long d = c.vit_d, f = c.vit_mlp;
+    take(d); take(d);                       // ln1
+    take(d * d); take(d); take(d * d); take(d); take(d * d); take(d);   // q, k, v
+    take(d * d); take(d);                   // o
+    take(d); take(d);                       // ln2
+    take(d * f); take(f); take(f * d); take(d);
+  }
+  if (c.vit_layers > 0) { take(c.vit_d); take(c.vit_d); take((long)c.vit_d * c.llm_d); take(c.llm_d); }
+  take((long)c.vocab * c.llm_d);
+  const long D = c.llm_d, Hq = (long)c.n_q * c.head_dim, Hk = (long)c.n_kv * c.head_dim, F = c.llm_mlp;
+  for (int l = 0; l < c.llm_layers; ++l) {
+    take(D); take(D * Hq); take(D * Hk); take(D * Hk); take(Hq * D); take(D); take(D * F); take(D * F); take(F * D);
+  }
+  const long A = c.action_dim, Da = c.act_d, Fa = c.act_mlp, td = c.time_dim > 0 ? c.time_dim : c.act_d;
+  if (c.head_kind == VLA_HEAD_JOINT) {
+    take(A * Da); take(Da); take(Da * Da); take(td * Da); take(Da); take(Da * Da); take(Da);
+    for (int l = 0; l < c.act_layers; ++l) {
+      take(Da); take(Da * Hq); take(Da * Hk); take(Da * Hk); take(Hq * Da); take(Da); take(Da * Fa); take(Da * Fa);
+      take(Fa * Da);
+    }
+    take(Da); take(Da * A); take(A);
+  } else {
+    take(D); take(D * Da); take(Da);
+    for (int l = 0; l < c.act_layers; ++l) { take(Da * Da); take(Da); take(Da * Da); take(Da); }
+    take((long)c.state_dim * Da); take(Da);
+    take(td * Da); take(Da); take(Da * Da); take(Da); take(A * Da); take(Da); take((long)(c.horizon + 1) * Da);
+    for (int l = 0; l < c.act_layers; ++l) {
+      take(Da * 6 * Da); take(6 * Da);
+      for (int j = 0; j < 6; ++j) { take(Da * Da); take(Da); }   // q, k, v, o, cross q, cross o
+      take(Da * Fa); take(Fa); take(Fa * Da); take(Da);
+    }
+    take(Da * 2 * Da); take(2 * Da); take(Da * A); take(A);
+  }
+}
+
+}  // namespace
+
+std::string vla_config_check(const vla_config& c) {
+  auto pos = [](int v) { return v > 0; };
+  if (c.dtype != VLA_F32 && c.dtype != VLA_BF16) return "dtype must be VLA_F32 or VLA_BF16";
+  if (c.head_kind != VLA_HEAD_JOINT && c.head_kind != VLA_HEAD_DIT) return "head_kind must be JOINT or DIT";
+  if (!pos(c.n_img) || !pos(c.img_hw) || !pos(c.patch) || c.img_hw % c.patch) return "image size must be a multiple of patch";
+  if (c.vit_layers < 0 || (c.vit_layers > 0 && (!pos(c.vit_d) || !pos(c.vit_heads) || !pos(c.vit_mlp) || c.vit_d % c.vit_heads)))
+    return "bad ViT shape";
+  if (c.vit_layers > 0 && ((c.vit_d / c.vit_heads) % 8 || c.vit_d / c.vit_heads > 256)) return "ViT head dim must be a multiple of 8, <= 256";
+  if (!pos(c.n_text) || !pos(c.vocab)) return "bad text shape";
+  if (!pos(c.llm_layers) || !pos(c.llm_d) || !pos(c.n_q) || !pos(c.n_kv) || !pos(c.head_dim) || !pos(c.llm_mlp)) return "bad LLM shape";
+  if (c.n_q % c.n_kv) return "n_q must be a multiple of n_kv";
+  if (c.head_dim % 8 || c.head_dim > 256) return "head_dim must be a multiple of 8, <= 256";
+  if (!pos(c.act_layers) || !pos(c.act_d) || !pos(c.act_mlp) || !pos(c.horizon) || !pos(c.action_dim)) return "bad action shape";
+  if (!pos(c.max_batch) || c.max_batch > 4096) return "max_batch must be in [1, 4096]";
+  if (c.time_dim < 0 || (c.time_dim > 0 && c.time_dim % 2)) return "time_dim must be even";
+  const int td = c.time_dim > 0 ? c.time_dim : c.act_d;
+  if (td % 2) return "time embedding width must be even";
+  if (c.head_kind == VLA_HEAD_JOINT) {
+    if (c.act_layers != c.llm_layers) return "joint head: act_layers must equal llm_layers";
+  } else {
+    if (!pos(c.act_heads) || c.act_d % c.act_heads) return "DiT: act_d must be a multiple of act_heads";
+    if ((c.act_d / c.act_heads) % 8 || c.act_d / c.act_heads > 256) return "DiT head dim must be a multiple of 8, <= 256";
+    if (c.state_dim < 0) return "bad state_dim";
+  }
+  if (c.dtype == VLA_BF16) {
+    // matrix-core path: every reduction length (except the zero-padded patch
+    // vector) must be a multiple of 8 elements
+    const int ks[] = {c.llm_d, c.n_q * c.head_dim, c.llm_mlp, c.act_d, c.act_mlp, c.action_dim, td};
+    for (int k : ks) if (k % 8) return "bf16 models need llm_d, n_q*head_dim, llm_mlp, act_d, act_mlp, action_dim, time_dim % 8 == 0";
+    if (c.vit_layers > 0 && (c.vit_d % 8 || c.vit_mlp % 8)) return "bf16 ViT widths must be multiples of 8";
+    if (c.head_kind == VLA_HEAD_DIT && c.state_dim % 8) return "bf16 DiT state_dim must be a multiple of 8";
+  }
+  if (!(c.norm_eps >= 0.f) || !(c.rope_base > 0.f)) return "bad norm_eps / rope_base";
+  return "";
+}
+
+size_t vla_weight_count_impl(const vla_config& c) {
+  size_t n = 0;
+  walk_params(c, [&](long k) { n += (size_t)k; });
+  return n;
+}
+
+void* vla_model_s::dalloc(size_t bytes) {
+  void* p = nullptr;
+  if (bytes == 0) bytes = 256;
+  hipError_t e = hipMalloc(&p, bytes);
+  if (e != hipSuccess) throw VlaError{2, "hipMalloc(" + std::to_string(bytes) + "): " + hipGetErrorString(e)};
+  allocs.push_back(p);
+  return p;
+}
+
+size_t vla_model_s::kv_bytes(int B) const {
+  const size_t es = elem_size(et);
+  if (cfg.head_kind == VLA_HEAD_JOINT) return (size_t)cfg.llm_layers * 2 * B * cfg.n_kv * P * cfg.head_dim * es;
+  return ((size_t)B * P * cfg.act_layers * 2 * Da + (size_t)B * Da) * es;
+}
+
+// ---------------------------------------------------------------- parameter upload
+namespace {
+
+struct Loader {
+  vla_model_s* m;
+  const float* host;
+  size_t off = 0, n = 0;
+  float* stage = nullptr;       // device fp32 staging
+  size_t stage_cap = 0;
+  int* rowmap = nullptr;        // device row map staging
+  size_t rowmap_cap = 0;
+  hipStream_t s = nullptr;
+
+  const float* next(size_t cnt) {
+    if (off + cnt > n) throw VlaError{1, "parameter buffer too short"};
+    const float* p = host + off;
+    off += cnt;
+    return p;
+  }
+  float* upload(const float* h, size_t cnt) {
+    if (cnt > stage_cap) throw VlaError{1, "internal: staging too small"};
+    VLA_HIP(hipMemcpyAsync(stage, h, cnt * sizeof(float), hipMemcpyHostToDevice, s));
+    return stage;
+  }
+  // vector parameter (gain, bias, table) -> fp32 device copy, rounded to bf16 for bf16 models
+  float* vec(size_t cnt, float* dst = nullptr) {
+    const float* h = next(cnt);
+    if (!dst) dst = (float*)m->dalloc(cnt * 4);
+    float* d = upload(h, cnt);
+    if (m->et == ET_BF16) launch_round_bf16_f32(d, (long)cnt, dst, s);
+    else VLA_HIP(hipMemcpyAsync(dst, d, cnt * 4, hipMemcpyDeviceToDevice, s));
+    VLA_HIP(hipStreamSynchronize(s));
+    return dst;
+  }
+  // matrix [K][N] (row-major [in, out]) -> rows of dst (transposed, ldk) via rowmap
+  void mat_into(Mat& dst, int K, int N, const std::vector<int>& rows) {
+    const float* h = next((size_t)K * N);
+    if ((size_t)K * N == 0) return;
+    float* d = upload(h, (size_t)K * N);
+    if (rows.size() > rowmap_cap) throw VlaError{1, "internal: rowmap staging too small"};
+    VLA_HIP(hipMemcpyAsync(rowmap, rows.data(), rows.size() * sizeof(int), hipMemcpyHostToDevice, s));
+    launch_transpose_convert(d, K, N, dst.p, dst.ldk, m->et, rowmap, s);
+    VLA_HIP(hipGetLastError());
+    VLA_HIP(hipStreamSynchronize(s));
+  }
+  Mat alloc_mat(int N, int K) {
+    Mat w;
+    w.N = N; w.K = K;
+    w.ldk = m->et == ET_BF16 ? round_up(K, 8) : K;
+    w.p = m->dalloc((size_t)N * w.ldk * elem_size(m->et));
+    VLA_HIP(hipMemsetAsync(w.p, 0, (size_t)N * w.ldk * elem_size(m->et), s));
+    return w;
+  }
+  static std::vector<int> iota(int n, int base) {
+    std::vector<int> r(n);
+    for (int i = 0; i < n; ++i) r[i] = base + i;
+    return r;
+  }
+  // RoPE pair interleave within each head: column h*hd + t -> row h*hd + 2t
+  // (t < hd/2) or h*hd + 2(t - hd/2) + 1.
+  static std::vector<int> rope_rows(int heads, int hd, int base) {
+    std::vector<int> r(heads * hd);
+    const int half = hd / 2;
+    for (int h = 0; h < heads; ++h)
+      for (int t = 0; t < hd; ++t) r[h * hd + t] = base + h * hd + (t < half ? 2 * t : 2 * (t - half) + 1);
+    return r;
+  }
+  static std::vector<int> stride_rows(int n, int stride, int base) {
+    std::vector<int> r(n);
+    for (int i = 0; i < n; ++i) r[i] = base + i * stride;
+    return r;
+  }
+  Mat mat(int K, int N) {
+    Mat w = alloc_mat(N, K);
+    mat_into(w, K, N, iota(N, 0));
+    return w;
+  }
+};
+
+}  // namespace
+
+void vla_model_s::init(const vla_config& c, const float* w, size_t n, int dev) {
+  cfg = c;
+  device = dev;
+  et = c.dtype == VLA_BF16 ? ET_BF16 : ET_F32;
+  T = (c.img_hw / c.patch) * (c.img_hw / c.patch);
+  P = c.n_img * T + c.n_text;
+  E = c.vit_layers > 0 ? c.vit_d : c.llm_d;
+  const int pd = 3 * c.patch * c.patch;
+  Kp = et == ET_BF16 ? round_up(pd, 8) : pd;
+  D = c.llm_d; hd = c.head_dim; Hq = c.n_q * hd; Hk = c.n_kv * hd;
+  Da = c.act_d; A = c.action_dim; H = c.horizon;
+  vhd = c.vit_layers > 0 ? c.vit_d / c.vit_heads : 0;
+  dhd = c.head_kind == VLA_HEAD_DIT ? c.act_d / c.act_heads : 0;
+  tdim = c.time_dim > 0 ? c.time_dim : c.act_d;
+  Ltok = H + (c.head_kind == VLA_HEAD_DIT ? 1 : 0);
+  const int Bm = c.max_batch;
+  const bool dit_head = c.head_kind == VLA_HEAD_DIT;
+
+  DeviceGuard g(dev);
+  Loader L{this, w};
+  L.n = n;
+  VLA_HIP(hipStreamCreateWithFlags(&L.s, hipStreamNonBlocking));
+  size_t max_t = 0;
+  walk_params(c, [&](long k) { max_t = std::max(max_t, (size_t)k); });
+  L.stage_cap = max_t;
+  L.stage = (float*)dalloc(max_t * 4);
+  L.rowmap_cap = (size_t)std::max({Hq + 2 * Hk, 2 * c.llm_mlp, 2 * c.act_mlp, 6 * Da, 2 * Da, c.vit_mlp, c.vocab, D, 3 * E, 64});
+  L.rowmap = (int*)dalloc(L.rowmap_cap * 4);
+
+  try {
+    // ---- vision front-end
+    patch = L.alloc_mat(E, pd);
+    patch.ldk = Kp;
+    L.mat_into(patch, pd, E, Loader::iota(E, 0));
+    patch.K = Kp;                     // the patch rows are zero-padded to Kp
+    patch_b = L.vec(E);
+    pos = L.vec((size_t)T * E);
+    for (int l = 0; l < c.vit_layers; ++l) {
+      VitLayer v{};
+      const int d = c.vit_d, f = c.vit_mlp;
+      v.ln1g = L.vec(d); v.ln1b = L.vec(d);
+      v.qkv = L.alloc_mat(3 * d, d);
+      v.bqkv = (float*)dalloc(3 * d * 4);
+      for (int j = 0; j < 3; ++j) {
+        L.mat_into(v.qkv, d, d, Loader::iota(d, j * d));
+        L.vec(d, v.bqkv + j * d);
+      }
+      v.wo = L.mat(d, d); v.bo = L.vec(d);
+      v.ln2g = L.vec(d); v.ln2b = L.vec(d);
+      v.w1 = L.mat(d, f); v.b1 = L.vec(f);
+      v.w2 = L.mat(f, d); v.b2 = L.vec(d);
+      vit.push_back(v);
+    }
+    if (c.vit_layers > 0) {
+      vit_lnf_g = L.vec(c.vit_d); vit_lnf_b = L.vec(c.vit_d);
+      proj = L.mat(c.vit_d, D); proj_b = L.vec(D);
+    }
+    {   // token embedding table, kept in the model dtype
+      const size_t cnt = (size_t)c.vocab * D;
+      const float* h = L.next(cnt);
+      float* d = L.upload(h, cnt);
+      embed = dalloc(cnt * elem_size(et));
+      launch_convert(d, (long)cnt, embed, et, L.s);
+      VLA_HIP(hipStreamSynchronize(L.s));
+    }
+    // ---- LLM
+    auto gemma_layer = [&](int din, int F) {
+      LlmLayer y{};
+      y.ln1 = L.vec(din);
+      y.qkv = L.alloc_mat(Hq + 2 * Hk, din);
+      L.mat_into(y.qkv, din, Hq, Loader::rope_rows(c.n_q, hd, 0));
+      L.mat_into(y.qkv, din, Hk, Loader::rope_rows(c.n_kv, hd, Hq));
+      L.mat_into(y.qkv, din, Hk, Loader::iota(Hk, Hq + Hk));
+      y.wo = L.mat(Hq, din);
+      y.ln2 = L.vec(din);
+      y.gu = L.alloc_mat(2 * F, din);
+      L.mat_into(y.gu, din, F, Loader::stride_rows(F, 2, 0));
+      L.mat_into(y.gu, din, F, Loader::stride_rows(F, 2, 1));
+      y.wd = L.mat(F, din);
+      return y;
+    };
+    for (int l = 0; l < c.llm_layers; ++l) llm.push_back(gemma_layer(D, c.llm_mlp));
+    // ---- action stage
+    const int Fa = c.act_mlp;
+    if (!dit_head) {
+      ain = L.mat(A, Da); ain_b = L.vec(Da);
+      t1a = L.mat(Da, Da); t1t = L.mat(tdim, Da); t1_b = L.vec(Da);
+      t2 = L.mat(Da, Da); t2_b = L.vec(Da);
+      for (int l = 0; l < c.act_layers; ++l) act.push_back(gemma_layer(Da, Fa));
+      lnf = L.vec(Da);
+      out = L.mat(Da, A); out_b = L.vec(A);
+    } else {
+      llm_lnf = L.vec(D);
+      vp = L.mat(D, Da); vp_b = L.vec(Da);
+      const int NL = c.act_layers;
+      xkv = L.alloc_mat(NL * 2 * Da, Da);
+      xkv_b = (float*)dalloc((size_t)NL * 2 * Da * 4);
+      for (int l = 0; l < NL; ++l) {
+        L.mat_into(xkv, Da, Da, Loader::iota(Da, (2 * l) * Da)); L.vec(Da, xkv_b + (2 * l) * Da);
+        L.mat_into(xkv, Da, Da, Loader::iota(Da, (2 * l + 1) * Da)); L.vec(Da, xkv_b + (2 * l + 1) * Da);
+      }
+      state_w = L.mat(std::max(c.state_dim, 0), Da); state_b = L.vec(Da);
+      dt1 = L.mat(tdim, Da); dt1_b = L.vec(Da);
+      dt2 = L.mat(Da, Da); dt2_b = L.vec(Da);
+      dain = L.mat(A, Da); dain_b = L.vec(Da);
+      dpos = L.vec((size_t)(H + 1) * Da);
+      mod_all = L.alloc_mat(NL * 6 * Da, Da);
+      mod_b = (float*)dalloc((size_t)NL * 6 * Da * 4);
+      for (int l = 0; l < NL; ++l) {
+        DitLayer y{};
+        L.mat_into(mod_all, Da, 6 * Da, Loader::iota(6 * Da, l * 6 * Da));
+        L.vec(6 * Da, mod_b + (size_t)l * 6 * Da);
+        y.qkv = L.alloc_mat(3 * Da, Da);
+        y.bqkv = (float*)dalloc(3 * Da * 4);
+        for (int j = 0; j < 3; ++j) { L.mat_into(y.qkv, Da, Da, Loader::iota(Da, j * Da)); L.vec(Da, y.bqkv + j * Da); }
+        y.wo = L.mat(Da, Da); y.bo = L.vec(Da);
+        y.cq = L.mat(Da, Da); y.bcq = L.vec(Da);
+        y.co = L.mat(Da, Da); y.bco = L.vec(Da);
+        y.w1 = L.mat(Da, Fa); y.b1 = L.vec(Fa);
+        y.w2 = L.mat(Fa, Da); y.b2 = L.vec(Da);
+        dit.push_back(y);
+      }
+      modf = L.mat(Da, 2 * Da); modf_b = L.vec(2 * Da);
+      dout = L.mat(Da, A); dout_b = L.vec(A);
+    }
+    if (L.off != n) throw VlaError{1, "parameter buffer has " + std::to_string(n) + " values, shape needs " +
+                                          std::to_string(L.off)};
+    // RoPE table for positions 0 .. P + horizon - 1
+    rope_cs = (float*)dalloc((size_t)(P + H) * (hd / 2) * 2 * 4);
+    launch_rope_table(P + H, hd, (double)c.rope_base, rope_cs, L.s);
+
+    // ---- workspaces (sized for max_batch)
+    const size_t es = elem_size(et);
+    const size_t Mi = (size_t)Bm * c.n_img * T, Mp = (size_t)Bm * P;
+    patches = dalloc(Mi * Kp * es);
+    if (c.vit_layers > 0) {
+      const size_t d = c.vit_d;
+      vx = (float*)dalloc(Mi * d * 4);
+      vz = dalloc(Mi * d * es); vq = dalloc(Mi * d * es); vk = dalloc(Mi * d * es); vv = dalloc(Mi * d * es);
+      vo = dalloc(Mi * d * es); vmlp = dalloc(Mi * c.vit_mlp * es);
+    }
+    h = (float*)dalloc(Mp * D * 4);
+    z = dalloc(Mp * D * es);
+    q = dalloc(Mp * Hq * es);
+    o = dalloc(Mp * Hq * es);
+    gu = dalloc(Mp * c.llm_mlp * es);
+    if (dit_head) {
+      kbuf = dalloc(Mp * Hk * es); vbuf = dalloc(Mp * Hk * es);
+      feat = dalloc(Mp * Da * es);
+      zero_state = (float*)dalloc((size_t)Bm * std::max(c.state_dim, 1) * 4);
+      VLA_HIP(hipMemsetAsync(zero_state, 0, (size_t)Bm * std::max(c.state_dim, 1) * 4, L.s));
+      const size_t Mt = (size_t)Bm * Ltok;
+      X = (float*)dalloc(Mt * Da * 4);
+      zd = dalloc(Mt * Da * es); qd = dalloc(Mt * Da * es); kd = dalloc(Mt * Da * es); vd = dalloc(Mt * Da * es);
+      qc = dalloc(Mt * Da * es); od = dalloc(Mt * Da * es); mlp = dalloc(Mt * Fa * es);
+      zf = dalloc((size_t)Bm * H * Da * es);
+    } else {
+      const size_t Ma = (size_t)Bm * H;
+      e = dalloc(Ma * Da * es); u = dalloc(Ma * Da * es);
+      ha = (float*)dalloc(Ma * Da * 4);
+      za = dalloc(Ma * Da * es);
+      qa = dalloc(Ma * Hq * es); ks = dalloc(Ma * Hk * es); vs = dalloc(Ma * Hk * es);
+      oa = dalloc(Ma * Hq * es); gua = dalloc(Ma * Fa * es);
+    }
+    VLA_HIP(hipStreamSynchronize(L.s));
+    for (int i = 0; i < 2; ++i) VLA_HIP(hipStreamCreateWithFlags(&cap_stream[i], hipStreamNonBlocking));
+  } catch (...) {
+    (void)hipStreamDestroy(L.s);
+    throw;
+  }
+  (void)hipStreamDestroy(L.s);
+}
+
+void vla_model_s::destroy() {
+  DeviceGuard g(device);
+  for (int st = 0; st < 2; ++st) {
+    for (auto& kv : graph_cache[st]) (void)hipGraphExecDestroy(kv.second);
+    graph_cache[st].clear();
+    if (cap_stream[st]) (void)hipStreamDestroy(cap_stream[st]);
+  }
+  (void)hipDeviceSynchronize();
+  for (void* p : allocs) (void)hipFree(p);
+  allocs.clear();
+}
+
+// ---------------------------------------------------------------- GEMM helpers
+namespace {
+
+GemmArgs gm(const vla_model_s& m, const Mat& w, int M, const void* A, int lda, int a_type) {
+  GemmArgs g{};
+  g.M = M; g.N = w.N; g.K = (m.et == ET_BF16) ? w.ldk : w.K;
+  g.A = A; g.lda = lda; g.a_type = a_type;
+  g.W = w.p; g.ldw = w.ldk; g.w_type = m.et;
+  g.mode = EPI_STORE; g.act = ACT_NONE;
+  g.tab_period = 1;
+  return g;
+}
+
+void store(GemmArgs g, void* out, int ldo, int out_type, const float* bias, int act, hipStream_t s) {
+  g.mode = EPI_STORE; g.out = out; g.ldo = ldo; g.out_type = out_type; g.bias = bias; g.act = act;
+  launch_gemm(g, s);
+}
+
+void resid(GemmArgs g, float* out, int ldo, const float* bias, const float* gate, hipStream_t s) {
+  g.mode = EPI_RESID; g.out = out; g.ldo = ldo; g.out_type = ET_F32; g.bias = bias; g.gate = gate;
+  launch_gemm(g, s);
+}
+
+void norm(int rows, int d, int kind, const float* in, int ld_in, void* out, int ld_out, int out_type, const float* g,
+          const float* b, float eps, hipStream_t s, int skip = 0, int skip_group = 1) {
+  NormArgs a{};
+  a.rows = rows; a.d = d; a.kind = kind; a.in = in; a.ld_in = ld_in; a.out = out; a.ld_out = ld_out;
+  a.out_type = out_type; a.g = g; a.b = b; a.eps = eps; a.skip = skip; a.skip_group = skip_group;
+  launch_norm(a, s);
+}
+
+AttnArgs attn(int B, int Hq, int Hkv, int Lq, int hd, int et) {
+  AttnArgs a{};
+  a.B = B; a.Hq = Hq; a.Hkv = Hkv; a.Lq = Lq; a.hd = hd; a.et = et;
+  a.scale = 1.0f / sqrtf((float)hd);
+  return a;
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------- VLM stage
+void vla_model_s::enqueue_prefill(int B, const float* pix, const int32_t* ids, const float* state, void* kv,
+                                  hipStream_t s) {
+  const vla_config& c = cfg;
+  const size_t es = elem_size(et);
+  const int nimg = B * c.n_img, Mi = nimg * T, Mp = B * P;
+  const float eps = c.norm_eps;
+  const bool dit_head = c.head_kind == VLA_HEAD_DIT;
+
+  launch_im2col(pix, nimg, c.img_hw, c.patch, patches, Kp, et, s);
+  if (c.vit_layers == 0) {
+    // patch embedding + position table straight into the prefix rows b*P + t
+    GemmArgs g = gm(*this, patch, Mi, patches, Kp, et);
+    g.tab = pos; g.tab_period = T; g.ldtab = E;
+    g.row_group = c.n_img * T; g.row_group_stride = (long)P * D;
+    store(g, h, D, ET_F32, patch_b, ACT_NONE, s);
+  } else {
+    const int d = c.vit_d, nh = c.vit_heads;
+    GemmArgs g = gm(*this, patch, Mi, patches, Kp, et);
+    g.tab = pos; g.tab_period = T; g.ldtab = E;
+    store(g, vx, d, ET_F32, patch_b, ACT_NONE, s);
+    for (int l = 0; l < c.vit_layers; ++l) {
+      const VitLayer& y = vit[l];
+      norm(Mi, d, 1, vx, d, vz, d, et, y.ln1g, y.ln1b, eps, s);
+      GemmArgs q3 = gm(*this, y.qkv, Mi, vz, d, et);
+      q3.mode = EPI_QKV; q3.bias = y.bqkv; q3.out_type = et;
+      QkvEpi& e3 = q3.qkv;
+      e3.n_q = nh; e3.n_kv = nh; e3.hd = vhd; e3.n_off = 0; e3.seq = T; e3.pos0 = -1;
+      e3.q = vq; e3.q_sb = (long)nh * T * vhd; e3.q_sh = (long)T * vhd; e3.q_si = vhd;
+      e3.k = vk; e3.k_sb = e3.q_sb; e3.k_sh = e3.q_sh; e3.k_si = vhd;
+      e3.v = vv; e3.v_sb = e3.q_sb; e3.v_sh = e3.q_sh; e3.v_si = vhd;
+      launch_gemm(q3, s);
+      AttnArgs at = attn(nimg, nh, nh, T, vhd, et);
+      at.q = vq; at.q_sb = e3.q_sb; at.q_sh = e3.q_sh; at.q_si = vhd;
+      at.seg[0] = AttnSeg{vk, e3.k_sb, e3.k_sh, vhd, vv, e3.v_sb, e3.v_sh, vhd, T};
+      at.seg[1].len = 0;
+      at.o = vo; at.o_sb = (long)T * d; at.o_sh = vhd; at.o_si = d;
+      launch_attention(at, s);
+      resid(gm(*this, y.wo, Mi, vo, d, et), vx, d, y.bo, nullptr, s);
+      norm(Mi, d, 1, vx, d, vz, d, et, y.ln2g, y.ln2b, eps, s);
+      store(gm(*this, y.w1, Mi, vz, d, et), vmlp, c.vit_mlp, et, y.b1, ACT_GELU, s);
+      resid(gm(*this, y.w2, Mi, vmlp, c.vit_mlp, et), vx, d, y.b2, nullptr, s);
+    }
+    norm(Mi, d, 1, vx, d, vz, d, et, vit_lnf_g, vit_lnf_b, eps, s);
+    GemmArgs gp = gm(*this, proj, Mi, vz, d, et);
+    gp.row_group = c.n_img * T; gp.row_group_stride = (long)P * D;
+    store(gp, h, D, ET_F32, proj_b, ACT_NONE, s);
+  }
+  launch_embed(ids, B, c.n_text, c.vocab, embed, et, D, h, P, c.n_img * T, s);
+
+  const int nq = c.n_q, nkv = c.n_kv;
+  for (int l = 0; l < c.llm_layers; ++l) {
+    const LlmLayer& y = llm[l];
+    const bool last_kv_only = !dit_head && l == c.llm_layers - 1;
+    void *kd_, *vd_;
+    if (!dit_head) {
+      const size_t per = (size_t)B * nkv * P * hd * es;
+      kd_ = (char*)kv + (size_t)(2 * l) * per;
+      vd_ = (char*)kv + (size_t)(2 * l + 1) * per;
+    } else {
+      kd_ = kbuf; vd_ = vbuf;
+    }
+    norm(Mp, D, 0, h, D, z, D, et, y.ln1, nullptr, eps, s);
+    GemmArgs q3 = gm(*this, y.qkv, Mp, z, D, et);
+    q3.mode = EPI_QKV; q3.out_type = et;
+    QkvEpi& e3 = q3.qkv;
+    e3.n_q = nq; e3.n_kv = nkv; e3.hd = hd; e3.seq = P; e3.pos0 = 0; e3.rope_cs = rope_cs;
+    e3.q = q; e3.q_sb = (long)nq * P * hd; e3.q_sh = (long)P * hd; e3.q_si = hd;
+    e3.k = kd_; e3.k_sb = (long)nkv * P * hd; e3.k_sh = (long)P * hd; e3.k_si = hd;
+    e3.v = vd_; e3.v_sb = e3.k_sb; e3.v_sh = e3.k_sh; e3.v_si = hd;
+    if (last_kv_only) {
+      // only this layer's keys and values are consumed downstream
+      q3.W = (const char*)y.qkv.p + (size_t)Hq * y.qkv.ldk * es;
+      q3.N = 2 * Hk; e3.n_off = Hq;
+    }
+    launch_gemm(q3, s);
+    if (last_kv_only) continue;
+    AttnArgs at = attn(B, nq, nkv, P, hd, et);
+    at.q = q; at.q_sb = e3.q_sb; at.q_sh = e3.q_sh; at.q_si = hd;
+    at.seg[0] = AttnSeg{kd_, e3.k_sb, e3.k_sh, hd, vd_, e3.v_sb, e3.v_sh, hd, P};
+    at.seg[1].len = 0;
+    at.o = o; at.o_sb = (long)P * Hq; at.o_sh = hd; at.o_si = Hq;
+    launch_attention(at, s);
+    resid(gm(*this, y.wo, Mp, o, Hq, et), h, D, nullptr, nullptr, s);
+    norm(Mp, D, 0, h, D, z, D, et, y.ln2, nullptr, eps, s);
+    GemmArgs gg = gm(*this, y.gu, Mp, z, D, et);
+    gg.mode = EPI_GEGLU; gg.out = gu; gg.ldo = c.llm_mlp; gg.out_type = et;
+    launch_gemm(gg, s);
+    resid(gm(*this, y.wd, Mp, gu, c.llm_mlp, et), h, D, nullptr, nullptr, s);
+  }
+  if (dit_head) {
+    const int NL = c.act_layers;
+    norm(Mp, D, 0, h, D, z, D, et, llm_lnf, nullptr, eps, s);
+    store(gm(*this, vp, Mp, z, D, et), feat, Da, et, vp_b, ACT_NONE, s);
+    store(gm(*this, xkv, Mp, feat, Da, et), kv, NL * 2 * Da, et, xkv_b, ACT_NONE, s);
+    void* st_out = (char*)kv + (size_t)B * P * NL * 2 * Da * es;
+    const float* st_in = state ? state : zero_state;
+    if (c.state_dim > 0) store(gm(*this, state_w, B, st_in, c.state_dim, ET_F32), st_out, Da, et, state_b, ACT_NONE, s);
+    else {
+      // no state input: the token is the bias alone (a K = 0 product)
+      GemmArgs g0 = gm(*this, state_w, B, zero_state, 1, ET_F32);
+      g0.K = 0;
+      store(g0, st_out, Da, et, state_b, ACT_NONE, s);
+    }
+  }
+}
+
+// ---------------------------------------------------------------- action stage
+const CondCache& vla_model_s::cond_for(int N, hipStream_t s) {
+  std::lock_guard<std::mutex> lk(cond_mu);
+  auto it = cond.find(N);
+  if (it != cond.end()) return it->second;
+  CondCache cc;
+  const bool dit_head = cfg.head_kind == VLA_HEAD_DIT;
+  cc.phi = (float*)dalloc((size_t)N * tdim * 4);
+  launch_time_embed(N, tdim, cc.phi, s);
+  if (!dit_head) {
+    cc.tb = (float*)dalloc((size_t)N * Da * 4);
+    store(gm(*this, t1t, N, cc.phi, tdim, ET_F32), cc.tb, Da, ET_F32, t1_b, ACT_NONE, s);
+  } else {
+    const int NL = cfg.act_layers;
+    cc.c1 = (float*)dalloc((size_t)N * Da * 4);
+    cc.c = (float*)dalloc((size_t)N * Da * 4);
+    cc.sc = (float*)dalloc((size_t)N * Da * 4);
+    cc.mods = (float*)dalloc((size_t)N * NL * 6 * Da * 4);
+    cc.modf = (float*)dalloc((size_t)N * 2 * Da * 4);
+    store(gm(*this, dt1, N, cc.phi, tdim, ET_F32), cc.c1, Da, ET_F32, dt1_b, ACT_SILU, s);
+    store(gm(*this, dt2, N, cc.c1, Da, ET_F32), cc.c, Da, ET_F32, dt2_b, ACT_NONE, s);
+    launch_silu_f32(cc.c, cc.sc, (long)N * Da, s);
+    store(gm(*this, mod_all, N, cc.sc, Da, ET_F32), cc.mods, NL * 6 * Da, ET_F32, mod_b, ACT_NONE, s);
+    store(gm(*this, modf, N, cc.sc, Da, ET_F32), cc.modf, 2 * Da, ET_F32, modf_b, ACT_NONE, s);
+  }
+  VLA_HIP(hipGetLastError());
+  VLA_HIP(hipStreamSynchronize(s));
+  return cond.emplace(N, cc).first->second;
+}
+
+void vla_model_s::enqueue_denoise(int B, const void* kv, const float* noise, int N, float* x, const CondCache& cc,
+                                  hipStream_t s) {
+  const vla_config& c = cfg;
+  const size_t es = elem_size(et);
+  const float eps = c.norm_eps;
+  const float dt = -1.0f / (float)N;
+  launch_copy_f32(noise, x, (long)B * H * A, s);
+
+  if (c.head_kind == VLA_HEAD_JOINT) {
+    const int M = B * H, nq = c.n_q, nkv = c.n_kv, Fa = c.act_mlp;
+    const size_t per = (size_t)B * nkv * P * hd * es;
+    for (int k = 0; k < N; ++k) {
+      store(gm(*this, ain, M, x, A, ET_F32), e, Da, et, ain_b, ACT_NONE, s);
+      store(gm(*this, t1a, M, e, Da, et), u, Da, et, cc.tb + (size_t)k * Da, ACT_SILU, s);
+      store(gm(*this, t2, M, u, Da, et), ha, Da, ET_F32, t2_b, ACT_NONE, s);
+      for (int l = 0; l < c.act_layers; ++l) {
+        const LlmLayer& y = act[l];
+        norm(M, Da, 0, ha, Da, za, Da, et, y.ln1, nullptr, eps, s);
+        GemmArgs q3 = gm(*this, y.qkv, M, za, Da, et);
+        q3.mode = EPI_QKV; q3.out_type = et;
+        QkvEpi& e3 = q3.qkv;
+        e3.n_q = nq; e3.n_kv = nkv; e3.hd = hd; e3.seq = H; e3.pos0 = P; e3.rope_cs = rope_cs;
+        e3.q = qa; e3.q_sb = (long)nq * H * hd; e3.q_sh = (long)H * hd; e3.q_si = hd;
+        e3.k = ks; e3.k_sb = (long)nkv * H * hd; e3.k_sh = (long)H * hd; e3.k_si = hd;
+        e3.v = vs; e3.v_sb = e3.k_sb; e3.v_sh = e3.k_sh; e3.v_si = hd;
+        launch_gemm(q3, s);
+        AttnArgs at = attn(B, nq, nkv, H, hd, et);
+        at.q = qa; at.q_sb = e3.q_sb; at.q_sh = e3.q_sh; at.q_si = hd;
+        const char* kl = (const char*)kv + (size_t)(2 * l) * per;
+        const char* vl = (const char*)kv + (size_t)(2 * l + 1) * per;
+        at.seg[0] = AttnSeg{kl, (long)nkv * P * hd, (long)P * hd, hd, vl, (long)nkv * P * hd, (long)P * hd, hd, P};
+        at.seg[1] = AttnSeg{ks, e3.k_sb, e3.k_sh, hd, vs, e3.v_sb, e3.v_sh, hd, H};
+        at.o = oa; at.o_sb = (long)H * Hq; at.o_sh = hd; at.o_si = Hq;
+        launch_attention(at, s);
+        resid(gm(*this, y.wo, M, oa, Hq, et), ha, Da, nullptr, nullptr, s);
+        norm(M, Da, 0, ha, Da, za, Da, et, y.ln2, nullptr, eps, s);
+        GemmArgs gg = gm(*this, y.gu, M, za, Da, et);
+        gg.mode = EPI_GEGLU; gg.out = gua; gg.ldo = Fa; gg.out_type = et;
+        launch_gemm(gg, s);
+        resid(gm(*this, y.wd, M, gua, Fa, et), ha, Da, nullptr, nullptr, s);
+      }
+      norm(M, Da, 0, ha, Da, za, Da, et, lnf, nullptr, eps, s);
+      GemmArgs go = gm(*this, out, M, za, Da, et);
+      go.mode = EPI_EULER; go.out = x; go.ldo = A; go.out_type = ET_F32; go.bias = out_b; go.dt = dt;
+      launch_gemm(go, s);
+    }
+    return;
+  }
+
+  // ---- DiT head
+  const int NL = c.act_layers, nh = c.act_heads, S = Ltok, M = B * S, Fa = c.act_mlp;
+  const char* xkv_base = (const char*)kv;
+  const void* st_tok = (const char*)kv + (size_t)B * P * NL * 2 * Da * es;
+  const long kv_row = (long)NL * 2 * Da;
+  for (int k = 0; k < N; ++k) {
+    const float* mk = cc.mods + (size_t)k * NL * 6 * Da;
+    launch_dit_state_rows(st_tok, et, B, Da, S, dpos, X, s);
+    GemmArgs ga = gm(*this, dain, B * H, x, A, ET_F32);
+    ga.tab = dpos + Da; ga.tab_period = H; ga.ldtab = Da;
+    ga.row_group = H; ga.row_group_stride = (long)S * Da;
+    store(ga, X + Da, Da, ET_F32, dain_b, ACT_NONE, s);
+    for (int l = 0; l < NL; ++l) {
+      const DitLayer& y = dit[l];
+      const float* m6 = mk + (size_t)l * 6 * Da;
+      norm(M, Da, 2, X, Da, zd, Da, et, m6 + 1 * Da, m6 + 0 * Da, eps, s);
+      GemmArgs q3 = gm(*this, y.qkv, M, zd, Da, et);
+      q3.mode = EPI_QKV; q3.out_type = et; q3.bias = y.bqkv;
+      QkvEpi& e3 = q3.qkv;
+      e3.n_q = nh; e3.n_kv = nh; e3.hd = dhd; e3.seq = S; e3.pos0 = -1;
+      e3.q = qd; e3.q_sb = (long)nh * S * dhd; e3.q_sh = (long)S * dhd; e3.q_si = dhd;
+      e3.k = kd; e3.k_sb = e3.q_sb; e3.k_sh = e3.q_sh; e3.k_si = dhd;
+      e3.v = vd; e3.v_sb = e3.q_sb; e3.v_sh = e3.q_sh; e3.v_si = dhd;
+      launch_gemm(q3, s);
+      AttnArgs at = attn(B, nh, nh, S, dhd, et);
+      at.q = qd; at.q_sb = e3.q_sb; at.q_sh = e3.q_sh; at.q_si = dhd;
+      at.seg[0] = AttnSeg{kd, e3.k_sb, e3.k_sh, dhd, vd, e3.v_sb, e3.v_sh, dhd, S};
+      at.seg[1].len = 0;
+      at.o = od; at.o_sb = (long)S * Da; at.o_sh = dhd; at.o_si = Da;
+      launch_attention(at, s);
+      resid(gm(*this, y.wo, M, od, Da, et), X, Da, y.bo, m6 + 2 * Da, s);
+      // cross-attention to the VLM features of the paired layer
+      norm(M, Da, 1, X, Da, zd, Da, et, nullptr, nullptr, eps, s);
+      store(gm(*this, y.cq, M, zd, Da, et), qc, Da, et, y.bcq, ACT_NONE, s);
+      AttnArgs ac = attn(B, nh, nh, S, dhd, et);
+      ac.q = qc; ac.q_sb = (long)S * Da; ac.q_sh = dhd; ac.q_si = Da;
+      const char* kl = xkv_base + (size_t)(2 * l) * Da * es;
+      const char* vl = xkv_base + (size_t)(2 * l + 1) * Da * es;
+      ac.seg[0] = AttnSeg{kl, (long)P * kv_row, dhd, kv_row, vl, (long)P * kv_row, dhd, kv_row, P};
+      ac.seg[1].len = 0;
+      ac.o = od; ac.o_sb = (long)S * Da; ac.o_sh = dhd; ac.o_si = Da;
+      launch_attention(ac, s);
+      resid(gm(*this, y.co, M, od, Da, et), X, Da, y.bco, nullptr, s);
+      norm(M, Da, 2, X, Da, zd, Da, et, m6 + 4 * Da, m6 + 3 * Da, eps, s);
+      store(gm(*this, y.w1, M, zd, Da, et), mlp, Fa, et, y.b1, ACT_GELU, s);
+      resid(gm(*this, y.w2, M, mlp, Fa, et), X, Da, y.b2, m6 + 5 * Da, s);
+    }
+    const float* mf = cc.modf + (size_t)k * 2 * Da;
+    norm(B * H, Da, 2, X, Da, zf, Da, et, mf + Da, mf, eps, s, /*skip=*/1, /*skip_group=*/H);
+    GemmArgs go = gm(*this, dout, B * H, zf, Da, et);
+    go.mode = EPI_EULER; go.out = x; go.ldo = A; go.out_type = ET_F32; go.bias = dout_b; go.dt = dt;
+    launch_gemm(go, s);
+  }
+}
+
+// ---------------------------------------------------------------- graphs
+void vla_model_s::run_graph(int stage, const GraphKey& key, hipStream_t s,
+                            const std::function<void(hipStream_t)>& body) {
+  if (!graphs) {
+    body(s);
+    VLA_HIP(hipGetLastError());
+    return;
+  }
+  std::lock_guard<std::mutex> lk(graph_mu[stage]);
+  auto& cache = graph_cache[stage];
+  auto& lru = graph_lru[stage];
+  auto it = cache.find(key);
+  if (it == cache.end()) {
+    hipStream_t cs = cap_stream[stage];
+    hipGraph_t graph = nullptr;
+    VLA_HIP(hipStreamBeginCapture(cs, hipStreamCaptureModeThreadLocal));
+    try {
+      body(cs);
+    } catch (...) {
+      (void)hipStreamEndCapture(cs, &graph);
+      if (graph) (void)hipGraphDestroy(graph);
+      throw;
+    }
+    VLA_HIP(hipStreamEndCapture(cs, &graph));
+    hipGraphExec_t exec = nullptr;
+    hipError_t e = hipGraphInstantiate(&exec, graph, nullptr, nullptr, 0);
+    (void)hipGraphDestroy(graph);
+    VLA_HIP(e);
+    if (cache.size() >= kMaxGraphs && !lru.empty()) {
+      auto old = cache.find(lru.back());
+      if (old != cache.end()) {
+        VLA_HIP(hipDeviceSynchronize());    // the evicted graph may still be queued
+        (void)hipGraphExecDestroy(old->second);
+        cache.erase(old);
+      }
+      lru.pop_back();
+    }
+    it = cache.emplace(key, exec).first;
+    lru.push_front(key);
+  } else {
+    lru.remove(key);
+    lru.push_front(key);
+  }
+  VLA_HIP(hipGraphLaunch(it->second, s));
+}
+
+void vla_model_s::prefill(int B, const float* pix, const int32_t* ids, const float* state, void* kv, hipStream_t s) {
+  GraphKey key{B, 0, pix, ids, state, kv};
+  run_graph(STAGE_PREFILL, key, s, [&](hipStream_t cs) { enqueue_prefill(B, pix, ids, state, kv, cs); });
+}
+
+void vla_model_s::denoise(int B, const void* kv, const float* noise, int N, float* act, hipStream_t s) {
+  const CondCache& cc = cond_for(N, s);
+  GraphKey key{B, N, kv, noise, act, nullptr};
+  run_graph(STAGE_DENOISE, key, s, [&](hipStream_t cs) { enqueue_denoise(B, kv, noise, N, act, cc, cs); });
+}

@@ -1,0 +1,209 @@
+"""ctypes binding of libvla.so (argument marshalling only).
+
+Names follow the C ABI in include/vla.h. Device buffers are torch tensors
+(PyTorch provides device memory and streams); every step of the computation
+runs in the library's HIP kernels. The library must have been built
+(``python -m paper_2609_12075_amd.build``); loading raises otherwise — there
+is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import numpy as np
+
+from . import synth
+
+_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libvla.so")
+_lib = None
+
+VLA_OK, VLA_EINVAL, VLA_ENOMEM, VLA_EHIP, VLA_EUNSUPPORTED = range(5)
+
+# every exported symbol declared by include/vla.h and include/vla_debug.h
+EXPORTS = ["vla_weight_count", "vla_create_model", "vla_destroy_model", "vla_set_graphs", "vla_kv_bytes",
+           "vla_prefill", "vla_prefill_ex", "vla_denoise", "vla_step", "vla_last_error",
+           "vla_debug_gemm", "vla_debug_attention", "vla_debug_cu_probe"]
+
+
+class VlaError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"vla status {status}: {msg}")
+        self.status = status
+
+
+class VlaConfigC(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int) for n in (
+        "dtype", "n_img", "img_hw", "patch", "vit_layers", "vit_d", "vit_heads", "vit_mlp", "n_text", "vocab",
+        "llm_layers", "llm_d", "n_q", "n_kv", "head_dim", "llm_mlp", "head_kind", "act_layers", "act_d",
+        "act_heads", "act_mlp", "horizon", "action_dim", "state_dim", "time_dim", "max_batch")] + [
+        ("rope_base", ctypes.c_float), ("norm_eps", ctypes.c_float)]
+
+
+class StepArgsC(ctypes.Structure):
+    _fields_ = [("vlm_model", ctypes.c_void_p), ("vlm_batch", ctypes.c_int),
+                ("pixels", ctypes.c_void_p), ("text_ids", ctypes.c_void_p), ("state", ctypes.c_void_p),
+                ("kv_out", ctypes.c_void_p),
+                ("adit_model", ctypes.c_void_p), ("adit_batch", ctypes.c_int),
+                ("kv_in", ctypes.c_void_p), ("noise", ctypes.c_void_p), ("steps", ctypes.c_int),
+                ("actions_out", ctypes.c_void_p),
+                ("vlm_cu_count", ctypes.c_int), ("adit_cu_count", ctypes.c_int)]
+
+
+def lib():
+    """Load libvla.so (once). Raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB_PATH):
+            raise RuntimeError(f"{_LIB_PATH} not built: run `python -m paper_2609_12075_amd.build`")
+        L = ctypes.CDLL(_LIB_PATH)
+        vp, ci, sz = ctypes.c_void_p, ctypes.c_int, ctypes.c_size_t
+        L.vla_weight_count.argtypes = [ctypes.POINTER(VlaConfigC)]; L.vla_weight_count.restype = sz
+        L.vla_create_model.argtypes = [ctypes.POINTER(VlaConfigC), vp, sz, ci, ctypes.POINTER(vp)]
+        L.vla_create_model.restype = ci
+        L.vla_destroy_model.argtypes = [vp]; L.vla_destroy_model.restype = None
+        L.vla_set_graphs.argtypes = [vp, ci]; L.vla_set_graphs.restype = ci
+        L.vla_kv_bytes.argtypes = [vp, ci]; L.vla_kv_bytes.restype = sz
+        L.vla_prefill.argtypes = [vp, ci, vp, vp, vp, vp]; L.vla_prefill.restype = ci
+        L.vla_prefill_ex.argtypes = [vp, ci, vp, vp, vp, vp, vp]; L.vla_prefill_ex.restype = ci
+        L.vla_denoise.argtypes = [vp, ci, vp, vp, ci, vp, vp]; L.vla_denoise.restype = ci
+        L.vla_step.argtypes = [ctypes.POINTER(StepArgsC), vp]; L.vla_step.restype = ci
+        L.vla_last_error.argtypes = []; L.vla_last_error.restype = ctypes.c_char_p
+        L.vla_debug_gemm.argtypes = [ci, ci, ci, vp, ci, ci, vp, ci, ci, vp, ci, vp, ci, vp]
+        L.vla_debug_gemm.restype = ci
+        L.vla_debug_attention.argtypes = [ci, ci, ci, ci, ci, ci, vp, vp, vp, ci, vp, vp, ci, vp, vp]
+        L.vla_debug_attention.restype = ci
+        L.vla_debug_cu_probe.argtypes = [ci, ci, ci, ci, ci, vp, vp]; L.vla_debug_cu_probe.restype = ci
+        _lib = L
+    return _lib
+
+
+def _check(status: int):
+    if status != VLA_OK:
+        raise VlaError(status, lib().vla_last_error().decode())
+
+
+def config_struct(c: synth.VLAConfig) -> VlaConfigC:
+    s = VlaConfigC()
+    for name, _ in VlaConfigC._fields_:
+        setattr(s, name, getattr(c, name))
+    return s
+
+
+def weight_count(c: synth.VLAConfig) -> int:
+    s = config_struct(c)
+    n = lib().vla_weight_count(ctypes.byref(s))
+    if n == 0:
+        raise VlaError(VLA_EINVAL, lib().vla_last_error().decode())
+    return int(n)
+
+
+def _ptr(t) -> Optional[int]:
+    if t is None:
+        return None
+    import torch
+    assert isinstance(t, torch.Tensor) and t.is_cuda and t.is_contiguous(), "device tensors must be contiguous"
+    return t.data_ptr()
+
+
+def _stream(stream) -> Optional[int]:
+    import torch
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+
+
+class Model:
+    """A model resident on one GPU (libvla's vla_model)."""
+
+    def __init__(self, cfg: synth.VLAConfig, weights: np.ndarray, device: int = 0):
+        self.cfg = cfg
+        w = np.ascontiguousarray(weights, dtype=np.float32)
+        s = config_struct(cfg)
+        h = ctypes.c_void_p()
+        _check(lib().vla_create_model(ctypes.byref(s), w.ctypes.data, w.size, device, ctypes.byref(h)))
+        self.handle = h
+        self.device = device
+
+    def close(self):
+        if getattr(self, "handle", None):
+            lib().vla_destroy_model(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def set_graphs(self, enabled: bool):
+        _check(lib().vla_set_graphs(self.handle, int(bool(enabled))))
+
+    def kv_bytes(self, batch: int) -> int:
+        n = lib().vla_kv_bytes(self.handle, batch)
+        if n == 0:
+            raise VlaError(VLA_EINVAL, lib().vla_last_error().decode())
+        return int(n)
+
+    def alloc_kv(self, batch: int):
+        import torch
+        return torch.empty(self.kv_bytes(batch), dtype=torch.uint8, device=f"cuda:{self.device}")
+
+    def prefill(self, batch, pixels, text_ids, kv_out, state=None, stream=None):
+        _check(lib().vla_prefill_ex(self.handle, batch, _ptr(pixels), _ptr(text_ids), _ptr(state), _ptr(kv_out),
+                                    _stream(stream)))
+
+    def denoise(self, batch, kv, noise, steps, actions_out, stream=None):
+        _check(lib().vla_denoise(self.handle, batch, _ptr(kv), _ptr(noise), steps, _ptr(actions_out),
+                                 _stream(stream)))
+
+
+def step(vlm_model: Optional[Model], vlm_batch: int, pixels, text_ids, kv_out,
+         adit_model: Optional[Model], adit_batch: int, kv_in, noise, steps: int, actions_out,
+         vlm_cu_count: int = 256, adit_cu_count: int = 0, state=None, join_stream=None):
+    """One lockstep: prefill(vlm_batch) on the CU-restricted stream alongside
+    denoise(adit_batch) on the action stream; join_stream waits for both."""
+    a = StepArgsC()
+    a.vlm_model = vlm_model.handle if vlm_model is not None else None
+    a.vlm_batch = vlm_batch
+    a.pixels, a.text_ids, a.state, a.kv_out = _ptr(pixels), _ptr(text_ids), _ptr(state), _ptr(kv_out)
+    a.adit_model = adit_model.handle if adit_model is not None else None
+    a.adit_batch = adit_batch
+    a.kv_in, a.noise, a.steps, a.actions_out = _ptr(kv_in), _ptr(noise), steps, _ptr(actions_out)
+    a.vlm_cu_count, a.adit_cu_count = vlm_cu_count, adit_cu_count
+    _check(lib().vla_step(ctypes.byref(a), _stream(join_stream)))
+
+
+# ---------------------------------------------------------------- test hooks
+def debug_gemm(A, Wt, bias=None, act=0, out=None, M=None, N=None, K=None, stream=None):
+    import torch
+    M = A.shape[0] if M is None else M
+    N = Wt.shape[0] if N is None else N
+    K = A.shape[1] if K is None else K
+    if out is None:
+        out = torch.empty(M, N, dtype=torch.float32, device=A.device)
+    at = 1 if A.dtype == torch.bfloat16 else 0
+    wt = 1 if Wt.dtype == torch.bfloat16 else 0
+    _check(lib().vla_debug_gemm(M, N, K, _ptr(A), A.shape[1], at, _ptr(Wt), Wt.shape[1], wt, _ptr(bias), act,
+                                _ptr(out), out.shape[1], _stream(stream)))
+    return out
+
+
+def debug_attention(q, k0, v0, k1=None, v1=None, stream=None):
+    import torch
+    B, Hq, Lq, hd = q.shape
+    Hkv, len0 = k0.shape[1], k0.shape[2]
+    len1 = 0 if k1 is None else k1.shape[2]
+    o = torch.empty(B, Lq, Hq * hd, dtype=q.dtype, device=q.device)
+    et = 1 if q.dtype == torch.bfloat16 else 0
+    _check(lib().vla_debug_attention(B, Hq, Hkv, Lq, hd, et, _ptr(q), _ptr(k0), _ptr(v0), len0, _ptr(k1), _ptr(v1),
+                                     len1, _ptr(o), _stream(stream)))
+    return o
+
+
+def debug_cu_probe(cu_count: int, blocks: int, spin: int = 200, from_top: bool = False, device: int = 0, stream=None):
+    import torch
+    out = torch.zeros(2 * blocks, dtype=torch.int32, device=f"cuda:{device}")
+    _check(lib().vla_debug_cu_probe(device, cu_count, int(from_top), blocks, spin, _ptr(out), _stream(stream)))
+    return out

@@ -1,0 +1,73 @@
+"""Host-only checks of the C ABI: the library loads, exports every symbol the
+headers declare, and rejects bad shapes before touching a GPU."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2609_12075_amd import synth, vla
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared_functions():
+    names = set()
+    for h in ("vla.h", "vla_debug.h", "vla_sched.h"):
+        p = os.path.join(ROOT, "include", h)
+        if not os.path.exists(p):
+            continue
+        src = open(p).read()
+        src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+        for m in re.finditer(r"\b(vla_\w+)\s*\(", src):
+            names.add(m.group(1))
+    return names
+
+
+def test_library_exports_every_declared_symbol():
+    L = vla.lib()
+    declared = declared_functions()
+    assert "vla_prefill" in declared and "vla_step" in declared
+    for name in sorted(declared):
+        assert hasattr(L, name), f"{name} declared in include/ but not exported"
+    for name in vla.EXPORTS:
+        assert name in declared
+
+
+def test_weight_count_matches_schema():
+    for cfg in list(synth.CONFIGS.values()) + [synth.reduced(c) for c in synth.CONFIGS.values()]:
+        assert vla.weight_count(cfg) == synth.weight_count(cfg), cfg.name
+
+
+@pytest.mark.parametrize("field,value,msg", [
+    ("n_q", 7, "multiple of n_kv"),
+    ("head_dim", 60, "head_dim"),
+    ("img_hw", 65, "multiple of patch"),
+    ("act_layers", 3, "act_layers"),
+    ("max_batch", 0, "max_batch"),
+])
+def test_invalid_shapes_rejected(field, value, msg):
+    cfg = synth.CONFIGS["smolvla"].with_(**{field: value})
+    with pytest.raises(vla.VlaError) as e:
+        vla.weight_count(cfg)
+    assert msg in str(e.value)
+
+
+def test_create_rejects_wrong_buffer_size_without_gpu():
+    cfg = synth.CONFIGS["tiny"]
+    s = vla.config_struct(cfg)
+    h = ctypes.c_void_p()
+    buf = (ctypes.c_float * 16)()
+    st = vla.lib().vla_create_model(ctypes.byref(s), buf, 16, 0, ctypes.byref(h))
+    assert st == vla.VLA_EINVAL
+    assert "shape needs" in vla.lib().vla_last_error().decode()
+    assert not h.value
+
+
+def test_null_arguments_rejected():
+    L = vla.lib()
+    assert L.vla_prefill(None, 1, None, None, None, None) == vla.VLA_EINVAL
+    assert L.vla_denoise(None, 1, None, None, 4, None, None) == vla.VLA_EINVAL
+    assert L.vla_kv_bytes(None, 1) == 0
+    assert L.vla_step(None, None) == vla.VLA_EINVAL
+    assert "null" in L.vla_last_error().decode()

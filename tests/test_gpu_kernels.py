@@ -1,0 +1,160 @@
+"""Per-kernel parity on the GPU (through the C ABI's test hooks): the
+projection kernel and the prefix-KV attention kernel against numpy fp64 on
+the same (bf16-representable) inputs, at the shapes of the VLA stages plus
+ragged edges; and the placement of work on CU-masked streams."""
+import numpy as np
+import pytest
+
+from oracle import vla as O
+from tests.gpu_util import log
+
+pytestmark = pytest.mark.gpu
+
+RNG = np.random.default_rng(2024)
+
+
+def _bf16(a):
+    return O.bf16_round(np.asarray(a, np.float32))
+
+
+GEMM_SHAPES = [
+    # (M, N, K): stage shapes and ragged edges
+    (1, 16, 8), (17, 32, 592), (50, 720, 720), (130, 200, 64), (300, 1000, 264), (4, 6144, 1024),
+    (800, 3840, 720), (3840, 960, 960), (240, 1600, 960), (37, 33, 40),
+]
+
+
+@pytest.mark.parametrize("M,N,K", GEMM_SHAPES)
+@pytest.mark.parametrize("a_fp32", [False, True])
+def test_gemm_bf16(M, N, K, a_fp32):
+    import torch
+    from paper_2609_12075_amd import vla
+    log(f"[gemm bf16] M={M} N={N} K={K} a_fp32={a_fp32}")
+    A = RNG.standard_normal((M, K)).astype(np.float32)
+    W = _bf16(RNG.standard_normal((N, K)) * 0.05)
+    bias = RNG.standard_normal(N).astype(np.float32)
+    Ab = _bf16(A)
+    ref = Ab.astype(np.float64) @ W.astype(np.float64).T + bias
+    At = torch.from_numpy(A).cuda() if a_fp32 else torch.from_numpy(Ab).to(torch.bfloat16).cuda()
+    Wt = torch.from_numpy(W).to(torch.bfloat16).cuda()
+    out = vla.debug_gemm(At, Wt, bias=torch.from_numpy(bias).cuda())
+    torch.cuda.synchronize()
+    got = out.cpu().numpy()
+    scale = np.sqrt(K) * 0.05 * 1.0 + 1.0
+    np.testing.assert_allclose(got, ref, rtol=1e-4, atol=1e-5 * scale)
+
+
+@pytest.mark.parametrize("act", [1, 2])
+def test_gemm_activations(act):
+    import torch
+    from paper_2609_12075_amd import vla
+    M, N, K = 70, 96, 128
+    A = _bf16(RNG.standard_normal((M, K)))
+    W = _bf16(RNG.standard_normal((N, K)) * 0.2)
+    ref = A.astype(np.float64) @ W.astype(np.float64).T
+    ref = O.silu(ref) if act == 1 else O.gelu_tanh(ref)
+    out = vla.debug_gemm(torch.from_numpy(A).to(torch.bfloat16).cuda(), torch.from_numpy(W).to(torch.bfloat16).cuda(),
+                         act=act)
+    torch.cuda.synchronize()
+    np.testing.assert_allclose(out.cpu().numpy(), ref, rtol=2e-4, atol=2e-5)
+
+
+@pytest.mark.parametrize("M,N,K", [(8, 7, 128), (80, 768, 256), (5, 128, 7), (65, 130, 1024)])
+def test_gemm_f32(M, N, K):
+    import torch
+    from paper_2609_12075_amd import vla
+    A = RNG.standard_normal((M, K)).astype(np.float32)
+    W = RNG.standard_normal((N, K)).astype(np.float32)
+    ref = A.astype(np.float64) @ W.astype(np.float64).T
+    out = vla.debug_gemm(torch.from_numpy(A).cuda(), torch.from_numpy(W).cuda())
+    torch.cuda.synchronize()
+    np.testing.assert_allclose(out.cpu().numpy(), ref, rtol=1e-5, atol=1e-5 * np.sqrt(K))
+
+
+ATTN_SHAPES = [
+    # (B, Hq, Hkv, Lq, hd, len0, len1)
+    (2, 8, 1, 50, 256, 816, 50),     # pi0-shaped action decode
+    (1, 8, 1, 100, 256, 100, 0),     # pi0-shaped prefill (short prefix)
+    (1, 15, 5, 240, 64, 240, 0),     # SmolVLA-shaped prefill
+    (2, 15, 5, 50, 64, 240, 50),     # SmolVLA-shaped action decode
+    (3, 16, 16, 256, 72, 256, 0),    # ViT per image, head dim 72
+    (2, 32, 32, 17, 32, 17, 0),      # DiT self-attention
+    (2, 32, 32, 17, 32, 296, 0),     # DiT cross-attention
+    (1, 4, 2, 7, 64, 5, 3),          # ragged, tiny
+    (1, 2, 1, 1, 8, 1, 0),           # single key
+]
+
+
+def _attn_ref(q, k0, v0, k1, v1):
+    B, Hq, Lq, hd = q.shape
+    out = np.zeros((B, Lq, Hq * hd))
+    for b in range(B):
+        k = k0[b] if k1 is None else np.concatenate([k0[b], k1[b]], axis=1)
+        v = v0[b] if v1 is None else np.concatenate([v0[b], v1[b]], axis=1)
+        out[b] = O.merge(O.attention(q[b].astype(np.float64), k.astype(np.float64), v.astype(np.float64)))
+    return out
+
+
+@pytest.mark.parametrize("B,Hq,Hkv,Lq,hd,len0,len1", ATTN_SHAPES)
+def test_attention_bf16(B, Hq, Hkv, Lq, hd, len0, len1):
+    import torch
+    from paper_2609_12075_amd import vla
+    log(f"[attn bf16] B={B} Hq={Hq} Hkv={Hkv} Lq={Lq} hd={hd} len0={len0} len1={len1}")
+    q = _bf16(RNG.standard_normal((B, Hq, Lq, hd)))
+    k0 = _bf16(RNG.standard_normal((B, Hkv, len0, hd)))
+    v0 = _bf16(RNG.standard_normal((B, Hkv, len0, hd)))
+    k1 = _bf16(RNG.standard_normal((B, Hkv, len1, hd))) if len1 else None
+    v1 = _bf16(RNG.standard_normal((B, Hkv, len1, hd))) if len1 else None
+    ref = _attn_ref(q, k0, v0, k1, v1)
+    t = lambda a: None if a is None else torch.from_numpy(a).to(torch.bfloat16).cuda()
+    o = vla.debug_attention(t(q), t(k0), t(v0), t(k1), t(v1))
+    torch.cuda.synchronize()
+    got = o.float().cpu().numpy()
+    # bf16 output and bf16 probabilities: ~2^-8 relative per element
+    rel = np.linalg.norm(got - ref) / np.linalg.norm(ref)
+    assert rel < 1e-2, rel
+    assert np.abs(got - ref).max() < 0.05 * np.abs(ref).max() + 1e-3
+
+
+@pytest.mark.parametrize("B,Hq,Hkv,Lq,hd,len0,len1", [(1, 4, 4, 8, 64, 80, 8), (2, 4, 2, 80, 64, 80, 0), (1, 2, 1, 3, 136, 70, 2)])
+def test_attention_f32(B, Hq, Hkv, Lq, hd, len0, len1):
+    import torch
+    from paper_2609_12075_amd import vla
+    q = RNG.standard_normal((B, Hq, Lq, hd)).astype(np.float32)
+    k0 = RNG.standard_normal((B, Hkv, len0, hd)).astype(np.float32)
+    v0 = RNG.standard_normal((B, Hkv, len0, hd)).astype(np.float32)
+    k1 = RNG.standard_normal((B, Hkv, len1, hd)).astype(np.float32) if len1 else None
+    v1 = RNG.standard_normal((B, Hkv, len1, hd)).astype(np.float32) if len1 else None
+    ref = _attn_ref(q, k0, v0, k1, v1)
+    t = lambda a: None if a is None else torch.from_numpy(a).cuda()
+    o = vla.debug_attention(t(q), t(k0), t(v0), t(k1), t(v1))
+    torch.cuda.synchronize()
+    np.testing.assert_allclose(o.cpu().numpy(), ref, rtol=1e-4, atol=1e-5)
+
+
+def _placements(words):
+    w = words.cpu().numpy().astype(np.uint32).reshape(-1, 2)
+    hw, xcc = w[:, 0], w[:, 1] & 0xF
+    cu, sh, se = (hw >> 8) & 0xF, (hw >> 12) & 0x1, (hw >> 13) & 0x7
+    return set(zip(xcc.tolist(), se.tolist(), sh.tolist(), cu.tolist()))
+
+
+def test_cu_masked_streams_confine_work():
+    import torch
+    from paper_2609_12075_amd import vla
+    full = _placements(vla.debug_cu_probe(256, 4096, spin=50))
+    torch.cuda.synchronize()
+    log(f"[cu probe] unrestricted: {len(full)} distinct CUs, XCCs {sorted({p[0] for p in full})}")
+    assert len(full) > 200
+    for k in (64, 128):
+        got = _placements(vla.debug_cu_probe(k, 4096, spin=50))
+        top = _placements(vla.debug_cu_probe(256 - k, 4096, spin=50, from_top=True))
+        torch.cuda.synchronize()
+        per_xcc = {}
+        for p in got:
+            per_xcc[p[0]] = per_xcc.get(p[0], 0) + 1
+        log(f"[cu probe] mask {k}: {len(got)} CUs, per XCC {per_xcc}; top {256 - k}: {len(top)} CUs, "
+            f"overlap {len(got & top)}")
+        assert len(got) <= k
+        assert len(top) <= 256 - k
+        assert not (got & top), "low and high masks must be disjoint"

@@ -1,0 +1,218 @@
+"""End-to-end parity of the HIP path (through the C ABI) against the CPU
+oracle on seeded inputs, plus the bit-exact bookkeeping properties:
+determinism, row permutation, batch-size invariance, prefix KV untouched by
+the action stage, graphs vs direct launches, and lockstep co-execution.
+
+Tolerances (final actions, rel-L2 over [B, H, A]): 1e-4 for the fp32 model,
+2e-2 for bf16 models."""
+import numpy as np
+import pytest
+
+from paper_2609_12075_amd import synth
+from tests.gpu_util import kv_arrays, log, model, oracle_run, rel_l2, run, to_dev
+
+pytestmark = pytest.mark.gpu
+
+TINY = synth.CONFIGS["tiny"]
+SMOL_R = synth.reduced(synth.CONFIGS["smolvla"], max_batch=4)
+PI0_R = synth.reduced(synth.CONFIGS["pi0"], vit_layers=2, max_batch=3)
+GR00T_R = synth.reduced(synth.CONFIGS["gr00t"], vit_layers=2, max_batch=3)
+
+TOL = {synth.DTYPE_F32: 1e-4, synth.DTYPE_BF16: 2e-2}
+
+
+def check_parity(cfg, B, steps=None, with_state=True):
+    inp = synth.make_inputs(cfg, B)
+    if not with_state and "state" in inp:
+        inp = {k: v for k, v in inp.items() if k != "state"}
+    act, kv = run(cfg, inp, steps=steps)
+    ref, pre = oracle_run(cfg, inp, steps=steps)
+    r = rel_l2(act, ref)
+    rd = rel_l2(act - inp["noise"], ref - inp["noise"])
+    log(f"[parity] {cfg.name} B={B}: actions rel-L2 {r:.3e}, displacement rel-L2 {rd:.3e}")
+    assert np.isfinite(act).all()
+    assert r <= TOL[cfg.dtype], r
+    # prefix hand-off
+    if cfg.head_kind == synth.HEAD_JOINT:
+        K = kv_arrays(cfg, kv, B)
+        for l in range(cfg.llm_layers):
+            rk = rel_l2(K[l, 0], np.stack([p["k"][l] for p in pre]))
+            rv = rel_l2(K[l, 1], np.stack([p["v"][l] for p in pre]))
+            assert rk <= TOL[cfg.dtype] and rv <= TOL[cfg.dtype], (l, rk, rv)
+    else:
+        xkv, st = kv_arrays(cfg, kv, B)
+        for l in range(cfg.act_layers):
+            rk = rel_l2(xkv[:, :, l, 0], np.stack([p["kc"][l] for p in pre]))
+            rv = rel_l2(xkv[:, :, l, 1], np.stack([p["vc"][l] for p in pre]))
+            assert rk <= TOL[cfg.dtype] and rv <= TOL[cfg.dtype], (l, rk, rv)
+        assert rel_l2(st, np.stack([p["state"] for p in pre])) <= TOL[cfg.dtype]
+    return act
+
+
+@pytest.mark.parametrize("B", [1, 3])
+def test_tiny_fp32(B):
+    check_parity(TINY, B)
+
+
+@pytest.mark.parametrize("B", [1, 3])
+def test_smolvla_reduced(B):
+    check_parity(SMOL_R, B)
+
+
+@pytest.mark.parametrize("B", [1, 2])
+def test_pi0_reduced(B):
+    check_parity(PI0_R, B)
+
+
+@pytest.mark.parametrize("B,with_state", [(1, True), (2, True), (2, False)])
+def test_gr00t_reduced(B, with_state):
+    check_parity(GR00T_R, B, with_state=with_state)
+
+
+def test_steps_one_and_max_batch():
+    check_parity(SMOL_R, SMOL_R.max_batch, steps=1)
+
+
+def test_smolvla_full_size_sampled_rows():
+    """Full SmolVLA-shaped model at its largest batch; the oracle evaluates two
+    rows (rows are independent, so a sample suffices)."""
+    cfg = synth.CONFIGS["smolvla"]
+    B = cfg.max_batch
+    inp = synth.make_inputs(cfg, B)
+    act, _ = run(cfg, inp)
+    rows = [0, B - 1]
+    ref, _ = oracle_run(cfg, inp, rows=rows)
+    r = rel_l2(act[rows], ref)
+    log(f"[parity] smolvla full B={B} rows {rows}: rel-L2 {r:.3e}")
+    assert r <= 2e-2
+
+
+# ---------------------------------------------------------------- bookkeeping (bit-exact)
+@pytest.mark.parametrize("cfg", [TINY, SMOL_R, GR00T_R], ids=lambda c: c.name)
+def test_determinism_permutation_and_batch_invariance(cfg):
+    B = 3
+    inp = synth.make_inputs(cfg, B)
+    a1, _ = run(cfg, inp)
+    a2, _ = run(cfg, inp)
+    np.testing.assert_array_equal(a1, a2)
+    perm = [2, 0, 1]
+    ap, _ = run(cfg, {k: v[perm] for k, v in inp.items()})
+    np.testing.assert_array_equal(ap, a1[perm])
+    one, _ = run(cfg, synth.make_inputs(cfg, 1, first_row=1))
+    np.testing.assert_array_equal(one[0], a1[1])
+
+
+@pytest.mark.parametrize("cfg", [TINY, SMOL_R], ids=lambda c: c.name)
+def test_graphs_match_direct_launches(cfg):
+    inp = synth.make_inputs(cfg, 2)
+    a_graph, kv_g = run(cfg, inp, graphs=True)
+    a_direct, kv_d = run(cfg, inp, graphs=False)
+    np.testing.assert_array_equal(a_graph, a_direct)
+    assert bool((kv_g == kv_d).all())
+    model(cfg).set_graphs(True)
+
+
+def test_graph_replays_stay_exact():
+    """Replaying the same captured graphs several times, with other work and
+    synchronisations in between, gives the eager result every time."""
+    import torch
+    cfg = SMOL_R
+    m = model(cfg)
+    inp = synth.make_inputs(cfg, 2)
+    ref, _ = run(cfg, inp, graphs=False)
+    m.set_graphs(True)
+    d = to_dev(inp)
+    kv = m.alloc_kv(2)
+    act = torch.empty_like(d["noise"])
+    for i in range(4):
+        m.prefill(2, d["pixels"], d["text_ids"], kv)
+        m.denoise(2, kv, d["noise"], cfg.steps, act)
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(act.cpu().numpy(), ref)
+        _ = (torch.ones(1000, device="cuda") * i).sum().item()
+
+
+def test_prefix_kv_untouched_by_action_stage():
+    import torch
+    cfg = SMOL_R
+    m = model(cfg)
+    d = to_dev(synth.make_inputs(cfg, 2))
+    kv = m.alloc_kv(2)
+    m.prefill(2, d["pixels"], d["text_ids"], kv)
+    torch.cuda.synchronize()
+    before = kv.clone()
+    act = torch.empty_like(d["noise"])
+    m.denoise(2, kv, d["noise"], cfg.steps, act)
+    torch.cuda.synchronize()
+    assert bool((kv == before).all())
+    # and the noise input is read-only
+    np.testing.assert_array_equal(d["noise"].cpu().numpy(), synth.make_noise(cfg, 2))
+
+
+@pytest.mark.parametrize("cu", [256, 128, 64])
+def test_lockstep_matches_separate_stages(cu):
+    """vla_step(prefill of batch k on a CU-restricted stream, denoise of batch
+    k-1 on the action stream) gives the same bits as running them alone."""
+    import torch
+    from paper_2609_12075_amd import vla
+    cfg = SMOL_R
+    m = model(cfg)
+    m.set_graphs(True)
+    prev = synth.make_inputs(cfg, 2, first_row=0)
+    cur = synth.make_inputs(cfg, 3, first_row=5)
+    ref_prev, _ = run(cfg, prev)
+    ref_cur, _ = run(cfg, cur)
+    dp, dc = to_dev(prev), to_dev(cur)
+    kv_prev, kv_cur = m.alloc_kv(2), m.alloc_kv(3)
+    m.prefill(2, dp["pixels"], dp["text_ids"], kv_prev)
+    act_prev = torch.empty_like(dp["noise"])
+    vla.step(m, 3, dc["pixels"], dc["text_ids"], kv_cur, m, 2, kv_prev, dp["noise"], cfg.steps, act_prev,
+             vlm_cu_count=cu)
+    act_cur = torch.empty_like(dc["noise"])
+    vla.step(None, 0, None, None, None, m, 3, kv_cur, dc["noise"], cfg.steps, act_cur, vlm_cu_count=cu)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(act_prev.cpu().numpy(), ref_prev)
+    np.testing.assert_array_equal(act_cur.cpu().numpy(), ref_cur)
+
+
+def test_two_models_colocated_lockstep():
+    """Two different models share the VLM and action streams (one lockstep
+    runs model A's prefill with model B's denoise)."""
+    import torch
+    from paper_2609_12075_amd import vla
+    a, b = TINY, SMOL_R
+    ma, mb = model(a), model(b)
+    ia, ib = synth.make_inputs(a, 1), synth.make_inputs(b, 2)
+    ref_a, _ = run(a, ia)
+    ref_b, _ = run(b, ib)
+    da, db = to_dev(ia), to_dev(ib)
+    kv_a, kv_b = ma.alloc_kv(1), mb.alloc_kv(2)
+    mb.prefill(2, db["pixels"], db["text_ids"], kv_b)
+    act_b = torch.empty_like(db["noise"])
+    vla.step(ma, 1, da["pixels"], da["text_ids"], kv_a, mb, 2, kv_b, db["noise"], b.steps, act_b, vlm_cu_count=192)
+    act_a = torch.empty_like(da["noise"])
+    vla.step(None, 0, None, None, None, ma, 1, kv_a, da["noise"], a.steps, act_a)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(act_a.cpu().numpy(), ref_a)
+    np.testing.assert_array_equal(act_b.cpu().numpy(), ref_b)
+
+
+def test_argument_errors_enqueue_nothing():
+    import torch
+    from paper_2609_12075_amd import vla
+    cfg = TINY
+    m = model(cfg)
+    d = to_dev(synth.make_inputs(cfg, 1))
+    kv = m.alloc_kv(1)
+    act = torch.empty_like(d["noise"])
+    with pytest.raises(vla.VlaError):
+        m.prefill(0, d["pixels"], d["text_ids"], kv)
+    with pytest.raises(vla.VlaError):
+        m.prefill(cfg.max_batch + 1, d["pixels"], d["text_ids"], kv)
+    with pytest.raises(vla.VlaError):
+        m.denoise(1, kv, d["noise"], 0, act)
+    with pytest.raises(vla.VlaError):
+        m.denoise(1, kv, d["noise"], 4, d["noise"])
+    with pytest.raises(vla.VlaError):
+        vla.step(m, 1, d["pixels"], d["text_ids"], kv, None, 0, None, None, 4, None, vlm_cu_count=100)
+    torch.cuda.synchronize()
