@@ -51,6 +51,18 @@ vla_status vla_debug_attention(int B, int Hq, int Hkv, int Lq, int hd, int et, c
 vla_status vla_debug_cu_probe(int device, int cu_count, int from_top, int blocks, int spin, uint32_t* out,
                               hipStream_t join);
 
+/*
+ * Enqueue `iters` launches of one projection of a model's stage, exactly as
+ * the stage launches it (same kernel, shape, epilogue, parameters and
+ * workspace buffers), on `stream`, and store the algorithmic flops of one
+ * launch (2 M N K) in *flops (may be NULL). For timing one kernel with events
+ * around the loop. It overwrites the stage's workspace: do not overlap it
+ * with that model's stages. which: 0 VLM LLM layer-0 MLP gate/up (GeGLU),
+ * 1 VLM LLM layer-0 MLP down, 2 action-stage layer-0 MLP up, 3 action-stage
+ * layer-0 MLP down, 4 ViT layer-0 MLP up.
+ */
+vla_status vla_debug_replay_gemm(vla_model m, int which, int batch, int iters, hipStream_t stream, double* flops);
+
 #ifdef __cplusplus
 }
 #endif

@@ -74,23 +74,60 @@ __global__ void __launch_bounds__(256) attn_mfma_kernel(AttnArgs a) {
   const float sl2 = a.scale * 1.4426950408889634f;   // scale * log2(e)
 
   const int len0 = a.seg[0].len, total = len0 + a.seg[1].len;
-  for (int k0 = 0; k0 < total; k0 += BKV) {
-    // ---- stage K (row-major) and V (transposed) tiles into LDS
-    for (int c = tid; c < BKV * CH; c += 256) {
+  // K/V tile chunks (8 elements) handled by this thread; with PREFETCH the
+  // next tile's chunks are loaded into registers while the current tile is
+  // consumed, hiding the global-load latency behind the matrix work.
+  constexpr int PER = BKV * CH / 256;
+  constexpr bool PREFETCH = HDP <= 128;
+  bf16x8 kreg[PER], vreg[PER];
+  auto load_regs = [&](int k0) {
+#pragma unroll
+    for (int j = 0; j < PER; ++j) {
+      const int c = tid + 256 * j;
       const int kr = c / CH, d8 = (c % CH) * 8;
       const int kg = k0 + kr;
-      bf16x8 kv = bf16x8{}, vv = bf16x8{};
+      kreg[j] = bf16x8{};
+      vreg[j] = bf16x8{};
       if (kg < total && d8 < hd) {
         const int which = kg < len0 ? 0 : 1;
         const int key = which ? kg - len0 : kg;
-        kv = *reinterpret_cast<const bf16x8*>(seg_row(a, which, b, g, key, false) + d8);
-        vv = *reinterpret_cast<const bf16x8*>(seg_row(a, which, b, g, key, true) + d8);
+        kreg[j] = *reinterpret_cast<const bf16x8*>(seg_row(a, which, b, g, key, false) + d8);
+        vreg[j] = *reinterpret_cast<const bf16x8*>(seg_row(a, which, b, g, key, true) + d8);
       }
-      *reinterpret_cast<bf16x8*>(&Ks[kr][d8]) = kv;
+    }
+  };
+  if constexpr (PREFETCH) load_regs(0);
+  for (int k0 = 0; k0 < total; k0 += BKV) {
+    // ---- stage K (row-major) and V (transposed) tiles into LDS
+    if constexpr (PREFETCH) {
 #pragma unroll
-      for (int e = 0; e < 8; ++e) Vt[d8 + e][kr] = vv[e];
+      for (int j = 0; j < PER; ++j) {
+        const int c = tid + 256 * j;
+        const int kr = c / CH, d8 = (c % CH) * 8;
+        *reinterpret_cast<bf16x8*>(&Ks[kr][d8]) = kreg[j];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) Vt[d8 + e][kr] = vreg[j][e];
+      }
+    } else {
+      for (int c = tid; c < BKV * CH; c += 256) {
+        const int kr = c / CH, d8 = (c % CH) * 8;
+        const int kg = k0 + kr;
+        bf16x8 kv = bf16x8{}, vv = bf16x8{};
+        if (kg < total && d8 < hd) {
+          const int which = kg < len0 ? 0 : 1;
+          const int key = which ? kg - len0 : kg;
+          kv = *reinterpret_cast<const bf16x8*>(seg_row(a, which, b, g, key, false) + d8);
+          vv = *reinterpret_cast<const bf16x8*>(seg_row(a, which, b, g, key, true) + d8);
+        }
+        *reinterpret_cast<bf16x8*>(&Ks[kr][d8]) = kv;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) Vt[d8 + e][kr] = vv[e];
+      }
     }
     __syncthreads();
+    if constexpr (PREFETCH) {
+      if (k0 + BKV < total) load_regs(k0 + BKV);
+    }
 
     // ---- S^T = K Q^T for 4 subtiles of 16 keys
     f32x4 s[4];

@@ -32,10 +32,11 @@ __device__ __forceinline__ void store_elem(void* base, long idx, int type, float
 }
 
 // Epilogue for output row m and the four columns n0..n0+3 (n0 % 4 == 0).
+template <int MODE>
 __device__ __forceinline__ void epilogue4(const GemmArgs& a, int m, int n0, float v[4]) {
   if (m >= a.M || n0 >= a.N) return;
   const int nv = min(4, a.N - n0);
-  switch (a.mode) {
+  switch (MODE) {
     case EPI_STORE: {
       long row = a.row_group > 0 ? (long)(m / a.row_group) * a.row_group_stride + (long)(m % a.row_group) * a.ldo
                                  : (long)m * a.ldo;
@@ -136,7 +137,7 @@ __device__ __forceinline__ void epilogue4(const GemmArgs& a, int m, int n0, floa
 // Block: 256 threads = 4 waves in a 2 x 2 grid over a BN (weight rows) x BM
 // (activation rows) tile; K advances in steps of 64 through a double-buffered
 // LDS tile whose rows are padded by 8 elements (conflict-free 16-byte reads).
-template <int BN, int BM, typename TA>
+template <int BN, int BM, typename TA, int MODE>
 __global__ void __launch_bounds__(256)
 gemm_mfma_kernel(GemmArgs a) {
   constexpr int BK = 64, LDK = BK + 8;
@@ -236,12 +237,13 @@ gemm_mfma_kernel(GemmArgs a) {
     const int mr = c / (BN / 4), nc = (c % (BN / 4)) * 4;
     f32x4 t = *reinterpret_cast<const f32x4*>(&Cs[mr][nc]);
     float v[4] = {t[0], t[1], t[2], t[3]};
-    epilogue4(a, m_blk + mr, n_blk + nc, v);
+    epilogue4<MODE>(a, m_blk + mr, n_blk + nc, v);
   }
 }
 
 // ---------------------------------------------------------------- fp32 VALU kernel
 // 64 x 64 tile, 256 threads, each thread 4 columns x 4 rows; K in steps of 16.
+template <int MODE>
 __global__ void __launch_bounds__(256) gemm_f32_kernel(GemmArgs a) {
   constexpr int BN = 64, BM = 64, BK = 16;
   __shared__ float Ws[BK][BN + 4];
@@ -274,28 +276,49 @@ __global__ void __launch_bounds__(256) gemm_f32_kernel(GemmArgs a) {
     __syncthreads();
   }
 #pragma unroll
-  for (int r = 0; r < 4; ++r) epilogue4(a, m_blk + tm + r, n_blk + tn, acc[r]);
+  for (int r = 0; r < 4; ++r) epilogue4<MODE>(a, m_blk + tm + r, n_blk + tn, acc[r]);
 }
 
 // ---------------------------------------------------------------- dispatch
-template <int BN, int BM>
+// Kernels are specialised on tile shape, activation type and epilogue; fp32
+// activations (the Euler state, conditioning vectors, robot state) only feed
+// plain stores.
+template <int BN, int BM, int MODE>
 static void launch_mfma(const GemmArgs& a, hipStream_t s) {
   dim3 grid((a.M + BM - 1) / BM, (a.N + BN - 1) / BN);
-  if (a.a_type == ET_BF16) hipLaunchKernelGGL((gemm_mfma_kernel<BN, BM, bf16>), grid, dim3(256), 0, s, a);
-  else hipLaunchKernelGGL((gemm_mfma_kernel<BN, BM, float>), grid, dim3(256), 0, s, a);
+  if constexpr (MODE == EPI_STORE) {
+    if (a.a_type == ET_F32) {
+      hipLaunchKernelGGL((gemm_mfma_kernel<BN, BM, float, MODE>), grid, dim3(256), 0, s, a);
+      return;
+    }
+  }
+  hipLaunchKernelGGL((gemm_mfma_kernel<BN, BM, bf16, MODE>), grid, dim3(256), 0, s, a);
 }
 
-void launch_gemm(const GemmArgs& a, hipStream_t s) {
-  if (a.M <= 0 || a.N <= 0) return;
+template <int MODE>
+static void launch_mode(const GemmArgs& a, hipStream_t s) {
   if (a.w_type == ET_F32) {
     dim3 grid((a.M + 63) / 64, (a.N + 63) / 64);
-    hipLaunchKernelGGL(gemm_f32_kernel, grid, dim3(256), 0, s, a);
+    hipLaunchKernelGGL(gemm_f32_kernel<MODE>, grid, dim3(256), 0, s, a);
     return;
   }
   // Pick the largest tile that still gives the chip (256 CUs) enough blocks.
   auto blocks = [&](int bn, int bm) { return (long)((a.M + bm - 1) / bm) * ((a.N + bn - 1) / bn); };
-  if (a.M >= 128 && blocks(128, 128) >= 256) launch_mfma<128, 128>(a, s);
-  else if (a.M >= 64 && blocks(128, 64) >= 256) launch_mfma<128, 64>(a, s);
-  else if (a.M > 32) launch_mfma<64, 64>(a, s);
-  else launch_mfma<64, 32>(a, s);
+  if (a.M >= 128 && blocks(128, 128) >= 256) launch_mfma<128, 128, MODE>(a, s);
+  else if (a.M >= 64 && blocks(128, 64) >= 256) launch_mfma<128, 64, MODE>(a, s);
+  else if (a.M > 32) launch_mfma<64, 64, MODE>(a, s);
+  else launch_mfma<64, 32, MODE>(a, s);
+}
+
+void launch_gemm(const GemmArgs& a, hipStream_t s) {
+  if (a.M <= 0 || a.N <= 0) return;
+  if (a.a_type == ET_F32 && a.w_type == ET_BF16 && a.mode != EPI_STORE)
+    throw VlaError{4, "fp32 activations with bf16 weights only feed plain stores"};
+  switch (a.mode) {
+    case EPI_STORE: launch_mode<EPI_STORE>(a, s); break;
+    case EPI_RESID: launch_mode<EPI_RESID>(a, s); break;
+    case EPI_GEGLU: launch_mode<EPI_GEGLU>(a, s); break;
+    case EPI_QKV: launch_mode<EPI_QKV>(a, s); break;
+    case EPI_EULER: launch_mode<EPI_EULER>(a, s); break;
+  }
 }

@@ -84,6 +84,7 @@ struct vla_model_s {
   std::map<int, CondCache> cond;
   std::mutex cond_mu;
 
+
   // ---- graphs
   bool graphs = true;
   hipStream_t cap_stream[2] = {nullptr, nullptr};
@@ -104,6 +105,8 @@ struct vla_model_s {
                        hipStream_t s);
   const CondCache& cond_for(int N, hipStream_t s);
   void run_graph(int stage, const GraphKey& key, hipStream_t s, const std::function<void(hipStream_t)>& body);
+  // One projection of a stage exactly as the stage launches it (for timing).
+  GemmArgs stage_gemm(int which, int B) const;
 };
 
 // Host-side validation of a shape; returns "" if valid, else the reason.

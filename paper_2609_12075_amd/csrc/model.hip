@@ -93,6 +93,9 @@ std::string vla_config_check(const vla_config& c) {
     if (c.head_kind == VLA_HEAD_DIT && c.state_dim % 8) return "bf16 DiT state_dim must be a multiple of 8";
   }
   if (!(c.norm_eps >= 0.f) || !(c.rope_base > 0.f)) return "bad norm_eps / rope_base";
+  // normalised widths: one wavefront holds a row in registers
+  for (int d : {c.llm_d, c.act_d, c.vit_layers > 0 ? c.vit_d : 4})
+    if (d % 4 || d > 2048) return "llm_d, act_d and vit_d must be multiples of 4 and <= 2048";
   return "";
 }
 
@@ -386,7 +389,9 @@ void vla_model_s::destroy() {
 // ---------------------------------------------------------------- GEMM helpers
 namespace {
 
-GemmArgs gm(const vla_model_s& m, const Mat& w, int M, const void* A, int lda, int a_type) {
+// A projection of stage `st` of the model.
+GemmArgs gm(const vla_model_s& m, int st, const Mat& w, int M, const void* A, int lda, int a_type) {
+  (void)st;
   GemmArgs g{};
   g.M = M; g.N = w.N; g.K = (m.et == ET_BF16) ? w.ldk : w.K;
   g.A = A; g.lda = lda; g.a_type = a_type;
@@ -426,6 +431,7 @@ AttnArgs attn(int B, int Hq, int Hkv, int Lq, int hd, int et) {
 // ---------------------------------------------------------------- VLM stage
 void vla_model_s::enqueue_prefill(int B, const float* pix, const int32_t* ids, const float* state, void* kv,
                                   hipStream_t s) {
+  constexpr int ST = STAGE_PREFILL;
   const vla_config& c = cfg;
   const size_t es = elem_size(et);
   const int nimg = B * c.n_img, Mi = nimg * T, Mp = B * P;
@@ -435,19 +441,19 @@ void vla_model_s::enqueue_prefill(int B, const float* pix, const int32_t* ids, c
   launch_im2col(pix, nimg, c.img_hw, c.patch, patches, Kp, et, s);
   if (c.vit_layers == 0) {
     // patch embedding + position table straight into the prefix rows b*P + t
-    GemmArgs g = gm(*this, patch, Mi, patches, Kp, et);
+    GemmArgs g = gm(*this, ST,patch, Mi, patches, Kp, et);
     g.tab = pos; g.tab_period = T; g.ldtab = E;
     g.row_group = c.n_img * T; g.row_group_stride = (long)P * D;
     store(g, h, D, ET_F32, patch_b, ACT_NONE, s);
   } else {
     const int d = c.vit_d, nh = c.vit_heads;
-    GemmArgs g = gm(*this, patch, Mi, patches, Kp, et);
+    GemmArgs g = gm(*this, ST,patch, Mi, patches, Kp, et);
     g.tab = pos; g.tab_period = T; g.ldtab = E;
     store(g, vx, d, ET_F32, patch_b, ACT_NONE, s);
     for (int l = 0; l < c.vit_layers; ++l) {
       const VitLayer& y = vit[l];
       norm(Mi, d, 1, vx, d, vz, d, et, y.ln1g, y.ln1b, eps, s);
-      GemmArgs q3 = gm(*this, y.qkv, Mi, vz, d, et);
+      GemmArgs q3 = gm(*this, ST,y.qkv, Mi, vz, d, et);
       q3.mode = EPI_QKV; q3.bias = y.bqkv; q3.out_type = et;
       QkvEpi& e3 = q3.qkv;
       e3.n_q = nh; e3.n_kv = nh; e3.hd = vhd; e3.n_off = 0; e3.seq = T; e3.pos0 = -1;
@@ -461,13 +467,13 @@ void vla_model_s::enqueue_prefill(int B, const float* pix, const int32_t* ids, c
       at.seg[1].len = 0;
       at.o = vo; at.o_sb = (long)T * d; at.o_sh = vhd; at.o_si = d;
       launch_attention(at, s);
-      resid(gm(*this, y.wo, Mi, vo, d, et), vx, d, y.bo, nullptr, s);
+      resid(gm(*this, ST,y.wo, Mi, vo, d, et), vx, d, y.bo, nullptr, s);
       norm(Mi, d, 1, vx, d, vz, d, et, y.ln2g, y.ln2b, eps, s);
-      store(gm(*this, y.w1, Mi, vz, d, et), vmlp, c.vit_mlp, et, y.b1, ACT_GELU, s);
-      resid(gm(*this, y.w2, Mi, vmlp, c.vit_mlp, et), vx, d, y.b2, nullptr, s);
+      store(gm(*this, ST,y.w1, Mi, vz, d, et), vmlp, c.vit_mlp, et, y.b1, ACT_GELU, s);
+      resid(gm(*this, ST,y.w2, Mi, vmlp, c.vit_mlp, et), vx, d, y.b2, nullptr, s);
     }
     norm(Mi, d, 1, vx, d, vz, d, et, vit_lnf_g, vit_lnf_b, eps, s);
-    GemmArgs gp = gm(*this, proj, Mi, vz, d, et);
+    GemmArgs gp = gm(*this, ST,proj, Mi, vz, d, et);
     gp.row_group = c.n_img * T; gp.row_group_stride = (long)P * D;
     store(gp, h, D, ET_F32, proj_b, ACT_NONE, s);
   }
@@ -486,7 +492,7 @@ void vla_model_s::enqueue_prefill(int B, const float* pix, const int32_t* ids, c
       kd_ = kbuf; vd_ = vbuf;
     }
     norm(Mp, D, 0, h, D, z, D, et, y.ln1, nullptr, eps, s);
-    GemmArgs q3 = gm(*this, y.qkv, Mp, z, D, et);
+    GemmArgs q3 = gm(*this, ST,y.qkv, Mp, z, D, et);
     q3.mode = EPI_QKV; q3.out_type = et;
     QkvEpi& e3 = q3.qkv;
     e3.n_q = nq; e3.n_kv = nkv; e3.hd = hd; e3.seq = P; e3.pos0 = 0; e3.rope_cs = rope_cs;
@@ -506,24 +512,24 @@ void vla_model_s::enqueue_prefill(int B, const float* pix, const int32_t* ids, c
     at.seg[1].len = 0;
     at.o = o; at.o_sb = (long)P * Hq; at.o_sh = hd; at.o_si = Hq;
     launch_attention(at, s);
-    resid(gm(*this, y.wo, Mp, o, Hq, et), h, D, nullptr, nullptr, s);
+    resid(gm(*this, ST,y.wo, Mp, o, Hq, et), h, D, nullptr, nullptr, s);
     norm(Mp, D, 0, h, D, z, D, et, y.ln2, nullptr, eps, s);
-    GemmArgs gg = gm(*this, y.gu, Mp, z, D, et);
+    GemmArgs gg = gm(*this, ST,y.gu, Mp, z, D, et);
     gg.mode = EPI_GEGLU; gg.out = gu; gg.ldo = c.llm_mlp; gg.out_type = et;
     launch_gemm(gg, s);
-    resid(gm(*this, y.wd, Mp, gu, c.llm_mlp, et), h, D, nullptr, nullptr, s);
+    resid(gm(*this, ST,y.wd, Mp, gu, c.llm_mlp, et), h, D, nullptr, nullptr, s);
   }
   if (dit_head) {
     const int NL = c.act_layers;
     norm(Mp, D, 0, h, D, z, D, et, llm_lnf, nullptr, eps, s);
-    store(gm(*this, vp, Mp, z, D, et), feat, Da, et, vp_b, ACT_NONE, s);
-    store(gm(*this, xkv, Mp, feat, Da, et), kv, NL * 2 * Da, et, xkv_b, ACT_NONE, s);
+    store(gm(*this, ST,vp, Mp, z, D, et), feat, Da, et, vp_b, ACT_NONE, s);
+    store(gm(*this, ST,xkv, Mp, feat, Da, et), kv, NL * 2 * Da, et, xkv_b, ACT_NONE, s);
     void* st_out = (char*)kv + (size_t)B * P * NL * 2 * Da * es;
     const float* st_in = state ? state : zero_state;
-    if (c.state_dim > 0) store(gm(*this, state_w, B, st_in, c.state_dim, ET_F32), st_out, Da, et, state_b, ACT_NONE, s);
+    if (c.state_dim > 0) store(gm(*this, ST,state_w, B, st_in, c.state_dim, ET_F32), st_out, Da, et, state_b, ACT_NONE, s);
     else {
       // no state input: the token is the bias alone (a K = 0 product)
-      GemmArgs g0 = gm(*this, state_w, B, zero_state, 1, ET_F32);
+      GemmArgs g0 = gm(*this, ST,state_w, B, zero_state, 1, ET_F32);
       g0.K = 0;
       store(g0, st_out, Da, et, state_b, ACT_NONE, s);
     }
@@ -532,6 +538,7 @@ void vla_model_s::enqueue_prefill(int B, const float* pix, const int32_t* ids, c
 
 // ---------------------------------------------------------------- action stage
 const CondCache& vla_model_s::cond_for(int N, hipStream_t s) {
+  constexpr int ST = STAGE_DENOISE;
   std::lock_guard<std::mutex> lk(cond_mu);
   auto it = cond.find(N);
   if (it != cond.end()) return it->second;
@@ -541,7 +548,7 @@ const CondCache& vla_model_s::cond_for(int N, hipStream_t s) {
   launch_time_embed(N, tdim, cc.phi, s);
   if (!dit_head) {
     cc.tb = (float*)dalloc((size_t)N * Da * 4);
-    store(gm(*this, t1t, N, cc.phi, tdim, ET_F32), cc.tb, Da, ET_F32, t1_b, ACT_NONE, s);
+    store(gm(*this, ST,t1t, N, cc.phi, tdim, ET_F32), cc.tb, Da, ET_F32, t1_b, ACT_NONE, s);
   } else {
     const int NL = cfg.act_layers;
     cc.c1 = (float*)dalloc((size_t)N * Da * 4);
@@ -549,11 +556,11 @@ const CondCache& vla_model_s::cond_for(int N, hipStream_t s) {
     cc.sc = (float*)dalloc((size_t)N * Da * 4);
     cc.mods = (float*)dalloc((size_t)N * NL * 6 * Da * 4);
     cc.modf = (float*)dalloc((size_t)N * 2 * Da * 4);
-    store(gm(*this, dt1, N, cc.phi, tdim, ET_F32), cc.c1, Da, ET_F32, dt1_b, ACT_SILU, s);
-    store(gm(*this, dt2, N, cc.c1, Da, ET_F32), cc.c, Da, ET_F32, dt2_b, ACT_NONE, s);
+    store(gm(*this, ST,dt1, N, cc.phi, tdim, ET_F32), cc.c1, Da, ET_F32, dt1_b, ACT_SILU, s);
+    store(gm(*this, ST,dt2, N, cc.c1, Da, ET_F32), cc.c, Da, ET_F32, dt2_b, ACT_NONE, s);
     launch_silu_f32(cc.c, cc.sc, (long)N * Da, s);
-    store(gm(*this, mod_all, N, cc.sc, Da, ET_F32), cc.mods, NL * 6 * Da, ET_F32, mod_b, ACT_NONE, s);
-    store(gm(*this, modf, N, cc.sc, Da, ET_F32), cc.modf, 2 * Da, ET_F32, modf_b, ACT_NONE, s);
+    store(gm(*this, ST,mod_all, N, cc.sc, Da, ET_F32), cc.mods, NL * 6 * Da, ET_F32, mod_b, ACT_NONE, s);
+    store(gm(*this, ST,modf, N, cc.sc, Da, ET_F32), cc.modf, 2 * Da, ET_F32, modf_b, ACT_NONE, s);
   }
   VLA_HIP(hipGetLastError());
   VLA_HIP(hipStreamSynchronize(s));
@@ -562,6 +569,7 @@ const CondCache& vla_model_s::cond_for(int N, hipStream_t s) {
 
 void vla_model_s::enqueue_denoise(int B, const void* kv, const float* noise, int N, float* x, const CondCache& cc,
                                   hipStream_t s) {
+  constexpr int ST = STAGE_DENOISE;
   const vla_config& c = cfg;
   const size_t es = elem_size(et);
   const float eps = c.norm_eps;
@@ -572,13 +580,13 @@ void vla_model_s::enqueue_denoise(int B, const void* kv, const float* noise, int
     const int M = B * H, nq = c.n_q, nkv = c.n_kv, Fa = c.act_mlp;
     const size_t per = (size_t)B * nkv * P * hd * es;
     for (int k = 0; k < N; ++k) {
-      store(gm(*this, ain, M, x, A, ET_F32), e, Da, et, ain_b, ACT_NONE, s);
-      store(gm(*this, t1a, M, e, Da, et), u, Da, et, cc.tb + (size_t)k * Da, ACT_SILU, s);
-      store(gm(*this, t2, M, u, Da, et), ha, Da, ET_F32, t2_b, ACT_NONE, s);
+      store(gm(*this, ST,ain, M, x, A, ET_F32), e, Da, et, ain_b, ACT_NONE, s);
+      store(gm(*this, ST,t1a, M, e, Da, et), u, Da, et, cc.tb + (size_t)k * Da, ACT_SILU, s);
+      store(gm(*this, ST,t2, M, u, Da, et), ha, Da, ET_F32, t2_b, ACT_NONE, s);
       for (int l = 0; l < c.act_layers; ++l) {
         const LlmLayer& y = act[l];
         norm(M, Da, 0, ha, Da, za, Da, et, y.ln1, nullptr, eps, s);
-        GemmArgs q3 = gm(*this, y.qkv, M, za, Da, et);
+        GemmArgs q3 = gm(*this, ST,y.qkv, M, za, Da, et);
         q3.mode = EPI_QKV; q3.out_type = et;
         QkvEpi& e3 = q3.qkv;
         e3.n_q = nq; e3.n_kv = nkv; e3.hd = hd; e3.seq = H; e3.pos0 = P; e3.rope_cs = rope_cs;
@@ -594,15 +602,15 @@ void vla_model_s::enqueue_denoise(int B, const void* kv, const float* noise, int
         at.seg[1] = AttnSeg{ks, e3.k_sb, e3.k_sh, hd, vs, e3.v_sb, e3.v_sh, hd, H};
         at.o = oa; at.o_sb = (long)H * Hq; at.o_sh = hd; at.o_si = Hq;
         launch_attention(at, s);
-        resid(gm(*this, y.wo, M, oa, Hq, et), ha, Da, nullptr, nullptr, s);
+        resid(gm(*this, ST,y.wo, M, oa, Hq, et), ha, Da, nullptr, nullptr, s);
         norm(M, Da, 0, ha, Da, za, Da, et, y.ln2, nullptr, eps, s);
-        GemmArgs gg = gm(*this, y.gu, M, za, Da, et);
+        GemmArgs gg = gm(*this, ST,y.gu, M, za, Da, et);
         gg.mode = EPI_GEGLU; gg.out = gua; gg.ldo = Fa; gg.out_type = et;
         launch_gemm(gg, s);
-        resid(gm(*this, y.wd, M, gua, Fa, et), ha, Da, nullptr, nullptr, s);
+        resid(gm(*this, ST,y.wd, M, gua, Fa, et), ha, Da, nullptr, nullptr, s);
       }
       norm(M, Da, 0, ha, Da, za, Da, et, lnf, nullptr, eps, s);
-      GemmArgs go = gm(*this, out, M, za, Da, et);
+      GemmArgs go = gm(*this, ST,out, M, za, Da, et);
       go.mode = EPI_EULER; go.out = x; go.ldo = A; go.out_type = ET_F32; go.bias = out_b; go.dt = dt;
       launch_gemm(go, s);
     }
@@ -617,7 +625,7 @@ void vla_model_s::enqueue_denoise(int B, const void* kv, const float* noise, int
   for (int k = 0; k < N; ++k) {
     const float* mk = cc.mods + (size_t)k * NL * 6 * Da;
     launch_dit_state_rows(st_tok, et, B, Da, S, dpos, X, s);
-    GemmArgs ga = gm(*this, dain, B * H, x, A, ET_F32);
+    GemmArgs ga = gm(*this, ST,dain, B * H, x, A, ET_F32);
     ga.tab = dpos + Da; ga.tab_period = H; ga.ldtab = Da;
     ga.row_group = H; ga.row_group_stride = (long)S * Da;
     store(ga, X + Da, Da, ET_F32, dain_b, ACT_NONE, s);
@@ -625,7 +633,7 @@ void vla_model_s::enqueue_denoise(int B, const void* kv, const float* noise, int
       const DitLayer& y = dit[l];
       const float* m6 = mk + (size_t)l * 6 * Da;
       norm(M, Da, 2, X, Da, zd, Da, et, m6 + 1 * Da, m6 + 0 * Da, eps, s);
-      GemmArgs q3 = gm(*this, y.qkv, M, zd, Da, et);
+      GemmArgs q3 = gm(*this, ST,y.qkv, M, zd, Da, et);
       q3.mode = EPI_QKV; q3.out_type = et; q3.bias = y.bqkv;
       QkvEpi& e3 = q3.qkv;
       e3.n_q = nh; e3.n_kv = nh; e3.hd = dhd; e3.seq = S; e3.pos0 = -1;
@@ -639,10 +647,10 @@ void vla_model_s::enqueue_denoise(int B, const void* kv, const float* noise, int
       at.seg[1].len = 0;
       at.o = od; at.o_sb = (long)S * Da; at.o_sh = dhd; at.o_si = Da;
       launch_attention(at, s);
-      resid(gm(*this, y.wo, M, od, Da, et), X, Da, y.bo, m6 + 2 * Da, s);
+      resid(gm(*this, ST,y.wo, M, od, Da, et), X, Da, y.bo, m6 + 2 * Da, s);
       // cross-attention to the VLM features of the paired layer
       norm(M, Da, 1, X, Da, zd, Da, et, nullptr, nullptr, eps, s);
-      store(gm(*this, y.cq, M, zd, Da, et), qc, Da, et, y.bcq, ACT_NONE, s);
+      store(gm(*this, ST,y.cq, M, zd, Da, et), qc, Da, et, y.bcq, ACT_NONE, s);
       AttnArgs ac = attn(B, nh, nh, S, dhd, et);
       ac.q = qc; ac.q_sb = (long)S * Da; ac.q_sh = dhd; ac.q_si = Da;
       const char* kl = xkv_base + (size_t)(2 * l) * Da * es;
@@ -651,14 +659,14 @@ void vla_model_s::enqueue_denoise(int B, const void* kv, const float* noise, int
       ac.seg[1].len = 0;
       ac.o = od; ac.o_sb = (long)S * Da; ac.o_sh = dhd; ac.o_si = Da;
       launch_attention(ac, s);
-      resid(gm(*this, y.co, M, od, Da, et), X, Da, y.bco, nullptr, s);
+      resid(gm(*this, ST,y.co, M, od, Da, et), X, Da, y.bco, nullptr, s);
       norm(M, Da, 2, X, Da, zd, Da, et, m6 + 4 * Da, m6 + 3 * Da, eps, s);
-      store(gm(*this, y.w1, M, zd, Da, et), mlp, Fa, et, y.b1, ACT_GELU, s);
-      resid(gm(*this, y.w2, M, mlp, Fa, et), X, Da, y.b2, m6 + 5 * Da, s);
+      store(gm(*this, ST,y.w1, M, zd, Da, et), mlp, Fa, et, y.b1, ACT_GELU, s);
+      resid(gm(*this, ST,y.w2, M, mlp, Fa, et), X, Da, y.b2, m6 + 5 * Da, s);
     }
     const float* mf = cc.modf + (size_t)k * 2 * Da;
     norm(B * H, Da, 2, X, Da, zf, Da, et, mf + Da, mf, eps, s, /*skip=*/1, /*skip_group=*/H);
-    GemmArgs go = gm(*this, dout, B * H, zf, Da, et);
+    GemmArgs go = gm(*this, ST,dout, B * H, zf, Da, et);
     go.mode = EPI_EULER; go.out = x; go.ldo = A; go.out_type = ET_F32; go.bias = dout_b; go.dt = dt;
     launch_gemm(go, s);
   }
@@ -719,4 +727,47 @@ void vla_model_s::denoise(int B, const void* kv, const float* noise, int N, floa
   const CondCache& cc = cond_for(N, s);
   GraphKey key{B, N, kv, noise, act, nullptr};
   run_graph(STAGE_DENOISE, key, s, [&](hipStream_t cs) { enqueue_denoise(B, kv, noise, N, act, cc, cs); });
+}
+
+// ---------------------------------------------------------------- timing hook
+GemmArgs vla_model_s::stage_gemm(int which, int B) const {
+  const int ST = (which == 2 || which == 3) ? STAGE_DENOISE : STAGE_PREFILL;
+  const vla_config& c = cfg;
+  GemmArgs g{};
+  switch (which) {
+    case 0:   // VLM stage: LLM layer 0 MLP gate/up (GeGLU epilogue)
+      g = gm(*this, ST,llm[0].gu, B * P, z, D, et);
+      g.mode = EPI_GEGLU; g.out = gu; g.ldo = c.llm_mlp; g.out_type = et;
+      break;
+    case 1:   // VLM stage: LLM layer 0 MLP down projection (+ residual)
+      g = gm(*this, ST,llm[0].wd, B * P, gu, c.llm_mlp, et);
+      g.mode = EPI_RESID; g.out = h; g.ldo = D; g.out_type = ET_F32;
+      break;
+    case 2:   // action stage: layer 0 MLP up (GeGLU for the joint expert, GELU for the DiT)
+      if (c.head_kind == VLA_HEAD_JOINT) {
+        g = gm(*this, ST,act[0].gu, B * H, za, Da, et);
+        g.mode = EPI_GEGLU; g.out = gua; g.ldo = c.act_mlp; g.out_type = et;
+      } else {
+        g = gm(*this, ST,dit[0].w1, B * Ltok, zd, Da, et);
+        g.mode = EPI_STORE; g.act = ACT_GELU; g.bias = dit[0].b1; g.out = mlp; g.ldo = c.act_mlp; g.out_type = et;
+      }
+      break;
+    case 3:   // action stage: layer 0 MLP down projection (+ residual)
+      if (c.head_kind == VLA_HEAD_JOINT) {
+        g = gm(*this, ST,act[0].wd, B * H, gua, c.act_mlp, et);
+        g.mode = EPI_RESID; g.out = ha; g.ldo = Da; g.out_type = ET_F32;
+      } else {
+        g = gm(*this, ST,dit[0].w2, B * Ltok, mlp, c.act_mlp, et);
+        g.mode = EPI_RESID; g.bias = dit[0].b2; g.out = X; g.ldo = Da; g.out_type = ET_F32;
+      }
+      break;
+    case 4:   // VLM stage: ViT layer 0 MLP up (GELU)
+      VLA_REQUIRE(c.vit_layers > 0, "model has no ViT");
+      g = gm(*this, ST,vit[0].w1, B * c.n_img * T, vz, c.vit_d, et);
+      g.mode = EPI_STORE; g.act = ACT_GELU; g.bias = vit[0].b1; g.out = vmlp; g.ldo = c.vit_mlp; g.out_type = et;
+      break;
+    default:
+      throw VlaError{1, "unknown projection index"};
+  }
+  return g;
 }

@@ -24,7 +24,7 @@ VLA_OK, VLA_EINVAL, VLA_ENOMEM, VLA_EHIP, VLA_EUNSUPPORTED = range(5)
 # every exported symbol declared by include/vla.h and include/vla_debug.h
 EXPORTS = ["vla_weight_count", "vla_create_model", "vla_destroy_model", "vla_set_graphs", "vla_kv_bytes",
            "vla_prefill", "vla_prefill_ex", "vla_denoise", "vla_step", "vla_last_error",
-           "vla_debug_gemm", "vla_debug_attention", "vla_debug_cu_probe"]
+           "vla_debug_gemm", "vla_debug_attention", "vla_debug_cu_probe", "vla_debug_replay_gemm"]
 
 
 class VlaError(RuntimeError):
@@ -75,6 +75,8 @@ def lib():
         L.vla_debug_attention.argtypes = [ci, ci, ci, ci, ci, ci, vp, vp, vp, ci, vp, vp, ci, vp, vp]
         L.vla_debug_attention.restype = ci
         L.vla_debug_cu_probe.argtypes = [ci, ci, ci, ci, ci, vp, vp]; L.vla_debug_cu_probe.restype = ci
+        L.vla_debug_replay_gemm.argtypes = [vp, ci, ci, ci, vp, ctypes.POINTER(ctypes.c_double)]
+        L.vla_debug_replay_gemm.restype = ci
         _lib = L
     return _lib
 
@@ -153,6 +155,12 @@ class Model:
     def prefill(self, batch, pixels, text_ids, kv_out, state=None, stream=None):
         _check(lib().vla_prefill_ex(self.handle, batch, _ptr(pixels), _ptr(text_ids), _ptr(state), _ptr(kv_out),
                                     _stream(stream)))
+
+    def replay_gemm(self, which: int, batch: int, iters: int, stream=None) -> float:
+        """Enqueue `iters` launches of one stage projection; returns its flops."""
+        f = ctypes.c_double(0.0)
+        _check(lib().vla_debug_replay_gemm(self.handle, which, batch, iters, _stream(stream), ctypes.byref(f)))
+        return f.value
 
     def denoise(self, batch, kv, noise, steps, actions_out, stream=None):
         _check(lib().vla_denoise(self.handle, batch, _ptr(kv), _ptr(noise), steps, _ptr(actions_out),
