@@ -62,6 +62,71 @@ def cpu_baseline(cfg, weights, budget_s):
                       f"steps), numpy fp64, {el:.1f} s"}
 
 
+def serve_main(args):
+    """Co-located serving (pi0-shaped + SmolVLA-shaped models on one GPU):
+    profile every lockstep combination under each CU restriction, build the
+    per-combination restriction table, sweep robot load in simulation on the
+    profiled durations, and check the chosen operating points in real time on
+    the GPU. Prints one JSON line."""
+    import numpy as np
+    import torch
+    from paper_2609_12075_amd import serve, synth, vla
+
+    names = args.serve_models.split(",")
+    mb = args.serve_batch
+    cfgs = [synth.CONFIGS[n].with_(max_batch=mb) for n in names]   # workspaces sized for the serving batch
+    slo = [args.slo_ms] * len(cfgs)
+    cus = [int(x) for x in args.serve_cus.split(",")]
+    t0 = time.perf_counter()
+    models = [vla.Model(c, synth.make_weights(c), device=0) for c in cfgs]
+    log(f"[serve] models {names} created in {time.perf_counter() - t0:.1f} s")
+    bufs = serve.alloc_io(models, mb)
+    for m, b in zip(models, bufs):          # both hand-off slots hold real prefixes
+        m.prefill(mb, b["pixels"], b["text_ids"], b["kv0"], state=b.get("state"))
+        m.prefill(mb, b["pixels"], b["text_ids"], b["kv1"], state=b.get("state"))
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    prof = serve.profile_locksteps(models, bufs, mb, cus, reps=3, log=log)
+    log(f"[serve] profiled {prof.size} lockstep entries in {time.perf_counter() - t0:.1f} s")
+    cu_table, dur_lut = serve.best_cu_table(prof, cus)
+    dur_static = {cu: prof[i] for i, cu in enumerate(cus)}
+    rates = [float(x) for x in args.serve_rates.split(",")]
+    robots = list(range(1, args.serve_max_robots + 1))
+    result = {"metric": METRIC, "unit": "action chunks/s", "n_gpus": 1, "dtype": "bf16",
+              "data": "synthetic Poisson robot traffic, seeded (6000 + epoch)",
+              "config": {"workload": "co-located " + " + ".join(f"{n}-shaped" for n in names),
+                         "max_batch": mb, "slo_ms": args.slo_ms, "cu_candidates": cus, "policy": "esf",
+                         "epochs": args.serve_epochs, "trace_s": args.serve_seconds},
+              "rates": {}}
+    for f in rates:
+        rows, best = serve.sweep_robots(dur_lut, slo, mb, robots, f, args.serve_seconds, args.serve_epochs)
+        static = {}
+        for cu, d in dur_static.items():
+            _, b = serve.sweep_robots(d, slo, mb, robots, f, args.serve_seconds, args.serve_epochs)
+            static[str(cu)] = b
+        entry = {"robots_at_98_sim": best, "chunks_per_s_at_98_sim": best * f,
+                 "static_cu_robots_at_98_sim": static, "sweep": rows}
+        if best > 0 and not args.serve_no_validate:
+            for R in sorted({best, best + 1}):
+                s = serve.Scheduler(slo, mb, "esf")
+                s.set_gpu(models, bufs)
+                s.set_cu(256, cu_table)
+                arr = synth.poisson_arrivals(R, f, args.validate_seconds, epoch=100, n_models=len(cfgs))
+                req, ls = s.run(arr, drain_ns=int(1e9))
+                s.close()
+                entry.setdefault("gpu_validation", []).append(
+                    {"robots": R, "attainment": serve.attainment(req), "p99_ms": serve.p99_ms(req),
+                     "locksteps": int(len(ls)), "requests": int(len(req))})
+                log(f"[serve] f={f} R={R}: GPU attainment {serve.attainment(req):.3f}, p99 {serve.p99_ms(req):.1f} ms")
+        result["rates"][str(f)] = entry
+        log(f"[serve] f={f} Hz: max robots at 98% (sim, CU table) {best}; static {static}")
+    result["cu_table"] = cu_table.tolist()
+    result["lockstep_ms_lut"] = (dur_lut / 1e6).round(3).tolist()
+    best_f = max(rates, key=lambda f: result["rates"][str(f)]["chunks_per_s_at_98_sim"])
+    result["value"] = result["rates"][str(best_f)]["chunks_per_s_at_98_sim"]
+    print(json.dumps(result), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -73,6 +138,17 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--roofline-iters", type=int, default=50)
+    ap.add_argument("--serve", action="store_true", help="co-located serving sweep instead of the lockstep bench")
+    ap.add_argument("--serve-models", default="pi0,smolvla")
+    ap.add_argument("--serve-batch", type=int, default=4)
+    ap.add_argument("--serve-cus", default="64,128,192,256")
+    ap.add_argument("--serve-rates", default="10,20,30")
+    ap.add_argument("--serve-max-robots", type=int, default=32)
+    ap.add_argument("--serve-seconds", type=float, default=30.0)
+    ap.add_argument("--serve-epochs", type=int, default=5)
+    ap.add_argument("--serve-no-validate", action="store_true")
+    ap.add_argument("--validate-seconds", type=float, default=8.0)
+    ap.add_argument("--slo-ms", type=float, default=100.0)
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -80,6 +156,9 @@ def main():
         print("bench.py runs on one GPU only: the serving hot path here is a single-GPU build "
               "(replicas on more GPUs would share nothing on the hot path). Use --gpus 1.", file=sys.stderr)
         sys.exit(2)
+    if args.serve:
+        serve_main(args)
+        return
 
     import numpy as np
     import torch

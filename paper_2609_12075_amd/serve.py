@@ -1,0 +1,244 @@
+"""Serving layer: ctypes binding of the host scheduler (include/vla_sched.h),
+lockstep-duration profiling on the GPU, and robot-load sweeps.
+
+The scheduler itself (queues, earliest-SLO-first choice, power-of-two
+batches, lockstep pairing, SLO accounting) is C++ inside libvla.so; this
+module marshals arguments and post-processes the records it returns.
+"""
+from __future__ import annotations
+
+import ctypes
+from typing import Dict, List, Optional, Sequence
+
+import numpy as np
+
+from . import synth, vla
+
+POLICIES = {"esf": 0, "rr": 1, "lqf": 2}
+
+REQ_DTYPE = np.dtype([("t_arrival_ns", np.int64), ("t_vlm_start_ns", np.int64), ("t_done_ns", np.int64),
+                      ("model", np.int32), ("met_slo", np.int32)])
+LS_DTYPE = np.dtype([("t_start_ns", np.int64), ("t_end_ns", np.int64), ("vlm_model", np.int32),
+                     ("vlm_batch", np.int32), ("adit_model", np.int32), ("adit_batch", np.int32),
+                     ("cu_count", np.int32), ("slot", np.int32)])
+
+
+class _Cfg(ctypes.Structure):
+    _fields_ = [("n_models", ctypes.c_int), ("slo_ms", ctypes.POINTER(ctypes.c_double)),
+                ("max_batch", ctypes.c_int), ("policy", ctypes.c_int)]
+
+
+class _IO(ctypes.Structure):
+    _fields_ = [("model", ctypes.c_void_p), ("pixels", ctypes.c_void_p), ("text_ids", ctypes.c_void_p),
+                ("state", ctypes.c_void_p), ("noise", ctypes.c_void_p), ("kv", ctypes.c_void_p * 2),
+                ("actions", ctypes.c_void_p * 2), ("steps", ctypes.c_int)]
+
+
+def _lib():
+    L = vla.lib()
+    if not getattr(L, "_sched_bound", False):
+        vp, ci, i64 = ctypes.c_void_p, ctypes.c_int, ctypes.c_int64
+        L.vla_sched_create.argtypes = [ctypes.POINTER(_Cfg), ctypes.POINTER(vp)]; L.vla_sched_create.restype = ci
+        L.vla_sched_destroy.argtypes = [vp]; L.vla_sched_destroy.restype = None
+        L.vla_sched_set_sim_executor.argtypes = [vp, vp, i64]; L.vla_sched_set_sim_executor.restype = ci
+        L.vla_sched_set_gpu_executor.argtypes = [vp, vp, vp]; L.vla_sched_set_gpu_executor.restype = ci
+        L.vla_sched_set_cu.argtypes = [vp, ci, vp]; L.vla_sched_set_cu.restype = ci
+        L.vla_sched_run.argtypes = [vp, vp, vp, ci, i64, vp, vp, ci, ctypes.POINTER(ci)]
+        L.vla_sched_run.restype = ci
+        L._sched_bound = True
+    return L
+
+
+def n_buckets(max_batch: int) -> int:
+    """Batch buckets of the duration / CU tables: 0 (no batch), 1, 2, 4, ..., max_batch."""
+    return int(np.log2(max_batch)) + 2
+
+
+def bucket(b: int) -> int:
+    return 0 if b <= 0 else int(np.log2(b)) + 1
+
+
+def bucket_batches(max_batch: int) -> List[int]:
+    return [0] + [1 << j for j in range(n_buckets(max_batch) - 1)]
+
+
+class Scheduler:
+    """One serving scheduler over co-located models (see include/vla_sched.h)."""
+
+    def __init__(self, slo_ms: Sequence[float], max_batch: int, policy: str = "esf"):
+        self.n_models = len(slo_ms)
+        self.max_batch = max_batch
+        self._slo = (ctypes.c_double * self.n_models)(*[float(x) for x in slo_ms])
+        cfg = _Cfg(self.n_models, self._slo, max_batch, POLICIES[policy])
+        h = ctypes.c_void_p()
+        vla._check(_lib().vla_sched_create(ctypes.byref(cfg), ctypes.byref(h)))
+        self.handle = h
+        self._keep = []
+
+    def close(self):
+        if getattr(self, "handle", None):
+            _lib().vla_sched_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def table_shape(self):
+        nb = n_buckets(self.max_batch)
+        return (self.n_models, nb, self.n_models, nb)
+
+    def set_sim(self, dur_ns: np.ndarray, host_overhead_ns: int = 0):
+        t = np.ascontiguousarray(dur_ns, dtype=np.int64)
+        assert t.shape == self.table_shape(), (t.shape, self.table_shape())
+        vla._check(_lib().vla_sched_set_sim_executor(self.handle, t.ctypes.data, int(host_overhead_ns)))
+
+    def set_cu(self, default_cu: int, table: Optional[np.ndarray] = None):
+        ptr = None
+        if table is not None:
+            t = np.ascontiguousarray(table, dtype=np.int32)
+            assert t.shape == self.table_shape()
+            self._keep.append(t)
+            ptr = t.ctypes.data
+        vla._check(_lib().vla_sched_set_cu(self.handle, int(default_cu), ptr))
+
+    def set_gpu(self, models: Sequence[vla.Model], bufs: Sequence[Dict], join_stream=None):
+        """bufs[m]: dict of torch tensors pixels, text_ids, noise, (state), kv0, kv1, act0, act1 (max_batch rows)."""
+        ios = (_IO * self.n_models)()
+        for i, (m, b) in enumerate(zip(models, bufs)):
+            io = ios[i]
+            io.model = m.handle.value
+            io.pixels, io.text_ids, io.noise = vla._ptr(b["pixels"]), vla._ptr(b["text_ids"]), vla._ptr(b["noise"])
+            io.state = vla._ptr(b.get("state"))
+            io.kv[0], io.kv[1] = vla._ptr(b["kv0"]), vla._ptr(b["kv1"])
+            io.actions[0], io.actions[1] = vla._ptr(b["act0"]), vla._ptr(b["act1"])
+            io.steps = m.cfg.steps
+        self._keep.append((models, bufs))
+        vla._check(_lib().vla_sched_set_gpu_executor(self.handle, ctypes.addressof(ios), vla._stream(join_stream)))
+
+    def run(self, arrivals: np.ndarray, drain_ns: int, ls_cap: int = 1 << 20):
+        """arrivals: structured array with t_ns (sorted) and model. Returns
+        (request records, lockstep records) as numpy structured arrays."""
+        t = np.ascontiguousarray(arrivals["t_ns"], dtype=np.int64)
+        mo = np.ascontiguousarray(arrivals["model"], dtype=np.int32)
+        n = len(t)
+        req = np.zeros(n, dtype=REQ_DTYPE)
+        ls = np.zeros(ls_cap, dtype=LS_DTYPE)
+        nls = ctypes.c_int(0)
+        vla._check(_lib().vla_sched_run(self.handle, t.ctypes.data if n else None, mo.ctypes.data if n else None, n,
+                                        int(drain_ns), req.ctypes.data if n else None, ls.ctypes.data, ls_cap,
+                                        ctypes.byref(nls)))
+        return req, ls[:min(nls.value, ls_cap)]
+
+
+# ---------------------------------------------------------------- metrics
+def attainment(req: np.ndarray) -> float:
+    """Fraction of requests that met their SLO (unfinished requests miss)."""
+    return float(req["met_slo"].mean()) if len(req) else 1.0
+
+
+def latency_ms(req: np.ndarray) -> np.ndarray:
+    done = req["t_done_ns"] >= 0
+    return (req["t_done_ns"][done] - req["t_arrival_ns"][done]) / 1e6
+
+
+def p99_ms(req: np.ndarray) -> float:
+    lat = latency_ms(req)
+    return float(np.percentile(lat, 99)) if len(lat) else float("inf")
+
+
+# ---------------------------------------------------------------- GPU profiling
+def alloc_io(models: Sequence[vla.Model], max_batch: int):
+    """Per-model device buffers for the GPU executor (seeded inputs, max_batch rows)."""
+    import torch
+    bufs = []
+    for m in models:
+        inp = synth.make_inputs(m.cfg, max_batch)
+        d = {k: torch.from_numpy(v).to(f"cuda:{m.device}") for k, v in inp.items()}
+        d["kv0"], d["kv1"] = m.alloc_kv(max_batch), m.alloc_kv(max_batch)
+        d["act0"], d["act1"] = torch.empty_like(d["noise"]), torch.empty_like(d["noise"])
+        bufs.append(d)
+    return bufs
+
+
+def profile_locksteps(models: Sequence[vla.Model], bufs, max_batch: int, cu_counts: Sequence[int],
+                      reps: int = 3, warmup: int = 1, log=None):
+    """Median duration (ns) of one lockstep for every (VLM model, VLM batch,
+    action model, action batch) combination and every CU restriction of the
+    VLM stream, timed with HIP events on the join stream. Returns
+    dur[k_index][mv][bv][ma][ba] (int64; combinations with both halves empty
+    are 0) — the profiling pass behind the restriction lookup table."""
+    import torch
+    nm, nb = len(models), n_buckets(max_batch)
+    bs = bucket_batches(max_batch)
+    out = np.zeros((len(cu_counts), nm, nb, nm, nb), dtype=np.int64)
+    stream = torch.cuda.current_stream()
+    for ki, cu in enumerate(cu_counts):
+        for mv in range(nm):
+            for iv, bv in enumerate(bs):
+                for ma in range(nm):
+                    for ia, ba in enumerate(bs):
+                        if bv == 0 and ba == 0:
+                            continue
+                        if bv == 0 and mv > 0:
+                            out[ki, mv, iv, ma, ia] = out[ki, 0, iv, ma, ia]   # no VLM half: model irrelevant
+                            continue
+                        if ba == 0 and ma > 0:
+                            out[ki, mv, iv, ma, ia] = out[ki, mv, iv, 0, ia]
+                            continue
+                        xv, xa = bufs[mv], bufs[ma]
+
+                        def one():
+                            vla.step(models[mv] if bv else None, bv, xv["pixels"], xv["text_ids"], xv["kv0"],
+                                     models[ma] if ba else None, ba, xa["kv1"], xa["noise"], models[ma].cfg.steps,
+                                     xa["act1"], vlm_cu_count=cu, state=xv.get("state"))
+                        for _ in range(warmup):
+                            one()
+                        ts = []
+                        for _ in range(reps):
+                            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                            e0.record(stream)
+                            one()
+                            e1.record(stream)
+                            e1.synchronize()
+                            ts.append(e0.elapsed_time(e1))
+                        out[ki, mv, iv, ma, ia] = int(np.median(ts) * 1e6)
+        if log:
+            log(f"[profile] cu={cu} done")
+    return out
+
+
+def best_cu_table(prof: np.ndarray, cu_counts: Sequence[int]):
+    """Per combination, the CU restriction with the shortest lockstep, and
+    the resulting duration table."""
+    best = np.argmin(np.where(prof > 0, prof, np.iinfo(np.int64).max), axis=0)
+    table = np.asarray(cu_counts, dtype=np.int32)[best]
+    dur = np.take_along_axis(prof, best[None], axis=0)[0]
+    return table, dur
+
+
+def sweep_robots(dur_ns: np.ndarray, slo_ms: Sequence[float], max_batch: int, robots: Sequence[int], rate_hz,
+                 duration_s: float, epochs: int, policy: str = "esf", host_overhead_ns: int = 0,
+                 traffic: str = "poisson", target: float = 0.98):
+    """Simulated robot-load sweep on a lockstep-duration table: for each robot
+    count, the mean SLO attainment over `epochs` seeded traces. Returns
+    (rows, max robots with attainment >= target)."""
+    rows, best = [], 0
+    gen = synth.poisson_arrivals if traffic == "poisson" else synth.periodic_arrivals
+    for R in robots:
+        att, p99 = [], []
+        for e in range(epochs):
+            arr = gen(R, rate_hz, duration_s, e, n_models=len(slo_ms))
+            s = Scheduler(slo_ms, max_batch, policy)
+            s.set_sim(dur_ns, host_overhead_ns)
+            req, _ = s.run(arr, drain_ns=int(1e9), ls_cap=16)
+            s.close()
+            att.append(attainment(req))
+            p99.append(p99_ms(req))
+        a = float(np.mean(att))
+        rows.append({"robots": int(R), "attainment": a, "p99_ms": float(np.mean(p99))})
+        if a >= target:
+            best = max(best, int(R))
+    return rows, best
