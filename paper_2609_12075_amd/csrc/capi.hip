@@ -104,6 +104,22 @@ hipStream_t adit_stream(int dev, int count) {
 
 void check_model(vla_model m) { VLA_REQUIRE(m != nullptr, "null model"); }
 
+// Split workspaces of the single-kernel test hooks: one per (device, kind),
+// allocated on first use and kept until the process ends.
+float* debug_ws(int kind, long floats) {
+  static std::mutex mu;
+  static std::map<std::pair<int, int>, float*> ws;
+  std::lock_guard<std::mutex> lk(mu);
+  int dev = 0;
+  VLA_HIP(hipGetDevice(&dev));
+  auto it = ws.find({dev, kind});
+  if (it != ws.end()) return it->second;
+  float* p = nullptr;
+  VLA_HIP(hipMalloc(&p, (size_t)floats * 4));
+  ws[{dev, kind}] = p;
+  return p;
+}
+
 void check_prefill(vla_model m, int B, const float* pix, const int32_t* ids, void* kv) {
   check_model(m);
   VLA_REQUIRE(B >= 1 && B <= m->cfg.max_batch,
@@ -252,6 +268,7 @@ vla_status vla_debug_gemm(int M, int N, int K, const void* A, int lda, int a_typ
     GemmArgs g{};
     g.M = M; g.N = N; g.K = K; g.A = A; g.lda = lda; g.a_type = a_type; g.W = Wt; g.ldw = ldw; g.w_type = w_type;
     g.mode = EPI_STORE; g.act = act; g.bias = bias; g.tab_period = 1; g.out = out; g.ldo = ldo; g.out_type = ET_F32;
+    g.ws = debug_ws(0, vla_model_s::kSplitKFloats); g.ws_floats = vla_model_s::kSplitKFloats;
     launch_gemm(g, s);
     VLA_HIP(hipGetLastError());
   });
@@ -272,6 +289,7 @@ vla_status vla_debug_attention(int B, int Hq, int Hkv, int Lq, int hd, int et, c
     a.seg[0] = AttnSeg{k0, (long)Hkv * len0 * hd, (long)len0 * hd, hd, v0, (long)Hkv * len0 * hd, (long)len0 * hd, hd, len0};
     a.seg[1] = AttnSeg{k1, (long)Hkv * len1 * hd, (long)len1 * hd, hd, v1, (long)Hkv * len1 * hd, (long)len1 * hd, hd, len1};
     a.o = o; a.o_sb = (long)Lq * Hq * hd; a.o_sh = hd; a.o_si = (long)Hq * hd;   // [B][Lq][Hq*hd]
+    a.ws = debug_ws(1, vla_model_s::kAttnFloats); a.ws_floats = vla_model_s::kAttnFloats;
     launch_attention(a, s);
     VLA_HIP(hipGetLastError());
   });

@@ -74,6 +74,14 @@ struct GemmArgs {
   int row_group; long row_group_stride;          // out row of m: (m/g)*stride + (m%g)*ldo
   float dt;                                       // EPI_EULER
   QkvEpi qkv;
+  // Optional split-K workspace (fp32). When the output tiles alone would
+  // leave most compute units idle (few activation rows, as in the action
+  // stage), launch_gemm cuts K into `splits` ranges: one kernel stores each
+  // range's fp32 partial product in ws[split][m][n], a second kernel adds the
+  // partials in split order and runs the epilogue (deterministic; no
+  // inter-block synchronisation).
+  float* ws; long ws_floats;
+  int splits, ksplit;                             // set by launch_gemm
 };
 
 void launch_gemm(const GemmArgs& a, hipStream_t s);
@@ -94,6 +102,12 @@ struct AttnArgs {
   AttnSeg seg[2];
   void* o; long o_sb, o_sh, o_si;
   int et;                   // element type of q, k, v, o
+  // Optional fp32 workspace for splitting the keys over blocks when the
+  // (row tile, KV head, request) blocks alone would leave the chip idle
+  // (decode at small batch): each key range stores its unnormalised output
+  // and softmax statistics, and a second kernel merges them in range order.
+  float* ws; long ws_floats;
+  int splits, kchunk;       // set by launch_attention
 };
 void launch_attention(const AttnArgs& a, hipStream_t s);
 

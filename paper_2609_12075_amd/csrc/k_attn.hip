@@ -15,6 +15,8 @@
 // probabilities then feed P V as the B operand without leaving registers,
 // with the key order inside each 32-key chunk permuted consistently on the
 // V side.
+#include <algorithm>
+
 #include "common.h"
 
 typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
@@ -45,7 +47,8 @@ __global__ void __launch_bounds__(256) attn_mfma_kernel(AttnArgs a) {
   __shared__ __attribute__((aligned(16))) bf16 Vt[HDP][LDV];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int b = blockIdx.z, g = blockIdx.y;
+  const int S = a.splits > 1 ? a.splits : 1;      // key ranges (split-KV)
+  const int b = blockIdx.z / S, split = blockIdx.z % S, g = blockIdx.y;
   const int G = a.Hq / a.Hkv;
   const int rows = G * a.Lq;
   const int hd = a.hd;
@@ -73,7 +76,9 @@ __global__ void __launch_bounds__(256) attn_mfma_kernel(AttnArgs a) {
   float m_run = -INFINITY, l_run = 0.f;
   const float sl2 = a.scale * 1.4426950408889634f;   // scale * log2(e)
 
-  const int len0 = a.seg[0].len, total = len0 + a.seg[1].len;
+  const int len0 = a.seg[0].len;
+  const int kbeg = S > 1 ? split * a.kchunk : 0;
+  const int kend = S > 1 ? min(len0 + a.seg[1].len, kbeg + a.kchunk) : len0 + a.seg[1].len;
   // K/V tile chunks (8 elements) handled by this thread; with PREFETCH the
   // next tile's chunks are loaded into registers while the current tile is
   // consumed, hiding the global-load latency behind the matrix work.
@@ -88,7 +93,7 @@ __global__ void __launch_bounds__(256) attn_mfma_kernel(AttnArgs a) {
       const int kg = k0 + kr;
       kreg[j] = bf16x8{};
       vreg[j] = bf16x8{};
-      if (kg < total && d8 < hd) {
+      if (kg < kend && d8 < hd) {
         const int which = kg < len0 ? 0 : 1;
         const int key = which ? kg - len0 : kg;
         kreg[j] = *reinterpret_cast<const bf16x8*>(seg_row(a, which, b, g, key, false) + d8);
@@ -96,8 +101,8 @@ __global__ void __launch_bounds__(256) attn_mfma_kernel(AttnArgs a) {
       }
     }
   };
-  if constexpr (PREFETCH) load_regs(0);
-  for (int k0 = 0; k0 < total; k0 += BKV) {
+  if constexpr (PREFETCH) load_regs(kbeg);
+  for (int k0 = kbeg; k0 < kend; k0 += BKV) {
     // ---- stage K (row-major) and V (transposed) tiles into LDS
     if constexpr (PREFETCH) {
 #pragma unroll
@@ -113,7 +118,7 @@ __global__ void __launch_bounds__(256) attn_mfma_kernel(AttnArgs a) {
         const int kr = c / CH, d8 = (c % CH) * 8;
         const int kg = k0 + kr;
         bf16x8 kv = bf16x8{}, vv = bf16x8{};
-        if (kg < total && d8 < hd) {
+        if (kg < kend && d8 < hd) {
           const int which = kg < len0 ? 0 : 1;
           const int key = which ? kg - len0 : kg;
           kv = *reinterpret_cast<const bf16x8*>(seg_row(a, which, b, g, key, false) + d8);
@@ -126,7 +131,7 @@ __global__ void __launch_bounds__(256) attn_mfma_kernel(AttnArgs a) {
     }
     __syncthreads();
     if constexpr (PREFETCH) {
-      if (k0 + BKV < total) load_regs(k0 + BKV);
+      if (k0 + BKV < kend) load_regs(k0 + BKV);
     }
 
     // ---- S^T = K Q^T for 4 subtiles of 16 keys
@@ -147,7 +152,7 @@ __global__ void __launch_bounds__(256) attn_mfma_kernel(AttnArgs a) {
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const int kg = k0 + st * 16 + grp * 4 + i;
-        float v = kg < total ? s[st][i] * sl2 : -INFINITY;
+        float v = kg < kend ? s[st][i] * sl2 : -INFINITY;
         s[st][i] = v;
         mx = fmaxf(mx, v);
       }
@@ -190,6 +195,22 @@ __global__ void __launch_bounds__(256) attn_mfma_kernel(AttnArgs a) {
   }
 
   if (!rvalid) return;
+  if (S > 1) {
+    // split-KV: unnormalised output and (max, sum) of this key range, fp32
+    const long row = ((long)b * a.Hq + h) * a.Lq + qi;
+    float* po = a.ws + (row * S + split) * hd;
+#pragma unroll
+    for (int t = 0; t < ND; ++t) {
+      const int d = t * 16 + grp * 4;
+      if (d < hd) *reinterpret_cast<f32x4*>(po + d) = o[t];
+    }
+    if (grp == 0) {
+      float* st = a.ws + (long)a.B * a.Hq * a.Lq * S * hd + (row * S + split) * 2;
+      st[0] = m_run;
+      st[1] = l_run;
+    }
+    return;
+  }
   const float inv = 1.0f / l_run;
   bf16* op = reinterpret_cast<bf16*>(a.o) + (long)b * a.o_sb + (long)h * a.o_sh + (long)qi * a.o_si;
 #pragma unroll
@@ -199,6 +220,29 @@ __global__ void __launch_bounds__(256) attn_mfma_kernel(AttnArgs a) {
       bf16x4 w = {(bf16)(o[t][0] * inv), (bf16)(o[t][1] * inv), (bf16)(o[t][2] * inv), (bf16)(o[t][3] * inv)};
       *reinterpret_cast<bf16x4*>(op + d) = w;
     }
+  }
+}
+
+// Split-KV merge: one wavefront per query row combines the key ranges in
+// order: m = max m_s, l = sum l_s 2^(m_s - m), o = sum o_s 2^(m_s - m) / l.
+__global__ void __launch_bounds__(256) attn_combine_kernel(AttnArgs a) {
+  const int lane = threadIdx.x & 63;
+  const long row = blockIdx.x * 4L + (threadIdx.x >> 6);
+  if (row >= (long)a.B * a.Hq * a.Lq) return;
+  const int S = a.splits, hd = a.hd;
+  const float* st = a.ws + (long)a.B * a.Hq * a.Lq * S * hd + row * S * 2;
+  float m = -INFINITY;
+  for (int s = 0; s < S; ++s) m = fmaxf(m, st[2 * s]);
+  float l = 0.f;
+  for (int s = 0; s < S; ++s) l += st[2 * s + 1] * exp2f(st[2 * s] - m);
+  const float inv = 1.0f / l;
+  const int qi = (int)(row % a.Lq), h = (int)((row / a.Lq) % a.Hq), b = (int)(row / ((long)a.Lq * a.Hq));
+  bf16* op = reinterpret_cast<bf16*>(a.o) + (long)b * a.o_sb + (long)h * a.o_sh + (long)qi * a.o_si;
+  const float* po = a.ws + row * S * hd;
+  for (int d = lane; d < hd; d += 64) {
+    float acc = 0.f;
+    for (int s = 0; s < S; ++s) acc += po[(long)s * hd + d] * exp2f(st[2 * s] - m);
+    op[d] = (bf16)(acc * inv);
   }
 }
 
@@ -270,10 +314,27 @@ void launch_attention(const AttnArgs& a, hipStream_t s) {
     hipLaunchKernelGGL(attn_f32_kernel, dim3(a.Lq, a.Hq, a.B), dim3(64), 0, s, a);
     return;
   }
+  AttnArgs b = a;
   const int rows = (a.Hq / a.Hkv) * a.Lq;
-  dim3 grid((rows + BQ - 1) / BQ, a.Hkv, a.B);
-  if (a.hd <= 32) hipLaunchKernelGGL(attn_mfma_kernel<32>, grid, dim3(256), 0, s, a);
-  else if (a.hd <= 64) hipLaunchKernelGGL(attn_mfma_kernel<64>, grid, dim3(256), 0, s, a);
-  else if (a.hd <= 96) hipLaunchKernelGGL(attn_mfma_kernel<96>, grid, dim3(256), 0, s, a);
-  else hipLaunchKernelGGL(attn_mfma_kernel<256>, grid, dim3(256), 0, s, a);
+  const long blocks = (long)((rows + BQ - 1) / BQ) * a.Hkv * a.B;
+  const int total = a.seg[0].len + a.seg[1].len, ntiles = (total + BKV - 1) / BKV;
+  // split the keys when the blocks alone would leave most CUs idle
+  b.splits = 1;
+  b.kchunk = ntiles * BKV;
+  if (a.ws && blocks < 128 && ntiles >= 2) {
+    int sp = (int)std::min<long>({(256 + blocks - 1) / blocks, (long)ntiles, 16L});
+    while (sp > 1 && (long)a.B * a.Hq * a.Lq * sp * (a.hd + 2) > a.ws_floats) --sp;
+    const int per = (ntiles + sp - 1) / sp;
+    b.kchunk = per * BKV;
+    b.splits = (ntiles + per - 1) / per;            // every range holds keys
+  }
+  dim3 grid((rows + BQ - 1) / BQ, a.Hkv, a.B * b.splits);
+  if (a.hd <= 32) hipLaunchKernelGGL(attn_mfma_kernel<32>, grid, dim3(256), 0, s, b);
+  else if (a.hd <= 64) hipLaunchKernelGGL(attn_mfma_kernel<64>, grid, dim3(256), 0, s, b);
+  else if (a.hd <= 96) hipLaunchKernelGGL(attn_mfma_kernel<96>, grid, dim3(256), 0, s, b);
+  else hipLaunchKernelGGL(attn_mfma_kernel<256>, grid, dim3(256), 0, s, b);
+  if (b.splits > 1) {
+    const long nrows = (long)a.B * a.Hq * a.Lq;
+    hipLaunchKernelGGL(attn_combine_kernel, dim3((unsigned)((nrows + 3) / 4)), dim3(256), 0, s, b);
+  }
 }

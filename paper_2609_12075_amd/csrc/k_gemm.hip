@@ -9,6 +9,8 @@
 // matrix instruction ends up owning four consecutive output columns of one
 // row: that makes the fused epilogues (bias, residual add, GeGLU pairs, RoPE
 // pairs, head scatter, Euler update) lane-local and the stores contiguous.
+#include <algorithm>
+
 #include "common.h"
 
 typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
@@ -153,8 +155,10 @@ gemm_mfma_kernel(GemmArgs a) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wn0 = (wave >> 1) * (BN / 2), wm0 = (wave & 1) * (BM / 2);
   const int n_blk = blockIdx.y * BN, m_blk = blockIdx.x * BM;
-  const int K = a.K;
-  const int nk = (K + BK - 1) / BK;
+  // K range of this block: split blockIdx.z covers [kbeg, kbeg + ksplit)
+  const int kbeg = blockIdx.z * a.ksplit;
+  const int K = min(a.K, kbeg + a.ksplit);
+  const int nk = K > kbeg ? (K - kbeg + BK - 1) / BK : 0;
   const bf16* W = reinterpret_cast<const bf16*>(a.W);
   const TA* A = reinterpret_cast<const TA*>(a.A);
 
@@ -162,7 +166,7 @@ gemm_mfma_kernel(GemmArgs a) {
   const int crow = tid >> 3, ccol = (tid & 7) * 8;
 
   auto load_tile = [&](int kt) {
-    const int k = kt * BK + ccol;
+    const int k = kbeg + kt * BK + ccol;
 #pragma unroll
     for (int j = 0; j < WCH; ++j) {
       const int n = n_blk + crow + 32 * j;
@@ -199,8 +203,10 @@ gemm_mfma_kernel(GemmArgs a) {
 #pragma unroll
     for (int j = 0; j < TM; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  load_tile(0);
-  store_tile(0);
+  if (nk > 0) {
+    load_tile(0);
+    store_tile(0);
+  }
   __syncthreads();
   const int lr = lane & 15, lk = (lane >> 4) * 8;
   for (int kt = 0; kt < nk; ++kt) {
@@ -232,6 +238,19 @@ gemm_mfma_kernel(GemmArgs a) {
     for (int j = 0; j < TM; ++j)
       *reinterpret_cast<f32x4*>(&Cs[wm0 + 16 * j + lr][wn0 + 16 * i + (lane >> 4) * 4]) = acc[i][j];
   __syncthreads();
+  if (a.splits > 1) {
+    // split-K: store this K range's partial tile; the reduce kernel finishes
+    const int ldp = (a.N + 3) & ~3;
+    float* part = a.ws + (long)blockIdx.z * a.M * ldp;
+#pragma unroll 1
+    for (int c = tid; c < BM * (BN / 4); c += 256) {
+      const int mr = c / (BN / 4), nc = (c % (BN / 4)) * 4;
+      const int m = m_blk + mr, n = n_blk + nc;
+      if (m < a.M && n < a.N)
+        *reinterpret_cast<f32x4*>(part + (long)m * ldp + n) = *reinterpret_cast<const f32x4*>(&Cs[mr][nc]);
+    }
+    return;
+  }
 #pragma unroll 1
   for (int c = tid; c < BM * (BN / 4); c += 256) {
     const int mr = c / (BN / 4), nc = (c % (BN / 4)) * 4;
@@ -239,6 +258,22 @@ gemm_mfma_kernel(GemmArgs a) {
     float v[4] = {t[0], t[1], t[2], t[3]};
     epilogue4<MODE>(a, m_blk + mr, n_blk + nc, v);
   }
+}
+
+// Split-K second pass: out = epilogue(sum over splits, in split order).
+// One thread per four consecutive output columns of a row.
+template <int MODE>
+__global__ void __launch_bounds__(256) splitk_reduce_kernel(GemmArgs a) {
+  const int ldp = (a.N + 3) & ~3, nc = ldp / 4;
+  const long c = blockIdx.x * 256L + threadIdx.x;
+  if (c >= (long)a.M * nc) return;
+  const int m = (int)(c / nc), n0 = (int)(c % nc) * 4;
+  const long stride = (long)a.M * ldp;
+  const f32x4* p = reinterpret_cast<const f32x4*>(a.ws + (long)m * ldp + n0);
+  f32x4 t = p[0];
+  for (int z = 1; z < a.splits; ++z) t += *reinterpret_cast<const f32x4*>(a.ws + z * stride + (long)m * ldp + n0);
+  float v[4] = {t[0], t[1], t[2], t[3]};
+  epilogue4<MODE>(a, m, n0, v);
 }
 
 // ---------------------------------------------------------------- fp32 VALU kernel
@@ -284,10 +319,36 @@ __global__ void __launch_bounds__(256) gemm_f32_kernel(GemmArgs a) {
 // activations (the Euler state, conditioning vectors, robot state) only feed
 // plain stores.
 template <int BN, int BM, int MODE>
-static void launch_mfma(const GemmArgs& a, hipStream_t s) {
-  dim3 grid((a.M + BM - 1) / BM, (a.N + BN - 1) / BN);
+static void launch_mfma(const GemmArgs& a0, hipStream_t s) {
+  constexpr int BK = 64;
+  GemmArgs a = a0;
+  const int gm = (a.M + BM - 1) / BM, gn = (a.N + BN - 1) / BN;
+  const long tiles = (long)gm * gn;
+  const int nk = (a.K + BK - 1) / BK;
+  // Split K when the output tiles would leave most of the 256 CUs idle: aim
+  // for ~2 blocks per CU, at least 2 K-steps per split, partials within ws.
+  int splits = 1;
+  const long ldp = (a.N + 3) & ~3;
+  if (a.ws && tiles < 192 && nk >= 4) {
+    splits = (int)std::min<long>({(512 + tiles - 1) / tiles, (long)nk / 2, 16L});
+    while (splits > 1 && (long)splits * a.M * ldp > a.ws_floats) --splits;
+  }
+  const int ksteps = std::max(1, (nk + splits - 1) / splits);
+  a.ksplit = ksteps * BK;
+  a.splits = std::max(1, (nk + ksteps - 1) / ksteps);   // no empty range
+  dim3 grid(gm, gn, a.splits);
+  bool f32a = false;
+  if constexpr (MODE == EPI_STORE) f32a = a.a_type == ET_F32;
+  if (a.splits > 1) {
+    // the partial pass does not use the epilogue: one instantiation serves all modes
+    if (f32a) hipLaunchKernelGGL((gemm_mfma_kernel<BN, BM, float, EPI_STORE>), grid, dim3(256), 0, s, a);
+    else hipLaunchKernelGGL((gemm_mfma_kernel<BN, BM, bf16, EPI_STORE>), grid, dim3(256), 0, s, a);
+    const long chunks = (long)a.M * (ldp / 4);
+    hipLaunchKernelGGL(splitk_reduce_kernel<MODE>, dim3((unsigned)((chunks + 255) / 256)), dim3(256), 0, s, a);
+    return;
+  }
   if constexpr (MODE == EPI_STORE) {
-    if (a.a_type == ET_F32) {
+    if (f32a) {
       hipLaunchKernelGGL((gemm_mfma_kernel<BN, BM, float, MODE>), grid, dim3(256), 0, s, a);
       return;
     }

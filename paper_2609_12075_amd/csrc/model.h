@@ -84,6 +84,13 @@ struct vla_model_s {
   std::map<int, CondCache> cond;
   std::mutex cond_mu;
 
+  // split-K partial products, one workspace per stage (fp32)
+  static constexpr long kSplitKFloats = 16L << 20;
+  float* splitk_ws[2] = {nullptr, nullptr};
+  // split-KV attention partials (fp32), one workspace per stage
+  static constexpr long kAttnFloats = 8L << 20;
+  float* attn_ws[2] = {nullptr, nullptr};
+
 
   // ---- graphs
   bool graphs = true;

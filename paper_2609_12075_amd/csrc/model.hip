@@ -365,6 +365,10 @@ void vla_model_s::init(const vla_config& c, const float* w, size_t n, int dev) {
       qa = dalloc(Ma * Hq * es); ks = dalloc(Ma * Hk * es); vs = dalloc(Ma * Hk * es);
       oa = dalloc(Ma * Hq * es); gua = dalloc(Ma * Fa * es);
     }
+    for (int i = 0; i < 2; ++i) {
+      splitk_ws[i] = (float*)dalloc((size_t)kSplitKFloats * 4);
+      attn_ws[i] = (float*)dalloc((size_t)kAttnFloats * 4);
+    }
     VLA_HIP(hipStreamSynchronize(L.s));
     for (int i = 0; i < 2; ++i) VLA_HIP(hipStreamCreateWithFlags(&cap_stream[i], hipStreamNonBlocking));
   } catch (...) {
@@ -389,15 +393,16 @@ void vla_model_s::destroy() {
 // ---------------------------------------------------------------- GEMM helpers
 namespace {
 
-// A projection of stage `st` of the model.
+// A projection of stage `st` of the model (each stage has its own split-K
+// workspace, so the two stages may run concurrently on different streams).
 GemmArgs gm(const vla_model_s& m, int st, const Mat& w, int M, const void* A, int lda, int a_type) {
-  (void)st;
   GemmArgs g{};
   g.M = M; g.N = w.N; g.K = (m.et == ET_BF16) ? w.ldk : w.K;
   g.A = A; g.lda = lda; g.a_type = a_type;
   g.W = w.p; g.ldw = w.ldk; g.w_type = m.et;
   g.mode = EPI_STORE; g.act = ACT_NONE;
   g.tab_period = 1;
+  g.ws = m.splitk_ws[st]; g.ws_floats = vla_model_s::kSplitKFloats;
   return g;
 }
 
@@ -419,10 +424,11 @@ void norm(int rows, int d, int kind, const float* in, int ld_in, void* out, int 
   launch_norm(a, s);
 }
 
-AttnArgs attn(int B, int Hq, int Hkv, int Lq, int hd, int et) {
+AttnArgs attn(const vla_model_s& m, int st, int B, int Hq, int Hkv, int Lq, int hd, int et) {
   AttnArgs a{};
   a.B = B; a.Hq = Hq; a.Hkv = Hkv; a.Lq = Lq; a.hd = hd; a.et = et;
   a.scale = 1.0f / sqrtf((float)hd);
+  a.ws = m.attn_ws[st]; a.ws_floats = vla_model_s::kAttnFloats;
   return a;
 }
 
@@ -461,7 +467,7 @@ void vla_model_s::enqueue_prefill(int B, const float* pix, const int32_t* ids, c
       e3.k = vk; e3.k_sb = e3.q_sb; e3.k_sh = e3.q_sh; e3.k_si = vhd;
       e3.v = vv; e3.v_sb = e3.q_sb; e3.v_sh = e3.q_sh; e3.v_si = vhd;
       launch_gemm(q3, s);
-      AttnArgs at = attn(nimg, nh, nh, T, vhd, et);
+      AttnArgs at = attn(*this, ST,nimg, nh, nh, T, vhd, et);
       at.q = vq; at.q_sb = e3.q_sb; at.q_sh = e3.q_sh; at.q_si = vhd;
       at.seg[0] = AttnSeg{vk, e3.k_sb, e3.k_sh, vhd, vv, e3.v_sb, e3.v_sh, vhd, T};
       at.seg[1].len = 0;
@@ -506,7 +512,7 @@ void vla_model_s::enqueue_prefill(int B, const float* pix, const int32_t* ids, c
     }
     launch_gemm(q3, s);
     if (last_kv_only) continue;
-    AttnArgs at = attn(B, nq, nkv, P, hd, et);
+    AttnArgs at = attn(*this, ST,B, nq, nkv, P, hd, et);
     at.q = q; at.q_sb = e3.q_sb; at.q_sh = e3.q_sh; at.q_si = hd;
     at.seg[0] = AttnSeg{kd_, e3.k_sb, e3.k_sh, hd, vd_, e3.v_sb, e3.v_sh, hd, P};
     at.seg[1].len = 0;
@@ -594,7 +600,7 @@ void vla_model_s::enqueue_denoise(int B, const void* kv, const float* noise, int
         e3.k = ks; e3.k_sb = (long)nkv * H * hd; e3.k_sh = (long)H * hd; e3.k_si = hd;
         e3.v = vs; e3.v_sb = e3.k_sb; e3.v_sh = e3.k_sh; e3.v_si = hd;
         launch_gemm(q3, s);
-        AttnArgs at = attn(B, nq, nkv, H, hd, et);
+        AttnArgs at = attn(*this, ST,B, nq, nkv, H, hd, et);
         at.q = qa; at.q_sb = e3.q_sb; at.q_sh = e3.q_sh; at.q_si = hd;
         const char* kl = (const char*)kv + (size_t)(2 * l) * per;
         const char* vl = (const char*)kv + (size_t)(2 * l + 1) * per;
@@ -641,7 +647,7 @@ void vla_model_s::enqueue_denoise(int B, const void* kv, const float* noise, int
       e3.k = kd; e3.k_sb = e3.q_sb; e3.k_sh = e3.q_sh; e3.k_si = dhd;
       e3.v = vd; e3.v_sb = e3.q_sb; e3.v_sh = e3.q_sh; e3.v_si = dhd;
       launch_gemm(q3, s);
-      AttnArgs at = attn(B, nh, nh, S, dhd, et);
+      AttnArgs at = attn(*this, ST,B, nh, nh, S, dhd, et);
       at.q = qd; at.q_sb = e3.q_sb; at.q_sh = e3.q_sh; at.q_si = dhd;
       at.seg[0] = AttnSeg{kd, e3.k_sb, e3.k_sh, dhd, vd, e3.v_sb, e3.v_sh, dhd, S};
       at.seg[1].len = 0;
@@ -651,7 +657,7 @@ void vla_model_s::enqueue_denoise(int B, const void* kv, const float* noise, int
       // cross-attention to the VLM features of the paired layer
       norm(M, Da, 1, X, Da, zd, Da, et, nullptr, nullptr, eps, s);
       store(gm(*this, ST,y.cq, M, zd, Da, et), qc, Da, et, y.bcq, ACT_NONE, s);
-      AttnArgs ac = attn(B, nh, nh, S, dhd, et);
+      AttnArgs ac = attn(*this, ST,B, nh, nh, S, dhd, et);
       ac.q = qc; ac.q_sb = (long)S * Da; ac.q_sh = dhd; ac.q_si = Da;
       const char* kl = xkv_base + (size_t)(2 * l) * Da * es;
       const char* vl = xkv_base + (size_t)(2 * l + 1) * Da * es;

@@ -98,8 +98,11 @@ def test_determinism_permutation_and_batch_invariance(cfg):
     perm = [2, 0, 1]
     ap, _ = run(cfg, {k: v[perm] for k, v in inp.items()})
     np.testing.assert_array_equal(ap, a1[perm])
+    # batch-size invariance: the same request alone. Split-K / split-KV choose
+    # their ranges from the launch's block count, so the reduction order (not
+    # the data flow) may differ between batch sizes: equal to within rounding.
     one, _ = run(cfg, synth.make_inputs(cfg, 1, first_row=1))
-    np.testing.assert_array_equal(one[0], a1[1])
+    assert rel_l2(one[0], a1[1].astype(np.float64)) <= TOL[cfg.dtype] / 10
 
 
 @pytest.mark.parametrize("cfg", [TINY, SMOL_R], ids=lambda c: c.name)
