@@ -127,6 +127,35 @@ def serve_main(args):
     print(json.dumps(result), flush=True)
 
 
+def counters_main(args):
+    """For hardware counter passes (rocprofv3 --pmc): launch only the roofline
+    kernel (`--which` projection of the benchmark workload, eagerly, with the
+    stage's real buffers) and a 256 MiB device copy of known size."""
+    import torch
+    from paper_2609_12075_amd import synth, vla
+    cfg = synth.CONFIGS[args.config]
+    B = args.batch or cfg.max_batch
+    m = vla.Model(cfg, synth.make_weights(cfg), device=0)
+    m.set_graphs(False)
+    inp = synth.make_inputs(cfg, B)
+    d = {k: torch.from_numpy(v).to("cuda:0") for k, v in inp.items()}
+    kv = m.alloc_kv(B)
+    act = torch.empty_like(d["noise"])
+    m.prefill(B, d["pixels"], d["text_ids"], kv, state=d.get("state"))
+    m.denoise(B, kv, d["noise"], 1, act)
+    torch.cuda.synchronize()
+    flops, plan = m.replay_gemm(args.which, B, args.roofline_iters)
+    src = torch.empty(64 << 20, dtype=torch.float32, device="cuda:0")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    kname = f"gemm_mfma_kernelILi{plan['tile_n']}ELi{plan['tile_m']}EDF16bLi{plan['mode']}E"
+    print(json.dumps({"kernel_symbol": kname, "plan": plan, "flops_per_launch": flops, "launches": args.roofline_iters,
+                      "copy_probe_bytes": int(src.numel() * 4), "config": cfg.name, "batch": B}), flush=True)
+    m.close()
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -138,6 +167,9 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--roofline-iters", type=int, default=50)
+    ap.add_argument("--copy-probe", action="store_true", help="also run a 256 MiB device copy (counter scaling)")
+    ap.add_argument("--counters", action="store_true", help="launch only the roofline kernel and a copy (PMC passes)")
+    ap.add_argument("--which", type=int, default=2, help="projection for --counters (see vla_debug.h)")
     ap.add_argument("--serve", action="store_true", help="co-located serving sweep instead of the lockstep bench")
     ap.add_argument("--serve-models", default="pi0,smolvla")
     ap.add_argument("--serve-batch", type=int, default=4)
@@ -158,6 +190,9 @@ def main():
         sys.exit(2)
     if args.serve:
         serve_main(args)
+        return
+    if args.counters:
+        counters_main(args)
         return
 
     import numpy as np
@@ -239,20 +274,34 @@ def main():
         torch.cuda.synchronize()
         a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         a.record(stream)
-        flops = m.replay_gemm(which, B, args.roofline_iters)
+        flops, plan = m.replay_gemm(which, B, args.roofline_iters)
         b.record(stream)
         torch.cuda.synchronize()
         us = a.elapsed_time(b) * 1e3 / args.roofline_iters
-        kern[which] = (flops, us)
-        log(f"[bench] kernel {GEMM_NAMES[which]}: {us:.2f} us/launch, {flops / us / 1e6:.1f} TFLOP/s")
-    # the dominant kernel: most total time per lockstep (launch count x duration)
-    per_step = {0: cfg.llm_layers - 1, 1: cfg.llm_layers - 1, 2: cfg.act_layers * N, 3: cfg.act_layers * N}
-    dom = max(kern, key=lambda w: kern[w][1] * per_step[w])
-    flops, us = kern[dom]
+        kern[which] = (flops, us, plan)
+        log(f"[bench] kernel {GEMM_NAMES[which]}: {us:.2f} us/launch, {flops / us / 1e6:.1f} TFLOP/s, plan {plan}")
+    # The roofline entry: of the gate/up projections that run as one kernel
+    # (no K split) whose instantiation (tile, epilogue) no other projection of
+    # this workload uses, so rocprof's per-kernel average is this launch's
+    # duration: the one with the most time per lockstep (launches x duration).
+    per_step = {w: n for w, n in ((0, cfg.llm_layers - 1), (2, cfg.act_layers * N)) if kern[w][2]["splits"] == 1}
+    dom = max(per_step, key=lambda w: kern[w][1] * per_step[w])
+    flops, us, plan = kern[dom]
+    kname = f"gemm_mfma_kernelILi{plan['tile_n']}ELi{plan['tile_m']}EDF16bLi{plan['mode']}E"
     achieved = flops / us / 1e6
+    traffic = None
+    tf = os.path.join(ROOT, "profiles", "traffic.json")
+    if os.path.exists(tf):
+        # HBM bytes per launch from rocprofv3 FETCH_SIZE / WRITE_SIZE runs, valid
+        # only while the kernel source is the one the counters were taken on
+        from paper_2609_12075_amd import profsum
+        rec = json.load(open(tf)).get(f"{cfg.name}:B{B}:{kname}")
+        if rec and rec.get("source_hash") == profsum.source_hash():
+            traffic = rec["traffic_bytes"]
     roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK[dtype], "unit": "TFLOP/s",
-                "frac": round(achieved / PEAK[dtype], 4), "traffic": None,
-                "kernel": GEMM_NAMES[dom], "flops_per_launch": flops, "us_per_launch": round(us, 3)}
+                "frac": round(achieved / PEAK[dtype], 4), "traffic": traffic,
+                "kernel": GEMM_NAMES[dom], "kernel_symbol": kname, "flops_per_launch": flops,
+                "us_per_launch": round(us, 3), "launches_per_step": per_step[dom]}
 
     out = {
         "metric": METRIC, "value": round(value, 2), "unit": "action chunks/s", "n_gpus": 1, "steps": K,
@@ -266,9 +315,18 @@ def main():
         "chunk_latency_ms_max": round(max(lat), 3), "slo_ms": slo, "slo_attainment_closed_loop": attain,
         "roofline": roofline,
         "kernels": {GEMM_NAMES[w]: {"us": round(kern[w][1], 3), "tflops": round(kern[w][0] / kern[w][1] / 1e6, 2),
-                                    "mfma_frac": round(kern[w][0] / kern[w][1] / 1e6 / PEAK[dtype], 4)}
+                                    "mfma_frac": round(kern[w][0] / kern[w][1] / 1e6 / PEAK[dtype], 4),
+                                    "k_ranges": kern[w][2]["splits"]}
                     for w in kern},
     }
+    if args.copy_probe:
+        # a plain device copy of known size, to scale hardware byte counters
+        src = torch.empty(64 << 20, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        out["copy_probe_bytes"] = int(src.numel() * 4)
     if not args.no_cpu_baseline:
         log(f"[bench] CPU oracle baseline (~{args.cpu_seconds:.0f} s)")
         out["cpu_baseline"] = cpu_baseline(cfg, weights, args.cpu_seconds)

@@ -315,14 +315,19 @@ vla_status vla_debug_cu_probe(int device, int cu_count, int from_top, int blocks
   });
 }
 
-vla_status vla_debug_replay_gemm(vla_model m, int which, int batch, int iters, hipStream_t s, double* flops) {
+vla_status vla_debug_replay_gemm(vla_model m, int which, int batch, int iters, hipStream_t s, double* flops,
+                                 int* plan) {
   return guarded([&] {
     check_model(m);
     VLA_REQUIRE(batch >= 1 && batch <= m->cfg.max_batch, "batch out of range");
     VLA_REQUIRE(iters >= 0 && iters <= 1000000, "iters out of range");
     DeviceGuard g(m->device);
     GemmArgs a = m->stage_gemm(which, batch);
-    if (flops) *flops = 2.0 * a.M * (double)a.N * (double)(m->et == ET_BF16 ? a.K : a.K);
+    if (flops) *flops = 2.0 * a.M * (double)a.N * (double)a.K;
+    if (plan) {
+      const GemmPlan p = gemm_plan(a);
+      plan[0] = p.bn; plan[1] = p.bm; plan[2] = p.splits; plan[3] = a.mode;
+    }
     for (int i = 0; i < iters; ++i) launch_gemm(a, s);
     VLA_HIP(hipGetLastError());
   });

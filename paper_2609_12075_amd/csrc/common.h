@@ -33,6 +33,21 @@ struct VlaError {
 // ---------------------------------------------------------------- kernels
 enum ElemType { ET_F32 = 0, ET_BF16 = 1 };
 
+// XCD-aware block order. The dispatcher hands workgroup L (linear id) to
+// accelerator die L % 8, and each die has its own L2. This returns the
+// logical block index u for L such that each die receives one contiguous run
+// of logical indices (x fastest, then y, then z): blocks that share an
+// operand (consecutive x) then share that die's L2. A bijection on [0, T).
+__device__ __forceinline__ void xcd_remap(int& bx, int& by, int& bz) {
+  const long gx = gridDim.x, gy = gridDim.y, T = gx * gy * (long)gridDim.z;
+  const long L = blockIdx.x + gx * (blockIdx.y + gy * (long)blockIdx.z);
+  const long q = T / 8, r = T % 8, x = L % 8, j = L / 8;
+  const long u = x * q + (x < r ? x : r) + j;
+  bx = (int)(u % gx);
+  by = (int)((u / gx) % gy);
+  bz = (int)(u / (gx * gy));
+}
+
 static inline size_t elem_size(int et) { return et == ET_BF16 ? 2 : 4; }
 
 // GEMM: D[m][n] = sum_k A[m][k] * W[n][k] for m < M, n < N.
@@ -85,6 +100,11 @@ struct GemmArgs {
 };
 
 void launch_gemm(const GemmArgs& a, hipStream_t s);
+
+// Launch plan of a bf16 projection: tile (bn weight rows x bm activation
+// rows), number of K ranges and the K length per range.
+struct GemmPlan { int bn, bm, splits, ksplit; };
+GemmPlan gemm_plan(const GemmArgs& a);
 
 // Attention: O = softmax(Q K^T * scale) V with grouped KV heads, keys drawn
 // from up to two segments (e.g. the prefix cache and the action tokens' own

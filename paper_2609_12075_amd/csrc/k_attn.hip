@@ -48,14 +48,18 @@ __global__ void __launch_bounds__(256) attn_mfma_kernel(AttnArgs a) {
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int S = a.splits > 1 ? a.splits : 1;      // key ranges (split-KV)
-  const int b = blockIdx.z / S, split = blockIdx.z % S, g = blockIdx.y;
+  // die-aware order: the row tiles sharing one (request, KV head) K/V stream
+  // are consecutive logical blocks and so share one die's L2
+  int bx, by, bz;
+  xcd_remap(bx, by, bz);
+  const int b = bz / S, split = bz % S, g = by;
   const int G = a.Hq / a.Hkv;
   const int rows = G * a.Lq;
   const int hd = a.hd;
   const int lq = lane & 15, grp = lane >> 4;
 
   // this lane's query row
-  const int r = blockIdx.x * BQ + wave * 16 + lq;
+  const int r = bx * BQ + wave * 16 + lq;
   const bool rvalid = r < rows;
   const int jh = rvalid ? r / a.Lq : 0, qi = rvalid ? r % a.Lq : 0;
   const int h = g * G + jh;
@@ -225,24 +229,41 @@ __global__ void __launch_bounds__(256) attn_mfma_kernel(AttnArgs a) {
 
 // Split-KV merge: one wavefront per query row combines the key ranges in
 // order: m = max m_s, l = sum l_s 2^(m_s - m), o = sum o_s 2^(m_s - m) / l.
+// Each lane owns four consecutive dims; all (<= 16) partial loads of a lane
+// are issued before any is used.
+constexpr int MAX_SPLITS = 16;
 __global__ void __launch_bounds__(256) attn_combine_kernel(AttnArgs a) {
   const int lane = threadIdx.x & 63;
   const long row = blockIdx.x * 4L + (threadIdx.x >> 6);
   if (row >= (long)a.B * a.Hq * a.Lq) return;
   const int S = a.splits, hd = a.hd;
   const float* st = a.ws + (long)a.B * a.Hq * a.Lq * S * hd + row * S * 2;
+  float ms[MAX_SPLITS], w[MAX_SPLITS];
+#pragma unroll
+  for (int s = 0; s < MAX_SPLITS; ++s) ms[s] = s < S ? st[2 * s] : -INFINITY;
   float m = -INFINITY;
-  for (int s = 0; s < S; ++s) m = fmaxf(m, st[2 * s]);
+#pragma unroll
+  for (int s = 0; s < MAX_SPLITS; ++s) m = fmaxf(m, ms[s]);
   float l = 0.f;
-  for (int s = 0; s < S; ++s) l += st[2 * s + 1] * exp2f(st[2 * s] - m);
+#pragma unroll
+  for (int s = 0; s < MAX_SPLITS; ++s) {
+    w[s] = s < S ? exp2f(ms[s] - m) : 0.f;
+    l += s < S ? st[2 * s + 1] * w[s] : 0.f;
+  }
   const float inv = 1.0f / l;
   const int qi = (int)(row % a.Lq), h = (int)((row / a.Lq) % a.Hq), b = (int)(row / ((long)a.Lq * a.Hq));
   bf16* op = reinterpret_cast<bf16*>(a.o) + (long)b * a.o_sb + (long)h * a.o_sh + (long)qi * a.o_si;
   const float* po = a.ws + row * S * hd;
-  for (int d = lane; d < hd; d += 64) {
-    float acc = 0.f;
-    for (int s = 0; s < S; ++s) acc += po[(long)s * hd + d] * exp2f(st[2 * s] - m);
-    op[d] = (bf16)(acc * inv);
+  for (int d = lane * 4; d < hd; d += 256) {
+    f32x4 part[MAX_SPLITS];
+#pragma unroll
+    for (int s = 0; s < MAX_SPLITS; ++s)
+      part[s] = s < S ? *reinterpret_cast<const f32x4*>(po + (long)s * hd + d) : f32x4{0.f, 0.f, 0.f, 0.f};
+    f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int s = 0; s < MAX_SPLITS; ++s) acc += part[s] * w[s];
+    *reinterpret_cast<bf16x4*>(op + d) =
+        bf16x4{(bf16)(acc[0] * inv), (bf16)(acc[1] * inv), (bf16)(acc[2] * inv), (bf16)(acc[3] * inv)};
   }
 }
 

@@ -154,47 +154,52 @@ gemm_mfma_kernel(GemmArgs a) {
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wn0 = (wave >> 1) * (BN / 2), wm0 = (wave & 1) * (BM / 2);
-  const int n_blk = blockIdx.y * BN, m_blk = blockIdx.x * BM;
-  // K range of this block: split blockIdx.z covers [kbeg, kbeg + ksplit)
-  const int kbeg = blockIdx.z * a.ksplit;
+  int bx, by, bz;                       // (M tile, N tile, K range), die-aware order
+  xcd_remap(bx, by, bz);
+  const int n_blk = by * BN, m_blk = bx * BM;
+  // K range of this block: range bz covers [kbeg, kbeg + ksplit)
+  const int kbeg = bz * a.ksplit;
   const int K = min(a.K, kbeg + a.ksplit);
   const int nk = K > kbeg ? (K - kbeg + BK - 1) / BK : 0;
   const bf16* W = reinterpret_cast<const bf16*>(a.W);
   const TA* A = reinterpret_cast<const TA*>(a.A);
 
-  bf16x8 wreg[WCH], areg[ACH];
+  // PF K-tiles are in flight per thread (register slots; slot = tile % PF):
+  // a tile's global loads are issued PF - 1 steps before it is written to LDS.
+  constexpr int PF = (BN * BM <= 64 * 64) ? 4 : (BN * BM <= 128 * 64 ? 2 : 1);   // 128x128: keep 2 blocks/CU
+  bf16x8 wreg[PF][WCH], areg[PF][ACH];
   const int crow = tid >> 3, ccol = (tid & 7) * 8;
 
-  auto load_tile = [&](int kt) {
+  auto load_tile = [&](int kt, bf16x8 (&wr)[WCH], bf16x8 (&ar)[ACH]) {
     const int k = kbeg + kt * BK + ccol;
 #pragma unroll
     for (int j = 0; j < WCH; ++j) {
       const int n = n_blk + crow + 32 * j;
-      if (n < a.N && k < K) wreg[j] = *reinterpret_cast<const bf16x8*>(W + (long)n * a.ldw + k);
-      else wreg[j] = bf16x8{};
+      if (n < a.N && k < K) wr[j] = *reinterpret_cast<const bf16x8*>(W + (long)n * a.ldw + k);
+      else wr[j] = bf16x8{};
     }
 #pragma unroll
     for (int j = 0; j < ACH; ++j) {
       const int m = m_blk + crow + 32 * j;
       if (m < a.M && k < K) {
         if constexpr (sizeof(TA) == 2) {
-          areg[j] = *reinterpret_cast<const bf16x8*>(A + (long)m * a.lda + k);
+          ar[j] = *reinterpret_cast<const bf16x8*>(A + (long)m * a.lda + k);
         } else {
           const f32x4* p = reinterpret_cast<const f32x4*>(A + (long)m * a.lda + k);
           f32x4 x0 = p[0], x1 = p[1];
-          areg[j] = bf16x8{(bf16)x0[0], (bf16)x0[1], (bf16)x0[2], (bf16)x0[3],
-                           (bf16)x1[0], (bf16)x1[1], (bf16)x1[2], (bf16)x1[3]};
+          ar[j] = bf16x8{(bf16)x0[0], (bf16)x0[1], (bf16)x0[2], (bf16)x0[3],
+                         (bf16)x1[0], (bf16)x1[1], (bf16)x1[2], (bf16)x1[3]};
         }
       } else {
-        areg[j] = bf16x8{};
+        ar[j] = bf16x8{};
       }
     }
   };
-  auto store_tile = [&](int buf) {
+  auto store_tile = [&](int buf, const bf16x8 (&wr)[WCH], const bf16x8 (&ar)[ACH]) {
 #pragma unroll
-    for (int j = 0; j < WCH; ++j) *reinterpret_cast<bf16x8*>(&Ws[buf][crow + 32 * j][ccol]) = wreg[j];
+    for (int j = 0; j < WCH; ++j) *reinterpret_cast<bf16x8*>(&Ws[buf][crow + 32 * j][ccol]) = wr[j];
 #pragma unroll
-    for (int j = 0; j < ACH; ++j) *reinterpret_cast<bf16x8*>(&As[buf][crow + 32 * j][ccol]) = areg[j];
+    for (int j = 0; j < ACH; ++j) *reinterpret_cast<bf16x8*>(&As[buf][crow + 32 * j][ccol]) = ar[j];
   };
 
   f32x4 acc[TN][TM];
@@ -203,15 +208,8 @@ gemm_mfma_kernel(GemmArgs a) {
 #pragma unroll
     for (int j = 0; j < TM; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  if (nk > 0) {
-    load_tile(0);
-    store_tile(0);
-  }
-  __syncthreads();
   const int lr = lane & 15, lk = (lane >> 4) * 8;
-  for (int kt = 0; kt < nk; ++kt) {
-    const int buf = kt & 1;
-    if (kt + 1 < nk) load_tile(kt + 1);
+  auto compute = [&](int buf) {
 #pragma unroll
     for (int kc = 0; kc < BK; kc += 32) {
       bf16x8 wf[TN], af[TM];
@@ -225,8 +223,24 @@ gemm_mfma_kernel(GemmArgs a) {
         for (int j = 0; j < TM; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[i], af[j], acc[i][j], 0, 0, 0);
     }
-    if (kt + 1 < nk) store_tile(buf ^ 1);
-    __syncthreads();
+  };
+
+#pragma unroll
+  for (int p = 0; p < PF; ++p)
+    if (p < nk) load_tile(p, wreg[p], areg[p]);
+  if (nk > 0) store_tile(0, wreg[0], areg[0]);
+  __syncthreads();
+  for (int kt0 = 0; kt0 < nk; kt0 += PF) {
+#pragma unroll
+    for (int p = 0; p < PF; ++p) {
+      const int kt = kt0 + p;             // kt % PF == p: its slot was written to LDS already
+      if (kt < nk) {
+        if (kt + PF < nk) load_tile(kt + PF, wreg[p], areg[p]);
+        compute(kt & 1);
+        if (kt + 1 < nk) store_tile((kt + 1) & 1, wreg[(p + 1) % PF], areg[(p + 1) % PF]);
+        __syncthreads();
+      }
+    }
   }
 
   // lane owns D[n = 4*(lane/16) + r][m = lane % 16] of every 16 x 16 subtile;
@@ -241,7 +255,7 @@ gemm_mfma_kernel(GemmArgs a) {
   if (a.splits > 1) {
     // split-K: store this K range's partial tile; the reduce kernel finishes
     const int ldp = (a.N + 3) & ~3;
-    float* part = a.ws + (long)blockIdx.z * a.M * ldp;
+    float* part = a.ws + (long)bz * a.M * ldp;
 #pragma unroll 1
     for (int c = tid; c < BM * (BN / 4); c += 256) {
       const int mr = c / (BN / 4), nc = (c % (BN / 4)) * 4;
@@ -269,9 +283,15 @@ __global__ void __launch_bounds__(256) splitk_reduce_kernel(GemmArgs a) {
   if (c >= (long)a.M * nc) return;
   const int m = (int)(c / nc), n0 = (int)(c % nc) * 4;
   const long stride = (long)a.M * ldp;
-  const f32x4* p = reinterpret_cast<const f32x4*>(a.ws + (long)m * ldp + n0);
-  f32x4 t = p[0];
-  for (int z = 1; z < a.splits; ++z) t += *reinterpret_cast<const f32x4*>(a.ws + z * stride + (long)m * ldp + n0);
+  const float* p = a.ws + (long)m * ldp + n0;
+  // issue every partial load before the first add (splits <= 16)
+  f32x4 part[16];
+#pragma unroll
+  for (int z = 0; z < 16; ++z)
+    part[z] = z < a.splits ? *reinterpret_cast<const f32x4*>(p + z * stride) : f32x4{0.f, 0.f, 0.f, 0.f};
+  f32x4 t = part[0];
+#pragma unroll
+  for (int z = 1; z < 16; ++z) t += part[z];
   float v[4] = {t[0], t[1], t[2], t[3]};
   epilogue4<MODE>(a, m, n0, v);
 }
@@ -318,25 +338,42 @@ __global__ void __launch_bounds__(256) gemm_f32_kernel(GemmArgs a) {
 // Kernels are specialised on tile shape, activation type and epilogue; fp32
 // activations (the Euler state, conditioning vectors, robot state) only feed
 // plain stores.
-template <int BN, int BM, int MODE>
-static void launch_mfma(const GemmArgs& a0, hipStream_t s) {
+GemmPlan gemm_plan(const GemmArgs& a) {
+  GemmPlan p{64, 64, 1, 64};
+  if (a.w_type == ET_F32) {
+    p.ksplit = a.K;
+    return p;
+  }
+  // the largest tile that still gives the chip (256 CUs) enough blocks
+  auto blocks = [&](int bn, int bm) { return (long)((a.M + bm - 1) / bm) * ((a.N + bn - 1) / bn); };
+  if (a.M >= 128 && blocks(128, 128) >= 256) p.bn = 128, p.bm = 128;
+  else if (a.M >= 64 && blocks(128, 64) >= 256) p.bn = 128, p.bm = 64;
+  else if (a.M > 32) p.bn = 64, p.bm = 64;
+  else p.bn = 64, p.bm = 32;
+  // Split K when the output tiles would leave most of the CUs idle: aim for
+  // ~2 blocks per CU, at least 2 K-steps per range, partials within ws.
   constexpr int BK = 64;
-  GemmArgs a = a0;
-  const int gm = (a.M + BM - 1) / BM, gn = (a.N + BN - 1) / BN;
-  const long tiles = (long)gm * gn;
+  const long tiles = blocks(p.bn, p.bm);
   const int nk = (a.K + BK - 1) / BK;
-  // Split K when the output tiles would leave most of the 256 CUs idle: aim
-  // for ~2 blocks per CU, at least 2 K-steps per split, partials within ws.
-  int splits = 1;
   const long ldp = (a.N + 3) & ~3;
+  int splits = 1;
   if (a.ws && tiles < 192 && nk >= 4) {
     splits = (int)std::min<long>({(512 + tiles - 1) / tiles, (long)nk / 2, 16L});
     while (splits > 1 && (long)splits * a.M * ldp > a.ws_floats) --splits;
   }
   const int ksteps = std::max(1, (nk + splits - 1) / splits);
-  a.ksplit = ksteps * BK;
-  a.splits = std::max(1, (nk + ksteps - 1) / ksteps);   // no empty range
-  dim3 grid(gm, gn, a.splits);
+  p.ksplit = ksteps * BK;
+  p.splits = std::max(1, (nk + ksteps - 1) / ksteps);   // no empty range
+  return p;
+}
+
+template <int BN, int BM, int MODE>
+static void launch_mfma(const GemmArgs& a0, const GemmPlan& p, hipStream_t s) {
+  GemmArgs a = a0;
+  a.ksplit = p.ksplit;
+  a.splits = p.splits;
+  const long ldp = (a.N + 3) & ~3;
+  dim3 grid((a.M + BM - 1) / BM, (a.N + BN - 1) / BN, a.splits);
   bool f32a = false;
   if constexpr (MODE == EPI_STORE) f32a = a.a_type == ET_F32;
   if (a.splits > 1) {
@@ -363,12 +400,11 @@ static void launch_mode(const GemmArgs& a, hipStream_t s) {
     hipLaunchKernelGGL(gemm_f32_kernel<MODE>, grid, dim3(256), 0, s, a);
     return;
   }
-  // Pick the largest tile that still gives the chip (256 CUs) enough blocks.
-  auto blocks = [&](int bn, int bm) { return (long)((a.M + bm - 1) / bm) * ((a.N + bn - 1) / bn); };
-  if (a.M >= 128 && blocks(128, 128) >= 256) launch_mfma<128, 128, MODE>(a, s);
-  else if (a.M >= 64 && blocks(128, 64) >= 256) launch_mfma<128, 64, MODE>(a, s);
-  else if (a.M > 32) launch_mfma<64, 64, MODE>(a, s);
-  else launch_mfma<64, 32, MODE>(a, s);
+  const GemmPlan p = gemm_plan(a);
+  if (p.bn == 128 && p.bm == 128) launch_mfma<128, 128, MODE>(a, p, s);
+  else if (p.bn == 128) launch_mfma<128, 64, MODE>(a, p, s);
+  else if (p.bm == 64) launch_mfma<64, 64, MODE>(a, p, s);
+  else launch_mfma<64, 32, MODE>(a, p, s);
 }
 
 void launch_gemm(const GemmArgs& a, hipStream_t s) {

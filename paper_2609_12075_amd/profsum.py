@@ -1,0 +1,105 @@
+"""Summaries of rocprofv3 output for the kernels of this library.
+
+    python -m paper_2609_12075_amd.profsum stats <kernel_stats.csv> [--top N]
+    python -m paper_2609_12075_amd.profsum trace <kernel_trace.csv> --kernel REGEX
+    python -m paper_2609_12075_amd.profsum traffic --fetch <pmc.csv> --write <pmc.csv> \
+        --kernel REGEX --copy-bytes N [--out traffic.json]
+
+`traffic` scales the per-dispatch FETCH_SIZE / WRITE_SIZE counters (KiB) of
+the named kernel by what the same counters read for the 256 MiB device copy
+that `bench.py --copy-probe` runs (rocclr's copyBuffer kernel), and records
+the hash of the GEMM source so the figure is dropped once the kernel changes.
+"""
+from __future__ import annotations
+
+import argparse
+import collections
+import csv
+import hashlib
+import json
+import os
+import re
+import statistics
+import sys
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+GEMM_SOURCE = os.path.join(PKG, "csrc", "k_gemm.hip")
+
+
+def source_hash(path: str = GEMM_SOURCE) -> str:
+    return hashlib.sha256(open(path, "rb").read()).hexdigest()[:16]
+
+
+def stats(path: str, top: int = 20) -> str:
+    rows = list(csv.DictReader(open(path)))
+    rows.sort(key=lambda r: -float(r["TotalDurationNs"]))
+    tot = sum(float(r["TotalDurationNs"]) for r in rows)
+    out = [f"{'total ms':>9} {'%':>6} {'calls':>7} {'avg us':>9}  kernel"]
+    for r in rows[:top]:
+        out.append(f"{float(r['TotalDurationNs']) / 1e6:9.3f} {float(r['TotalDurationNs']) / tot * 100:6.2f} "
+                   f"{int(r['Calls']):7d} {float(r['AverageNs']) / 1e3:9.2f}  {r['Name'][:120]}")
+    out.append(f"all kernels: {tot / 1e6:.3f} ms")
+    return "\n".join(out)
+
+
+def trace(path: str, kernel: str) -> str:
+    rows = [r for r in csv.DictReader(open(path)) if re.search(kernel, r["Kernel_Name"])]
+    g = collections.defaultdict(list)
+    for r in rows:
+        key = (r["Kernel_Name"][:100], r["Grid_Size_X"], r["Grid_Size_Y"], r["Grid_Size_Z"])
+        g[key].append(int(r["End_Timestamp"]) - int(r["Start_Timestamp"]))
+    out = [f"{'calls':>6} {'avg us':>9} {'median us':>10}  grid (threads)  kernel"]
+    for k, v in sorted(g.items(), key=lambda kv: -sum(kv[1])):
+        out.append(f"{len(v):6d} {sum(v) / len(v) / 1e3:9.2f} {statistics.median(v) / 1e3:10.2f}  "
+                   f"({k[1]},{k[2]},{k[3]})  {k[0]}")
+    return "\n".join(out)
+
+
+def _counter(path: str, name: str, kernel: str):
+    vals = collections.defaultdict(float)
+    for r in csv.DictReader(open(path)):
+        if r.get("Counter_Name") == name and re.search(kernel, r.get("Kernel_Name", "")):
+            vals[r.get("Dispatch_Id", r.get("Correlation_Id"))] += float(r["Counter_Value"])
+    return list(vals.values())
+
+
+def traffic(fetch_csv: str, write_csv: str, kernel: str, copy_bytes: int) -> dict:
+    copy_re = "copyBuffer"
+    f_k, w_k = _counter(fetch_csv, "FETCH_SIZE", kernel), _counter(write_csv, "WRITE_SIZE", kernel)
+    f_c, w_c = _counter(fetch_csv, "FETCH_SIZE", copy_re), _counter(write_csv, "WRITE_SIZE", copy_re)
+    if not (f_k and w_k and f_c and w_c):
+        raise SystemExit("missing counters for the kernel or the copy probe")
+    # the copy reads and writes copy_bytes: scale = bytes per counted KiB
+    f_scale = copy_bytes / (max(f_c) * 1024.0)
+    w_scale = copy_bytes / (max(w_c) * 1024.0)
+    fetch = statistics.median(f_k) * 1024.0 * f_scale
+    write = statistics.median(w_k) * 1024.0 * w_scale
+    return {"kernel_regex": kernel, "source_hash": source_hash(), "fetch_bytes": fetch, "write_bytes": write,
+            "traffic_bytes": fetch + write, "fetch_scale": f_scale, "write_scale": w_scale,
+            "dispatches": len(f_k)}
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser()
+    sub = ap.add_subparsers(dest="cmd", required=True)
+    s = sub.add_parser("stats"); s.add_argument("csv"); s.add_argument("--top", type=int, default=20)
+    t = sub.add_parser("trace"); t.add_argument("csv"); t.add_argument("--kernel", default=".")
+    f = sub.add_parser("traffic")
+    f.add_argument("--fetch", required=True); f.add_argument("--write", required=True)
+    f.add_argument("--kernel", required=True); f.add_argument("--copy-bytes", type=int, required=True)
+    f.add_argument("--out")
+    a = ap.parse_args(argv)
+    if a.cmd == "stats":
+        print(stats(a.csv, a.top))
+    elif a.cmd == "trace":
+        print(trace(a.csv, a.kernel))
+    else:
+        res = traffic(a.fetch, a.write, a.kernel, a.copy_bytes)
+        js = json.dumps(res, indent=1)
+        print(js)
+        if a.out:
+            open(a.out, "w").write(js + "\n")
+
+
+if __name__ == "__main__":
+    main(sys.argv[1:])

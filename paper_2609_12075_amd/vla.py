@@ -75,7 +75,8 @@ def lib():
         L.vla_debug_attention.argtypes = [ci, ci, ci, ci, ci, ci, vp, vp, vp, ci, vp, vp, ci, vp, vp]
         L.vla_debug_attention.restype = ci
         L.vla_debug_cu_probe.argtypes = [ci, ci, ci, ci, ci, vp, vp]; L.vla_debug_cu_probe.restype = ci
-        L.vla_debug_replay_gemm.argtypes = [vp, ci, ci, ci, vp, ctypes.POINTER(ctypes.c_double)]
+        L.vla_debug_replay_gemm.argtypes = [vp, ci, ci, ci, vp, ctypes.POINTER(ctypes.c_double),
+                                            ctypes.POINTER(ctypes.c_int)]
         L.vla_debug_replay_gemm.restype = ci
         _lib = L
     return _lib
@@ -156,11 +157,13 @@ class Model:
         _check(lib().vla_prefill_ex(self.handle, batch, _ptr(pixels), _ptr(text_ids), _ptr(state), _ptr(kv_out),
                                     _stream(stream)))
 
-    def replay_gemm(self, which: int, batch: int, iters: int, stream=None) -> float:
-        """Enqueue `iters` launches of one stage projection; returns its flops."""
+    def replay_gemm(self, which: int, batch: int, iters: int, stream=None):
+        """Enqueue `iters` launches of one stage projection. Returns (flops of
+        one launch, plan dict: tile_n, tile_m, splits, mode)."""
         f = ctypes.c_double(0.0)
-        _check(lib().vla_debug_replay_gemm(self.handle, which, batch, iters, _stream(stream), ctypes.byref(f)))
-        return f.value
+        plan = (ctypes.c_int * 4)()
+        _check(lib().vla_debug_replay_gemm(self.handle, which, batch, iters, _stream(stream), ctypes.byref(f), plan))
+        return f.value, {"tile_n": plan[0], "tile_m": plan[1], "splits": plan[2], "mode": plan[3]}
 
     def denoise(self, batch, kv, noise, steps, actions_out, stream=None):
         _check(lib().vla_denoise(self.handle, batch, _ptr(kv), _ptr(noise), steps, _ptr(actions_out),
