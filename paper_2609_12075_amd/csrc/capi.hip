@@ -116,6 +116,7 @@ float* debug_ws(int kind, long floats) {
   if (it != ws.end()) return it->second;
   float* p = nullptr;
   VLA_HIP(hipMalloc(&p, (size_t)floats * 4));
+  VLA_HIP(hipMemset(p, 0, (size_t)floats * 4));   // zero (kind 2 is the operand zero buffer)
   ws[{dev, kind}] = p;
   return p;
 }
@@ -269,6 +270,7 @@ vla_status vla_debug_gemm(int M, int N, int K, const void* A, int lda, int a_typ
     g.M = M; g.N = N; g.K = K; g.A = A; g.lda = lda; g.a_type = a_type; g.W = Wt; g.ldw = ldw; g.w_type = w_type;
     g.mode = EPI_STORE; g.act = act; g.bias = bias; g.tab_period = 1; g.out = out; g.ldo = ldo; g.out_type = ET_F32;
     g.ws = debug_ws(0, vla_model_s::kSplitKFloats); g.ws_floats = vla_model_s::kSplitKFloats;
+    g.zeros = debug_ws(2, 64);
     launch_gemm(g, s);
     VLA_HIP(hipGetLastError());
   });

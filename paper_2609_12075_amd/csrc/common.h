@@ -97,13 +97,16 @@ struct GemmArgs {
   // inter-block synchronisation).
   float* ws; long ws_floats;
   int splits, ksplit;                             // set by launch_gemm
+  // >= 16 zero bytes in device memory: operand chunks outside [0,M)x[0,K) or
+  // [0,N)x[0,K) are read from here (exact zero fill, no out-of-range reads)
+  const void* zeros;
 };
 
 void launch_gemm(const GemmArgs& a, hipStream_t s);
 
 // Launch plan of a bf16 projection: tile (bn weight rows x bm activation
 // rows), number of K ranges and the K length per range.
-struct GemmPlan { int bn, bm, splits, ksplit; };
+struct GemmPlan { int bn, bm, splits, ksplit, kind; };   // kind 0: register-pipelined, 1: multi-stage
 GemmPlan gemm_plan(const GemmArgs& a);
 
 // Attention: O = softmax(Q K^T * scale) V with grouped KV heads, keys drawn

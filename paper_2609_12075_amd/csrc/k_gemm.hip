@@ -296,6 +296,121 @@ __global__ void __launch_bounds__(256) splitk_reduce_kernel(GemmArgs a) {
   epilogue4<MODE>(a, m, n0, v);
 }
 
+// ---------------------------------------------------------------- multi-stage kernel
+// For products with many activation rows (the VLM stage; the action stage at
+// larger batches). Operand tiles move global -> LDS with the CDNA4 direct
+// loads (global_load_lds_dwordx4: each lane's 16 bytes land at LDS base +
+// 16 * lane, one wave writes 1 KiB contiguous) through STAGES buffers, so
+// STAGES - 1 K-steps of loads are in flight without holding registers.
+// LDS rows are 64 bf16 (128 bytes) without padding; the 16-byte chunk c of
+// row r is stored in slot c ^ ((r >> 1) & 7), which makes the matrix-core
+// fragment reads (16 rows, one chunk) conflict-free. Chunks outside the
+// operand (rows >= M or N, columns >= K) are read from a zero buffer, which
+// zero-fills K tails exactly. Block: 4 waves in a 2 x 2 grid, wave tile
+// (BN/2) x (BM/2) of 16 x 16 x 32 products.
+template <int BN, int BM, int STAGES, int MODE>
+__global__ void __launch_bounds__(256)
+gemm_stage_kernel(GemmArgs a) {
+  constexpr int BK = 64, ROWB = BK * 2;                 // bytes per LDS row
+  constexpr int TN = BN / 32, TM = BM / 32;
+  constexpr int STAGE_BYTES = (BN + BM) * ROWB;
+  constexpr int WG = BN / 8 / 4, AG = BM / 8 / 4;       // 8-row groups per wave (W, A)
+  constexpr int LOADS = WG + AG;                        // direct loads per thread per stage
+  constexpr int LDC = BN + 4;
+  constexpr int SMEM = STAGES * STAGE_BYTES > BM * LDC * 4 ? STAGES * STAGE_BYTES : BM * LDC * 4;
+  __shared__ __attribute__((aligned(1024))) char smem[SMEM];
+  auto Cs = reinterpret_cast<float (*)[LDC]>(smem);
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wn0 = (wave >> 1) * (BN / 2), wm0 = (wave & 1) * (BM / 2);
+  int bx, by, bz;
+  xcd_remap(bx, by, bz);
+  const int n_blk = by * BN, m_blk = bx * BM;
+  const int K = a.K, nk = (K + BK - 1) / BK;
+  const bf16* W = reinterpret_cast<const bf16*>(a.W);
+  const bf16* A = reinterpret_cast<const bf16*>(a.A);
+  const bf16* Z = reinterpret_cast<const bf16*>(a.zeros);
+
+  // this lane's row within an 8-row group and its LDS slot; the slot holds
+  // logical chunk (slot ^ swz(row)) of the row
+  const int lrow = lane >> 3, slot = lane & 7;
+  auto issue = [&](int kt, int buf) {
+    char* st = smem + buf * STAGE_BYTES;
+#pragma unroll
+    for (int j = 0; j < WG; ++j) {
+      const int grp = j * 4 + wave, r = grp * 8 + lrow;
+      const int c = slot ^ ((r >> 1) & 7), k = kt * BK + c * 8, n = n_blk + r;
+      const bf16* src = (n < a.N && k < K) ? W + (long)n * a.ldw + k : Z;
+      __builtin_amdgcn_global_load_lds(src, st + grp * 8 * ROWB, 16, 0, 0);
+    }
+#pragma unroll
+    for (int j = 0; j < AG; ++j) {
+      const int grp = j * 4 + wave, r = grp * 8 + lrow;
+      const int c = slot ^ ((r >> 1) & 7), k = kt * BK + c * 8, m = m_blk + r;
+      const bf16* src = (m < a.M && k < K) ? A + (long)m * a.lda + k : Z;
+      __builtin_amdgcn_global_load_lds(src, st + BN * ROWB + grp * 8 * ROWB, 16, 0, 0);
+    }
+  };
+
+  f32x4 acc[TN][TM];
+#pragma unroll
+  for (int i = 0; i < TN; ++i)
+#pragma unroll
+    for (int j = 0; j < TM; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  const int lr = lane & 15, lq = lane >> 4;
+#pragma unroll
+  for (int s = 0; s < STAGES - 1; ++s)
+    if (s < nk) issue(s, s);
+  for (int kt = 0; kt < nk; ++kt) {
+    // Stage kt has landed once at most the later stages' loads are pending;
+    // then a plain barrier (no fence, which would wait for every pending
+    // load): after it every wave's stage-kt data is in LDS and every wave has
+    // consumed stage kt-1 (its fragments fed the matrix instructions).
+    if (kt + STAGES - 2 < nk) {
+      asm volatile("s_waitcnt vmcnt(%0)\n\ts_waitcnt lgkmcnt(0)\n\ts_barrier" ::"n"((STAGES - 2) * LOADS) : "memory");
+    } else {
+      asm volatile("s_waitcnt vmcnt(0)\n\ts_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    }
+    if (kt + STAGES - 1 < nk) issue(kt + STAGES - 1, (kt + STAGES - 1) % STAGES);
+    const char* st = smem + (kt % STAGES) * STAGE_BYTES;
+#pragma unroll
+    for (int kc = 0; kc < 2; ++kc) {
+      bf16x8 wf[TN], af[TM];
+      const int c = kc * 4 + lq;
+#pragma unroll
+      for (int i = 0; i < TN; ++i) {
+        const int r = wn0 + 16 * i + lr;
+        wf[i] = *reinterpret_cast<const bf16x8*>(st + r * ROWB + ((c ^ ((r >> 1) & 7)) << 4));
+      }
+#pragma unroll
+      for (int j = 0; j < TM; ++j) {
+        const int r = wm0 + 16 * j + lr;
+        af[j] = *reinterpret_cast<const bf16x8*>(st + BN * ROWB + r * ROWB + ((c ^ ((r >> 1) & 7)) << 4));
+      }
+#pragma unroll
+      for (int i = 0; i < TN; ++i)
+#pragma unroll
+        for (int j = 0; j < TM; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[i], af[j], acc[i][j], 0, 0, 0);
+    }
+  }
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < TN; ++i)
+#pragma unroll
+    for (int j = 0; j < TM; ++j)
+      *reinterpret_cast<f32x4*>(&Cs[wm0 + 16 * j + lr][wn0 + 16 * i + (lane >> 4) * 4]) = acc[i][j];
+  __syncthreads();
+#pragma unroll 1
+  for (int c = tid; c < BM * (BN / 4); c += 256) {
+    const int mr = c / (BN / 4), nc = (c % (BN / 4)) * 4;
+    f32x4 t = *reinterpret_cast<const f32x4*>(&Cs[mr][nc]);
+    float v[4] = {t[0], t[1], t[2], t[3]};
+    epilogue4<MODE>(a, m_blk + mr, n_blk + nc, v);
+  }
+}
+
 // ---------------------------------------------------------------- fp32 VALU kernel
 // 64 x 64 tile, 256 threads, each thread 4 columns x 4 rows; K in steps of 16.
 template <int MODE>
@@ -339,13 +454,25 @@ __global__ void __launch_bounds__(256) gemm_f32_kernel(GemmArgs a) {
 // activations (the Euler state, conditioning vectors, robot state) only feed
 // plain stores.
 GemmPlan gemm_plan(const GemmArgs& a) {
-  GemmPlan p{64, 64, 1, 64};
+  GemmPlan p{64, 64, 1, 64, 0};
   if (a.w_type == ET_F32) {
     p.ksplit = a.K;
     return p;
   }
-  // the largest tile that still gives the chip (256 CUs) enough blocks
   auto blocks = [&](int bn, int bm) { return (long)((a.M + bm - 1) / bm) * ((a.N + bn - 1) / bn); };
+  // many activation rows: the LDS-staged kernel (two stages: 64 / 48 KiB, two
+  // blocks per CU, which measured faster than deeper pipelines at one block
+  // per CU), largest tile that still yields enough blocks for the 256 CUs
+  if (a.a_type == ET_BF16 && a.zeros) {
+    if (a.M >= 128 && blocks(128, 128) >= 256) { p.bn = 128; p.bm = 128; p.kind = 1; }
+    else if (a.M >= 64 && blocks(128, 64) >= 128) { p.bn = 128; p.bm = 64; p.kind = 1; }
+    if (p.kind == 1) {
+      p.ksplit = (a.K + 63) / 64 * 64;
+      return p;
+    }
+  }
+  // otherwise the register-pipelined kernel with the largest tile that still
+  // gives the chip enough blocks
   if (a.M >= 128 && blocks(128, 128) >= 256) p.bn = 128, p.bm = 128;
   else if (a.M >= 64 && blocks(128, 64) >= 256) p.bn = 128, p.bm = 64;
   else if (a.M > 32) p.bn = 64, p.bm = 64;
@@ -365,6 +492,15 @@ GemmPlan gemm_plan(const GemmArgs& a) {
   p.ksplit = ksteps * BK;
   p.splits = std::max(1, (nk + ksteps - 1) / ksteps);   // no empty range
   return p;
+}
+
+template <int BN, int BM, int MODE>
+static void launch_staged(const GemmArgs& a0, const GemmPlan& p, hipStream_t s) {
+  GemmArgs a = a0;
+  a.ksplit = p.ksplit;
+  a.splits = 1;
+  dim3 grid((a.M + BM - 1) / BM, (a.N + BN - 1) / BN, 1);
+  hipLaunchKernelGGL((gemm_stage_kernel<BN, BM, 2, MODE>), grid, dim3(256), 0, s, a);
 }
 
 template <int BN, int BM, int MODE>
@@ -401,6 +537,11 @@ static void launch_mode(const GemmArgs& a, hipStream_t s) {
     return;
   }
   const GemmPlan p = gemm_plan(a);
+  if (p.kind == 1) {
+    if (p.bm == 128) launch_staged<128, 128, MODE>(a, p, s);
+    else launch_staged<128, 64, MODE>(a, p, s);
+    return;
+  }
   if (p.bn == 128 && p.bm == 128) launch_mfma<128, 128, MODE>(a, p, s);
   else if (p.bn == 128) launch_mfma<128, 64, MODE>(a, p, s);
   else if (p.bm == 64) launch_mfma<64, 64, MODE>(a, p, s);

@@ -90,6 +90,7 @@ struct vla_model_s {
   // split-KV attention partials (fp32), one workspace per stage
   static constexpr long kAttnFloats = 8L << 20;
   float* attn_ws[2] = {nullptr, nullptr};
+  void* zeros = nullptr;       // 256 zero bytes (operand zero fill of the multi-stage projection)
 
 
   // ---- graphs

@@ -369,6 +369,8 @@ void vla_model_s::init(const vla_config& c, const float* w, size_t n, int dev) {
       splitk_ws[i] = (float*)dalloc((size_t)kSplitKFloats * 4);
       attn_ws[i] = (float*)dalloc((size_t)kAttnFloats * 4);
     }
+    zeros = dalloc(256);
+    VLA_HIP(hipMemsetAsync(zeros, 0, 256, L.s));
     VLA_HIP(hipStreamSynchronize(L.s));
     for (int i = 0; i < 2; ++i) VLA_HIP(hipStreamCreateWithFlags(&cap_stream[i], hipStreamNonBlocking));
   } catch (...) {
@@ -403,6 +405,7 @@ GemmArgs gm(const vla_model_s& m, int st, const Mat& w, int M, const void* A, in
   g.mode = EPI_STORE; g.act = ACT_NONE;
   g.tab_period = 1;
   g.ws = m.splitk_ws[st]; g.ws_floats = vla_model_s::kSplitKFloats;
+  g.zeros = m.zeros;
   return g;
 }
 

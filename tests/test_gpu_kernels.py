@@ -21,6 +21,9 @@ GEMM_SHAPES = [
     # (M, N, K): stage shapes and ragged edges
     (1, 16, 8), (17, 32, 592), (50, 720, 720), (130, 200, 64), (300, 1000, 264), (4, 6144, 1024),
     (800, 3840, 720), (3840, 960, 960), (240, 1600, 960), (37, 33, 40),
+    # multi-stage kernel tiles: 256x128 with a K tail, 128x128 with a K tail,
+    # 256x128 with ragged M, N and K
+    (2048, 4096, 592), (2048, 2048, 4304), (4000, 5000, 200),
 ]
 
 
