@@ -150,7 +150,7 @@ def counters_main(args):
     for _ in range(3):
         dst.copy_(src)
     torch.cuda.synchronize()
-    kname = f"gemm_mfma_kernelILi{plan['tile_n']}ELi{plan['tile_m']}EDF16bLi{plan['mode']}E"
+    kname = vla.Model.kernel_symbol(plan)
     print(json.dumps({"kernel_symbol": kname, "plan": plan, "flops_per_launch": flops, "launches": args.roofline_iters,
                       "copy_probe_bytes": int(src.numel() * 4), "config": cfg.name, "batch": B}), flush=True)
     m.close()
@@ -287,7 +287,7 @@ def main():
     per_step = {w: n for w, n in ((0, cfg.llm_layers - 1), (2, cfg.act_layers * N)) if kern[w][2]["splits"] == 1}
     dom = max(per_step, key=lambda w: kern[w][1] * per_step[w])
     flops, us, plan = kern[dom]
-    kname = f"gemm_mfma_kernelILi{plan['tile_n']}ELi{plan['tile_m']}EDF16bLi{plan['mode']}E"
+    kname = vla.Model.kernel_symbol(plan)
     achieved = flops / us / 1e6
     traffic = None
     tf = os.path.join(ROOT, "profiles", "traffic.json")

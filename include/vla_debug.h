@@ -59,9 +59,10 @@ vla_status vla_debug_cu_probe(int device, int cu_count, int from_top, int blocks
  * around the loop. It overwrites the stage's workspace: do not overlap it
  * with that model's stages. which: 0 VLM LLM layer-0 MLP gate/up (GeGLU),
  * 1 VLM LLM layer-0 MLP down, 2 action-stage layer-0 MLP up, 3 action-stage
- * layer-0 MLP down, 4 ViT layer-0 MLP up. plan (may be NULL): int[4] set to
+ * layer-0 MLP down, 4 ViT layer-0 MLP up. plan (may be NULL): int[5] set to
  * the kernel's tile (weight rows, activation rows), number of K ranges
- * (1 = one kernel, > 1 = partial + reduce kernels) and epilogue mode.
+ * (1 = one kernel, > 1 = partial + reduce kernels), epilogue mode and kernel
+ * kind (0 register-pipelined, 1 LDS-staged, 2 small-M).
  */
 vla_status vla_debug_replay_gemm(vla_model m, int which, int batch, int iters, hipStream_t stream, double* flops,
                                  int* plan);

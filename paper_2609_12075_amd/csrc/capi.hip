@@ -328,7 +328,7 @@ vla_status vla_debug_replay_gemm(vla_model m, int which, int batch, int iters, h
     if (flops) *flops = 2.0 * a.M * (double)a.N * (double)a.K;
     if (plan) {
       const GemmPlan p = gemm_plan(a);
-      plan[0] = p.bn; plan[1] = p.bm; plan[2] = p.splits; plan[3] = a.mode;
+      plan[0] = p.bn; plan[1] = p.bm; plan[2] = p.splits; plan[3] = a.mode; plan[4] = p.kind;
     }
     for (int i = 0; i < iters; ++i) launch_gemm(a, s);
     VLA_HIP(hipGetLastError());

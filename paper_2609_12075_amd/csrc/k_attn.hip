@@ -88,21 +88,65 @@ __global__ void __launch_bounds__(256) attn_mfma_kernel(AttnArgs a) {
   // consumed, hiding the global-load latency behind the matrix work.
   constexpr int PER = BKV * CH / 256;
   constexpr bool PREFETCH = HDP <= 128;
+  // Chunk j of this thread: key row kr, dims d8..d8+7. When the chunk count
+  // divides by 4, a thread owns R = CH/4 consecutive keys of one 8-dim chunk,
+  // so its V^T values for one dim are R consecutive bf16 (one vector store).
+  constexpr bool GROUPED = CH % 4 == 0 && 256 % CH == 0;
+  constexpr int R = GROUPED ? CH / 4 : 1;
+  auto chunk_of = [&](int j, int& kr, int& d8) {
+    if constexpr (GROUPED) {
+      d8 = (tid % CH) * 8;
+      kr = (tid / CH) * R + j;
+    } else {
+      const int c = tid + 256 * j;
+      kr = c / CH;
+      d8 = (c % CH) * 8;
+    }
+  };
+  auto load_chunk = [&](int k0, int kr, int d8, bool is_v) {
+    const int kg = k0 + kr;
+    if (kg < kend && d8 < hd) {
+      const int which = kg < len0 ? 0 : 1;
+      const int key = which ? kg - len0 : kg;
+      return *reinterpret_cast<const bf16x8*>(seg_row(a, which, b, g, key, is_v) + d8);
+    }
+    return bf16x8{};
+  };
+  // V^T store of this thread's PER chunks (R keys per dim when grouped)
+  auto store_vt = [&](const bf16x8 (&vr)[PER]) {
+    int kr, d8;
+    if constexpr (GROUPED) {
+      chunk_of(0, kr, d8);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        if constexpr (R == 1) {
+          Vt[d8 + e][kr] = vr[0][e];
+        } else if constexpr (R == 2) {
+          typedef __attribute__((ext_vector_type(2))) __bf16 v2;
+          *reinterpret_cast<v2*>(&Vt[d8 + e][kr]) = v2{vr[0][e], vr[1][e]};
+        } else {
+          static_assert(R == 8, "grouped staging supports 1, 2 or 8 keys per thread");
+          *reinterpret_cast<bf16x8*>(&Vt[d8 + e][kr]) =
+              bf16x8{vr[0][e], vr[1][e], vr[2][e], vr[3][e], vr[4][e], vr[5][e], vr[6][e], vr[7][e]};
+        }
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < PER; ++j) {
+        chunk_of(j, kr, d8);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) Vt[d8 + e][kr] = vr[j][e];
+      }
+    }
+  };
   bf16x8 kreg[PER], vreg[PER];
   auto load_regs = [&](int k0) {
 #pragma unroll
     for (int j = 0; j < PER; ++j) {
-      const int c = tid + 256 * j;
-      const int kr = c / CH, d8 = (c % CH) * 8;
-      const int kg = k0 + kr;
-      kreg[j] = bf16x8{};
-      vreg[j] = bf16x8{};
-      if (kg < kend && d8 < hd) {
-        const int which = kg < len0 ? 0 : 1;
-        const int key = which ? kg - len0 : kg;
-        kreg[j] = *reinterpret_cast<const bf16x8*>(seg_row(a, which, b, g, key, false) + d8);
-        vreg[j] = *reinterpret_cast<const bf16x8*>(seg_row(a, which, b, g, key, true) + d8);
-      }
+      int kr, d8;
+      chunk_of(j, kr, d8);
+      kreg[j] = load_chunk(k0, kr, d8, false);
+      vreg[j] = load_chunk(k0, kr, d8, true);
     }
   };
   if constexpr (PREFETCH) load_regs(kbeg);
@@ -111,27 +155,32 @@ __global__ void __launch_bounds__(256) attn_mfma_kernel(AttnArgs a) {
     if constexpr (PREFETCH) {
 #pragma unroll
       for (int j = 0; j < PER; ++j) {
-        const int c = tid + 256 * j;
-        const int kr = c / CH, d8 = (c % CH) * 8;
+        int kr, d8;
+        chunk_of(j, kr, d8);
         *reinterpret_cast<bf16x8*>(&Ks[kr][d8]) = kreg[j];
-#pragma unroll
-        for (int e = 0; e < 8; ++e) Vt[d8 + e][kr] = vreg[j][e];
       }
+      store_vt(vreg);
     } else {
-      for (int c = tid; c < BKV * CH; c += 256) {
-        const int kr = c / CH, d8 = (c % CH) * 8;
-        const int kg = k0 + kr;
-        bf16x8 kv = bf16x8{}, vv = bf16x8{};
-        if (kg < kend && d8 < hd) {
-          const int which = kg < len0 ? 0 : 1;
-          const int key = which ? kg - len0 : kg;
-          kv = *reinterpret_cast<const bf16x8*>(seg_row(a, which, b, g, key, false) + d8);
-          vv = *reinterpret_cast<const bf16x8*>(seg_row(a, which, b, g, key, true) + d8);
-        }
-        *reinterpret_cast<bf16x8*>(&Ks[kr][d8]) = kv;
+      // K then V, PER chunks each in flight at once
 #pragma unroll
-        for (int e = 0; e < 8; ++e) Vt[d8 + e][kr] = vv[e];
+      for (int j = 0; j < PER; ++j) {
+        int kr, d8;
+        chunk_of(j, kr, d8);
+        kreg[j] = load_chunk(k0, kr, d8, false);
       }
+#pragma unroll
+      for (int j = 0; j < PER; ++j) {
+        int kr, d8;
+        chunk_of(j, kr, d8);
+        *reinterpret_cast<bf16x8*>(&Ks[kr][d8]) = kreg[j];
+      }
+#pragma unroll
+      for (int j = 0; j < PER; ++j) {
+        int kr, d8;
+        chunk_of(j, kr, d8);
+        vreg[j] = load_chunk(k0, kr, d8, true);
+      }
+      store_vt(vreg);
     }
     __syncthreads();
     if constexpr (PREFETCH) {

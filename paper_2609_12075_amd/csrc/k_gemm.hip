@@ -112,16 +112,23 @@ __device__ __forceinline__ void epilogue4(const GemmArgs& a, int m, int n0, floa
       else { dst = q.v; idx = (long)b * q.v_sb + (long)head * q.v_sh + (long)i * q.v_si; }
       if (seg < 2 && q.pos0 >= 0) {
         // weight rows of q and k are stored pair-interleaved per head:
-        // row 2t holds dimension t and row 2t + 1 holds dimension t + hd/2
-        const int half = hd >> 1, pos = q.pos0 + i;
-        for (int j = 0; j < 4; j += 2) {
-          const int t = (j0 + j) >> 1;
-          const float cs = q.rope_cs[((long)pos * half + t) * 2 + 0];
-          const float sn = q.rope_cs[((long)pos * half + t) * 2 + 1];
-          const float x1 = x[j], x2 = x[j + 1];
-          store_elem(dst, idx + t, a.out_type, x1 * cs - x2 * sn);
-          store_elem(dst, idx + t + half, a.out_type, x2 * cs + x1 * sn);
+        // row 2t holds dimension t and row 2t + 1 holds dimension t + hd/2,
+        // so these four columns are dims (t, t+1) and (t+hd/2, t+1+hd/2)
+        const int half = hd >> 1, pos = q.pos0 + i, t = j0 >> 1;
+        const f32x4 cs = *reinterpret_cast<const f32x4*>(q.rope_cs + ((long)pos * half + t) * 2);  // c_t s_t c_t+1 s_t+1
+        const float lo0 = x[0] * cs[0] - x[1] * cs[1], hi0 = x[1] * cs[0] + x[0] * cs[1];
+        const float lo1 = x[2] * cs[2] - x[3] * cs[3], hi1 = x[3] * cs[2] + x[2] * cs[3];
+        if (a.out_type == ET_BF16) {
+          bf16* d = reinterpret_cast<bf16*>(dst) + idx;
+          *reinterpret_cast<bf16x2*>(d + t) = bf16x2{(bf16)lo0, (bf16)lo1};
+          *reinterpret_cast<bf16x2*>(d + t + half) = bf16x2{(bf16)hi0, (bf16)hi1};
+        } else {
+          float* d = reinterpret_cast<float*>(dst) + idx;
+          d[t] = lo0; d[t + 1] = lo1; d[t + half] = hi0; d[t + half + 1] = hi1;
         }
+      } else if (a.out_type == ET_BF16 && nv == 4) {
+        *reinterpret_cast<bf16x4*>(reinterpret_cast<bf16*>(dst) + idx + j0) =
+            bf16x4{(bf16)x[0], (bf16)x[1], (bf16)x[2], (bf16)x[3]};
       } else {
         for (int j = 0; j < nv; ++j) store_elem(dst, idx + j0 + j, a.out_type, x[j]);
       }
@@ -296,6 +303,99 @@ __global__ void __launch_bounds__(256) splitk_reduce_kernel(GemmArgs a) {
   epilogue4<MODE>(a, m, n0, v);
 }
 
+// ---------------------------------------------------------------- small-M kernel
+// For products with few activation rows (the action stage at small batch),
+// where a tile's work is a short K loop and the cost is the memory round
+// trip rather than the matrix work. A block owns 16 * TN weight rows and 64
+// activation rows; its four waves take interleaved 32-wide K chunks (wave w:
+// chunks w, w + 4, ...) and each wave issues the loads of CPW chunks before
+// its first matrix instruction, so one round trip covers 4 * CPW * 32 of K.
+// Loads are unconditional from clamped addresses (out-of-range fragments are
+// zeroed after the load), which keeps them all in flight together. The wave
+// partials are summed in LDS in wave order and the epilogue runs once per
+// output (no atomics: results do not depend on timing).
+template <int TN, int MODE>
+__global__ void __launch_bounds__(256) gemm_skinny_kernel(GemmArgs a) {
+  constexpr int BM = 64, BN = 16 * TN, CPW = 8;
+  __shared__ __attribute__((aligned(16))) float red[4][BM][BN];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  int bx, by, bz;
+  xcd_remap(bx, by, bz);
+  const int m0 = bx * BM, n0 = by * BN;
+  (void)bz;
+  const int kbeg = 0, kend = a.K;
+  const bf16* W = reinterpret_cast<const bf16*>(a.W);
+  const bf16* A = reinterpret_cast<const bf16*>(a.A);
+  const int lr = lane & 15, lk = (lane >> 4) * 8;
+  // this lane's fragment rows (clamped into the operands) and their validity
+  const bf16* wrow[TN];
+  bool wok[TN];
+#pragma unroll
+  for (int i = 0; i < TN; ++i) {
+    const int n = n0 + i * 16 + lr;
+    wok[i] = n < a.N;
+    wrow[i] = W + (long)min(n, a.N - 1) * a.ldw;
+  }
+  const bf16* arow[4];
+  bool aok[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int m = m0 + j * 16 + lr;
+    aok[j] = m < a.M;
+    arow[j] = A + (long)min(m, a.M - 1) * a.lda;
+  }
+  f32x4 acc[TN][4];
+#pragma unroll
+  for (int i = 0; i < TN; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  for (int k0 = kbeg + wave * 32; k0 < kend; k0 += 4 * 32 * CPW) {
+    bf16x8 wf[CPW][TN], af[CPW][4];
+#pragma unroll
+    for (int c = 0; c < CPW; ++c) {
+      const int k = k0 + c * 128 + lk;
+      const int kc = min(k, a.K - 8);
+#pragma unroll
+      for (int i = 0; i < TN; ++i) wf[c][i] = *reinterpret_cast<const bf16x8*>(wrow[i] + kc);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) af[c][j] = *reinterpret_cast<const bf16x8*>(arow[j] + kc);
+    }
+    // keep every load of the round ahead of the matrix work
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int c = 0; c < CPW; ++c) {
+      const bool kok = k0 + c * 128 + lk < kend;
+#pragma unroll
+      for (int i = 0; i < TN; ++i)
+        if (!(kok && wok[i])) wf[c][i] = bf16x8{};
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        if (!(kok && aok[j])) af[c][j] = bf16x8{};
+#pragma unroll
+      for (int i = 0; i < TN; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[c][i], af[c][j], acc[i][j], 0, 0, 0);
+    }
+  }
+  // lane holds rows n = 16 i + 4 (lane >> 4) + e, column m = 16 j + (lane & 15)
+#pragma unroll
+  for (int i = 0; i < TN; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      *reinterpret_cast<f32x4*>(&red[wave][j * 16 + lr][i * 16 + (lane >> 4) * 4]) = acc[i][j];
+  __syncthreads();
+#pragma unroll
+  for (int c = tid; c < BM * BN / 4; c += 256) {
+    const int mr = c / (BN / 4), nc = (c % (BN / 4)) * 4;
+    const f32x4 t = *reinterpret_cast<const f32x4*>(&red[0][mr][nc]) + *reinterpret_cast<const f32x4*>(&red[1][mr][nc]) +
+                    *reinterpret_cast<const f32x4*>(&red[2][mr][nc]) + *reinterpret_cast<const f32x4*>(&red[3][mr][nc]);
+    float v[4] = {t[0], t[1], t[2], t[3]};
+    epilogue4<MODE>(a, m0 + mr, n0 + nc, v);
+  }
+}
+
 // ---------------------------------------------------------------- multi-stage kernel
 // For products with many activation rows (the VLM stage; the action stage at
 // larger batches). Operand tiles move global -> LDS with the CDNA4 direct
@@ -326,7 +426,10 @@ gemm_stage_kernel(GemmArgs a) {
   int bx, by, bz;
   xcd_remap(bx, by, bz);
   const int n_blk = by * BN, m_blk = bx * BM;
-  const int K = a.K, nk = (K + BK - 1) / BK;
+  // K range of this block (range bz of a split product)
+  const int kbeg = bz * a.ksplit;
+  const int K = min(a.K, kbeg + a.ksplit);
+  const int nk = K > kbeg ? (K - kbeg + BK - 1) / BK : 0;
   const bf16* W = reinterpret_cast<const bf16*>(a.W);
   const bf16* A = reinterpret_cast<const bf16*>(a.A);
   const bf16* Z = reinterpret_cast<const bf16*>(a.zeros);
@@ -339,14 +442,14 @@ gemm_stage_kernel(GemmArgs a) {
 #pragma unroll
     for (int j = 0; j < WG; ++j) {
       const int grp = j * 4 + wave, r = grp * 8 + lrow;
-      const int c = slot ^ ((r >> 1) & 7), k = kt * BK + c * 8, n = n_blk + r;
+      const int c = slot ^ ((r >> 1) & 7), k = kbeg + kt * BK + c * 8, n = n_blk + r;
       const bf16* src = (n < a.N && k < K) ? W + (long)n * a.ldw + k : Z;
       __builtin_amdgcn_global_load_lds(src, st + grp * 8 * ROWB, 16, 0, 0);
     }
 #pragma unroll
     for (int j = 0; j < AG; ++j) {
       const int grp = j * 4 + wave, r = grp * 8 + lrow;
-      const int c = slot ^ ((r >> 1) & 7), k = kt * BK + c * 8, m = m_blk + r;
+      const int c = slot ^ ((r >> 1) & 7), k = kbeg + kt * BK + c * 8, m = m_blk + r;
       const bf16* src = (m < a.M && k < K) ? A + (long)m * a.lda + k : Z;
       __builtin_amdgcn_global_load_lds(src, st + BN * ROWB + grp * 8 * ROWB, 16, 0, 0);
     }
@@ -402,6 +505,19 @@ gemm_stage_kernel(GemmArgs a) {
     for (int j = 0; j < TM; ++j)
       *reinterpret_cast<f32x4*>(&Cs[wm0 + 16 * j + lr][wn0 + 16 * i + (lane >> 4) * 4]) = acc[i][j];
   __syncthreads();
+  if (a.splits > 1) {
+    // split-K: store this K range's partial tile; the reduce kernel finishes
+    const int ldp = (a.N + 3) & ~3;
+    float* part = a.ws + (long)bz * a.M * ldp;
+#pragma unroll 1
+    for (int c = tid; c < BM * (BN / 4); c += 256) {
+      const int mr = c / (BN / 4), nc = (c % (BN / 4)) * 4;
+      const int m = m_blk + mr, n = n_blk + nc;
+      if (m < a.M && n < a.N)
+        *reinterpret_cast<f32x4*>(part + (long)m * ldp + n) = *reinterpret_cast<const f32x4*>(&Cs[mr][nc]);
+    }
+    return;
+  }
 #pragma unroll 1
   for (int c = tid; c < BM * (BN / 4); c += 256) {
     const int mr = c / (BN / 4), nc = (c % (BN / 4)) * 4;
@@ -454,43 +570,56 @@ __global__ void __launch_bounds__(256) gemm_f32_kernel(GemmArgs a) {
 // activations (the Euler state, conditioning vectors, robot state) only feed
 // plain stores.
 GemmPlan gemm_plan(const GemmArgs& a) {
-  GemmPlan p{64, 64, 1, 64, 0};
+  constexpr int BK = 64;
+  GemmPlan p{64, 32, 1, 64, 0};
   if (a.w_type == ET_F32) {
+    p.bm = 64;
     p.ksplit = a.K;
     return p;
   }
   auto blocks = [&](int bn, int bm) { return (long)((a.M + bm - 1) / bm) * ((a.N + bn - 1) / bn); };
-  // many activation rows: the LDS-staged kernel (two stages: 64 / 48 KiB, two
-  // blocks per CU, which measured faster than deeper pipelines at one block
-  // per CU), largest tile that still yields enough blocks for the 256 CUs
+  const int nk = (a.K + BK - 1) / BK;
+  const long ldp = (a.N + 3) & ~3;
+  // largest split count <= want whose partials fit the workspace, with the K
+  // steps spread evenly (no empty range)
+  auto set_splits = [&](int want) {
+    int splits = std::max(1, std::min(want, 16));
+    while (splits > 1 && (long)splits * a.M * ldp > a.ws_floats) --splits;
+    const int ksteps = std::max(1, (nk + splits - 1) / splits);
+    p.ksplit = ksteps * BK;
+    p.splits = std::max(1, (nk + ksteps - 1) / ksteps);
+  };
   if (a.a_type == ET_BF16 && a.zeros) {
+    // few activation rows and many weight rows: the small-M kernel (one
+    // memory round trip per 1024 of K, no K split)
+    if (a.M <= 64 && a.N >= 1536) {
+      p.kind = 2;
+      p.bn = a.N >= 6144 ? 32 : 16;
+      p.bm = 64;
+      p.ksplit = a.K;
+      return p;
+    }
+    // many activation rows: the LDS-staged kernel (two stages, two blocks per
+    // CU, which measured faster than deeper pipelines at one block per CU),
+    // largest tile that still yields enough blocks for the 256 CUs; when even
+    // 128 x 64 tiles are few and K is long, K ranges of that kernel
     if (a.M >= 128 && blocks(128, 128) >= 256) { p.bn = 128; p.bm = 128; p.kind = 1; }
     else if (a.M >= 64 && blocks(128, 64) >= 128) { p.bn = 128; p.bm = 64; p.kind = 1; }
+    else if (a.M >= 512 && nk >= 24 && a.ws) { p.bn = 128; p.bm = 64; p.kind = 1; }
     if (p.kind == 1) {
-      p.ksplit = (a.K + 63) / 64 * 64;
+      p.ksplit = nk * BK;
+      if (blocks(128, p.bm) < 128) set_splits((int)std::min<long>((448 + blocks(128, 64) - 1) / blocks(128, 64), nk / 4));
       return p;
     }
   }
-  // otherwise the register-pipelined kernel with the largest tile that still
-  // gives the chip enough blocks
+  // otherwise the register-pipelined kernel: 128-row tiles only for large
+  // products, else 64 x 32 tiles (measured best up to a few hundred rows);
+  // split K when the tiles leave the CUs short of work, keeping >= 3 K steps
+  // per range
   if (a.M >= 128 && blocks(128, 128) >= 256) p.bn = 128, p.bm = 128;
-  else if (a.M >= 64 && blocks(128, 64) >= 256) p.bn = 128, p.bm = 64;
-  else if (a.M > 32) p.bn = 64, p.bm = 64;
-  else p.bn = 64, p.bm = 32;
-  // Split K when the output tiles would leave most of the CUs idle: aim for
-  // ~2 blocks per CU, at least 2 K-steps per range, partials within ws.
-  constexpr int BK = 64;
+  p.ksplit = nk * BK;
   const long tiles = blocks(p.bn, p.bm);
-  const int nk = (a.K + BK - 1) / BK;
-  const long ldp = (a.N + 3) & ~3;
-  int splits = 1;
-  if (a.ws && tiles < 192 && nk >= 4) {
-    splits = (int)std::min<long>({(512 + tiles - 1) / tiles, (long)nk / 2, 16L});
-    while (splits > 1 && (long)splits * a.M * ldp > a.ws_floats) --splits;
-  }
-  const int ksteps = std::max(1, (nk + splits - 1) / splits);
-  p.ksplit = ksteps * BK;
-  p.splits = std::max(1, (nk + ksteps - 1) / ksteps);   // no empty range
+  if (a.ws && tiles < 256 && nk >= 6) set_splits((int)std::min<long>((256 + tiles - 1) / tiles, nk / 3));
   return p;
 }
 
@@ -498,9 +627,22 @@ template <int BN, int BM, int MODE>
 static void launch_staged(const GemmArgs& a0, const GemmPlan& p, hipStream_t s) {
   GemmArgs a = a0;
   a.ksplit = p.ksplit;
-  a.splits = 1;
-  dim3 grid((a.M + BM - 1) / BM, (a.N + BN - 1) / BN, 1);
+  a.splits = p.splits;
+  dim3 grid((a.M + BM - 1) / BM, (a.N + BN - 1) / BN, a.splits);
+  if (a.splits > 1) {
+    // partial pass without epilogue, then the ordered reduce applies it
+    hipLaunchKernelGGL((gemm_stage_kernel<BN, BM, 2, EPI_STORE>), grid, dim3(256), 0, s, a);
+    const long chunks = (long)a.M * (((a.N + 3) & ~3) / 4);
+    hipLaunchKernelGGL(splitk_reduce_kernel<MODE>, dim3((unsigned)((chunks + 255) / 256)), dim3(256), 0, s, a);
+    return;
+  }
   hipLaunchKernelGGL((gemm_stage_kernel<BN, BM, 2, MODE>), grid, dim3(256), 0, s, a);
+}
+
+template <int TN, int MODE>
+static void launch_skinny(const GemmArgs& a, hipStream_t s) {
+  dim3 grid((a.M + 63) / 64, (a.N + 16 * TN - 1) / (16 * TN), 1);
+  hipLaunchKernelGGL((gemm_skinny_kernel<TN, MODE>), grid, dim3(256), 0, s, a);
 }
 
 template <int BN, int BM, int MODE>
@@ -537,14 +679,17 @@ static void launch_mode(const GemmArgs& a, hipStream_t s) {
     return;
   }
   const GemmPlan p = gemm_plan(a);
+  if (p.kind == 2) {
+    if (p.bn == 32) launch_skinny<2, MODE>(a, s);
+    else launch_skinny<1, MODE>(a, s);
+    return;
+  }
   if (p.kind == 1) {
     if (p.bm == 128) launch_staged<128, 128, MODE>(a, p, s);
     else launch_staged<128, 64, MODE>(a, p, s);
     return;
   }
-  if (p.bn == 128 && p.bm == 128) launch_mfma<128, 128, MODE>(a, p, s);
-  else if (p.bn == 128) launch_mfma<128, 64, MODE>(a, p, s);
-  else if (p.bm == 64) launch_mfma<64, 64, MODE>(a, p, s);
+  if (p.bn == 128) launch_mfma<128, 128, MODE>(a, p, s);
   else launch_mfma<64, 32, MODE>(a, p, s);
 }
 

@@ -24,6 +24,13 @@ GEMM_SHAPES = [
     # multi-stage kernel tiles: 256x128 with a K tail, 128x128 with a K tail,
     # 256x128 with ragged M, N and K
     (2048, 4096, 592), (2048, 2048, 4304), (4000, 5000, 200),
+    # small-M kernel: one and two weight-row subtiles, K tails, several K
+    # rounds, ragged N
+    (50, 3840, 720), (17, 1600, 1000), (63, 1537, 3000), (64, 8192, 1024),
+    # K ranges of the LDS-staged kernel (partial + ordered reduce), ragged
+    (800, 720, 1920), (600, 1000, 1544),
+    # register-pipelined 64 x 32 tiles with K ranges
+    (100, 1024, 4096), (200, 720, 1920),
 ]
 
 
