@@ -30,6 +30,20 @@ vla_status vla_debug_gemm(int M, int N, int K, const void* A, int lda, int a_typ
                           int w_type, const float* bias, int act, float* out, int ldo, hipStream_t stream);
 
 /*
+ * Residual projection followed by the row norm of its output (every
+ * transformer block: x += o W_o, then the next sublayer's norm):
+ *   x[m][n] += gate[n] * (sum_k A[m][k] Wt[n][k] + bias[n])   (x in place)
+ *   z[m][:] = norm(x[m][:])  kind 0: RMSNorm * g; 1: LayerNorm * g + b
+ *                             (g, b optional); 2: LayerNorm * (1 + g) + b
+ * A bf16 [M][K], Wt bf16 [N][K], bias/gate fp32 [N] or NULL, x fp32 [M][N],
+ * z bf16 [M][N]. K % 8 == 0, N % 4 == 0, N <= 2048. When the projection is
+ * split over K the norm runs inside the split reduce.
+ */
+vla_status vla_debug_resid_norm(int M, int N, int K, const void* A, const void* Wt, const float* bias, const float* gate,
+                                float* x, int kind, const float* g, const float* b, float eps, void* z,
+                                hipStream_t stream);
+
+/*
  * o = softmax(q k^T / sqrt(hd)) v over the keys [k0 ; k1] (segment 1 may be
  * empty), grouped KV heads (query head h uses KV head h / (Hq / Hkv)).
  *  q  device [B][Hq][Lq][hd]; k0, v0 [B][Hkv][len0][hd]; k1, v1 [B][Hkv][len1][hd];

@@ -276,6 +276,26 @@ vla_status vla_debug_gemm(int M, int N, int K, const void* A, int lda, int a_typ
   });
 }
 
+vla_status vla_debug_resid_norm(int M, int N, int K, const void* A, const void* Wt, const float* bias, const float* gate,
+                                float* x, int kind, const float* g, const float* b, float eps, void* z,
+                                hipStream_t s) {
+  return guarded([&] {
+    VLA_REQUIRE(M >= 1 && N >= 4 && K >= 8 && A && Wt && x && z, "bad resid_norm arguments");
+    VLA_REQUIRE(K % 8 == 0 && N % 4 == 0 && N <= 2048, "resid_norm needs K % 8 == 0, N % 4 == 0, N <= 2048");
+    VLA_REQUIRE(kind >= 0 && kind <= 2 && (kind != 2 || (g && b)), "bad norm kind");
+    GemmArgs a{};
+    a.M = M; a.N = N; a.K = K; a.A = A; a.lda = K; a.a_type = ET_BF16; a.W = Wt; a.ldw = K; a.w_type = ET_BF16;
+    a.mode = EPI_RESID; a.bias = bias; a.gate = gate; a.tab_period = 1; a.out = x; a.ldo = N; a.out_type = ET_F32;
+    a.ws = debug_ws(0, vla_model_s::kSplitKFloats); a.ws_floats = vla_model_s::kSplitKFloats;
+    a.zeros = debug_ws(2, 64);
+    NormArgs n{};
+    n.rows = M; n.d = N; n.kind = kind; n.in = x; n.ld_in = N; n.out = z; n.ld_out = N; n.out_type = ET_BF16;
+    n.g = g; n.b = b; n.eps = eps;
+    launch_gemm_norm(a, n, s);
+    VLA_HIP(hipGetLastError());
+  });
+}
+
 vla_status vla_debug_attention(int B, int Hq, int Hkv, int Lq, int hd, int et, const void* q, const void* k0,
                                const void* v0, int len0, const void* k1, const void* v1, int len1, void* o,
                                hipStream_t s) {

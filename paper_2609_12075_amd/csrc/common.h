@@ -150,6 +150,13 @@ struct NormArgs {
 };
 void launch_norm(const NormArgs& a, hipStream_t s);
 
+// A residual projection (mode EPI_RESID into a.out) followed by the row norm
+// n of its output (n.in == a.out). When the projection splits K, the norm
+// runs inside the split-K reduce (one kernel fewer); otherwise the two run
+// back to back. Either way the results are those of launch_gemm then
+// launch_norm with the same plan.
+void launch_gemm_norm(const GemmArgs& a, const NormArgs& n, hipStream_t s);
+
 // Patch extraction: pixels [n_images][3][hw][hw] fp32 -> rows
 // [n_images * (hw/p)^2][ldo] of type out_type in (c, dy, dx) order; columns
 // >= 3 p^2 are zero-filled.

@@ -3,76 +3,31 @@
 // patch extraction, token embedding, the flow-time sinusoid, RoPE tables,
 // parameter conversion and a placement probe for CU-masked streams.
 #include "common.h"
+#include "rownorm.h"
 
 namespace {
-
-__device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
-  return v;
-}
 
 __device__ __forceinline__ float round_bf16(float x) { return (float)(bf16)x; }
 
 // ---------------------------------------------------------------- norms
 // One wavefront per row. The row is read once into registers with 16-byte
 // loads that are all issued before the first reduction (one memory round
-// trip), statistics are two-pass over registers, and the result is written
-// with 8/16-byte stores. Requires d % 4 == 0 and d <= 256 * NV.
+// trip); statistics and output as in rownorm::store_row. Requires d % 4 == 0
+// and d <= 256 * NV.
 template <int NV>
 __global__ void __launch_bounds__(256) norm_kernel(NormArgs a) {
-  typedef __attribute__((ext_vector_type(4))) float f4;
-  typedef __attribute__((ext_vector_type(4))) __bf16 b4;
   const int lane = threadIdx.x & 63;
   const int r = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (r >= a.rows) return;
   const int rin = a.skip > 0 ? r + (r / a.skip_group + 1) * a.skip : r;
   const float* x = a.in + (long)rin * a.ld_in;
-  const int d = a.d;
-  f4 v[NV];
+  rownorm::f4 v[NV];
 #pragma unroll
   for (int j = 0; j < NV; ++j) {
     const int i = (j * 64 + lane) * 4;
-    v[j] = i < d ? *reinterpret_cast<const f4*>(x + i) : f4{0.f, 0.f, 0.f, 0.f};
+    v[j] = i < a.d ? *reinterpret_cast<const rownorm::f4*>(x + i) : rownorm::f4{0.f, 0.f, 0.f, 0.f};
   }
-  float mean = 0.f;
-  if (a.kind != 0) {
-    float s = 0.f;
-#pragma unroll
-    for (int j = 0; j < NV; ++j) s += (v[j][0] + v[j][1]) + (v[j][2] + v[j][3]);
-    mean = wave_sum(s) / d;
-  }
-  float ss = 0.f;
-#pragma unroll
-  for (int j = 0; j < NV; ++j) {
-    const int i = (j * 64 + lane) * 4;
-    if (i < d)
-#pragma unroll
-      for (int e = 0; e < 4; ++e) { const float t = v[j][e] - mean; ss = fmaf(t, t, ss); }
-  }
-  const float rstd = rsqrtf(wave_sum(ss) / d + a.eps);
-#pragma unroll
-  for (int j = 0; j < NV; ++j) {
-    const int i = (j * 64 + lane) * 4;
-    if (i >= d) continue;
-    f4 y;
-#pragma unroll
-    for (int e = 0; e < 4; ++e) y[e] = (v[j][e] - mean) * rstd;
-    if (a.kind == 2) {
-      const f4 sc = *reinterpret_cast<const f4*>(a.g + i), sh = *reinterpret_cast<const f4*>(a.b + i);
-#pragma unroll
-      for (int e = 0; e < 4; ++e) y[e] = y[e] * (1.0f + sc[e]) + sh[e];
-    } else {
-      if (a.g) { const f4 g = *reinterpret_cast<const f4*>(a.g + i); y *= g; }
-      if (a.b) { const f4 b = *reinterpret_cast<const f4*>(a.b + i); y += b; }
-    }
-    if (a.out_type == ET_BF16) {
-      *reinterpret_cast<b4*>(reinterpret_cast<bf16*>(a.out) + (long)r * a.ld_out + i) =
-          b4{(bf16)y[0], (bf16)y[1], (bf16)y[2], (bf16)y[3]};
-    } else {
-      *reinterpret_cast<f4*>(reinterpret_cast<float*>(a.out) + (long)r * a.ld_out + i) = y;
-    }
-  }
+  rownorm::store_row<NV>(a, r, v, lane);
 }
 
 // ---------------------------------------------------------------- staging

@@ -12,6 +12,7 @@
 #include <algorithm>
 
 #include "common.h"
+#include "rownorm.h"
 
 typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
 typedef __attribute__((ext_vector_type(4))) __bf16 bf16x4;
@@ -301,6 +302,54 @@ __global__ void __launch_bounds__(256) splitk_reduce_kernel(GemmArgs a) {
   for (int z = 1; z < 16; ++z) t += part[z];
   float v[4] = {t[0], t[1], t[2], t[3]};
   epilogue4<MODE>(a, m, n0, v);
+}
+
+// Split-K second pass of a residual projection fused with the row norm that
+// follows it: one wavefront per output row sums the partials in split order,
+// applies the residual epilogue (x += gate * (sum + bias)) exactly as the
+// plain reduce does, writes x, and normalises the new row into n.out (the
+// same arithmetic as the norm kernel). Requires N == n.d <= 256 * NV and
+// contiguous rows (no row groups).
+template <int NV>
+__global__ void __launch_bounds__(256) splitk_reduce_norm_kernel(GemmArgs a, NormArgs n) {
+  const int lane = threadIdx.x & 63;
+  const int r = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (r >= a.M) return;
+  const int ldp = (a.N + 3) & ~3;
+  const long stride = (long)a.M * ldp;
+  const float* p = a.ws + (long)r * ldp;
+  float* x = reinterpret_cast<float*>(a.out) + (long)r * a.ldo;
+  // every load of the row (partials in split order, old x) before the first
+  // store, so they share one memory round trip
+  rownorm::f4 v[NV];
+  f32x4 t[NV], bs[NV], gt[NV];
+  const bool has_bias = a.bias != nullptr, has_gate = a.gate != nullptr;
+#pragma unroll
+  for (int j = 0; j < NV; ++j) {
+    const int i = min((j * 64 + lane) * 4, a.N - 4);
+    f32x4 part[16];
+#pragma unroll
+    for (int z = 0; z < 16; ++z)
+      part[z] = z < a.splits ? *reinterpret_cast<const f32x4*>(p + z * stride + i) : f32x4{0.f, 0.f, 0.f, 0.f};
+    t[j] = part[0];
+#pragma unroll
+    for (int z = 1; z < 16; ++z) t[j] += part[z];
+    v[j] = *reinterpret_cast<const f32x4*>(x + i);
+    bs[j] = has_bias ? *reinterpret_cast<const f32x4*>(a.bias + i) : f32x4{0.f, 0.f, 0.f, 0.f};
+    gt[j] = has_gate ? *reinterpret_cast<const f32x4*>(a.gate + i) : f32x4{1.f, 1.f, 1.f, 1.f};
+  }
+#pragma unroll
+  for (int j = 0; j < NV; ++j) {
+    const int i = (j * 64 + lane) * 4;
+    if (i >= a.N) {
+      v[j] = rownorm::f4{0.f, 0.f, 0.f, 0.f};
+      continue;
+    }
+    // as the residual epilogue: x += (sum + bias) * gate (gate 1 when absent)
+    v[j] += (t[j] + bs[j]) * gt[j];
+    *reinterpret_cast<f32x4*>(x + i) = v[j];
+  }
+  rownorm::store_row<NV>(n, r, v, lane);
 }
 
 // ---------------------------------------------------------------- small-M kernel
@@ -623,8 +672,26 @@ GemmPlan gemm_plan(const GemmArgs& a) {
   return p;
 }
 
+// Second pass of a split product: the ordered reduce with the epilogue, or
+// for a residual projection with a following row norm, the fused reduce.
+template <int MODE>
+static void launch_reduce(const GemmArgs& a, const NormArgs* fuse, hipStream_t s) {
+  if constexpr (MODE == EPI_RESID) {
+    if (fuse) {
+      const dim3 grid((a.M + 3) / 4);
+      if (a.N <= 256) hipLaunchKernelGGL(splitk_reduce_norm_kernel<1>, grid, dim3(256), 0, s, a, *fuse);
+      else if (a.N <= 512) hipLaunchKernelGGL(splitk_reduce_norm_kernel<2>, grid, dim3(256), 0, s, a, *fuse);
+      else if (a.N <= 1024) hipLaunchKernelGGL(splitk_reduce_norm_kernel<4>, grid, dim3(256), 0, s, a, *fuse);
+      else hipLaunchKernelGGL(splitk_reduce_norm_kernel<8>, grid, dim3(256), 0, s, a, *fuse);
+      return;
+    }
+  }
+  const long chunks = (long)a.M * (((a.N + 3) & ~3) / 4);
+  hipLaunchKernelGGL(splitk_reduce_kernel<MODE>, dim3((unsigned)((chunks + 255) / 256)), dim3(256), 0, s, a);
+}
+
 template <int BN, int BM, int MODE>
-static void launch_staged(const GemmArgs& a0, const GemmPlan& p, hipStream_t s) {
+static void launch_staged(const GemmArgs& a0, const GemmPlan& p, const NormArgs* fuse, hipStream_t s) {
   GemmArgs a = a0;
   a.ksplit = p.ksplit;
   a.splits = p.splits;
@@ -632,8 +699,7 @@ static void launch_staged(const GemmArgs& a0, const GemmPlan& p, hipStream_t s) 
   if (a.splits > 1) {
     // partial pass without epilogue, then the ordered reduce applies it
     hipLaunchKernelGGL((gemm_stage_kernel<BN, BM, 2, EPI_STORE>), grid, dim3(256), 0, s, a);
-    const long chunks = (long)a.M * (((a.N + 3) & ~3) / 4);
-    hipLaunchKernelGGL(splitk_reduce_kernel<MODE>, dim3((unsigned)((chunks + 255) / 256)), dim3(256), 0, s, a);
+    launch_reduce<MODE>(a, fuse, s);
     return;
   }
   hipLaunchKernelGGL((gemm_stage_kernel<BN, BM, 2, MODE>), grid, dim3(256), 0, s, a);
@@ -646,11 +712,10 @@ static void launch_skinny(const GemmArgs& a, hipStream_t s) {
 }
 
 template <int BN, int BM, int MODE>
-static void launch_mfma(const GemmArgs& a0, const GemmPlan& p, hipStream_t s) {
+static void launch_mfma(const GemmArgs& a0, const GemmPlan& p, const NormArgs* fuse, hipStream_t s) {
   GemmArgs a = a0;
   a.ksplit = p.ksplit;
   a.splits = p.splits;
-  const long ldp = (a.N + 3) & ~3;
   dim3 grid((a.M + BM - 1) / BM, (a.N + BN - 1) / BN, a.splits);
   bool f32a = false;
   if constexpr (MODE == EPI_STORE) f32a = a.a_type == ET_F32;
@@ -658,8 +723,7 @@ static void launch_mfma(const GemmArgs& a0, const GemmPlan& p, hipStream_t s) {
     // the partial pass does not use the epilogue: one instantiation serves all modes
     if (f32a) hipLaunchKernelGGL((gemm_mfma_kernel<BN, BM, float, EPI_STORE>), grid, dim3(256), 0, s, a);
     else hipLaunchKernelGGL((gemm_mfma_kernel<BN, BM, bf16, EPI_STORE>), grid, dim3(256), 0, s, a);
-    const long chunks = (long)a.M * (ldp / 4);
-    hipLaunchKernelGGL(splitk_reduce_kernel<MODE>, dim3((unsigned)((chunks + 255) / 256)), dim3(256), 0, s, a);
+    launch_reduce<MODE>(a, fuse, s);
     return;
   }
   if constexpr (MODE == EPI_STORE) {
@@ -671,37 +735,54 @@ static void launch_mfma(const GemmArgs& a0, const GemmPlan& p, hipStream_t s) {
   hipLaunchKernelGGL((gemm_mfma_kernel<BN, BM, bf16, MODE>), grid, dim3(256), 0, s, a);
 }
 
+// fuse: a row norm of the output to run inside the split-K reduce (only
+// passed when the plan splits K and the product is a residual projection)
 template <int MODE>
-static void launch_mode(const GemmArgs& a, hipStream_t s) {
+static void launch_mode(const GemmArgs& a, const GemmPlan& p, const NormArgs* fuse, hipStream_t s) {
   if (a.w_type == ET_F32) {
     dim3 grid((a.M + 63) / 64, (a.N + 63) / 64);
     hipLaunchKernelGGL(gemm_f32_kernel<MODE>, grid, dim3(256), 0, s, a);
     return;
   }
-  const GemmPlan p = gemm_plan(a);
   if (p.kind == 2) {
     if (p.bn == 32) launch_skinny<2, MODE>(a, s);
     else launch_skinny<1, MODE>(a, s);
     return;
   }
   if (p.kind == 1) {
-    if (p.bm == 128) launch_staged<128, 128, MODE>(a, p, s);
-    else launch_staged<128, 64, MODE>(a, p, s);
+    if (p.bm == 128) launch_staged<128, 128, MODE>(a, p, fuse, s);
+    else launch_staged<128, 64, MODE>(a, p, fuse, s);
     return;
   }
-  if (p.bn == 128) launch_mfma<128, 128, MODE>(a, p, s);
-  else launch_mfma<64, 32, MODE>(a, p, s);
+  if (p.bn == 128) launch_mfma<128, 128, MODE>(a, p, fuse, s);
+  else launch_mfma<64, 32, MODE>(a, p, fuse, s);
 }
 
 void launch_gemm(const GemmArgs& a, hipStream_t s) {
   if (a.M <= 0 || a.N <= 0) return;
   if (a.a_type == ET_F32 && a.w_type == ET_BF16 && a.mode != EPI_STORE)
     throw VlaError{4, "fp32 activations with bf16 weights only feed plain stores"};
+  const GemmPlan p = a.w_type == ET_F32 ? GemmPlan{} : gemm_plan(a);
   switch (a.mode) {
-    case EPI_STORE: launch_mode<EPI_STORE>(a, s); break;
-    case EPI_RESID: launch_mode<EPI_RESID>(a, s); break;
-    case EPI_GEGLU: launch_mode<EPI_GEGLU>(a, s); break;
-    case EPI_QKV: launch_mode<EPI_QKV>(a, s); break;
-    case EPI_EULER: launch_mode<EPI_EULER>(a, s); break;
+    case EPI_STORE: launch_mode<EPI_STORE>(a, p, nullptr, s); break;
+    case EPI_RESID: launch_mode<EPI_RESID>(a, p, nullptr, s); break;
+    case EPI_GEGLU: launch_mode<EPI_GEGLU>(a, p, nullptr, s); break;
+    case EPI_QKV: launch_mode<EPI_QKV>(a, p, nullptr, s); break;
+    case EPI_EULER: launch_mode<EPI_EULER>(a, p, nullptr, s); break;
   }
+}
+
+void launch_gemm_norm(const GemmArgs& a, const NormArgs& n, hipStream_t s) {
+  const bool fusable = a.M > 0 && a.N > 0 && a.mode == EPI_RESID && a.w_type == ET_BF16 && a.row_group == 0 &&
+                       n.skip == 0 && n.rows == a.M && n.d == a.N && n.in == a.out && n.ld_in == a.ldo &&
+                       a.N % 4 == 0 && a.ldo % 4 == 0 && n.ld_out % 4 == 0 && a.N <= 2048;
+  if (fusable) {
+    const GemmPlan p = gemm_plan(a);
+    if (p.splits > 1) {
+      launch_mode<EPI_RESID>(a, p, &n, s);
+      return;
+    }
+  }
+  launch_gemm(a, s);
+  launch_norm(n, s);
 }

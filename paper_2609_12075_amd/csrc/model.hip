@@ -419,12 +419,24 @@ void resid(GemmArgs g, float* out, int ldo, const float* bias, const float* gate
   launch_gemm(g, s);
 }
 
-void norm(int rows, int d, int kind, const float* in, int ld_in, void* out, int ld_out, int out_type, const float* g,
-          const float* b, float eps, hipStream_t s, int skip = 0, int skip_group = 1) {
+NormArgs nargs(int rows, int d, int kind, const float* in, int ld_in, void* out, int ld_out, int out_type,
+               const float* g, const float* b, float eps, int skip = 0, int skip_group = 1) {
   NormArgs a{};
   a.rows = rows; a.d = d; a.kind = kind; a.in = in; a.ld_in = ld_in; a.out = out; a.ld_out = ld_out;
   a.out_type = out_type; a.g = g; a.b = b; a.eps = eps; a.skip = skip; a.skip_group = skip_group;
-  launch_norm(a, s);
+  return a;
+}
+
+void norm(int rows, int d, int kind, const float* in, int ld_in, void* out, int ld_out, int out_type, const float* g,
+          const float* b, float eps, hipStream_t s, int skip = 0, int skip_group = 1) {
+  launch_norm(nargs(rows, d, kind, in, ld_in, out, ld_out, out_type, g, b, eps, skip, skip_group), s);
+}
+
+// residual projection into out, then the row norm n of the updated rows
+void resid_norm(GemmArgs g, float* out, int ldo, const float* bias, const float* gate, const NormArgs& n,
+                hipStream_t s) {
+  g.mode = EPI_RESID; g.out = out; g.ldo = ldo; g.out_type = ET_F32; g.bias = bias; g.gate = gate;
+  launch_gemm_norm(g, n, s);
 }
 
 AttnArgs attn(const vla_model_s& m, int st, int B, int Hq, int Hkv, int Lq, int hd, int et) {
@@ -459,9 +471,10 @@ void vla_model_s::enqueue_prefill(int B, const float* pix, const int32_t* ids, c
     GemmArgs g = gm(*this, ST,patch, Mi, patches, Kp, et);
     g.tab = pos; g.tab_period = T; g.ldtab = E;
     store(g, vx, d, ET_F32, patch_b, ACT_NONE, s);
+    norm(Mi, d, 1, vx, d, vz, d, et, vit[0].ln1g, vit[0].ln1b, eps, s);
     for (int l = 0; l < c.vit_layers; ++l) {
       const VitLayer& y = vit[l];
-      norm(Mi, d, 1, vx, d, vz, d, et, y.ln1g, y.ln1b, eps, s);
+      // vz holds LN1(vx) of this layer (written by the previous step)
       GemmArgs q3 = gm(*this, ST,y.qkv, Mi, vz, d, et);
       q3.mode = EPI_QKV; q3.bias = y.bqkv; q3.out_type = et;
       QkvEpi& e3 = q3.qkv;
@@ -476,12 +489,15 @@ void vla_model_s::enqueue_prefill(int B, const float* pix, const int32_t* ids, c
       at.seg[1].len = 0;
       at.o = vo; at.o_sb = (long)T * d; at.o_sh = vhd; at.o_si = d;
       launch_attention(at, s);
-      resid(gm(*this, ST,y.wo, Mi, vo, d, et), vx, d, y.bo, nullptr, s);
-      norm(Mi, d, 1, vx, d, vz, d, et, y.ln2g, y.ln2b, eps, s);
+      resid_norm(gm(*this, ST,y.wo, Mi, vo, d, et), vx, d, y.bo, nullptr,
+                 nargs(Mi, d, 1, vx, d, vz, d, et, y.ln2g, y.ln2b, eps), s);
       store(gm(*this, ST,y.w1, Mi, vz, d, et), vmlp, c.vit_mlp, et, y.b1, ACT_GELU, s);
-      resid(gm(*this, ST,y.w2, Mi, vmlp, c.vit_mlp, et), vx, d, y.b2, nullptr, s);
+      // then LN1 of the next layer, or the final LN
+      const bool last = l + 1 == c.vit_layers;
+      resid_norm(gm(*this, ST,y.w2, Mi, vmlp, c.vit_mlp, et), vx, d, y.b2, nullptr,
+                 nargs(Mi, d, 1, vx, d, vz, d, et, last ? vit_lnf_g : vit[l + 1].ln1g,
+                       last ? vit_lnf_b : vit[l + 1].ln1b, eps), s);
     }
-    norm(Mi, d, 1, vx, d, vz, d, et, vit_lnf_g, vit_lnf_b, eps, s);
     GemmArgs gp = gm(*this, ST,proj, Mi, vz, d, et);
     gp.row_group = c.n_img * T; gp.row_group_stride = (long)P * D;
     store(gp, h, D, ET_F32, proj_b, ACT_NONE, s);
@@ -489,6 +505,7 @@ void vla_model_s::enqueue_prefill(int B, const float* pix, const int32_t* ids, c
   launch_embed(ids, B, c.n_text, c.vocab, embed, et, D, h, P, c.n_img * T, s);
 
   const int nq = c.n_q, nkv = c.n_kv;
+  norm(Mp, D, 0, h, D, z, D, et, llm[0].ln1, nullptr, eps, s);
   for (int l = 0; l < c.llm_layers; ++l) {
     const LlmLayer& y = llm[l];
     const bool last_kv_only = !dit_head && l == c.llm_layers - 1;
@@ -500,7 +517,7 @@ void vla_model_s::enqueue_prefill(int B, const float* pix, const int32_t* ids, c
     } else {
       kd_ = kbuf; vd_ = vbuf;
     }
-    norm(Mp, D, 0, h, D, z, D, et, y.ln1, nullptr, eps, s);
+    // z holds RMSNorm(h) with this layer's gain (written by the previous step)
     GemmArgs q3 = gm(*this, ST,y.qkv, Mp, z, D, et);
     q3.mode = EPI_QKV; q3.out_type = et;
     QkvEpi& e3 = q3.qkv;
@@ -521,16 +538,21 @@ void vla_model_s::enqueue_prefill(int B, const float* pix, const int32_t* ids, c
     at.seg[1].len = 0;
     at.o = o; at.o_sb = (long)P * Hq; at.o_sh = hd; at.o_si = Hq;
     launch_attention(at, s);
-    resid(gm(*this, ST,y.wo, Mp, o, Hq, et), h, D, nullptr, nullptr, s);
-    norm(Mp, D, 0, h, D, z, D, et, y.ln2, nullptr, eps, s);
+    resid_norm(gm(*this, ST,y.wo, Mp, o, Hq, et), h, D, nullptr, nullptr,
+               nargs(Mp, D, 0, h, D, z, D, et, y.ln2, nullptr, eps), s);
     GemmArgs gg = gm(*this, ST,y.gu, Mp, z, D, et);
     gg.mode = EPI_GEGLU; gg.out = gu; gg.ldo = c.llm_mlp; gg.out_type = et;
     launch_gemm(gg, s);
-    resid(gm(*this, ST,y.wd, Mp, gu, c.llm_mlp, et), h, D, nullptr, nullptr, s);
+    // then the next layer's RMSNorm (the DiT head's final one after the last)
+    const bool last = l + 1 == c.llm_layers;
+    if (!last || dit_head)
+      resid_norm(gm(*this, ST,y.wd, Mp, gu, c.llm_mlp, et), h, D, nullptr, nullptr,
+                 nargs(Mp, D, 0, h, D, z, D, et, last ? llm_lnf : llm[l + 1].ln1, nullptr, eps), s);
+    else
+      resid(gm(*this, ST,y.wd, Mp, gu, c.llm_mlp, et), h, D, nullptr, nullptr, s);
   }
   if (dit_head) {
     const int NL = c.act_layers;
-    norm(Mp, D, 0, h, D, z, D, et, llm_lnf, nullptr, eps, s);
     store(gm(*this, ST,vp, Mp, z, D, et), feat, Da, et, vp_b, ACT_NONE, s);
     store(gm(*this, ST,xkv, Mp, feat, Da, et), kv, NL * 2 * Da, et, xkv_b, ACT_NONE, s);
     void* st_out = (char*)kv + (size_t)B * P * NL * 2 * Da * es;
@@ -592,9 +614,10 @@ void vla_model_s::enqueue_denoise(int B, const void* kv, const float* noise, int
       store(gm(*this, ST,ain, M, x, A, ET_F32), e, Da, et, ain_b, ACT_NONE, s);
       store(gm(*this, ST,t1a, M, e, Da, et), u, Da, et, cc.tb + (size_t)k * Da, ACT_SILU, s);
       store(gm(*this, ST,t2, M, u, Da, et), ha, Da, ET_F32, t2_b, ACT_NONE, s);
+      norm(M, Da, 0, ha, Da, za, Da, et, act[0].ln1, nullptr, eps, s);
       for (int l = 0; l < c.act_layers; ++l) {
         const LlmLayer& y = act[l];
-        norm(M, Da, 0, ha, Da, za, Da, et, y.ln1, nullptr, eps, s);
+        // za holds RMSNorm(ha) with this layer's gain
         GemmArgs q3 = gm(*this, ST,y.qkv, M, za, Da, et);
         q3.mode = EPI_QKV; q3.out_type = et;
         QkvEpi& e3 = q3.qkv;
@@ -611,14 +634,16 @@ void vla_model_s::enqueue_denoise(int B, const void* kv, const float* noise, int
         at.seg[1] = AttnSeg{ks, e3.k_sb, e3.k_sh, hd, vs, e3.v_sb, e3.v_sh, hd, H};
         at.o = oa; at.o_sb = (long)H * Hq; at.o_sh = hd; at.o_si = Hq;
         launch_attention(at, s);
-        resid(gm(*this, ST,y.wo, M, oa, Hq, et), ha, Da, nullptr, nullptr, s);
-        norm(M, Da, 0, ha, Da, za, Da, et, y.ln2, nullptr, eps, s);
+        resid_norm(gm(*this, ST,y.wo, M, oa, Hq, et), ha, Da, nullptr, nullptr,
+                   nargs(M, Da, 0, ha, Da, za, Da, et, y.ln2, nullptr, eps), s);
         GemmArgs gg = gm(*this, ST,y.gu, M, za, Da, et);
         gg.mode = EPI_GEGLU; gg.out = gua; gg.ldo = Fa; gg.out_type = et;
         launch_gemm(gg, s);
-        resid(gm(*this, ST,y.wd, M, gua, Fa, et), ha, Da, nullptr, nullptr, s);
+        // then the next layer's RMSNorm, or the final one
+        const float* gn = l + 1 < c.act_layers ? act[l + 1].ln1 : lnf;
+        resid_norm(gm(*this, ST,y.wd, M, gua, Fa, et), ha, Da, nullptr, nullptr,
+                   nargs(M, Da, 0, ha, Da, za, Da, et, gn, nullptr, eps), s);
       }
-      norm(M, Da, 0, ha, Da, za, Da, et, lnf, nullptr, eps, s);
       GemmArgs go = gm(*this, ST,out, M, za, Da, et);
       go.mode = EPI_EULER; go.out = x; go.ldo = A; go.out_type = ET_F32; go.bias = out_b; go.dt = dt;
       launch_gemm(go, s);
@@ -638,10 +663,11 @@ void vla_model_s::enqueue_denoise(int B, const void* kv, const float* noise, int
     ga.tab = dpos + Da; ga.tab_period = H; ga.ldtab = Da;
     ga.row_group = H; ga.row_group_stride = (long)S * Da;
     store(ga, X + Da, Da, ET_F32, dain_b, ACT_NONE, s);
+    norm(M, Da, 2, X, Da, zd, Da, et, mk + 1 * Da, mk + 0 * Da, eps, s);
     for (int l = 0; l < NL; ++l) {
       const DitLayer& y = dit[l];
       const float* m6 = mk + (size_t)l * 6 * Da;
-      norm(M, Da, 2, X, Da, zd, Da, et, m6 + 1 * Da, m6 + 0 * Da, eps, s);
+      // zd holds the adaLN-modulated LN of X for this layer's self-attention
       GemmArgs q3 = gm(*this, ST,y.qkv, M, zd, Da, et);
       q3.mode = EPI_QKV; q3.out_type = et; q3.bias = y.bqkv;
       QkvEpi& e3 = q3.qkv;
@@ -656,9 +682,9 @@ void vla_model_s::enqueue_denoise(int B, const void* kv, const float* noise, int
       at.seg[1].len = 0;
       at.o = od; at.o_sb = (long)S * Da; at.o_sh = dhd; at.o_si = Da;
       launch_attention(at, s);
-      resid(gm(*this, ST,y.wo, M, od, Da, et), X, Da, y.bo, m6 + 2 * Da, s);
+      resid_norm(gm(*this, ST,y.wo, M, od, Da, et), X, Da, y.bo, m6 + 2 * Da,
+                 nargs(M, Da, 1, X, Da, zd, Da, et, nullptr, nullptr, eps), s);
       // cross-attention to the VLM features of the paired layer
-      norm(M, Da, 1, X, Da, zd, Da, et, nullptr, nullptr, eps, s);
       store(gm(*this, ST,y.cq, M, zd, Da, et), qc, Da, et, y.bcq, ACT_NONE, s);
       AttnArgs ac = attn(*this, ST,B, nh, nh, S, dhd, et);
       ac.q = qc; ac.q_sb = (long)S * Da; ac.q_sh = dhd; ac.q_si = Da;
@@ -668,10 +694,17 @@ void vla_model_s::enqueue_denoise(int B, const void* kv, const float* noise, int
       ac.seg[1].len = 0;
       ac.o = od; ac.o_sb = (long)S * Da; ac.o_sh = dhd; ac.o_si = Da;
       launch_attention(ac, s);
-      resid(gm(*this, ST,y.co, M, od, Da, et), X, Da, y.bco, nullptr, s);
-      norm(M, Da, 2, X, Da, zd, Da, et, m6 + 4 * Da, m6 + 3 * Da, eps, s);
+      resid_norm(gm(*this, ST,y.co, M, od, Da, et), X, Da, y.bco, nullptr,
+                 nargs(M, Da, 2, X, Da, zd, Da, et, m6 + 4 * Da, m6 + 3 * Da, eps), s);
       store(gm(*this, ST,y.w1, M, zd, Da, et), mlp, Fa, et, y.b1, ACT_GELU, s);
-      resid(gm(*this, ST,y.w2, M, mlp, Fa, et), X, Da, y.b2, m6 + 5 * Da, s);
+      if (l + 1 < NL) {
+        // then the next layer's self-attention adaLN
+        const float* n6 = m6 + 6 * Da;
+        resid_norm(gm(*this, ST,y.w2, M, mlp, Fa, et), X, Da, y.b2, m6 + 5 * Da,
+                   nargs(M, Da, 2, X, Da, zd, Da, et, n6 + 1 * Da, n6 + 0 * Da, eps), s);
+      } else {
+        resid(gm(*this, ST,y.w2, M, mlp, Fa, et), X, Da, y.b2, m6 + 5 * Da, s);
+      }
     }
     const float* mf = cc.modf + (size_t)k * 2 * Da;
     norm(B * H, Da, 2, X, Da, zf, Da, et, mf + Da, mf, eps, s, /*skip=*/1, /*skip_group=*/H);

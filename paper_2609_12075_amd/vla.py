@@ -24,7 +24,7 @@ VLA_OK, VLA_EINVAL, VLA_ENOMEM, VLA_EHIP, VLA_EUNSUPPORTED = range(5)
 # every exported symbol declared by include/vla.h and include/vla_debug.h
 EXPORTS = ["vla_weight_count", "vla_create_model", "vla_destroy_model", "vla_set_graphs", "vla_kv_bytes",
            "vla_prefill", "vla_prefill_ex", "vla_denoise", "vla_step", "vla_last_error",
-           "vla_debug_gemm", "vla_debug_attention", "vla_debug_cu_probe", "vla_debug_replay_gemm"]
+           "vla_debug_gemm", "vla_debug_resid_norm", "vla_debug_attention", "vla_debug_cu_probe", "vla_debug_replay_gemm"]
 
 
 class VlaError(RuntimeError):
@@ -72,6 +72,8 @@ def lib():
         L.vla_last_error.argtypes = []; L.vla_last_error.restype = ctypes.c_char_p
         L.vla_debug_gemm.argtypes = [ci, ci, ci, vp, ci, ci, vp, ci, ci, vp, ci, vp, ci, vp]
         L.vla_debug_gemm.restype = ci
+        L.vla_debug_resid_norm.argtypes = [ci, ci, ci, vp, vp, vp, vp, vp, ci, vp, vp, ctypes.c_float, vp, vp]
+        L.vla_debug_resid_norm.restype = ci
         L.vla_debug_attention.argtypes = [ci, ci, ci, ci, ci, ci, vp, vp, vp, ci, vp, vp, ci, vp, vp]
         L.vla_debug_attention.restype = ci
         L.vla_debug_cu_probe.argtypes = [ci, ci, ci, ci, ci, vp, vp]; L.vla_debug_cu_probe.restype = ci
@@ -210,6 +212,17 @@ def debug_gemm(A, Wt, bias=None, act=0, out=None, M=None, N=None, K=None, stream
     _check(lib().vla_debug_gemm(M, N, K, _ptr(A), A.shape[1], at, _ptr(Wt), Wt.shape[1], wt, _ptr(bias), act,
                                 _ptr(out), out.shape[1], _stream(stream)))
     return out
+
+
+def debug_resid_norm(A, Wt, x, kind, g=None, b=None, bias=None, gate=None, eps=1e-6, stream=None):
+    """x += gate * (A Wt^T + bias) in place; returns z = norm(x) (bf16)."""
+    import torch
+    M, K = A.shape
+    N = Wt.shape[0]
+    z = torch.empty(M, N, dtype=torch.bfloat16, device=A.device)
+    _check(lib().vla_debug_resid_norm(M, N, K, _ptr(A), _ptr(Wt), _ptr(bias), _ptr(gate), _ptr(x), kind, _ptr(g),
+                                      _ptr(b), ctypes.c_float(eps), _ptr(z), _stream(stream)))
+    return z
 
 
 def debug_attention(q, k0, v0, k1=None, v1=None, stream=None):

@@ -81,6 +81,42 @@ def test_gemm_f32(M, N, K):
     np.testing.assert_allclose(out.cpu().numpy(), ref, rtol=1e-5, atol=1e-5 * np.sqrt(K))
 
 
+@pytest.mark.parametrize("M,N,K,kind", [(50, 720, 960, 0), (50, 720, 1920, 0), (800, 720, 1920, 0),
+                                          (17, 1024, 4096, 2), (200, 1024, 2048, 1), (3840, 960, 960, 0),
+                                          (7, 36, 72, 1)])
+def test_resid_norm(M, N, K, kind):
+    """Residual projection + row norm (fused into the split-K reduce when
+    the projection splits K) against fp64."""
+    import torch
+    from paper_2609_12075_amd import vla
+    log(f"[resid_norm] M={M} N={N} K={K} kind={kind}")
+    A = _bf16(RNG.standard_normal((M, K)))
+    W = _bf16(RNG.standard_normal((N, K)) * 0.05)
+    x0 = RNG.standard_normal((M, N)).astype(np.float32)
+    bias = RNG.standard_normal(N).astype(np.float32) * 0.1
+    gate = (1 + 0.1 * RNG.standard_normal(N)).astype(np.float32) if kind == 2 else None
+    g = (1 + 0.1 * RNG.standard_normal(N)).astype(np.float32) if kind != 1 else None
+    b = (0.1 * RNG.standard_normal(N)).astype(np.float32) if kind == 2 else None
+    y = A.astype(np.float64) @ W.astype(np.float64).T + bias
+    if gate is not None:
+        y = y * gate
+    x_ref = x0.astype(np.float64) + y
+    if kind == 0:
+        z_ref = O.rmsnorm(x_ref, g.astype(np.float64), 1e-6)
+    else:
+        z_ref = O.layernorm(x_ref, None, None, 1e-6)
+        if kind == 2:
+            z_ref = z_ref * (1 + g) + b
+    t = lambda a: None if a is None else torch.from_numpy(a).cuda()
+    x = t(x0)
+    z = vla.debug_resid_norm(torch.from_numpy(A).to(torch.bfloat16).cuda(), torch.from_numpy(W).to(torch.bfloat16).cuda(),
+                             x, kind, g=t(g), b=t(b), bias=t(bias), gate=t(gate))
+    torch.cuda.synchronize()
+    np.testing.assert_allclose(x.cpu().numpy(), x_ref, rtol=1e-4, atol=1e-4)
+    zg = z.float().cpu().numpy()
+    assert np.abs(zg - z_ref).max() < 2e-2 * np.abs(z_ref).max(), np.abs(zg - z_ref).max()
+
+
 ATTN_SHAPES = [
     # (B, Hq, Hkv, Lq, hd, len0, len1)
     (2, 8, 1, 50, 256, 816, 50),     # pi0-shaped action decode
