@@ -124,6 +124,43 @@ def serve_main(args):
     result["lockstep_ms_lut"] = (dur_lut / 1e6).round(3).tolist()
     best_f = max(rates, key=lambda f: result["rates"][str(f)]["chunks_per_s_at_98_sim"])
     result["value"] = result["rates"][str(best_f)]["chunks_per_s_at_98_sim"]
+
+    # ---- controls and studies on the same profiled durations (simulated)
+    T, E = args.serve_seconds, args.serve_epochs
+    f0 = rates[0]
+    studies = {}
+    for label, d, kw in (("stage_disaggregated_esf", dur_lut, {}),
+                         ("monolithic_esf", dur_static[max(cus)], {"mode": "monolithic"}),
+                         ("stage_disaggregated_rr", dur_lut, {"policy": "rr"}),
+                         ("stage_disaggregated_lqf", dur_lut, {"policy": "lqf"})):
+        b, rows = serve.max_robots(d, slo, mb, f0, T, E, **kw)
+        at = {str(x["robots"]): round(x["attainment"], 4) for x in rows}
+        studies[label] = {"robots_at_98_sim": b, "chunks_per_s": b * f0, "attainment_by_robots": at}
+        log(f"[serve] study {label} @ {f0} Hz Poisson: {b} robots at 98%")
+    # the paper's traffic shape: periodic requests with a random phase per robot
+    # at 2 Hz, per-model SLOs (pi0-shaped 156 ms, SmolVLA-shaped 50 ms)
+    paper_slo = [{"pi0": 156.0, "smolvla": 50.0, "gr00t": 53.0}.get(n, args.slo_ms) for n in names]
+    for label, d, kw in (("periodic_2hz_paper_slo_disaggregated", dur_lut, {}),
+                         ("periodic_2hz_paper_slo_monolithic", dur_static[max(cus)], {"mode": "monolithic"})):
+        b, _ = serve.max_robots(d, paper_slo, mb, 2.0, T, E, traffic="periodic", r_max=512, **kw)
+        studies[label] = {"robots_at_98_sim": b, "chunks_per_s": b * 2.0, "slo_ms": paper_slo}
+        log(f"[serve] study {label}: {b} robots at 98%")
+    # per-model GPU robot limits (each model alone) and the traffic controller
+    # assignment they imply for a two-GPU server hosting both models
+    limits = []
+    for i, n in enumerate(names):
+        c, _ = serve.robot_limit(dur_lut, i, slo[i], mb, f0, T, E)
+        limits.append(max(c, 1))
+    # populations shaped like the paper's worked example: 1.5 GPUs' worth of
+    # the first model's robots, half a GPU's worth of the others (sum <= 2)
+    pops = [max(1, int(1.5 * limits[0]))] + [max(1, int(0.5 * c / max(1, len(names) - 1))) for c in limits[1:]]
+    r, obj, opt = serve.traffic_assign(np.ones((len(names), 2), dtype=int), pops, limits)
+    studies["robot_limits_alone"] = {n: c for n, c in zip(names, limits)}
+    studies["traffic_controller_2gpu_example"] = {"populations": dict(zip(names, pops)), "assignment": r.tolist(),
+                                                  "objective": obj, "optimal": opt}
+    log(f"[serve] robot limits alone {dict(zip(names, limits))}; 2-GPU assignment for {pops}: {r.tolist()} "
+        f"(eq (3) = {obj})")
+    result["studies"] = studies
     print(json.dumps(result), flush=True)
 
 

@@ -39,6 +39,13 @@ typedef struct vla_sched_s* vla_sched;
  * largest queue first (the paper's comparison policies, Section 5.3) */
 enum { VLA_SCHED_ESF = 0, VLA_SCHED_RR = 1, VLA_SCHED_LQF = 2 };
 
+/* execution modes: stage-disaggregated locksteps (the paper's design, the
+ * default) or Monolithic, the paper's control (Section 5): each admitted
+ * batch runs the VLM stage then the action stage back to back on the whole
+ * GPU and completes before the next batch starts (simulated duration: the
+ * two stages' stand-alone table entries plus two host overheads). */
+enum { VLA_SCHED_LOCKSTEP = 0, VLA_SCHED_MONOLITHIC = 1 };
+
 typedef struct {
   int n_models;            /* 1 .. 16 */
   const double* slo_ms;    /* [n_models] per-model deadline (ms), copied */
@@ -89,6 +96,10 @@ typedef struct {
 } vla_sched_model_io;
 vla_status vla_sched_set_gpu_executor(vla_sched s, const vla_sched_model_io* io, hipStream_t join);
 
+/* Execution mode (VLA_SCHED_LOCKSTEP or VLA_SCHED_MONOLITHIC); the default
+ * is LOCKSTEP. Monolithic ignores the CU table. */
+vla_status vla_sched_set_mode(vla_sched s, int mode);
+
 /* CU restriction of the VLM stream per lockstep: `default_cu` (multiple of 8,
  * 8 .. 256) unless `cu_table` (same indexing as the duration table, entries 0
  * = use default) names another count for the batch combination (the
@@ -105,6 +116,27 @@ vla_status vla_sched_set_cu(vla_sched s, int default_cu, const int* cu_table);
 vla_status vla_sched_run(vla_sched s, const int64_t* t_arrival_ns, const int32_t* model, int n,
                          int64_t drain_ns, vla_request_rec* req_out, vla_lockstep_rec* ls_out, int ls_cap,
                          int* n_ls_out);
+
+/*
+ * Adaptive traffic controller (Section 4.2.2): robot-to-GPU assignment for a
+ * multi-GPU server, solved once at initialisation on the host.
+ *   host      [n_models][n_gpus] placement, 1 where GPU j hosts model i
+ *   n_robots  [n_models] robot population N_i (>= 0)
+ *   limits    [n_models] C_i >= 1: robots of model i one GPU sustains at the
+ *             SLO-attainment target (found by benchmarking the model alone)
+ *   r_out     [n_models][n_gpus] robots of model i assigned to GPU j
+ * Constraints: eq (1) sum_j r[i][j] = N_i; eq (2) sum_i r[i][j] / C_i <= 1
+ * (exact rational test); r[i][j] = 0 where not hosted. Objective, eq (3):
+ * minimise sum_j sum_{i<k} r[i][j] r[k][j] (per-GPU traffic concentrated on
+ * few models). Exact branch and bound; it stops after max_nodes search nodes
+ * and sets *optimal = 1 only when the optimum was proven. Optimal
+ * assignments need not be unique (interchangeable GPUs); *objective is.
+ * Returns VLA_EINVAL when no assignment satisfies the constraints ("change
+ * the placement or add GPUs"), VLA_EUNSUPPORTED when the node limit is hit
+ * before any feasible assignment is found. Host-only; no GPU is used.
+ */
+vla_status vla_traffic_assign(int n_models, int n_gpus, const int* host, const int* n_robots, const int* limits,
+                              long long max_nodes, int* r_out, long long* objective, int* optimal);
 
 #ifdef __cplusplus
 }

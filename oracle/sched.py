@@ -18,6 +18,11 @@ no code with the library's C++ scheduler.
   largest-queue-first are the comparison policies of Section 5.3.
 * Section 5.1: a request meets its SLO when its end-to-end latency is within
   the deadline (network latency taken as zero here).
+* Monolithic, the paper's control system (Section 5): no stage
+  disaggregation; the admitted batch runs the VLM stage and then the action
+  stage back to back on the whole GPU and completes before the next batch is
+  admitted (duration: the two stand-alone table entries plus two host
+  overheads).
 
 The executor is a table of lockstep durations indexed by
 (VLM model, VLM batch bucket, action model, action batch bucket), bucket 0 =
@@ -43,7 +48,7 @@ def largest_pow2_at_most(x):
 
 
 def simulate(arrivals, slo_ms, max_batch, dur_ns, policy="esf", drain_ns=10 ** 9, overhead_ns=0,
-             cu_default=256, cu_table=None):
+             cu_default=256, cu_table=None, mode="lockstep"):
     """arrivals: list of (t_ns, model) sorted by time. dur_ns: nested lists
     [mv][bv_bucket][ma][ba_bucket]. Returns (requests, locksteps): requests =
     list of dicts (t_arrival, t_vlm_start, t_done, model, met), locksteps =
@@ -82,6 +87,15 @@ def simulate(arrivals, slo_ms, max_batch, dur_ns, policy="esf", drain_ns=10 ** 9
                 mv = min(candidates, key=lambda m: (-len(queues[m]), m))
             bv = largest_pow2_at_most(min(len(queues[mv]), max_batch))
         admitted = [queues[mv].popleft() for _ in range(bv)]
+        if mode == "monolithic":
+            end = now + dur_ns[mv][bucket(bv)][0][0] + dur_ns[0][0][mv][bucket(bv)] + 2 * overhead_ns
+            for r in admitted:
+                reqs[r]["t_vlm_start"] = now
+                reqs[r]["t_done"] = end
+            locksteps.append((now, end, mv, bv, mv, bv, 256, 0))
+            k += 1
+            now = end
+            continue
         ma, ba = (handoff_model, len(handoff)) if handoff else (-1, 0)
         slot = k % 2
         iv, ia = bucket(bv), bucket(ba)

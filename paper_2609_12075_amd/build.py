@@ -22,7 +22,7 @@ OUT = os.path.join(PKG, "libvla.so")
 BUILD_DIR = os.path.join(ROOT, "_build")
 ARCH = "gfx950"
 
-SOURCES = ["k_gemm.hip", "k_attn.hip", "k_elem.hip", "model.hip", "capi.hip", "sched.hip"]
+SOURCES = ["k_gemm.hip", "k_attn.hip", "k_elem.hip", "model.hip", "capi.hip", "sched.hip", "traffic.hip"]
 FLAGS = ["--offload-arch=" + ARCH, "-O3", "-fPIC", "-std=c++17", "-Wall", "-Wno-unused-result",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops", "-I", INCLUDE, "-I", CSRC]
 

@@ -32,6 +32,7 @@ int pow2_floor(int x) {
 
 struct vla_sched_s {
   int n_models = 0, max_batch = 1, policy = VLA_SCHED_ESF, n_buckets = 2;
+  int mode = VLA_SCHED_LOCKSTEP;
   std::vector<int64_t> slo_ns;
   // executor
   int exec_kind = 0;                       // 0 none, 1 simulated, 2 GPU
@@ -112,6 +113,19 @@ vla_status vla_sched_set_gpu_executor(vla_sched s, const vla_sched_model_io* io,
     s->io.assign(io, io + s->n_models);
     s->join = join;
     s->exec_kind = 2;
+    return VLA_OK;
+  } catch (const VlaError& e) {
+    vla_set_error(e.msg);
+    return (vla_status)e.status;
+  }
+}
+
+vla_status vla_sched_set_mode(vla_sched s, int mode) {
+  try {
+    vla_clear_error();
+    VLA_REQUIRE(s, "null scheduler");
+    VLA_REQUIRE(mode == VLA_SCHED_LOCKSTEP || mode == VLA_SCHED_MONOLITHIC, "unknown execution mode");
+    s->mode = mode;
     return VLA_OK;
   } catch (const VlaError& e) {
     vla_set_error(e.msg);
@@ -207,6 +221,37 @@ vla_status vla_sched_run(vla_sched s, const int64_t* t_arr, const int32_t* model
       }
       std::vector<int> vreq;
       for (int j = 0; j < bv; ++j) vreq.push_back(q[mv].front()), q[mv].pop_front();
+      if (s->mode == VLA_SCHED_MONOLITHIC) {
+        // the batch runs both stages back to back, unrestricted, and completes
+        int64_t t_end;
+        if (sim) {
+          t_end = now + s->dur_ns[s->combo(mv, bv, -1, 0)] + s->dur_ns[s->combo(-1, 0, mv, bv)] +
+                  2 * s->host_overhead_ns;
+        } else {
+          const vla_sched_model_io& x = s->io[mv];
+          vla_step_args a{};
+          a.vlm_model = x.model; a.vlm_batch = bv;
+          a.pixels = x.pixels; a.text_ids = x.text_ids; a.state = x.state; a.kv_out = x.kv[0];
+          a.vlm_cu_count = 256;
+          vla_status st = vla_step(&a, s->join);
+          if (st == VLA_OK) {
+            vla_step_args d{};
+            d.adit_model = x.model; d.adit_batch = bv;
+            d.kv_in = x.kv[0]; d.noise = x.noise; d.steps = x.steps; d.actions_out = x.actions[0];
+            d.vlm_cu_count = 256;
+            st = vla_step(&d, s->join);
+          }
+          if (st != VLA_OK) throw VlaError{(int)st, std::string("monolithic step: ") + vla_last_error()};
+          VLA_HIP(hipStreamSynchronize(s->join));
+          t_end = wall_ns();
+        }
+        for (int r : vreq) req_out[r].t_vlm_start_ns = now, req_out[r].t_done_ns = t_end;
+        if (n_ls < ls_cap) ls_out[n_ls] = vla_lockstep_rec{now, t_end, mv, bv, mv, bv, 256, 0};
+        ++n_ls;
+        ++k;
+        if (sim) t_sim = t_end;
+        continue;
+      }
       const int ma = buf.empty() ? -1 : buf_model, ba = (int)buf.size();
       const int slot = k & 1;
       int cu = s->default_cu;

@@ -15,6 +15,7 @@ import numpy as np
 from . import synth, vla
 
 POLICIES = {"esf": 0, "rr": 1, "lqf": 2}
+MODES = {"lockstep": 0, "monolithic": 1}
 
 REQ_DTYPE = np.dtype([("t_arrival_ns", np.int64), ("t_vlm_start_ns", np.int64), ("t_done_ns", np.int64),
                       ("model", np.int32), ("met_slo", np.int32)])
@@ -43,8 +44,12 @@ def _lib():
         L.vla_sched_set_sim_executor.argtypes = [vp, vp, i64]; L.vla_sched_set_sim_executor.restype = ci
         L.vla_sched_set_gpu_executor.argtypes = [vp, vp, vp]; L.vla_sched_set_gpu_executor.restype = ci
         L.vla_sched_set_cu.argtypes = [vp, ci, vp]; L.vla_sched_set_cu.restype = ci
+        L.vla_sched_set_mode.argtypes = [vp, ci]; L.vla_sched_set_mode.restype = ci
         L.vla_sched_run.argtypes = [vp, vp, vp, ci, i64, vp, vp, ci, ctypes.POINTER(ci)]
         L.vla_sched_run.restype = ci
+        L.vla_traffic_assign.argtypes = [ci, ci, vp, vp, vp, ctypes.c_longlong, vp, ctypes.POINTER(ctypes.c_longlong),
+                                         ctypes.POINTER(ci)]
+        L.vla_traffic_assign.restype = ci
         L._sched_bound = True
     return L
 
@@ -65,7 +70,7 @@ def bucket_batches(max_batch: int) -> List[int]:
 class Scheduler:
     """One serving scheduler over co-located models (see include/vla_sched.h)."""
 
-    def __init__(self, slo_ms: Sequence[float], max_batch: int, policy: str = "esf"):
+    def __init__(self, slo_ms: Sequence[float], max_batch: int, policy: str = "esf", mode: str = "lockstep"):
         self.n_models = len(slo_ms)
         self.max_batch = max_batch
         self._slo = (ctypes.c_double * self.n_models)(*[float(x) for x in slo_ms])
@@ -74,6 +79,7 @@ class Scheduler:
         vla._check(_lib().vla_sched_create(ctypes.byref(cfg), ctypes.byref(h)))
         self.handle = h
         self._keep = []
+        vla._check(_lib().vla_sched_set_mode(self.handle, MODES[mode]))
 
     def close(self):
         if getattr(self, "handle", None):
@@ -221,7 +227,7 @@ def best_cu_table(prof: np.ndarray, cu_counts: Sequence[int]):
 
 def sweep_robots(dur_ns: np.ndarray, slo_ms: Sequence[float], max_batch: int, robots: Sequence[int], rate_hz,
                  duration_s: float, epochs: int, policy: str = "esf", host_overhead_ns: int = 0,
-                 traffic: str = "poisson", target: float = 0.98):
+                 traffic: str = "poisson", target: float = 0.98, mode: str = "lockstep"):
     """Simulated robot-load sweep on a lockstep-duration table: for each robot
     count, the mean SLO attainment over `epochs` seeded traces. Returns
     (rows, max robots with attainment >= target)."""
@@ -231,7 +237,7 @@ def sweep_robots(dur_ns: np.ndarray, slo_ms: Sequence[float], max_batch: int, ro
         att, p99 = [], []
         for e in range(epochs):
             arr = gen(R, rate_hz, duration_s, e, n_models=len(slo_ms))
-            s = Scheduler(slo_ms, max_batch, policy)
+            s = Scheduler(slo_ms, max_batch, policy, mode)
             s.set_sim(dur_ns, host_overhead_ns)
             req, _ = s.run(arr, drain_ns=int(1e9), ls_cap=16)
             s.close()
@@ -242,3 +248,60 @@ def sweep_robots(dur_ns: np.ndarray, slo_ms: Sequence[float], max_batch: int, ro
         if a >= target:
             best = max(best, int(R))
     return rows, best
+
+
+def max_robots(dur_ns: np.ndarray, slo_ms: Sequence[float], max_batch: int, rate_hz, duration_s: float,
+               epochs: int, policy: str = "esf", traffic: str = "poisson", mode: str = "lockstep",
+               target: float = 0.98, r_max: int = 256, patience: int = 3, host_overhead_ns: int = 0):
+    """Largest robot count with mean simulated SLO attainment >= target,
+    scanning upwards and stopping after `patience` consecutive failures.
+    Returns (robots, rows)."""
+    rows, best, fails = [], 0, 0
+    for R in range(1, r_max + 1):
+        r, _ = sweep_robots(dur_ns, slo_ms, max_batch, [R], rate_hz, duration_s, epochs, policy, host_overhead_ns,
+                            traffic, target, mode)
+        rows += r
+        if r[0]["attainment"] >= target:
+            best, fails = R, 0
+        else:
+            fails += 1
+            if fails >= patience:
+                break
+    return best, rows
+
+
+def robot_limit(dur_ns: np.ndarray, model: int, slo_ms: float, max_batch: int, rate_hz, duration_s: float,
+                epochs: int, target: float = 0.98, max_robots: int = 256, policy: str = "esf",
+                traffic: str = "poisson", host_overhead_ns: int = 0):
+    """Robots one GPU sustains for `model` served alone (Section 4.2.2,
+    finding GPU robot limits): raise the robot count until the simulated SLO
+    attainment on the model's own lockstep durations falls below `target`;
+    returns (limit, rows). dur_ns is a co-location table; its (model, model)
+    slice is used."""
+    sub = np.ascontiguousarray(dur_ns[model:model + 1, :, model:model + 1, :])
+    rows, limit = [], 0
+    for R in range(1, max_robots + 1):
+        r, _ = sweep_robots(sub, [slo_ms], max_batch, [R], rate_hz, duration_s, epochs, policy, host_overhead_ns,
+                            traffic, target)
+        rows += r
+        if r[0]["attainment"] < target:
+            break
+        limit = R
+    return limit, rows
+
+
+def traffic_assign(host, n_robots, limits, max_nodes: int = 10_000_000):
+    """Robot-to-GPU assignment of the adaptive traffic controller (eqs (1)-(3)
+    of Section 4.2.2) by the library's exact search. host: [models][gpus] 0/1;
+    returns (r [models][gpus], objective, proven_optimal)."""
+    host = np.ascontiguousarray(host, dtype=np.int32)
+    n = np.ascontiguousarray(n_robots, dtype=np.int32)
+    c = np.ascontiguousarray(limits, dtype=np.int32)
+    M, G = host.shape
+    if n.shape != (M,) or c.shape != (M,):
+        raise ValueError("n_robots and limits need one entry per model")
+    r = np.zeros((M, G), dtype=np.int32)
+    obj, opt = ctypes.c_longlong(0), ctypes.c_int(0)
+    vla._check(_lib().vla_traffic_assign(M, G, host.ctypes.data, n.ctypes.data, c.ctypes.data, int(max_nodes),
+                                         r.ctypes.data, ctypes.byref(obj), ctypes.byref(opt)))
+    return r, int(obj.value), bool(opt.value)

@@ -22,8 +22,8 @@ def const_table(n_models, max_batch, ns):
     return t
 
 
-def run(items, slo, max_batch, table, policy="esf", drain=10 ** 9, overhead=0):
-    s = serve.Scheduler(slo, max_batch, policy)
+def run(items, slo, max_batch, table, policy="esf", drain=10 ** 9, overhead=0, mode="lockstep"):
+    s = serve.Scheduler(slo, max_batch, policy, mode)
     s.set_sim(table, overhead)
     req, ls = s.run(arr(items), drain)
     s.close()
@@ -141,6 +141,33 @@ def test_matches_reference_scheduler(seed):
     for a, b in zip(req, rreq):
         assert (int(a["t_arrival_ns"]), int(a["t_vlm_start_ns"]), int(a["t_done_ns"]), int(a["model"]),
                 int(a["met_slo"])) == (b["t_arrival"], b["t_vlm_start"], b["t_done"], b["model"], b["met"])
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_monolithic_matches_reference(seed):
+    items, slo, mb, table, policy, overhead = _random_case(seed + 100)
+    req, ls = run(items, slo, mb, table, policy=policy, overhead=overhead, mode="monolithic")
+    rreq, rls = REF.simulate(items, slo, mb, table.tolist(), policy=policy, overhead_ns=overhead, mode="monolithic")
+    assert [tuple(int(v) for v in a) for a in ls] == [tuple(b) for b in rls]
+    for a, b in zip(req, rreq):
+        assert (int(a["t_vlm_start_ns"]), int(a["t_done_ns"]), int(a["met_slo"])) == \
+            (b["t_vlm_start"], b["t_done"], b["met"])
+
+
+def test_monolithic_serialises_stages():
+    """Monolithic: a batch's latency is VLM-alone + action-alone, with no
+    overlap across batches; the lockstep pipeline finishes the same single
+    batch after two locksteps."""
+    mb = 1
+    nb = serve.n_buckets(mb)
+    table = np.zeros((1, nb, 1, nb), dtype=np.int64)
+    table[0, 1, 0, 0] = 7 * MS        # VLM alone
+    table[0, 0, 0, 1] = 5 * MS        # action stage alone
+    table[0, 1, 0, 1] = 9 * MS        # co-executed
+    req, ls = run([(0, 0), (0, 0)], [100.0], mb, table, mode="monolithic")
+    assert req["t_done_ns"].tolist() == [12 * MS, 24 * MS]
+    req, ls = run([(0, 0), (0, 0)], [100.0], mb, table)
+    assert req["t_done_ns"].tolist() == [16 * MS, 21 * MS]     # 7 | 9 | 5
 
 
 def test_overrun_and_starvation_injection():
