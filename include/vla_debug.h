@@ -71,9 +71,11 @@ vla_status vla_debug_cu_probe(int device, int cu_count, int from_top, int blocks
  * workspace buffers), on `stream`, and store the algorithmic flops of one
  * launch (2 M N K) in *flops (may be NULL). For timing one kernel with events
  * around the loop. It overwrites the stage's workspace: do not overlap it
- * with that model's stages. which: 0 VLM LLM layer-0 MLP gate/up (GeGLU),
- * 1 VLM LLM layer-0 MLP down, 2 action-stage layer-0 MLP up, 3 action-stage
- * layer-0 MLP down, 4 ViT layer-0 MLP up. plan (may be NULL): int[5] set to
+ * with that model's stages. which: 0 VLM LLM MLP gate/up (GeGLU), 1 VLM LLM
+ * MLP down, 2 action-stage MLP up, 3 action-stage MLP down, 4 ViT MLP up;
+ * launch i uses layer (i mod layer count)'s weights, so, as in a pass over
+ * the stage, each launch reads weights the previous launches did not.
+ * plan (may be NULL): int[5] set to
  * the kernel's tile (weight rows, activation rows), number of K ranges
  * (1 = one kernel, > 1 = partial + reduce kernels), epilogue mode and kernel
  * kind (0 register-pipelined, 1 LDS-staged, 2 small-M).

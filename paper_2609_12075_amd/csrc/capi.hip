@@ -350,7 +350,9 @@ vla_status vla_debug_replay_gemm(vla_model m, int which, int batch, int iters, h
       const GemmPlan p = gemm_plan(a);
       plan[0] = p.bn; plan[1] = p.bm; plan[2] = p.splits; plan[3] = a.mode; plan[4] = p.kind;
     }
-    for (int i = 0; i < iters; ++i) launch_gemm(a, s);
+    // launch i uses layer i's weights (cycling), so weights are re-read from
+    // memory as in a pass over the stage rather than served from cache
+    for (int i = 0; i < iters; ++i) launch_gemm(m->stage_gemm(which, batch, i), s);
     VLA_HIP(hipGetLastError());
   });
 }

@@ -114,7 +114,7 @@ struct vla_model_s {
   const CondCache& cond_for(int N, hipStream_t s);
   void run_graph(int stage, const GraphKey& key, hipStream_t s, const std::function<void(hipStream_t)>& body);
   // One projection of a stage exactly as the stage launches it (for timing).
-  GemmArgs stage_gemm(int which, int B) const;
+  GemmArgs stage_gemm(int which, int B, int layer = 0) const;
 };
 
 // Host-side validation of a shape; returns "" if valid, else the reason.

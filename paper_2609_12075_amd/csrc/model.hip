@@ -772,41 +772,43 @@ void vla_model_s::denoise(int B, const void* kv, const float* noise, int N, floa
 }
 
 // ---------------------------------------------------------------- timing hook
-GemmArgs vla_model_s::stage_gemm(int which, int B) const {
+GemmArgs vla_model_s::stage_gemm(int which, int B, int layer) const {
   const int ST = (which == 2 || which == 3) ? STAGE_DENOISE : STAGE_PREFILL;
   const vla_config& c = cfg;
   GemmArgs g{};
+  const int ll = layer % std::max(1, c.llm_layers), la = layer % std::max(1, c.act_layers);
+  const int lv = layer % std::max(1, c.vit_layers);
   switch (which) {
-    case 0:   // VLM stage: LLM layer 0 MLP gate/up (GeGLU epilogue)
-      g = gm(*this, ST,llm[0].gu, B * P, z, D, et);
+    case 0:   // VLM stage: LLM layer MLP gate/up (GeGLU epilogue)
+      g = gm(*this, ST,llm[ll].gu, B * P, z, D, et);
       g.mode = EPI_GEGLU; g.out = gu; g.ldo = c.llm_mlp; g.out_type = et;
       break;
-    case 1:   // VLM stage: LLM layer 0 MLP down projection (+ residual)
-      g = gm(*this, ST,llm[0].wd, B * P, gu, c.llm_mlp, et);
+    case 1:   // VLM stage: LLM layer MLP down projection (+ residual)
+      g = gm(*this, ST,llm[ll].wd, B * P, gu, c.llm_mlp, et);
       g.mode = EPI_RESID; g.out = h; g.ldo = D; g.out_type = ET_F32;
       break;
-    case 2:   // action stage: layer 0 MLP up (GeGLU for the joint expert, GELU for the DiT)
+    case 2:   // action stage: layer MLP up (GeGLU for the joint expert, GELU for the DiT)
       if (c.head_kind == VLA_HEAD_JOINT) {
-        g = gm(*this, ST,act[0].gu, B * H, za, Da, et);
+        g = gm(*this, ST,act[la].gu, B * H, za, Da, et);
         g.mode = EPI_GEGLU; g.out = gua; g.ldo = c.act_mlp; g.out_type = et;
       } else {
-        g = gm(*this, ST,dit[0].w1, B * Ltok, zd, Da, et);
-        g.mode = EPI_STORE; g.act = ACT_GELU; g.bias = dit[0].b1; g.out = mlp; g.ldo = c.act_mlp; g.out_type = et;
+        g = gm(*this, ST,dit[la].w1, B * Ltok, zd, Da, et);
+        g.mode = EPI_STORE; g.act = ACT_GELU; g.bias = dit[la].b1; g.out = mlp; g.ldo = c.act_mlp; g.out_type = et;
       }
       break;
-    case 3:   // action stage: layer 0 MLP down projection (+ residual)
+    case 3:   // action stage: layer MLP down projection (+ residual)
       if (c.head_kind == VLA_HEAD_JOINT) {
-        g = gm(*this, ST,act[0].wd, B * H, gua, c.act_mlp, et);
+        g = gm(*this, ST,act[la].wd, B * H, gua, c.act_mlp, et);
         g.mode = EPI_RESID; g.out = ha; g.ldo = Da; g.out_type = ET_F32;
       } else {
-        g = gm(*this, ST,dit[0].w2, B * Ltok, mlp, c.act_mlp, et);
-        g.mode = EPI_RESID; g.bias = dit[0].b2; g.out = X; g.ldo = Da; g.out_type = ET_F32;
+        g = gm(*this, ST,dit[la].w2, B * Ltok, mlp, c.act_mlp, et);
+        g.mode = EPI_RESID; g.bias = dit[la].b2; g.out = X; g.ldo = Da; g.out_type = ET_F32;
       }
       break;
-    case 4:   // VLM stage: ViT layer 0 MLP up (GELU)
+    case 4:   // VLM stage: ViT layer MLP up (GELU)
       VLA_REQUIRE(c.vit_layers > 0, "model has no ViT");
-      g = gm(*this, ST,vit[0].w1, B * c.n_img * T, vz, c.vit_d, et);
-      g.mode = EPI_STORE; g.act = ACT_GELU; g.bias = vit[0].b1; g.out = vmlp; g.ldo = c.vit_mlp; g.out_type = et;
+      g = gm(*this, ST,vit[lv].w1, B * c.n_img * T, vz, c.vit_d, et);
+      g.mode = EPI_STORE; g.act = ACT_GELU; g.bias = vit[lv].b1; g.out = vmlp; g.ldo = c.vit_mlp; g.out_type = et;
       break;
     default:
       throw VlaError{1, "unknown projection index"};

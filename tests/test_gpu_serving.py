@@ -42,3 +42,30 @@ def test_scheduler_on_gpu_two_models():
         got = bufs[m]["act%d" % slot][:b].cpu().numpy()
         ref, _ = run(cfg, synth.make_inputs(cfg, b))
         np.testing.assert_array_equal(got, ref)
+
+
+def test_monolithic_on_gpu():
+    """The Monolithic control on the GPU: each batch runs the VLM stage and then
+    the action stage back to back; every request is served and the last
+    batch's actions equal a standalone run."""
+    import torch
+    from paper_2609_12075_amd import serve
+    ma, mb = model(A), model(B)
+    mbatch = 4
+    bufs = serve.alloc_io([ma, mb], mbatch)
+    s = serve.Scheduler([100.0, 100.0], mbatch, "esf", "monolithic")
+    s.set_gpu([ma, mb], bufs)
+    arr = synth.poisson_arrivals(4, 20.0, 0.5, epoch=1, n_models=2)
+    log(f"[serving] monolithic: {len(arr)} requests over 0.5 s")
+    req, ls = s.run(arr, drain_ns=int(2e9))
+    torch.cuda.synchronize()
+    s.close()
+    assert (req["t_done_ns"] > 0).all()
+    assert (ls["vlm_model"] == ls["adit_model"]).all() and (ls["vlm_batch"] == ls["adit_batch"]).all()
+    assert int(ls["vlm_batch"].sum()) == len(arr)
+    for m, cfg in ((0, A), (1, B)):
+        last = [x for x in ls if x["vlm_model"] == m][-1]
+        b = int(last["vlm_batch"])
+        got = bufs[m]["act0"][:b].cpu().numpy()
+        ref, _ = run(cfg, synth.make_inputs(cfg, b))
+        np.testing.assert_array_equal(got, ref)
