@@ -312,6 +312,7 @@ vla_status vla_debug_attention(int B, int Hq, int Hkv, int Lq, int hd, int et, c
     a.seg[1] = AttnSeg{k1, (long)Hkv * len1 * hd, (long)len1 * hd, hd, v1, (long)Hkv * len1 * hd, (long)len1 * hd, hd, len1};
     a.o = o; a.o_sb = (long)Lq * Hq * hd; a.o_sh = hd; a.o_si = (long)Hq * hd;   // [B][Lq][Hq*hd]
     a.ws = debug_ws(1, vla_model_s::kAttnFloats); a.ws_floats = vla_model_s::kAttnFloats;
+    a.zeros = debug_ws(2, 64);
     launch_attention(a, s);
     VLA_HIP(hipGetLastError());
   });

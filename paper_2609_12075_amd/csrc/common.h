@@ -48,6 +48,26 @@ __device__ __forceinline__ void xcd_remap(int& bx, int& by, int& bz) {
   bz = (int)(u / (gx * gy));
 }
 
+// The same die assignment for a matrix product's (M tile, N tile, K range)
+// grid, with the logical order grouped: GM M tiles at a time, N tiles within
+// a group, M fastest within a column of the group. A die's contiguous run of
+// logical blocks, and so the ~64 blocks it holds at once, then covers a
+// compact GM x (64 / GM) patch of output tiles, whose operand slices its L2
+// shares, instead of every M tile of a few columns (which would stream all
+// of A through the L2 again for every few columns).
+__device__ __forceinline__ void xcd_remap_grouped(int& bx, int& by, int& bz, int GM) {
+  const long gx = gridDim.x, gy = gridDim.y, T = gx * gy * (long)gridDim.z;
+  const long L = blockIdx.x + gx * (blockIdx.y + gy * (long)blockIdx.z);
+  const long q = T / 8, r = T % 8, x = L % 8, j = L / 8;
+  const long u = x * q + (x < r ? x : r) + j;
+  const long plane = gx * gy, v = u % plane;
+  bz = (int)(u / plane);
+  const long g = v / (GM * gy), m0 = g * GM, gm = gx - m0 < GM ? gx - m0 : GM;
+  const long local = v - g * GM * gy;
+  bx = (int)(m0 + local % gm);
+  by = (int)(local / gm);
+}
+
 static inline size_t elem_size(int et) { return et == ET_BF16 ? 2 : 4; }
 
 // GEMM: D[m][n] = sum_k A[m][k] * W[n][k] for m < M, n < N.
@@ -131,6 +151,7 @@ struct AttnArgs {
   // and softmax statistics, and a second kernel merges them in range order.
   float* ws; long ws_floats;
   int splits, kchunk;       // set by launch_attention
+  const void* zeros;        // >= 16 zero bytes (fill of chunks past hd); required for bf16
 };
 void launch_attention(const AttnArgs& a, hipStream_t s);
 

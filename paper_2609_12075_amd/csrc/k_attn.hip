@@ -376,7 +376,320 @@ __global__ void __launch_bounds__(64) attn_f32_kernel(AttnArgs a) {
   }
 }
 
+
+// ---------------------------------------------------------------- v2 kernel
+// Same row decomposition, softmax and products as attn_mfma_kernel, with the
+// K/V staging of the multi-stage projection kernel: tiles move global -> LDS
+// with the CDNA4 direct loads (global_load_lds_dwordx4, lane l's 16 bytes at
+// LDS base + 16 l) through a ring of NS tiles, so the next round of tiles
+// loads while this one is consumed, without registers. Rows are unpadded and
+// key-major for both K and V; the 16-byte chunk c of row r sits in slot
+// c ^ swz(r), which makes the 16-row fragment reads conflict-free. The P V
+// product needs V^T fragments (one dimension, 8 keys per lane); they come
+// from the transposing LDS read (ds_read_b64_tr_b16): within each 16-lane
+// group, source lane s points at 4 dimensions of one key row (row
+// 4-block + s / 4, dims 4 (s % 4) ..), and lane i receives dimension i of the
+// group's 4 keys. Chunks past hd and keys past the range read zeros.
+//
+// KS > 1 splits the block's key range over KS groups of 4 waves (tile t goes
+// to group t % KS), so short decode ranges run KS tiles at a time with KS
+// waves per SIMD; the groups' (max, sum, output) are merged through LDS at
+// the end in group order (as the split-KV combine does across blocks).
+typedef short v4s __attribute__((ext_vector_type(4)));
+
+template <int HDP>
+struct V2 {
+  static constexpr int BKV = HDP >= 256 ? 32 : 64;          // keys per tile
+  static constexpr int CR = HDP / 8;                          // 16-byte chunks per row
+  static constexpr int ROWB = HDP * 2;
+  static constexpr int TILE = BKV * ROWB;                     // bytes of a K (or V) tile
+  static constexpr int NS = 2 * TILE <= 16384 ? 4 : 2;        // ring depth in tiles (KS = 1)
+  static constexpr int RP = CR >= 16 ? 1 : 16 / CR;           // rows per 256 bytes (one bank cycle)
+  static constexpr int SWM = (CR >= 16 ? 16 : CR) - 1;
+  __device__ static constexpr int swz(int r) { return (r / RP) & SWM; }
+};
+
+template <int HDP, int KS>
+__global__ void __launch_bounds__(256 * KS) attn_v2_kernel(AttnArgs a) {
+  using C = V2<HDP>;
+  constexpr int BKV = C::BKV, ROWB = C::ROWB, TILE = C::TILE, CR = C::CR;
+  constexpr int NW = 4 * KS;                       // waves per block
+  constexpr int IW = TILE / 1024 / NW;             // 1 KiB direct loads per wave per tile (K or V)
+  static_assert(IW >= 1 && IW * NW * 1024 == TILE, "tile loads must spread evenly over the waves");
+  constexpr int NR = KS == 1 ? C::NS : 2;          // ring depth in rounds of KS tiles
+  constexpr int NC = HDP / 32, ND = HDP / 16;
+  constexpr int RING = NR * KS * 2 * TILE;
+  constexpr int MST = ND * 4 + 4;                   // merge record: o, m, l, pad (16-byte aligned)
+  constexpr int MERGE = KS > 1 ? (KS - 1) * 256 * MST * 4 : 0;
+  __shared__ __attribute__((aligned(1024))) char smem[RING > MERGE ? RING : MERGE];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int kg = wave >> 2, wrow = wave & 3;       // key group, row group
+  const int S = a.splits > 1 ? a.splits : 1;
+  int bx, by, bz;
+  xcd_remap(bx, by, bz);
+  const int b = bz / S, split = bz % S, g = by;
+  const int G = a.Hq / a.Hkv;
+  const int rows = G * a.Lq;
+  const int hd = a.hd;
+  const int lq = lane & 15, grp = lane >> 4;
+
+  const int r = bx * BQ + wrow * 16 + lq;
+  const bool rvalid = r < rows;
+  const int jh = rvalid ? r / a.Lq : 0, qi = rvalid ? r % a.Lq : 0;
+  const int h = g * G + jh;
+
+  bf16x8 qf[NC];
+  {
+    const bf16* qp = reinterpret_cast<const bf16*>(a.q) + (long)b * a.q_sb + (long)h * a.q_sh + (long)qi * a.q_si;
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+      const int d = c * 32 + grp * 8;
+      qf[c] = (rvalid && d < hd) ? *reinterpret_cast<const bf16x8*>(qp + d) : bf16x8{};
+    }
+  }
+
+  const int len0 = a.seg[0].len;
+  const int kbeg = S > 1 ? split * a.kchunk : 0;
+  const int kend = S > 1 ? min(len0 + a.seg[1].len, kbeg + a.kchunk) : len0 + a.seg[1].len;
+  const int nt = kend > kbeg ? (kend - kbeg + BKV - 1) / BKV : 0;
+  const int nrounds = (nt + KS - 1) / KS;
+  const bf16* Z = reinterpret_cast<const bf16*>(a.zeros);
+
+  // round p holds tiles p KS .. p KS + KS - 1 in ring slot p % NR; each tile
+  // is its K tile then its V tile. 16-byte unit u of a tile is (row u / CR,
+  // slot u % CR); wave w loads units [(i NW + w) 64, + 64) for i < IW.
+  auto issue = [&](int p) {
+    char* base = smem + (p % NR) * KS * 2 * TILE;
+#pragma unroll
+    for (int q = 0; q < KS; ++q) {
+      const int t = p * KS + q;
+      char* kt = base + q * 2 * TILE;
+      const int k0 = kbeg + t * BKV;
+#pragma unroll
+      for (int i = 0; i < IW; ++i) {
+        const int u = (i * NW + wave) * 64 + lane, row = u / CR, c = (u % CR) ^ C::swz(row), d8 = c * 8;
+        const int kk = k0 + row;
+        const bf16 *ks = Z, *vs = Z;
+        if (t < nt && kk < kend && d8 < hd) {
+          const int which = kk < len0 ? 0 : 1;
+          const int key = which ? kk - len0 : kk;
+          ks = seg_row(a, which, b, g, key, false) + d8;
+          vs = seg_row(a, which, b, g, key, true) + d8;
+        }
+        __builtin_amdgcn_global_load_lds(ks, kt + (i * NW + wave) * 1024, 16, 0, 0);
+        __builtin_amdgcn_global_load_lds(vs, kt + TILE + (i * NW + wave) * 1024, 16, 0, 0);
+      }
+    }
+  };
+
+  f32x4 o[ND];
+#pragma unroll
+  for (int u = 0; u < ND; ++u) o[u] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float m_run = -INFINITY, l_run = 0.f;
+  const float sl2 = a.scale * 1.4426950408889634f;   // scale * log2(e)
+  constexpr int PER_ROUND = KS * 2 * IW;             // direct loads per wave per round
+
+#pragma unroll
+  for (int p = 0; p < NR - 1; ++p)
+    if (p < nrounds) issue(p);
+  for (int p = 0; p < nrounds; ++p) {
+    // round p has landed once at most the NR - 2 later rounds' loads are
+    // pending; the barrier (no fence) then also guarantees every wave is done
+    // with round p - 1, whose slot the next issue overwrites
+    if (p + NR - 2 < nrounds) {
+      asm volatile("s_waitcnt vmcnt(%0)\n\ts_waitcnt lgkmcnt(0)\n\ts_barrier" ::"n"((NR - 2) * PER_ROUND) : "memory");
+    } else {
+      asm volatile("s_waitcnt vmcnt(0)\n\ts_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    }
+    if (p + NR - 1 < nrounds) issue(p + NR - 1);
+    const int t = p * KS + kg;
+    if (t >= nt) continue;
+    const char* Kt = smem + (p % NR) * KS * 2 * TILE + kg * 2 * TILE;
+    const char* Vt = Kt + TILE;
+    const int k0 = kbeg + t * BKV;
+
+    // ---- S^T = K Q^T over BKV / 16 subtiles of 16 keys
+    constexpr int NST = BKV / 16;
+    f32x4 sc[NST];
+#pragma unroll
+    for (int st = 0; st < NST; ++st) {
+      sc[st] = f32x4{0.f, 0.f, 0.f, 0.f};
+      const int row = st * 16 + lq;
+#pragma unroll
+      for (int c = 0; c < NC; ++c) {
+        const int cc = c * 4 + grp;
+        bf16x8 kf = *reinterpret_cast<const bf16x8*>(Kt + row * ROWB + ((cc ^ C::swz(row)) << 4));
+        sc[st] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[c], sc[st], 0, 0, 0);
+      }
+    }
+    // keys past the range exist only in a range's last tile; exp2 arguments
+    // are <= 0 (or -inf), so the plain hardware exp2 suffices and maps -inf
+    // to 0
+    float mx = -INFINITY;
+    const bool full = k0 + BKV <= kend;
+#pragma unroll
+    for (int st = 0; st < NST; ++st)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int kk = k0 + st * 16 + grp * 4 + i;
+        const float v = (full || kk < kend) ? sc[st][i] * sl2 : -INFINITY;
+        sc[st][i] = v;
+        mx = fmaxf(mx, v);
+      }
+    mx = fmaxf(mx, __shfl_xor(mx, 16));
+    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    const float m_new = fmaxf(m_run, mx);
+    const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+    float psum = 0.f;
+#pragma unroll
+    for (int st = 0; st < NST; ++st)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float pv = __builtin_amdgcn_exp2f(sc[st][i] - m_new);
+        sc[st][i] = pv;
+        psum += pv;
+      }
+    psum += __shfl_xor(psum, 16);
+    psum += __shfl_xor(psum, 32);
+    l_run = l_run * alpha + psum;
+    m_run = m_new;
+#pragma unroll
+    for (int u = 0; u < ND; ++u) o[u] *= alpha;
+
+    // ---- O^T += V^T P^T per 32-key chunk; K-slot jj of lane group grp is key
+    // 4 grp + jj (jj < 4) or 16 + 4 grp + jj - 4 (jj >= 4) of the chunk
+    const int s4 = lane & 15;
+#pragma unroll
+    for (int kc = 0; kc < BKV / 32; ++kc) {
+      bf16x8 pf = {(bf16)sc[2 * kc][0], (bf16)sc[2 * kc][1], (bf16)sc[2 * kc][2], (bf16)sc[2 * kc][3],
+                   (bf16)sc[2 * kc + 1][0], (bf16)sc[2 * kc + 1][1], (bf16)sc[2 * kc + 1][2], (bf16)sc[2 * kc + 1][3]};
+      const int r_lo = kc * 32 + 4 * grp + (s4 >> 2), r_hi = r_lo + 16;
+#pragma unroll
+      for (int u = 0; u < ND; ++u) {
+        const int cc = 2 * u + ((s4 & 3) >> 1), off = (s4 & 1) << 3;
+        const char* plo = Vt + r_lo * ROWB + ((cc ^ C::swz(r_lo)) << 4) + off;
+        const char* phi = Vt + r_hi * ROWB + ((cc ^ C::swz(r_hi)) << 4) + off;
+        const v4s lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) v4s*)(plo));
+        const v4s hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) v4s*)(phi));
+        const bf16x4 l4 = __builtin_bit_cast(bf16x4, lo), h4 = __builtin_bit_cast(bf16x4, hi);
+        const bf16x8 vf = {l4[0], l4[1], l4[2], l4[3], h4[0], h4[1], h4[2], h4[3]};
+        o[u] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf, o[u], 0, 0, 0);
+      }
+    }
+  }
+
+  if constexpr (KS > 1) {
+    // merge the key groups into group 0, in group order: m = max m_q,
+    // l = sum l_q 2^(m_q - m), o = sum o_q 2^(m_q - m)
+    __syncthreads();                               // the ring is free from here on
+    float* mg = reinterpret_cast<float*>(smem);
+    const int slot = wrow * 64 + lane;             // lane of a row group
+    if (kg > 0) {
+      float* dst = mg + ((kg - 1) * 256 + slot) * MST;
+#pragma unroll
+      for (int u = 0; u < ND; ++u) *reinterpret_cast<f32x4*>(dst + 4 * u) = o[u];
+      dst[ND * 4] = m_run;
+      dst[ND * 4 + 1] = l_run;
+    }
+    __syncthreads();
+    if (kg > 0) return;
+    float mq[KS], lq_[KS];
+    mq[0] = m_run; lq_[0] = l_run;
+#pragma unroll
+    for (int q = 1; q < KS; ++q) {
+      const float* src = mg + ((q - 1) * 256 + slot) * MST;
+      mq[q] = src[ND * 4]; lq_[q] = src[ND * 4 + 1];
+    }
+    float m = mq[0];
+#pragma unroll
+    for (int q = 1; q < KS; ++q) m = fmaxf(m, mq[q]);
+    float l = 0.f, w[KS];
+#pragma unroll
+    for (int q = 0; q < KS; ++q) {
+      w[q] = __builtin_amdgcn_exp2f(mq[q] - m);
+      l += lq_[q] * w[q];
+    }
+#pragma unroll
+    for (int u = 0; u < ND; ++u) {
+      f32x4 acc = o[u] * w[0];
+#pragma unroll
+      for (int q = 1; q < KS; ++q)
+        acc += *reinterpret_cast<const f32x4*>(mg + ((q - 1) * 256 + slot) * MST + 4 * u) * w[q];
+      o[u] = acc;
+    }
+    m_run = m;
+    l_run = l;
+  }
+
+  if (!rvalid) return;
+  if (S > 1) {
+    const long row = ((long)b * a.Hq + h) * a.Lq + qi;
+    float* po = a.ws + (row * S + split) * hd;
+#pragma unroll
+    for (int u = 0; u < ND; ++u) {
+      const int d = u * 16 + grp * 4;
+      if (d < hd) *reinterpret_cast<f32x4*>(po + d) = o[u];
+    }
+    if (grp == 0) {
+      float* st = a.ws + (long)a.B * a.Hq * a.Lq * S * hd + (row * S + split) * 2;
+      st[0] = m_run;
+      st[1] = l_run;
+    }
+    return;
+  }
+  const float inv = 1.0f / l_run;
+  bf16* op = reinterpret_cast<bf16*>(a.o) + (long)b * a.o_sb + (long)h * a.o_sh + (long)qi * a.o_si;
+#pragma unroll
+  for (int u = 0; u < ND; ++u) {
+    const int d = u * 16 + grp * 4;
+    if (d < hd) {
+      bf16x4 wv = {(bf16)(o[u][0] * inv), (bf16)(o[u][1] * inv), (bf16)(o[u][2] * inv), (bf16)(o[u][3] * inv)};
+      *reinterpret_cast<bf16x4*>(op + d) = wv;
+    }
+  }
+}
+
 }  // namespace
+
+// Launch plan of a bf16 attention. Direct-load kernel: key groups inside a
+// block (KS = 2) whenever the grid leaves CUs without a second block (short
+// decode and small prefill grids), and key ranges over blocks (split-KV,
+// merged by attn_combine_kernel) only when the rounds of tiles they save
+// outweigh the merge: the count S minimises rounds x tile time + merge time
+// (measured on MI355X: a round of 64 keys ~0.8 us at head dim 32, ~1.4 us
+// at 64, of 32 keys ~2.1 us at 256; the merge ~3.5 us), at most one block
+// per CU.
+// Register-staged kernel (head dim 72): split when fewer than 128 blocks.
+static void attn_plan(const AttnArgs& a, int& splits, int& kchunk, int& ks) {
+  const int rows = (a.Hq / a.Hkv) * a.Lq;
+  const long blocks = (long)((rows + BQ - 1) / BQ) * a.Hkv * a.B;
+  const int total = a.seg[0].len + a.seg[1].len, ntiles = (total + BKV - 1) / BKV;
+  const bool v2 = a.zeros && (a.hd <= 64 || a.hd > 96);
+  ks = (v2 && a.hd > 32 && blocks < 256) ? 2 : 1;
+  splits = 1;
+  kchunk = ntiles * BKV;
+  if (!a.ws || ntiles < 2) return;
+  int best = 1;
+  if (v2) {
+    const int tile = a.hd >= 256 ? 32 : 64;                      // keys per kernel tile
+    const double t_tile = a.hd <= 32 ? 0.8 : (a.hd <= 64 ? 1.4 : (a.hd <= 128 ? 1.7 : 2.1)), t_merge = 3.5;
+    const int smax = (int)std::min<long>(16, std::max<long>(1, 256 / blocks));
+    double best_t = 1e30;
+    for (int sp = 1; sp <= std::min(smax, ntiles); ++sp) {
+      const int per = (ntiles + sp - 1) / sp;                   // 64-key units per range
+      const int rounds = ((per * BKV + tile - 1) / tile + ks - 1) / ks;
+      const double t = rounds * t_tile + (sp > 1 ? t_merge : 0.0);
+      if (t < best_t - 1e-9) { best_t = t; best = sp; }
+    }
+  } else if (blocks < 128) {
+    best = (int)std::min<long>({(256 + blocks - 1) / blocks, (long)ntiles, 16L});
+  }
+  while (best > 1 && (long)a.B * a.Hq * a.Lq * best * (a.hd + 2) > a.ws_floats) --best;
+  const int per = (ntiles + best - 1) / best;
+  kchunk = per * BKV;
+  splits = (ntiles + per - 1) / per;              // every range holds keys
+}
 
 void launch_attention(const AttnArgs& a, hipStream_t s) {
   if (a.B <= 0 || a.Lq <= 0) return;
@@ -385,21 +698,22 @@ void launch_attention(const AttnArgs& a, hipStream_t s) {
     return;
   }
   AttnArgs b = a;
+  int ks;
+  attn_plan(a, b.splits, b.kchunk, ks);
   const int rows = (a.Hq / a.Hkv) * a.Lq;
-  const long blocks = (long)((rows + BQ - 1) / BQ) * a.Hkv * a.B;
-  const int total = a.seg[0].len + a.seg[1].len, ntiles = (total + BKV - 1) / BKV;
-  // split the keys when the blocks alone would leave most CUs idle
-  b.splits = 1;
-  b.kchunk = ntiles * BKV;
-  if (a.ws && blocks < 128 && ntiles >= 2) {
-    int sp = (int)std::min<long>({(256 + blocks - 1) / blocks, (long)ntiles, 16L});
-    while (sp > 1 && (long)a.B * a.Hq * a.Lq * sp * (a.hd + 2) > a.ws_floats) --sp;
-    const int per = (ntiles + sp - 1) / sp;
-    b.kchunk = per * BKV;
-    b.splits = (ntiles + per - 1) / per;            // every range holds keys
-  }
   dim3 grid((rows + BQ - 1) / BQ, a.Hkv, a.B * b.splits);
-  if (a.hd <= 32) hipLaunchKernelGGL(attn_mfma_kernel<32>, grid, dim3(256), 0, s, b);
+  // head dims whose rows are a power-of-two number of 16-byte chunks use the
+  // direct-load kernel; 72 (the ViT's, padded to 96) and callers without a
+  // zero buffer use the register-staged one
+  const bool v2 = a.zeros && (a.hd <= 64 || a.hd > 96);
+  if (v2 && a.hd <= 32) hipLaunchKernelGGL((attn_v2_kernel<32, 1>), grid, dim3(256), 0, s, b);
+  else if (v2 && a.hd <= 64 && ks == 2) hipLaunchKernelGGL((attn_v2_kernel<64, 2>), grid, dim3(512), 0, s, b);
+  else if (v2 && a.hd <= 64) hipLaunchKernelGGL((attn_v2_kernel<64, 1>), grid, dim3(256), 0, s, b);
+  else if (v2 && a.hd <= 128 && ks == 2) hipLaunchKernelGGL((attn_v2_kernel<128, 2>), grid, dim3(512), 0, s, b);
+  else if (v2 && a.hd <= 128) hipLaunchKernelGGL((attn_v2_kernel<128, 1>), grid, dim3(256), 0, s, b);
+  else if (v2 && ks == 2) hipLaunchKernelGGL((attn_v2_kernel<256, 2>), grid, dim3(512), 0, s, b);
+  else if (v2) hipLaunchKernelGGL((attn_v2_kernel<256, 1>), grid, dim3(256), 0, s, b);
+  else if (a.hd <= 32) hipLaunchKernelGGL(attn_mfma_kernel<32>, grid, dim3(256), 0, s, b);
   else if (a.hd <= 64) hipLaunchKernelGGL(attn_mfma_kernel<64>, grid, dim3(256), 0, s, b);
   else if (a.hd <= 96) hipLaunchKernelGGL(attn_mfma_kernel<96>, grid, dim3(256), 0, s, b);
   else hipLaunchKernelGGL(attn_mfma_kernel<256>, grid, dim3(256), 0, s, b);

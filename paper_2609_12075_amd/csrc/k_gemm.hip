@@ -163,7 +163,7 @@ gemm_mfma_kernel(GemmArgs a) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wn0 = (wave >> 1) * (BN / 2), wm0 = (wave & 1) * (BM / 2);
   int bx, by, bz;                       // (M tile, N tile, K range), die-aware order
-  xcd_remap(bx, by, bz);
+  xcd_remap_grouped(bx, by, bz, 8);
   const int n_blk = by * BN, m_blk = bx * BM;
   // K range of this block: range bz covers [kbeg, kbeg + ksplit)
   const int kbeg = bz * a.ksplit;
@@ -369,7 +369,7 @@ __global__ void __launch_bounds__(256) gemm_skinny_kernel(GemmArgs a) {
   __shared__ __attribute__((aligned(16))) float red[4][BM][BN];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   int bx, by, bz;
-  xcd_remap(bx, by, bz);
+  xcd_remap_grouped(bx, by, bz, 8);
   const int m0 = bx * BM, n0 = by * BN;
   (void)bz;
   const int kbeg = 0, kend = a.K;
@@ -473,7 +473,7 @@ gemm_stage_kernel(GemmArgs a) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wn0 = (wave >> 1) * (BN / 2), wm0 = (wave & 1) * (BM / 2);
   int bx, by, bz;
-  xcd_remap(bx, by, bz);
+  xcd_remap_grouped(bx, by, bz, 8);
   const int n_blk = by * BN, m_blk = bx * BM;
   // K range of this block (range bz of a split product)
   const int kbeg = bz * a.ksplit;

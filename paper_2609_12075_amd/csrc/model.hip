@@ -444,6 +444,7 @@ AttnArgs attn(const vla_model_s& m, int st, int B, int Hq, int Hkv, int Lq, int 
   a.B = B; a.Hq = Hq; a.Hkv = Hkv; a.Lq = Lq; a.hd = hd; a.et = et;
   a.scale = 1.0f / sqrtf((float)hd);
   a.ws = m.attn_ws[st]; a.ws_floats = vla_model_s::kAttnFloats;
+  a.zeros = m.zeros;
   return a;
 }
 

@@ -128,6 +128,12 @@ ATTN_SHAPES = [
     (2, 32, 32, 17, 32, 296, 0),     # DiT cross-attention
     (1, 4, 2, 7, 64, 5, 3),          # ragged, tiny
     (1, 2, 1, 1, 8, 1, 0),           # single key
+    # many blocks (one key group per block): prefill-sized grids
+    (8, 15, 5, 240, 64, 240, 0),
+    (24, 8, 1, 100, 256, 150, 7),
+    (70, 4, 1, 64, 128, 70, 0),
+    # head dim 128 with key groups, two segments
+    (2, 4, 2, 40, 128, 200, 10),
 ]
 
 
