@@ -78,7 +78,7 @@ vla_status vla_debug_cu_probe(int device, int cu_count, int from_top, int blocks
  * plan (may be NULL): int[5] set to
  * the kernel's tile (weight rows, activation rows), number of K ranges
  * (1 = one kernel, > 1 = partial + reduce kernels), epilogue mode and kernel
- * kind (0 register-pipelined, 1 LDS-staged, 2 small-M).
+ * kind (0 register-pipelined, 1 LDS-staged, 2 small-M, 3 large-tile).
  */
 vla_status vla_debug_replay_gemm(vla_model m, int which, int batch, int iters, hipStream_t stream, double* flops,
                                  int* plan);

@@ -451,20 +451,25 @@ __global__ void __launch_bounds__(256) gemm_skinny_kernel(GemmArgs a) {
 // loads (global_load_lds_dwordx4: each lane's 16 bytes land at LDS base +
 // 16 * lane, one wave writes 1 KiB contiguous) through STAGES buffers, so
 // STAGES - 1 K-steps of loads are in flight without holding registers.
-// LDS rows are 64 bf16 (128 bytes) without padding; the 16-byte chunk c of
-// row r is stored in slot c ^ ((r >> 1) & 7), which makes the matrix-core
-// fragment reads (16 rows, one chunk) conflict-free. Chunks outside the
-// operand (rows >= M or N, columns >= K) are read from a zero buffer, which
-// zero-fills K tails exactly. Block: 4 waves in a 2 x 2 grid, wave tile
-// (BN/2) x (BM/2) of 16 x 16 x 32 products.
-template <int BN, int BM, int STAGES, int MODE>
+// LDS rows are BK bf16 without padding; the 16-byte chunk c of row r is
+// stored in slot c ^ swz(r) (BK 64: (r >> 1) & 7; BK 32: (r >> 2) & 3), which
+// makes the matrix-core fragment reads (16 rows, one chunk) conflict-free.
+// Chunks outside the operand (rows >= M or N, columns >= K) are read from a
+// zero buffer, which zero-fills K tails exactly. Block: 4 waves in a 2 x 2
+// grid, wave tile (BN/2) x (BM/2) of 16 x 16 x 32 products. BK 32 with more
+// stages keeps the same LDS per block but more K-steps of loads in flight.
+template <int BN, int BM, int STAGES, int MODE, int BK = 64>
 __global__ void __launch_bounds__(256)
 gemm_stage_kernel(GemmArgs a) {
-  constexpr int BK = 64, ROWB = BK * 2;                 // bytes per LDS row
+  constexpr int ROWB = BK * 2;                          // bytes per LDS row
+  constexpr int CPR = BK / 8;                           // 16-byte chunks per row
+  constexpr int RPI = 64 / CPR;                         // rows per wave load instruction
+  constexpr int SWS = BK == 64 ? 1 : 2;                 // swizzle: slot = c ^ ((r >> SWS) & (CPR - 1))
   constexpr int TN = BN / 32, TM = BM / 32;
   constexpr int STAGE_BYTES = (BN + BM) * ROWB;
-  constexpr int WG = BN / 8 / 4, AG = BM / 8 / 4;       // 8-row groups per wave (W, A)
+  constexpr int WG = BN / RPI / 4, AG = BM / RPI / 4;   // row groups per wave (W, A)
   constexpr int LOADS = WG + AG;                        // direct loads per thread per stage
+  static_assert(BK == 64 || BK == 32, "BK must be 32 or 64");
   constexpr int LDC = BN + 4;
   constexpr int SMEM = STAGES * STAGE_BYTES > BM * LDC * 4 ? STAGES * STAGE_BYTES : BM * LDC * 4;
   __shared__ __attribute__((aligned(1024))) char smem[SMEM];
@@ -483,24 +488,24 @@ gemm_stage_kernel(GemmArgs a) {
   const bf16* A = reinterpret_cast<const bf16*>(a.A);
   const bf16* Z = reinterpret_cast<const bf16*>(a.zeros);
 
-  // this lane's row within an 8-row group and its LDS slot; the slot holds
+  // this lane's row within a row group and its LDS slot; the slot holds
   // logical chunk (slot ^ swz(row)) of the row
-  const int lrow = lane >> 3, slot = lane & 7;
+  const int lrow = lane / CPR, slot = lane % CPR;
   auto issue = [&](int kt, int buf) {
     char* st = smem + buf * STAGE_BYTES;
 #pragma unroll
     for (int j = 0; j < WG; ++j) {
-      const int grp = j * 4 + wave, r = grp * 8 + lrow;
-      const int c = slot ^ ((r >> 1) & 7), k = kbeg + kt * BK + c * 8, n = n_blk + r;
+      const int grp = j * 4 + wave, r = grp * RPI + lrow;
+      const int c = slot ^ ((r >> SWS) & (CPR - 1)), k = kbeg + kt * BK + c * 8, n = n_blk + r;
       const bf16* src = (n < a.N && k < K) ? W + (long)n * a.ldw + k : Z;
-      __builtin_amdgcn_global_load_lds(src, st + grp * 8 * ROWB, 16, 0, 0);
+      __builtin_amdgcn_global_load_lds(src, st + grp * RPI * ROWB, 16, 0, 0);
     }
 #pragma unroll
     for (int j = 0; j < AG; ++j) {
-      const int grp = j * 4 + wave, r = grp * 8 + lrow;
-      const int c = slot ^ ((r >> 1) & 7), k = kbeg + kt * BK + c * 8, m = m_blk + r;
+      const int grp = j * 4 + wave, r = grp * RPI + lrow;
+      const int c = slot ^ ((r >> SWS) & (CPR - 1)), k = kbeg + kt * BK + c * 8, m = m_blk + r;
       const bf16* src = (m < a.M && k < K) ? A + (long)m * a.lda + k : Z;
-      __builtin_amdgcn_global_load_lds(src, st + BN * ROWB + grp * 8 * ROWB, 16, 0, 0);
+      __builtin_amdgcn_global_load_lds(src, st + BN * ROWB + grp * RPI * ROWB, 16, 0, 0);
     }
   };
 
@@ -526,25 +531,41 @@ gemm_stage_kernel(GemmArgs a) {
     }
     if (kt + STAGES - 1 < nk) issue(kt + STAGES - 1, (kt + STAGES - 1) % STAGES);
     const char* st = smem + (kt % STAGES) * STAGE_BYTES;
+    // all fragments of the K-step, then the products; the scheduler is told
+    // to interleave the second chunk's fragment reads with the first chunk's
+    // matrix instructions, so LDS latency hides behind matrix work
+    constexpr int KC = BK / 32;
+    bf16x8 wf[KC][TN], af[KC][TM];
 #pragma unroll
-    for (int kc = 0; kc < 2; ++kc) {
-      bf16x8 wf[TN], af[TM];
+    for (int kc = 0; kc < KC; ++kc) {
       const int c = kc * 4 + lq;
 #pragma unroll
       for (int i = 0; i < TN; ++i) {
         const int r = wn0 + 16 * i + lr;
-        wf[i] = *reinterpret_cast<const bf16x8*>(st + r * ROWB + ((c ^ ((r >> 1) & 7)) << 4));
+        wf[kc][i] = *reinterpret_cast<const bf16x8*>(st + r * ROWB + ((c ^ ((r >> SWS) & (CPR - 1))) << 4));
       }
 #pragma unroll
       for (int j = 0; j < TM; ++j) {
         const int r = wm0 + 16 * j + lr;
-        af[j] = *reinterpret_cast<const bf16x8*>(st + BN * ROWB + r * ROWB + ((c ^ ((r >> 1) & 7)) << 4));
+        af[kc][j] = *reinterpret_cast<const bf16x8*>(st + BN * ROWB + r * ROWB + ((c ^ ((r >> SWS) & (CPR - 1))) << 4));
       }
+    }
+#pragma unroll
+    for (int kc = 0; kc < KC; ++kc)
 #pragma unroll
       for (int i = 0; i < TN; ++i)
 #pragma unroll
         for (int j = 0; j < TM; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[i], af[j], acc[i][j], 0, 0, 0);
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[kc][i], af[kc][j], acc[i][j], 0, 0, 0);
+    if constexpr (KC == 2) {
+      constexpr int NRD = TN + TM, NMF = TN * TM, R = NMF / NRD > 0 ? NMF / NRD : 1;
+      __builtin_amdgcn_sched_group_barrier(0x100, NRD, 0);      // chunk 0 reads
+#pragma unroll
+      for (int q = 0; q < NRD; ++q) {
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);      // one chunk-1 read
+        __builtin_amdgcn_sched_group_barrier(0x008, R, 0);      // R chunk-0 products
+      }
+      __builtin_amdgcn_sched_group_barrier(0x008, 2 * NMF - NRD * R, 0);
     }
   }
   __syncthreads();
@@ -573,6 +594,114 @@ gemm_stage_kernel(GemmArgs a) {
     f32x4 t = *reinterpret_cast<const f32x4*>(&Cs[mr][nc]);
     float v[4] = {t[0], t[1], t[2], t[3]};
     epilogue4<MODE>(a, m_blk + mr, n_blk + nc, v);
+  }
+}
+
+// ---------------------------------------------------------------- large-tile kernel
+// For large products (the VLM stage at batch >= 1): 256 x 256 output tiles,
+// 8 waves in a 4 (weight rows) x 2 (activation rows) grid, each wave
+// 64 x 128 = 4 x 8 subtiles, so a 32-wide K chunk costs 12 fragment reads
+// for 32 matrix instructions. Operands move global -> LDS with direct loads
+// through two 64 KiB stages (one block per CU, two waves per SIMD); per
+// output this loads half the bytes of a 128 x 128 tile, and each stage's
+// loads have a K-step of 2048 matrix cycles per SIMD to land in. Rows are
+// XOR-swizzled as in the multi-stage kernel. The epilogue stages the fp32
+// tile through LDS in two halves of 128 rows.
+template <int MODE>
+__global__ void __launch_bounds__(512) gemm_big_kernel(GemmArgs a) {
+  constexpr int BN = 256, BM = 256, BK = 64, ROWB = BK * 2;
+  constexpr int TN = 4, TM = 8;
+  constexpr int STAGE_BYTES = (BN + BM) * ROWB;                  // 64 KiB
+  constexpr int LDC = BN + 4;
+  constexpr int SMEM = 2 * STAGE_BYTES > 128 * LDC * 4 ? 2 * STAGE_BYTES : 128 * LDC * 4;
+  __shared__ __attribute__((aligned(1024))) char smem[SMEM];
+  auto Cs = reinterpret_cast<float (*)[LDC]>(smem);
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wn0 = (wave >> 1) * 64, wm0 = (wave & 1) * 128;
+  int bx, by, bz;
+  xcd_remap_grouped(bx, by, bz, 8);
+  const int n_blk = by * BN, m_blk = bx * BM;
+  const int K = a.K;
+  const int nk = (K + BK - 1) / BK;
+  const bf16* W = reinterpret_cast<const bf16*>(a.W);
+  const bf16* A = reinterpret_cast<const bf16*>(a.A);
+  const bf16* Z = reinterpret_cast<const bf16*>(a.zeros);
+
+  // 8-row groups: 32 of W and 32 of A per stage, 4 + 4 per wave
+  const int lrow = lane >> 3, slot = lane & 7;
+  auto issue = [&](int kt, int buf) {
+    char* st = smem + buf * STAGE_BYTES;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int grp = j * 8 + wave, r = grp * 8 + lrow;
+      const int c = slot ^ ((r >> 1) & 7), k = kt * BK + c * 8, n = n_blk + r;
+      const bf16* src = (n < a.N && k < K) ? W + (long)n * a.ldw + k : Z;
+      __builtin_amdgcn_global_load_lds(src, st + grp * 8 * ROWB, 16, 0, 0);
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int grp = j * 8 + wave, r = grp * 8 + lrow;
+      const int c = slot ^ ((r >> 1) & 7), k = kt * BK + c * 8, m = m_blk + r;
+      const bf16* src = (m < a.M && k < K) ? A + (long)m * a.lda + k : Z;
+      __builtin_amdgcn_global_load_lds(src, st + BN * ROWB + grp * 8 * ROWB, 16, 0, 0);
+    }
+  };
+
+  f32x4 acc[TN][TM];
+#pragma unroll
+  for (int i = 0; i < TN; ++i)
+#pragma unroll
+    for (int j = 0; j < TM; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  const int lr = lane & 15, lq = lane >> 4;
+  if (nk > 0) issue(0, 0);
+  for (int kt = 0; kt < nk; ++kt) {
+    // stage kt landed (nothing later is pending yet), and every wave is done
+    // with stage kt - 1, whose buffer the next issue overwrites
+    asm volatile("s_waitcnt vmcnt(0)\n\ts_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    if (kt + 1 < nk) issue(kt + 1, (kt + 1) & 1);
+    const char* st = smem + (kt & 1) * STAGE_BYTES;
+#pragma unroll
+    for (int kc = 0; kc < 2; ++kc) {
+      bf16x8 wf[TN], af[TM];
+      const int c = kc * 4 + lq;
+#pragma unroll
+      for (int i = 0; i < TN; ++i) {
+        const int r = wn0 + 16 * i + lr;
+        wf[i] = *reinterpret_cast<const bf16x8*>(st + r * ROWB + ((c ^ ((r >> 1) & 7)) << 4));
+      }
+#pragma unroll
+      for (int j = 0; j < TM; ++j) {
+        const int r = wm0 + 16 * j + lr;
+        af[j] = *reinterpret_cast<const bf16x8*>(st + BN * ROWB + r * ROWB + ((c ^ ((r >> 1) & 7)) << 4));
+      }
+#pragma unroll
+      for (int i = 0; i < TN; ++i)
+#pragma unroll
+        for (int j = 0; j < TM; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[i], af[j], acc[i][j], 0, 0, 0);
+    }
+  }
+  // epilogue in two halves of 128 activation rows (waves with wm0 == 128 h)
+#pragma unroll 1
+  for (int h = 0; h < 2; ++h) {
+    __syncthreads();
+    if (wm0 == 128 * h) {
+#pragma unroll
+      for (int i = 0; i < TN; ++i)
+#pragma unroll
+        for (int j = 0; j < TM; ++j)
+          *reinterpret_cast<f32x4*>(&Cs[16 * j + lr][wn0 + 16 * i + (lane >> 4) * 4]) = acc[i][j];
+    }
+    __syncthreads();
+#pragma unroll 1
+    for (int c = tid; c < 128 * (BN / 4); c += 512) {
+      const int mr = c / (BN / 4), nc = (c % (BN / 4)) * 4;
+      f32x4 t = *reinterpret_cast<const f32x4*>(&Cs[mr][nc]);
+      float v[4] = {t[0], t[1], t[2], t[3]};
+      epilogue4<MODE>(a, m_blk + 128 * h + mr, n_blk + nc, v);
+    }
   }
 }
 
@@ -652,6 +781,13 @@ GemmPlan gemm_plan(const GemmArgs& a) {
     // CU, which measured faster than deeper pipelines at one block per CU),
     // largest tile that still yields enough blocks for the 256 CUs; when even
     // 128 x 64 tiles are few and K is long, K ranges of that kernel
+    // long-K products with enough 256 x 256 tiles: the large-tile kernel
+    // (measured ahead of the staged tiles from K = 2048 on)
+    if (a.M >= 256 && a.K >= 2048 && blocks(256, 256) >= 128) {
+      p.bn = 256; p.bm = 256; p.kind = 3;
+      p.ksplit = nk * BK;
+      return p;
+    }
     if (a.M >= 128 && blocks(128, 128) >= 256) { p.bn = 128; p.bm = 128; p.kind = 1; }
     else if (a.M >= 64 && blocks(128, 64) >= 128) { p.bn = 128; p.bm = 64; p.kind = 1; }
     else if (a.M >= 512 && nk >= 24 && a.ws) { p.bn = 128; p.bm = 64; p.kind = 1; }
@@ -705,6 +841,12 @@ static void launch_staged(const GemmArgs& a0, const GemmPlan& p, const NormArgs*
   hipLaunchKernelGGL((gemm_stage_kernel<BN, BM, 2, MODE>), grid, dim3(256), 0, s, a);
 }
 
+template <int MODE>
+static void launch_big(const GemmArgs& a, hipStream_t s) {
+  dim3 grid((a.M + 255) / 256, (a.N + 255) / 256, 1);
+  hipLaunchKernelGGL(gemm_big_kernel<MODE>, grid, dim3(512), 0, s, a);
+}
+
 template <int TN, int MODE>
 static void launch_skinny(const GemmArgs& a, hipStream_t s) {
   dim3 grid((a.M + 63) / 64, (a.N + 16 * TN - 1) / (16 * TN), 1);
@@ -742,6 +884,10 @@ static void launch_mode(const GemmArgs& a, const GemmPlan& p, const NormArgs* fu
   if (a.w_type == ET_F32) {
     dim3 grid((a.M + 63) / 64, (a.N + 63) / 64);
     hipLaunchKernelGGL(gemm_f32_kernel<MODE>, grid, dim3(256), 0, s, a);
+    return;
+  }
+  if (p.kind == 3) {
+    launch_big<MODE>(a, s);
     return;
   }
   if (p.kind == 2) {

@@ -176,6 +176,8 @@ class Model:
             return f"gemm_stage_kernelILi{plan['tile_n']}ELi{plan['tile_m']}ELi2ELi{mode}E"
         if plan["kind"] == 2:
             return f"gemm_skinny_kernelILi{plan['tile_n'] // 16}ELi{mode}E"
+        if plan["kind"] == 3:
+            return f"gemm_big_kernelILi{mode}E"
         return f"gemm_mfma_kernelILi{plan['tile_n']}ELi{plan['tile_m']}EDF16bLi{mode}E"
 
     def denoise(self, batch, kv, noise, steps, actions_out, stream=None):

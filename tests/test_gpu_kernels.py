@@ -31,6 +31,8 @@ GEMM_SHAPES = [
     (800, 720, 1920), (600, 1000, 1544),
     # register-pipelined 64 x 32 tiles with K ranges
     (100, 1024, 4096), (200, 720, 1920),
+    # large-tile kernel (256 x 256, K >= 2048), ragged M, N and K
+    (2000, 4100, 2056),
 ]
 
 
