@@ -777,23 +777,37 @@ GemmPlan gemm_plan(const GemmArgs& a) {
       p.ksplit = a.K;
       return p;
     }
-    // many activation rows: the LDS-staged kernel (two stages, two blocks per
-    // CU, which measured faster than deeper pipelines at one block per CU),
-    // largest tile that still yields enough blocks for the 256 CUs; when even
-    // 128 x 64 tiles are few and K is long, K ranges of that kernel
     // long-K products with enough 256 x 256 tiles: the large-tile kernel
     // (measured ahead of the staged tiles from K = 2048 on)
-    if (a.M >= 256 && a.K >= 2048 && blocks(256, 256) >= 128) {
+    if (a.M >= 256 && a.K >= 2048 && blocks(256, 256) >= 160) {
       p.bn = 256; p.bm = 256; p.kind = 3;
       p.ksplit = nk * BK;
       return p;
     }
-    if (a.M >= 128 && blocks(128, 128) >= 256) { p.bn = 128; p.bm = 128; p.kind = 1; }
-    else if (a.M >= 64 && blocks(128, 64) >= 128) { p.bn = 128; p.bm = 64; p.kind = 1; }
-    else if (a.M >= 512 && nk >= 24 && a.ws) { p.bn = 128; p.bm = 64; p.kind = 1; }
-    if (p.kind == 1) {
-      p.ksplit = nk * BK;
-      if (blocks(128, p.bm) < 128) set_splits((int)std::min<long>((448 + blocks(128, 64) - 1) / blocks(128, 64), nk / 4));
+    // many activation rows: the LDS-staged kernel (two stages, two blocks per
+    // CU). Tile (128 x 128 or 128 x 64) and K ranges from a cost model fitted
+    // to measured sweeps: K ranges until the blocks fill both slots of every
+    // CU (>= 8 K-steps per range); time = rounds of resident blocks x K-steps
+    // per range x step time (0.87 us for 128 x 128, 0.59 us for 128 x 64)
+    // + the ordered reduce (its fp32 partial traffic at ~5 TB/s + 3 us).
+    const bool staged = (a.M >= 64 && blocks(128, 64) >= 128) || (a.M >= 512 && nk >= 24 && a.ws);
+    if (staged) {
+      double best_t = 1e30;
+      for (int bm = 128; bm >= 64; bm -= 64) {
+        if (bm == 128 && a.M < 128) continue;
+        const long tiles = blocks(128, bm);
+        int sp = a.ws ? (int)std::max<long>(1, std::min<long>({512 / tiles, nk / 8, 16L})) : 1;
+        while (sp > 1 && (long)sp * a.M * ldp > a.ws_floats) --sp;
+        const int ksteps = (nk + sp - 1) / sp;
+        sp = (nk + ksteps - 1) / ksteps;
+        const long rounds = (tiles * sp + 511) / 512;
+        double t = rounds * ksteps * (bm == 128 ? 0.87 : 0.59);
+        if (sp > 1) t += 4.0 * sp * a.M * ldp / 5e6 + 3.0;
+        if (t < best_t) {
+          best_t = t;
+          p.bn = 128; p.bm = bm; p.kind = 1; p.splits = sp; p.ksplit = ksteps * BK;
+        }
+      }
       return p;
     }
   }

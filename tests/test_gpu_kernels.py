@@ -32,7 +32,7 @@ GEMM_SHAPES = [
     # register-pipelined 64 x 32 tiles with K ranges
     (100, 1024, 4096), (200, 720, 1920),
     # large-tile kernel (256 x 256, K >= 2048), ragged M, N and K
-    (2000, 4100, 2056),
+    (2600, 4100, 2056),
 ]
 
 
