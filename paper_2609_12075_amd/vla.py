@@ -173,7 +173,7 @@ class Model:
         (the partial pass of a K-split plan is the STORE instantiation)."""
         mode = plan["mode"] if plan["splits"] == 1 else 0
         if plan["kind"] == 1:
-            return f"gemm_stage_kernelILi{plan['tile_n']}ELi{plan['tile_m']}ELi2ELi{mode}E"
+            return f"gemm_stage_kernelILi{plan['tile_n']}ELi{plan['tile_m']}ELi2ELi{mode}ELi64E"
         if plan["kind"] == 2:
             return f"gemm_skinny_kernelILi{plan['tile_n'] // 16}ELi{mode}E"
         if plan["kind"] == 3:
