@@ -598,27 +598,32 @@ gemm_stage_kernel(GemmArgs a) {
 }
 
 // ---------------------------------------------------------------- large-tile kernel
-// For large products (the VLM stage at batch >= 1): 256 x 256 output tiles,
-// 8 waves in a 4 (weight rows) x 2 (activation rows) grid, each wave
-// 64 x 128 = 4 x 8 subtiles, so a 32-wide K chunk costs 12 fragment reads
-// for 32 matrix instructions. Operands move global -> LDS with direct loads
-// through two 64 KiB stages (one block per CU, two waves per SIMD); per
-// output this loads half the bytes of a 128 x 128 tile, and each stage's
-// loads have a K-step of 2048 matrix cycles per SIMD to land in. Rows are
-// XOR-swizzled as in the multi-stage kernel. The epilogue stages the fp32
-// tile through LDS in two halves of 128 rows.
-template <int MODE>
-__global__ void __launch_bounds__(512) gemm_big_kernel(GemmArgs a) {
+// For large products (the VLM stage): 256 x 256 output tiles, NW waves in a
+// (NW / 2) x 2 grid: 8 waves of 64 x 128 (12 fragment reads per 32 matrix
+// instructions) or 4 waves of 128 x 128 (16 reads per 64 instructions: half
+// the LDS read traffic per product of a 64 x 64 wave tile; LDS bandwidth,
+// which the operand stores into LDS share, is what bounds the smaller
+// tiles). Operands move global -> LDS with direct loads through two 64 KiB
+// stages (one block per CU); per output this loads half the bytes of a
+// 128 x 128 tile. Rows are XOR-swizzled as in the multi-stage kernel; the
+// second K chunk's fragment reads are interleaved with the first chunk's
+// products. The epilogue stages the fp32 tile through LDS in two halves of
+// 128 rows.
+template <int MODE, int NW>
+__global__ void __launch_bounds__(NW * 64) gemm_big_kernel(GemmArgs a) {
   constexpr int BN = 256, BM = 256, BK = 64, ROWB = BK * 2;
-  constexpr int TN = 4, TM = 8;
+  constexpr int WGN = NW / 2;                                    // waves along the weight rows
+  constexpr int WTN = BN / WGN, WTM = BM / 2;                    // wave tile
+  constexpr int TN = WTN / 16, TM = WTM / 16;
   constexpr int STAGE_BYTES = (BN + BM) * ROWB;                  // 64 KiB
   constexpr int LDC = BN + 4;
   constexpr int SMEM = 2 * STAGE_BYTES > 128 * LDC * 4 ? 2 * STAGE_BYTES : 128 * LDC * 4;
+  constexpr int GPW = 32 / NW;                                   // 8-row groups per wave per operand
   __shared__ __attribute__((aligned(1024))) char smem[SMEM];
   auto Cs = reinterpret_cast<float (*)[LDC]>(smem);
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wn0 = (wave >> 1) * 64, wm0 = (wave & 1) * 128;
+  const int wn0 = (wave >> 1) * WTN, wm0 = (wave & 1) * WTM;
   int bx, by, bz;
   xcd_remap_grouped(bx, by, bz, 8);
   const int n_blk = by * BN, m_blk = bx * BM;
@@ -628,20 +633,20 @@ __global__ void __launch_bounds__(512) gemm_big_kernel(GemmArgs a) {
   const bf16* A = reinterpret_cast<const bf16*>(a.A);
   const bf16* Z = reinterpret_cast<const bf16*>(a.zeros);
 
-  // 8-row groups: 32 of W and 32 of A per stage, 4 + 4 per wave
+  // 8-row groups: 32 of W and 32 of A per stage
   const int lrow = lane >> 3, slot = lane & 7;
   auto issue = [&](int kt, int buf) {
     char* st = smem + buf * STAGE_BYTES;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int grp = j * 8 + wave, r = grp * 8 + lrow;
+    for (int j = 0; j < GPW; ++j) {
+      const int grp = j * NW + wave, r = grp * 8 + lrow;
       const int c = slot ^ ((r >> 1) & 7), k = kt * BK + c * 8, n = n_blk + r;
       const bf16* src = (n < a.N && k < K) ? W + (long)n * a.ldw + k : Z;
       __builtin_amdgcn_global_load_lds(src, st + grp * 8 * ROWB, 16, 0, 0);
     }
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int grp = j * 8 + wave, r = grp * 8 + lrow;
+    for (int j = 0; j < GPW; ++j) {
+      const int grp = j * NW + wave, r = grp * 8 + lrow;
       const int c = slot ^ ((r >> 1) & 7), k = kt * BK + c * 8, m = m_blk + r;
       const bf16* src = (m < a.M && k < K) ? A + (long)m * a.lda + k : Z;
       __builtin_amdgcn_global_load_lds(src, st + BN * ROWB + grp * 8 * ROWB, 16, 0, 0);
@@ -662,25 +667,37 @@ __global__ void __launch_bounds__(512) gemm_big_kernel(GemmArgs a) {
     asm volatile("s_waitcnt vmcnt(0)\n\ts_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
     if (kt + 1 < nk) issue(kt + 1, (kt + 1) & 1);
     const char* st = smem + (kt & 1) * STAGE_BYTES;
+    bf16x8 wf[2][TN], af[2][TM];
 #pragma unroll
     for (int kc = 0; kc < 2; ++kc) {
-      bf16x8 wf[TN], af[TM];
       const int c = kc * 4 + lq;
 #pragma unroll
       for (int i = 0; i < TN; ++i) {
         const int r = wn0 + 16 * i + lr;
-        wf[i] = *reinterpret_cast<const bf16x8*>(st + r * ROWB + ((c ^ ((r >> 1) & 7)) << 4));
+        wf[kc][i] = *reinterpret_cast<const bf16x8*>(st + r * ROWB + ((c ^ ((r >> 1) & 7)) << 4));
       }
 #pragma unroll
       for (int j = 0; j < TM; ++j) {
         const int r = wm0 + 16 * j + lr;
-        af[j] = *reinterpret_cast<const bf16x8*>(st + BN * ROWB + r * ROWB + ((c ^ ((r >> 1) & 7)) << 4));
+        af[kc][j] = *reinterpret_cast<const bf16x8*>(st + BN * ROWB + r * ROWB + ((c ^ ((r >> 1) & 7)) << 4));
       }
+    }
+#pragma unroll
+    for (int kc = 0; kc < 2; ++kc)
 #pragma unroll
       for (int i = 0; i < TN; ++i)
 #pragma unroll
         for (int j = 0; j < TM; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[i], af[j], acc[i][j], 0, 0, 0);
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[kc][i], af[kc][j], acc[i][j], 0, 0, 0);
+    {
+      constexpr int NRD = TN + TM, NMF = TN * TM, R = NMF / NRD > 0 ? NMF / NRD : 1;
+      __builtin_amdgcn_sched_group_barrier(0x100, NRD, 0);      // chunk 0 reads
+#pragma unroll
+      for (int q = 0; q < NRD; ++q) {
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);      // one chunk-1 read
+        __builtin_amdgcn_sched_group_barrier(0x008, R, 0);      // R chunk-0 products
+      }
+      __builtin_amdgcn_sched_group_barrier(0x008, 2 * NMF - NRD * R, 0);
     }
   }
   // epilogue in two halves of 128 activation rows (waves with wm0 == 128 h)
@@ -696,7 +713,7 @@ __global__ void __launch_bounds__(512) gemm_big_kernel(GemmArgs a) {
     }
     __syncthreads();
 #pragma unroll 1
-    for (int c = tid; c < 128 * (BN / 4); c += 512) {
+    for (int c = tid; c < 128 * (BN / 4); c += NW * 64) {
       const int mr = c / (BN / 4), nc = (c % (BN / 4)) * 4;
       f32x4 t = *reinterpret_cast<const f32x4*>(&Cs[mr][nc]);
       float v[4] = {t[0], t[1], t[2], t[3]};
@@ -855,10 +872,10 @@ static void launch_staged(const GemmArgs& a0, const GemmPlan& p, const NormArgs*
   hipLaunchKernelGGL((gemm_stage_kernel<BN, BM, 2, MODE>), grid, dim3(256), 0, s, a);
 }
 
-template <int MODE>
+template <int MODE, int NW = 8>
 static void launch_big(const GemmArgs& a, hipStream_t s) {
   dim3 grid((a.M + 255) / 256, (a.N + 255) / 256, 1);
-  hipLaunchKernelGGL(gemm_big_kernel<MODE>, grid, dim3(512), 0, s, a);
+  hipLaunchKernelGGL((gemm_big_kernel<MODE, NW>), grid, dim3(NW * 64), 0, s, a);
 }
 
 template <int TN, int MODE>
