@@ -160,6 +160,40 @@ def serve_main(args):
                                                   "objective": obj, "optimal": opt}
     log(f"[serve] robot limits alone {dict(zip(names, limits))}; 2-GPU assignment for {pops}: {r.tolist()} "
         f"(eq (3) = {obj})")
+    # fine-tuned variants: two variants of each architecture (different
+    # weights, same shapes) co-located on the GPU, robot i -> model i mod 4;
+    # the variants reuse the architectures' profile
+    nv = args.serve_variants
+    if nv > 1:
+        arch_of = [i % len(names) for i in range(nv * len(names))]
+        vdur, vcu = serve.expand_tables(dur_lut, cu_table, arch_of)
+        vslo = [args.slo_ms] * len(arch_of)
+        b, rows = serve.max_robots(vdur, vslo, mb, f0, T, E)
+        entry = {"models": [f"{names[a]}-v{i // len(names)}" for i, a in enumerate(arch_of)],
+                 "robots_at_98_sim": b, "chunks_per_s": b * f0,
+                 "attainment_by_robots": {str(x["robots"]): round(x["attainment"], 4) for x in rows}}
+        log(f"[serve] study {nv} variants per architecture ({len(arch_of)} models) @ {f0} Hz: {b} robots at 98%")
+        if b > 0 and not args.serve_no_validate:
+            vcfgs = [cfgs[a].with_(seed=cfgs[a].seed + 17 * (i // len(names))) for i, a in enumerate(arch_of)]
+            vmodels = [models[a] if i < len(names) else vla.Model(c, synth.make_weights(c), device=0)
+                       for i, (a, c) in enumerate(zip(arch_of, vcfgs))]
+            vbufs = [bufs[a] if i < len(names) else serve.alloc_io([m], mb)[0] for i, (a, m) in enumerate(zip(arch_of, vmodels))]
+            for m, bb in list(zip(vmodels, vbufs))[len(names):]:
+                m.prefill(mb, bb["pixels"], bb["text_ids"], bb["kv0"], state=bb.get("state"))
+                m.prefill(mb, bb["pixels"], bb["text_ids"], bb["kv1"], state=bb.get("state"))
+            torch.cuda.synchronize()
+            sch = serve.Scheduler(vslo, mb, "esf")
+            sch.set_gpu(vmodels, vbufs)
+            sch.set_cu(256, vcu)
+            arr = synth.poisson_arrivals(b, f0, args.validate_seconds, epoch=100, n_models=len(arch_of))
+            req, ls = sch.run(arr, drain_ns=int(1e9))
+            sch.close()
+            entry["gpu_validation"] = {"robots": b, "attainment": serve.attainment(req), "p99_ms": serve.p99_ms(req),
+                                       "locksteps": int(len(ls)), "requests": int(len(req))}
+            log(f"[serve] variants: GPU attainment {serve.attainment(req):.3f} at {b} robots, p99 {serve.p99_ms(req):.1f} ms")
+            for m in vmodels[len(names):]:
+                m.close()
+        studies["fine_tuned_variants"] = entry
     result["studies"] = studies
     print(json.dumps(result), flush=True)
 
@@ -216,6 +250,7 @@ def main():
     ap.add_argument("--serve-seconds", type=float, default=30.0)
     ap.add_argument("--serve-epochs", type=int, default=5)
     ap.add_argument("--serve-no-validate", action="store_true")
+    ap.add_argument("--serve-variants", type=int, default=2, help="fine-tuned variants per architecture in the co-location study")
     ap.add_argument("--validate-seconds", type=float, default=8.0)
     ap.add_argument("--slo-ms", type=float, default=100.0)
     args = ap.parse_args()

@@ -225,6 +225,15 @@ def best_cu_table(prof: np.ndarray, cu_counts: Sequence[int]):
     return table, dur
 
 
+def expand_tables(dur_ns: np.ndarray, cu_table: np.ndarray, arch_of: Sequence[int]):
+    """Duration and CU tables for co-located fine-tuned variants: models with
+    the same architecture have the same shapes, so their lockstep entries are
+    those of the architecture's profile (one profile serves every variant).
+    arch_of[i] = index of model i's architecture in the profiled tables."""
+    a = np.asarray(arch_of)
+    return (np.ascontiguousarray(dur_ns[a][:, :, a]), np.ascontiguousarray(cu_table[a][:, :, a]))
+
+
 def sweep_robots(dur_ns: np.ndarray, slo_ms: Sequence[float], max_batch: int, robots: Sequence[int], rate_hz,
                  duration_s: float, epochs: int, policy: str = "esf", host_overhead_ns: int = 0,
                  traffic: str = "poisson", target: float = 0.98, mode: str = "lockstep"):

@@ -213,3 +213,24 @@ def test_sweep_finds_capacity_knee():
     att = [r["attainment"] for r in rows]
     assert att[0] >= 0.98 and att[-1] < 0.5
     assert best in (2, 8, 32)
+
+
+def test_variant_tables_reuse_the_architecture_profile():
+    """Fine-tuned variants share their architecture's lockstep entries."""
+    mb = 2
+    nb = serve.n_buckets(mb)
+    rng = np.random.default_rng(3)
+    dur = rng.integers(1, 100, size=(2, nb, 2, nb)).astype(np.int64)
+    cu = rng.integers(1, 32, size=(2, nb, 2, nb)).astype(np.int32) * 8
+    arch = [0, 1, 0, 1]
+    vd, vc = serve.expand_tables(dur, cu, arch)
+    assert vd.shape == (4, nb, 4, nb) and vc.shape == (4, nb, 4, nb)
+    for i in range(4):
+        for j in range(4):
+            assert (vd[i, :, j, :] == dur[arch[i], :, arch[j], :]).all()
+            assert (vc[i, :, j, :] == cu[arch[i], :, arch[j], :]).all()
+    # four models run through the scheduler with the expanded table
+    items = [(k * MS, k % 4) for k in range(40)]
+    req, ls = run(items, [100.0] * 4, mb, vd * MS)
+    assert (req["t_done_ns"] > 0).all()
+    assert {int(x["vlm_model"]) for x in ls if x["vlm_batch"] > 0} == {0, 1, 2, 3}
