@@ -231,6 +231,6 @@ def test_variant_tables_reuse_the_architecture_profile():
             assert (vc[i, :, j, :] == cu[arch[i], :, arch[j], :]).all()
     # four models run through the scheduler with the expanded table
     items = [(k * MS, k % 4) for k in range(40)]
-    req, ls = run(items, [100.0] * 4, mb, vd * MS)
+    req, ls = run(items, [100.0] * 4, mb, vd * (MS // 20), drain=10 ** 10)
     assert (req["t_done_ns"] > 0).all()
     assert {int(x["vlm_model"]) for x in ls if x["vlm_batch"] > 0} == {0, 1, 2, 3}
