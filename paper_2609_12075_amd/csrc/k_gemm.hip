@@ -808,6 +808,13 @@ GemmPlan gemm_plan(const GemmArgs& a) {
     // per range x step time (0.87 us for 128 x 128, 0.59 us for 128 x 64)
     // + the ordered reduce (its fp32 partial traffic at ~5 TB/s + 3 us).
     const bool staged = (a.M >= 64 && blocks(128, 64) >= 128) || (a.M >= 512 && nk >= 24 && a.ws);
+    // short K and under ~1.25 128 x 64 tiles per CU (the action stage at
+    // batch 8-16): 64 x 64 tiles, up to four blocks per CU (measured 15-25 %
+    // faster there)
+    if (staged && a.M <= 1024 && nk <= 24 && blocks(128, 64) < 320) {
+      p.bn = 64; p.bm = 64; p.kind = 1; p.splits = 1; p.ksplit = nk * BK;
+      return p;
+    }
     if (staged) {
       double best_t = 1e30;
       for (int bm = 128; bm >= 64; bm -= 64) {
@@ -928,6 +935,7 @@ static void launch_mode(const GemmArgs& a, const GemmPlan& p, const NormArgs* fu
   }
   if (p.kind == 1) {
     if (p.bm == 128) launch_staged<128, 128, MODE>(a, p, fuse, s);
+    else if (p.bn == 64) launch_staged<64, 64, MODE>(a, p, fuse, s);
     else launch_staged<128, 64, MODE>(a, p, fuse, s);
     return;
   }

@@ -33,6 +33,8 @@ GEMM_SHAPES = [
     (100, 1024, 4096), (200, 720, 1920),
     # large-tile kernel (256 x 256, K >= 2048), ragged M, N and K
     (2600, 4100, 2056),
+    # staged 64 x 64 tiles (short K, mid-sized M), ragged
+    (800, 1600, 720), (431, 2500, 1000),
 ]
 
 
