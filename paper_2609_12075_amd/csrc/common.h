@@ -120,6 +120,9 @@ struct GemmArgs {
   // >= 16 zero bytes in device memory: operand chunks outside [0,M)x[0,K) or
   // [0,N)x[0,K) are read from here (exact zero fill, no out-of-range reads)
   const void* zeros;
+  // set by launch_gemm: every epilogue access of four consecutive columns is
+  // a single aligned vector access (N % 4 == 0, aligned bases and strides)
+  int epi_vec;
 };
 
 void launch_gemm(const GemmArgs& a, hipStream_t s);

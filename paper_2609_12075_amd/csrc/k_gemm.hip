@@ -143,6 +143,183 @@ __device__ __forceinline__ void epilogue4(const GemmArgs& a, int m, int n0, floa
   }
 }
 
+// ---------------------------------------------------------------- tile epilogue
+// Epilogue of a whole output tile staged in LDS as fp32 (ROWS rows of BN
+// columns, row stride LDC floats). Thread t finishes the four columns
+// nc = (t % (BN/4)) * 4 of rows t / (BN/4) + it * (NT / (BN/4)). What depends
+// only on the columns (bias, gate, QKV head and destination) is read or
+// computed once per thread, and every load that depends on the row (the old
+// residual or Euler state, the position table, the RoPE angles) is issued for
+// all of the thread's rows before the first store, so the row loads share one
+// memory round trip instead of one each. Arithmetic per element is that of
+// epilogue4. Valid when a.epi_vec is set (N % 4 == 0 and every vector access
+// aligned; see epi_vec_ok); otherwise callers use epilogue4.
+// The epilogue of NIT rows ms[] (valid where ok[]) of the four columns
+// n0..n0+3 (n0 < N), given their sums t[].
+template <int MODE, int NIT>
+__device__ __forceinline__ void epi_rows(const GemmArgs& a, const f32x4 (&t)[NIT], const int (&ms)[NIT],
+                                         const bool (&ok)[NIT], int n0) {
+  const f32x4 zero = {0.f, 0.f, 0.f, 0.f};
+  const f32x4 bias = a.bias ? *reinterpret_cast<const f32x4*>(a.bias + n0) : zero;
+  auto row_off = [&](int m) -> long {
+    return a.row_group > 0 ? (long)(m / a.row_group) * a.row_group_stride + (long)(m % a.row_group) * a.ldo
+                           : (long)m * a.ldo;
+  };
+  if constexpr (MODE == EPI_STORE) {
+    f32x4 tb[NIT];
+#pragma unroll
+    for (int it = 0; it < NIT; ++it)
+      tb[it] = (a.tab && ok[it]) ? *reinterpret_cast<const f32x4*>(a.tab + (long)(ms[it] % a.tab_period) * a.ldtab + n0)
+                                 : zero;
+#pragma unroll
+    for (int it = 0; it < NIT; ++it) {
+      if (!ok[it]) continue;
+      f32x4 x = t[it] + bias + tb[it];
+      if (a.act != ACT_NONE) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) x[j] = act_apply(x[j], a.act);
+      }
+      const long o = row_off(ms[it]) + n0;
+      if (a.out_type == ET_BF16)
+        *reinterpret_cast<bf16x4*>(reinterpret_cast<bf16*>(a.out) + o) = bf16x4{(bf16)x[0], (bf16)x[1], (bf16)x[2], (bf16)x[3]};
+      else
+        *reinterpret_cast<f32x4*>(reinterpret_cast<float*>(a.out) + o) = x;
+    }
+  } else if constexpr (MODE == EPI_RESID || MODE == EPI_EULER) {
+    float* out = reinterpret_cast<float*>(a.out);
+    const f32x4 gate = (MODE == EPI_RESID && a.gate) ? *reinterpret_cast<const f32x4*>(a.gate + n0) : f32x4{1.f, 1.f, 1.f, 1.f};
+    f32x4 old[NIT];
+    long off[NIT];
+#pragma unroll
+    for (int it = 0; it < NIT; ++it) {
+      off[it] = (MODE == EPI_RESID ? row_off(ms[it]) : (long)ms[it] * a.ldo) + n0;
+      old[it] = ok[it] ? *reinterpret_cast<const f32x4*>(out + off[it]) : zero;
+    }
+#pragma unroll
+    for (int it = 0; it < NIT; ++it) {
+      if (!ok[it]) continue;
+      f32x4 r;
+      if constexpr (MODE == EPI_RESID) r = old[it] + (t[it] + bias) * gate;
+      else r = old[it] + a.dt * (t[it] + bias);
+      *reinterpret_cast<f32x4*>(out + off[it]) = r;
+    }
+  } else if constexpr (MODE == EPI_GEGLU) {
+    // weight rows interleaved: column 2f = gate f, 2f + 1 = up f
+#pragma unroll
+    for (int it = 0; it < NIT; ++it) {
+      if (!ok[it]) continue;
+      const f32x4 x = t[it] + bias;
+      const float r0v = act_apply(x[0], ACT_GELU) * x[1], r1v = act_apply(x[2], ACT_GELU) * x[3];
+      const long o = (long)ms[it] * a.ldo + (n0 >> 1);
+      if (a.out_type == ET_BF16)
+        *reinterpret_cast<bf16x2*>(reinterpret_cast<bf16*>(a.out) + o) = bf16x2{(bf16)r0v, (bf16)r1v};
+      else {
+        float* of = reinterpret_cast<float*>(a.out) + o;
+        of[0] = r0v;
+        of[1] = r1v;
+      }
+    }
+  } else if constexpr (MODE == EPI_QKV) {
+    const QkvEpi& q = a.qkv;
+    const int c0 = q.n_off + n0, hd = q.hd;
+    int seg, head, j0;
+    if (c0 < q.n_q * hd) { seg = 0; head = c0 / hd; j0 = c0 % hd; }
+    else if (c0 < (q.n_q + q.n_kv) * hd) { seg = 1; head = (c0 - q.n_q * hd) / hd; j0 = (c0 - q.n_q * hd) % hd; }
+    else { seg = 2; head = (c0 - (q.n_q + q.n_kv) * hd) / hd; j0 = (c0 - (q.n_q + q.n_kv) * hd) % hd; }
+    void* dst = seg == 0 ? q.q : seg == 1 ? q.k : q.v;
+    const long sb = seg == 0 ? q.q_sb : seg == 1 ? q.k_sb : q.v_sb;
+    const long sh = seg == 0 ? q.q_sh : seg == 1 ? q.k_sh : q.v_sh;
+    const long si = seg == 0 ? q.q_si : seg == 1 ? q.k_si : q.v_si;
+    const bool rope = seg < 2 && q.pos0 >= 0;
+    const int half = hd >> 1, tt = j0 >> 1;
+    long idx[NIT];
+    f32x4 cs[NIT];
+#pragma unroll
+    for (int it = 0; it < NIT; ++it) {
+      const int b = ms[it] / q.seq, i = ms[it] % q.seq;
+      idx[it] = (long)b * sb + (long)head * sh + (long)i * si;
+      // (cos, sin) of dims t and t + 1 at position pos0 + i
+      cs[it] = (rope && ok[it]) ? *reinterpret_cast<const f32x4*>(q.rope_cs + ((long)(q.pos0 + i) * half + tt) * 2) : zero;
+    }
+#pragma unroll
+    for (int it = 0; it < NIT; ++it) {
+      if (!ok[it]) continue;
+      const f32x4 x = t[it] + bias;
+      if (rope) {
+        // columns are dims (t, t+1) and (t+hd/2, t+1+hd/2): weight rows of q and
+        // k are stored pair-interleaved per head
+        const f32x4 c = cs[it];
+        const float lo0 = x[0] * c[0] - x[1] * c[1], hi0 = x[1] * c[0] + x[0] * c[1];
+        const float lo1 = x[2] * c[2] - x[3] * c[3], hi1 = x[3] * c[2] + x[2] * c[3];
+        if (a.out_type == ET_BF16) {
+          bf16* d = reinterpret_cast<bf16*>(dst) + idx[it];
+          *reinterpret_cast<bf16x2*>(d + tt) = bf16x2{(bf16)lo0, (bf16)lo1};
+          *reinterpret_cast<bf16x2*>(d + tt + half) = bf16x2{(bf16)hi0, (bf16)hi1};
+        } else {
+          float* d = reinterpret_cast<float*>(dst) + idx[it];
+          d[tt] = lo0; d[tt + 1] = lo1; d[tt + half] = hi0; d[tt + half + 1] = hi1;
+        }
+      } else if (a.out_type == ET_BF16) {
+        *reinterpret_cast<bf16x4*>(reinterpret_cast<bf16*>(dst) + idx[it] + j0) = bf16x4{(bf16)x[0], (bf16)x[1], (bf16)x[2], (bf16)x[3]};
+      } else {
+        *reinterpret_cast<f32x4*>(reinterpret_cast<float*>(dst) + idx[it] + j0) = x;
+      }
+    }
+  }
+}
+
+// Thread tid of NT finishes the tile's rows r0 + it * RS of its four columns
+// (see above), GRP rows per memory round trip (GRP bounds the registers the
+// row loads hold); the tile is the sum of NSUM fp32 planes in LDS (plane
+// stride ROWS * LDC floats), added in plane order.
+template <int MODE, int BN, int ROWS, int NT, int LDC, int NSUM = 1, int GRP = 8>
+__device__ __forceinline__ void tile_epilogue(const GemmArgs& a, const float* Cs, int m_blk, int n_blk, int tid) {
+  // GeGLU has no row loads to overlap and its activation is long: two rows at
+  // a time keep its registers within the kernels' budget
+  constexpr int GR = MODE == EPI_GEGLU ? 2 : GRP;
+  constexpr int CPT = BN / 4, RS = NT / CPT, NIT = (ROWS + RS - 1) / RS, G = NIT < GR ? NIT : GR;
+  static_assert(NT % CPT == 0, "threads must cover whole rows");
+  const int nc = (tid % CPT) * 4, r0 = tid / CPT, n0 = n_blk + nc;
+  if (n0 >= a.N) return;
+#pragma unroll
+  for (int g0 = 0; g0 < NIT; g0 += G) {
+    f32x4 t[G];
+    int ms[G];
+    bool ok[G];
+#pragma unroll
+    for (int it = 0; it < G; ++it) {
+      const int mr = r0 + (g0 + it) * RS;
+      ms[it] = m_blk + mr;
+      ok[it] = g0 + it < NIT && (ROWS % RS == 0 || mr < ROWS) && ms[it] < a.M;
+      t[it] = f32x4{0.f, 0.f, 0.f, 0.f};
+      if (ok[it]) {
+        t[it] = *reinterpret_cast<const f32x4*>(Cs + mr * LDC + nc);
+#pragma unroll
+        for (int z = 1; z < NSUM; ++z) t[it] += *reinterpret_cast<const f32x4*>(Cs + z * ROWS * LDC + mr * LDC + nc);
+      }
+    }
+    epi_rows<MODE, G>(a, t, ms, ok, n0);
+  }
+}
+
+// Epilogue of the split-K partial pass: the fp32 tile goes to the workspace
+// slice of K range bz unchanged (the reduce kernel runs the epilogue).
+template <int BN, int ROWS, int NT, int LDC>
+__device__ __forceinline__ void tile_store_partial(const GemmArgs& a, const float* Cs, int m_blk, int n_blk, int bz,
+                                                   int tid) {
+  constexpr int CPT = BN / 4, RS = NT / CPT, NIT = (ROWS + RS - 1) / RS;
+  const int ldp = (a.N + 3) & ~3;
+  float* part = a.ws + (long)bz * a.M * ldp;
+  const int nc = (tid % CPT) * 4, r0 = tid / CPT, n = n_blk + nc;
+  if (n >= a.N) return;
+#pragma unroll
+  for (int it = 0; it < NIT; ++it) {
+    const int mr = r0 + it * RS, m = m_blk + mr;
+    if ((ROWS % RS == 0 || mr < ROWS) && m < a.M)
+      *reinterpret_cast<f32x4*>(part + (long)m * ldp + n) = *reinterpret_cast<const f32x4*>(Cs + mr * LDC + nc);
+  }
+}
+
 // ---------------------------------------------------------------- bf16 MFMA kernel
 // Block: 256 threads = 4 waves in a 2 x 2 grid over a BN (weight rows) x BM
 // (activation rows) tile; K advances in steps of 64 through a double-buffered
@@ -262,15 +439,11 @@ gemm_mfma_kernel(GemmArgs a) {
   __syncthreads();
   if (a.splits > 1) {
     // split-K: store this K range's partial tile; the reduce kernel finishes
-    const int ldp = (a.N + 3) & ~3;
-    float* part = a.ws + (long)bz * a.M * ldp;
-#pragma unroll 1
-    for (int c = tid; c < BM * (BN / 4); c += 256) {
-      const int mr = c / (BN / 4), nc = (c % (BN / 4)) * 4;
-      const int m = m_blk + mr, n = n_blk + nc;
-      if (m < a.M && n < a.N)
-        *reinterpret_cast<f32x4*>(part + (long)m * ldp + n) = *reinterpret_cast<const f32x4*>(&Cs[mr][nc]);
-    }
+    tile_store_partial<BN, BM, 256, LDC>(a, &Cs[0][0], m_blk, n_blk, bz, tid);
+    return;
+  }
+  if (a.epi_vec) {
+    tile_epilogue<MODE, BN, BM, 256, LDC>(a, &Cs[0][0], m_blk, n_blk, tid);
     return;
   }
 #pragma unroll 1
@@ -300,6 +473,13 @@ __global__ void __launch_bounds__(256) splitk_reduce_kernel(GemmArgs a) {
   f32x4 t = part[0];
 #pragma unroll
   for (int z = 1; z < 16; ++z) t += part[z];
+  if (a.epi_vec) {
+    const f32x4 tt[1] = {t};
+    const int mm[1] = {m};
+    const bool ok[1] = {true};
+    epi_rows<MODE, 1>(a, tt, mm, ok, n0);
+    return;
+  }
   float v[4] = {t[0], t[1], t[2], t[3]};
   epilogue4<MODE>(a, m, n0, v);
 }
@@ -435,6 +615,10 @@ __global__ void __launch_bounds__(256) gemm_skinny_kernel(GemmArgs a) {
     for (int j = 0; j < 4; ++j)
       *reinterpret_cast<f32x4*>(&red[wave][j * 16 + lr][i * 16 + (lane >> 4) * 4]) = acc[i][j];
   __syncthreads();
+  if (a.epi_vec) {
+    tile_epilogue<MODE, BN, BM, 256, BN, 4>(a, &red[0][0][0], m0, n0, tid);
+    return;
+  }
 #pragma unroll
   for (int c = tid; c < BM * BN / 4; c += 256) {
     const int mr = c / (BN / 4), nc = (c % (BN / 4)) * 4;
@@ -577,15 +761,11 @@ gemm_stage_kernel(GemmArgs a) {
   __syncthreads();
   if (a.splits > 1) {
     // split-K: store this K range's partial tile; the reduce kernel finishes
-    const int ldp = (a.N + 3) & ~3;
-    float* part = a.ws + (long)bz * a.M * ldp;
-#pragma unroll 1
-    for (int c = tid; c < BM * (BN / 4); c += 256) {
-      const int mr = c / (BN / 4), nc = (c % (BN / 4)) * 4;
-      const int m = m_blk + mr, n = n_blk + nc;
-      if (m < a.M && n < a.N)
-        *reinterpret_cast<f32x4*>(part + (long)m * ldp + n) = *reinterpret_cast<const f32x4*>(&Cs[mr][nc]);
-    }
+    tile_store_partial<BN, BM, 256, LDC>(a, &Cs[0][0], m_blk, n_blk, bz, tid);
+    return;
+  }
+  if (a.epi_vec) {
+    tile_epilogue<MODE, BN, BM, 256, LDC>(a, &Cs[0][0], m_blk, n_blk, tid);
     return;
   }
 #pragma unroll 1
@@ -712,6 +892,10 @@ __global__ void __launch_bounds__(NW * 64) gemm_big_kernel(GemmArgs a) {
           *reinterpret_cast<f32x4*>(&Cs[16 * j + lr][wn0 + 16 * i + (lane >> 4) * 4]) = acc[i][j];
     }
     __syncthreads();
+    if (a.epi_vec) {
+      tile_epilogue<MODE, BN, 128, NW * 64, LDC, 1, 4>(a, &Cs[0][0], m_blk + 128 * h, n_blk, tid);
+      continue;
+    }
 #pragma unroll 1
     for (int c = tid; c < 128 * (BN / 4); c += NW * 64) {
       const int mr = c / (BN / 4), nc = (c % (BN / 4)) * 4;
@@ -943,10 +1127,40 @@ static void launch_mode(const GemmArgs& a, const GemmPlan& p, const NormArgs* fu
   else launch_mfma<64, 32, MODE>(a, p, fuse, s);
 }
 
-void launch_gemm(const GemmArgs& a, hipStream_t s) {
-  if (a.M <= 0 || a.N <= 0) return;
-  if (a.a_type == ET_F32 && a.w_type == ET_BF16 && a.mode != EPI_STORE)
+// True when the tile epilogue may use one vector access per four columns:
+// N a multiple of 4 and every base address and stride it touches aligned.
+static bool epi_vec_ok(const GemmArgs& a) {
+  auto al = [](const void* p, uintptr_t b) { return (reinterpret_cast<uintptr_t>(p) & (b - 1)) == 0; };
+  if (a.N % 4 != 0) return false;
+  if (a.bias && !al(a.bias, 16)) return false;
+  switch (a.mode) {
+    case EPI_STORE:
+      if (a.tab && (!al(a.tab, 16) || a.ldtab % 4 != 0 || a.tab_period <= 0)) return false;
+      return al(a.out, 16) && a.ldo % 4 == 0 && (a.row_group <= 0 || a.row_group_stride % 4 == 0);
+    case EPI_RESID:
+      if (a.gate && !al(a.gate, 16)) return false;
+      return al(a.out, 16) && a.ldo % 4 == 0 && (a.row_group <= 0 || a.row_group_stride % 4 == 0);
+    case EPI_EULER:
+      return al(a.out, 16) && a.ldo % 4 == 0;
+    case EPI_GEGLU:
+      return al(a.out, 8) && a.ldo % 2 == 0;
+    case EPI_QKV: {
+      const QkvEpi& q = a.qkv;
+      const bool strides = q.q_sb % 4 == 0 && q.q_sh % 4 == 0 && q.q_si % 4 == 0 && q.k_sb % 4 == 0 &&
+                           q.k_sh % 4 == 0 && q.k_si % 4 == 0 && q.v_sb % 4 == 0 && q.v_sh % 4 == 0 && q.v_si % 4 == 0;
+      return strides && q.hd % 4 == 0 && q.n_off % 4 == 0 && q.seq > 0 && al(q.q, 16) && al(q.k, 16) && al(q.v, 16) &&
+             (q.pos0 < 0 || al(q.rope_cs, 16));
+    }
+  }
+  return false;
+}
+
+void launch_gemm(const GemmArgs& a0, hipStream_t s) {
+  if (a0.M <= 0 || a0.N <= 0) return;
+  if (a0.a_type == ET_F32 && a0.w_type == ET_BF16 && a0.mode != EPI_STORE)
     throw VlaError{4, "fp32 activations with bf16 weights only feed plain stores"};
+  GemmArgs a = a0;
+  a.epi_vec = epi_vec_ok(a) ? 1 : 0;
   const GemmPlan p = a.w_type == ET_F32 ? GemmPlan{} : gemm_plan(a);
   switch (a.mode) {
     case EPI_STORE: launch_mode<EPI_STORE>(a, p, nullptr, s); break;
@@ -964,7 +1178,9 @@ void launch_gemm_norm(const GemmArgs& a, const NormArgs& n, hipStream_t s) {
   if (fusable) {
     const GemmPlan p = gemm_plan(a);
     if (p.splits > 1) {
-      launch_mode<EPI_RESID>(a, p, &n, s);
+      GemmArgs av = a;
+      av.epi_vec = epi_vec_ok(av) ? 1 : 0;
+      launch_mode<EPI_RESID>(av, p, &n, s);
       return;
     }
   }
