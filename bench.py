@@ -234,7 +234,10 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--config", default="smolvla")
     ap.add_argument("--batch", type=int, default=0, help="requests per stage batch (default: max_batch)")
-    ap.add_argument("--cu", type=int, default=256, help="compute units the VLM stream may use (multiple of 8)")
+    ap.add_argument("--cu", type=int, default=0,
+                    help="compute units the VLM stream may use (multiple of 8); 0: the fastest of --cu-candidates, "
+                         "profiled before the timed steps")
+    ap.add_argument("--cu-candidates", default="256,192,160,128,96,64,48,32")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--roofline-iters", type=int, default=50)
@@ -276,7 +279,7 @@ def main():
     N = cfg.steps
     dtype = "bf16" if cfg.dtype == synth.DTYPE_BF16 else "f32"
     dev = torch.device("cuda:0")
-    log(f"[bench] config {cfg.name} B={B} steps/chunk={N} vlm_cu={args.cu}")
+    log(f"[bench] config {cfg.name} B={B} steps/chunk={N} vlm_cu={args.cu or 'auto'}")
     t0 = time.perf_counter()
     weights = synth.make_weights(cfg)
     m = vla.Model(cfg, weights, device=0)
@@ -293,11 +296,35 @@ def main():
         vla.step(m, B, d["pixels"], d["text_ids"], kv[k % 2], m, adit_b, kv[(k - 1) % 2], d["noise"], N,
                  act[(k - 1) % 2], vlm_cu_count=args.cu, state=d.get("state"))
 
+    auto_cu = args.cu == 0
+    if auto_cu:
+        args.cu = 256
     t0 = time.perf_counter()
     for k in range(args.warmup):
         lockstep(k)
     torch.cuda.synchronize()
     log(f"[bench] warmup ({args.warmup} locksteps incl. graph capture) {time.perf_counter() - t0:.1f} s")
+
+    # The VLM stream's CU restriction for this (VLM batch, action batch)
+    # combination: the fastest candidate in a short profile (the paper's
+    # offline restriction table, for the one combination the benchmark runs).
+    cu_profile = None
+    if auto_cu:
+        cu_profile = {}
+        for cu in [int(x) for x in args.cu_candidates.split(",")]:
+            args.cu = cu
+            for k in range(1, 3):
+                lockstep(k)
+            torch.cuda.synchronize()
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(stream)
+            for k in range(1, 5):
+                lockstep(k)
+            b.record(stream)
+            torch.cuda.synchronize()
+            cu_profile[cu] = round(a.elapsed_time(b) / 4, 4)
+        args.cu = min(cu_profile, key=cu_profile.get)
+        log(f"[bench] lockstep ms by VLM CU count {cu_profile}: using {args.cu}")
 
     K = args.steps
     evs = [torch.cuda.Event(enable_timing=True) for _ in range(K + 2)]
@@ -383,6 +410,7 @@ def main():
         "config": {"workload": f"{cfg.name}-shaped VLA, one lockstep = prefill(batch k) || denoise(batch k-1)",
                    "batch": B, "euler_steps": N, "prefix_tokens": cfg.prefix_len, "horizon": cfg.horizon,
                    "vlm_cu_count": args.cu, "parallelism": "single GPU, two streams"},
+        "lockstep_ms_by_vlm_cu": cu_profile,
         "adit_step_ms": round(den_ms / N, 4), "prefill_ms": round(pre_ms, 4), "denoise_ms": round(den_ms, 4),
         "chunk_latency_ms_max": round(max(lat), 3), "slo_ms": slo, "slo_attainment_closed_loop": attain,
         "roofline": roofline,

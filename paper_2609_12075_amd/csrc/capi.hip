@@ -4,6 +4,7 @@
 // always finds free units; one lockstep = one VLM batch alongside one action
 // batch).
 #include <cstring>
+#include <list>
 #include <map>
 #include <mutex>
 
@@ -44,8 +45,18 @@ namespace {
 struct DevicePool {
   std::map<int, hipStream_t> vlm;     // key: cu count (256 = unrestricted)
   std::map<int, hipStream_t> adit;    // key: cu count from the top of the mask
+  std::list<std::pair<bool, int>> masked_lru;   // (is adit, cu count) of live masked streams, most recent first
   hipEvent_t ev_start = nullptr, ev_v = nullptr, ev_a = nullptr;
+  int cu_total = 0;
 };
+
+// At most this many CU-masked streams are alive per device. Measured on
+// MI355X (ROCm 7, four hardware queues per process): with a fourth masked
+// stream alive, every kernel replayed from a graph on the streams sharing its
+// hardware queue costs ~20 us more (the action stage's ~1200 kernels per
+// denoise went from 13.8 to 36 ms); with three or fewer there is no cost. A
+// request for a further CU count first retires the least recently used one.
+constexpr int kMaxMaskedStreams = 3;
 
 std::mutex g_pool_mu;
 std::map<int, DevicePool> g_pools;
@@ -56,8 +67,7 @@ int device_cu_count(int dev) {
   return p.multiProcessorCount;
 }
 
-hipStream_t make_masked(int dev, int count, bool from_top) {
-  const int total = device_cu_count(dev);
+hipStream_t make_masked(int total, int count, bool from_top) {
   hipStream_t s = nullptr;
   if (count >= total) {
     VLA_HIP(hipStreamCreateWithFlags(&s, hipStreamNonBlocking));
@@ -76,31 +86,53 @@ hipStream_t make_masked(int dev, int count, bool from_top) {
 DevicePool& pool(int dev) {
   auto& p = g_pools[dev];
   if (!p.ev_start) {
+    p.cu_total = device_cu_count(dev);
     VLA_HIP(hipEventCreateWithFlags(&p.ev_start, hipEventDisableTiming));
     VLA_HIP(hipEventCreateWithFlags(&p.ev_v, hipEventDisableTiming));
     VLA_HIP(hipEventCreateWithFlags(&p.ev_a, hipEventDisableTiming));
+    // The two unrestricted streams are created before any CU-masked one.
+    // Measured on MI355X (ROCm 7): when a masked stream is created first,
+    // every kernel later replayed from a graph, on any stream of the
+    // process, costs ~20 us more; created in this order, up to
+    // kMaxMaskedStreams masked streams cost nothing extra.
+    p.vlm[256] = make_masked(p.cu_total, 256, false);
+    p.adit[256] = make_masked(p.cu_total, 256, true);
   }
   return p;
 }
 
-hipStream_t vlm_stream(int dev, int count) {
+// The stream restricted to `count` CUs (from the bottom of the mask for the
+// VLM side, from the top for the action side); count >= the device's CUs is
+// the unrestricted stream. Caller holds g_pool_mu.
+hipStream_t pool_stream(int dev, int count, bool adit) {
   auto& p = pool(dev);
-  auto it = p.vlm.find(count);
-  if (it != p.vlm.end()) return it->second;
-  hipStream_t s = make_masked(dev, count, false);
-  p.vlm[count] = s;
+  if (count >= p.cu_total) count = 256;
+  auto& m = adit ? p.adit : p.vlm;
+  auto it = m.find(count);
+  if (count == 256) return it->second;
+  const std::pair<bool, int> key{adit, count};
+  if (it != m.end()) {
+    p.masked_lru.remove(key);
+    p.masked_lru.push_front(key);
+    return it->second;
+  }
+  while ((int)p.masked_lru.size() >= kMaxMaskedStreams) {
+    const auto old = p.masked_lru.back();
+    p.masked_lru.pop_back();
+    auto& om = old.first ? p.adit : p.vlm;
+    hipStream_t os = om[old.second];
+    VLA_HIP(hipStreamSynchronize(os));
+    VLA_HIP(hipStreamDestroy(os));
+    om.erase(old.second);
+  }
+  hipStream_t s = make_masked(p.cu_total, count, adit);
+  m[count] = s;
+  p.masked_lru.push_front(key);
   return s;
 }
 
-hipStream_t adit_stream(int dev, int count) {
-  auto& p = pool(dev);
-  if (count <= 0) count = 256;
-  auto it = p.adit.find(count);
-  if (it != p.adit.end()) return it->second;
-  hipStream_t s = make_masked(dev, count, true);
-  p.adit[count] = s;
-  return s;
-}
+hipStream_t vlm_stream(int dev, int count) { return pool_stream(dev, count, false); }
+hipStream_t adit_stream(int dev, int count) { return pool_stream(dev, count <= 0 ? 256 : count, true); }
 
 void check_model(vla_model m) { VLA_REQUIRE(m != nullptr, "null model"); }
 
@@ -235,9 +267,8 @@ vla_status vla_step(const vla_step_args* a, hipStream_t join) {
     DeviceGuard g(dev);
     std::lock_guard<std::mutex> lk(g_pool_mu);
     DevicePool& p = pool(dev);
-    const int total = device_cu_count(dev);
-    hipStream_t vs = vlm_stream(dev, a->vlm_cu_count >= total ? 256 : a->vlm_cu_count);
-    hipStream_t as = adit_stream(dev, a->adit_cu_count == 0 || a->adit_cu_count >= total ? 256 : a->adit_cu_count);
+    hipStream_t vs = vlm_stream(dev, a->vlm_cu_count);
+    hipStream_t as = adit_stream(dev, a->adit_cu_count);
     // both halves start after the work already queued on the join stream
     VLA_HIP(hipEventRecord(p.ev_start, join));
     if (do_v) VLA_HIP(hipStreamWaitEvent(vs, p.ev_start, 0));
@@ -326,9 +357,7 @@ vla_status vla_debug_cu_probe(int device, int cu_count, int from_top, int blocks
     DeviceGuard g(device);
     std::lock_guard<std::mutex> lk(g_pool_mu);
     DevicePool& p = pool(device);
-    const int total = device_cu_count(device);
-    hipStream_t s = from_top ? adit_stream(device, cu_count >= total ? 256 : cu_count)
-                             : vlm_stream(device, cu_count >= total ? 256 : cu_count);
+    hipStream_t s = from_top ? adit_stream(device, cu_count) : vlm_stream(device, cu_count);
     VLA_HIP(hipEventRecord(p.ev_start, join));
     VLA_HIP(hipStreamWaitEvent(s, p.ev_start, 0));
     launch_cu_probe(out, blocks, spin, s);

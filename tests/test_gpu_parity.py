@@ -178,6 +178,34 @@ def test_lockstep_matches_separate_stages(cu):
     np.testing.assert_array_equal(act_cur.cpu().numpy(), ref_cur)
 
 
+def test_lockstep_many_cu_counts():
+    """More distinct CU restrictions than the library keeps streams for (it
+    retires the least recently used masked stream): every lockstep still gives
+    the bits of the stages run alone, on both the VLM and the action side."""
+    import torch
+    from paper_2609_12075_amd import vla
+    cfg = SMOL_R
+    m = model(cfg)
+    m.set_graphs(True)
+    inp = synth.make_inputs(cfg, 2, first_row=3)
+    ref_act, ref_kv = run(cfg, inp)
+    ref_kv = ref_kv.cpu()
+    d = to_dev(inp)
+    kv_in, kv_out = m.alloc_kv(2), m.alloc_kv(2)
+    m.prefill(2, d["pixels"], d["text_ids"], kv_in)
+    act = torch.empty_like(d["noise"])
+    plan = [(32, 0), (48, 0), (64, 0), (96, 0), (128, 0), (160, 0), (192, 0), (224, 0), (32, 0), (96, 0),
+            (64, 192), (128, 128), (96, 64), (256, 0)]
+    for vcu, acu in plan:
+        kv_out.zero_()
+        act.zero_()
+        vla.step(m, 2, d["pixels"], d["text_ids"], kv_out, m, 2, kv_in, d["noise"], cfg.steps, act,
+                 vlm_cu_count=vcu, adit_cu_count=acu)
+        torch.cuda.synchronize()
+        np.testing.assert_array_equal(act.cpu().numpy(), ref_act, err_msg=f"vlm {vcu} adit {acu}")
+        assert bool((kv_out.cpu() == ref_kv).all()), f"vlm {vcu} adit {acu}"
+
+
 def test_two_models_colocated_lockstep():
     """Two different models share the VLM and action streams (one lockstep
     runs model A's prefill with model B's denoise)."""
