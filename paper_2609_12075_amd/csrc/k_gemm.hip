@@ -636,7 +636,7 @@ __global__ void __launch_bounds__(256) gemm_skinny_kernel(GemmArgs a) {
 // 16 * lane, one wave writes 1 KiB contiguous) through STAGES buffers, so
 // STAGES - 1 K-steps of loads are in flight without holding registers.
 // LDS rows are BK bf16 without padding; the 16-byte chunk c of row r is
-// stored in slot c ^ swz(r) (BK 64: (r >> 1) & 7; BK 32: (r >> 2) & 3), which
+// stored in slot c ^ swz(r) (BK 128: r & 15; BK 64: (r >> 1) & 7; BK 32: (r >> 2) & 3), which
 // makes the matrix-core fragment reads (16 rows, one chunk) conflict-free.
 // Chunks outside the operand (rows >= M or N, columns >= K) are read from a
 // zero buffer, which zero-fills K tails exactly. Block: 4 waves in a 2 x 2
@@ -648,12 +648,12 @@ gemm_stage_kernel(GemmArgs a) {
   constexpr int ROWB = BK * 2;                          // bytes per LDS row
   constexpr int CPR = BK / 8;                           // 16-byte chunks per row
   constexpr int RPI = 64 / CPR;                         // rows per wave load instruction
-  constexpr int SWS = BK == 64 ? 1 : 2;                 // swizzle: slot = c ^ ((r >> SWS) & (CPR - 1))
+  constexpr int SWS = BK == 128 ? 0 : (BK == 64 ? 1 : 2);   // swizzle: slot = c ^ ((r >> SWS) & (CPR - 1))
   constexpr int TN = BN / 32, TM = BM / 32;
   constexpr int STAGE_BYTES = (BN + BM) * ROWB;
   constexpr int WG = BN / RPI / 4, AG = BM / RPI / 4;   // row groups per wave (W, A)
   constexpr int LOADS = WG + AG;                        // direct loads per thread per stage
-  static_assert(BK == 64 || BK == 32, "BK must be 32 or 64");
+  static_assert(BK == 128 || BK == 64 || BK == 32, "BK must be 32, 64 or 128");
   constexpr int LDC = BN + 4;
   constexpr int SMEM = STAGES * STAGE_BYTES > BM * LDC * 4 ? STAGES * STAGE_BYTES : BM * LDC * 4;
   __shared__ __attribute__((aligned(1024))) char smem[SMEM];
@@ -985,6 +985,34 @@ GemmPlan gemm_plan(const GemmArgs& a) {
       p.ksplit = nk * BK;
       return p;
     }
+    // a few hundred activation rows (the action stage at batch 2-16, short
+    // prefills): 64 x 64 tiles with K-steps of 128 while they fit in one
+    // round of two blocks per CU (<= 512 blocks), three stages when one block
+    // per CU suffices; the number of K ranges s from a cost model fitted to
+    // measured sweeps: ceil(K-steps / s) x step time (0.55 us at one block
+    // per CU, 0.75 us at two) + for s > 1 the reduce (~1 us + its fp32
+    // partial traffic at ~5 TB/s, 8 M N s bytes)
+    if (a.M <= 1024 && a.K <= 4096 && (a.M > 64 || (a.N < 1536 && a.K >= 2048))) {
+      const long t64 = blocks(64, 64);
+      const int nk128 = (a.K + 127) / 128;
+      double best_t = 1e30;
+      int best_s = 0;
+      for (int sp = 1; sp <= 8; sp *= 2) {
+        if (t64 * sp > 512 || (sp > 1 && (nk128 < 2 * sp || !a.ws || (long)sp * a.M * ldp > a.ws_floats))) continue;
+        const int ksteps = (nk128 + sp - 1) / sp;
+        double t = ksteps * (t64 * sp <= 256 ? 0.55 : 0.75);
+        if (sp > 1) t += 1.0 + 8.0 * a.M * (double)a.N * sp / 5e6;
+        if (t < best_t) { best_t = t; best_s = sp; }
+      }
+      if (best_s > 0) {
+        const int ksteps = (nk128 + best_s - 1) / best_s;
+        p.bn = 64; p.bm = 64; p.kind = 4; p.bk = 128;
+        p.stages = t64 * best_s <= 256 ? 3 : 2;
+        p.ksplit = ksteps * 128;
+        p.splits = (nk128 + ksteps - 1) / ksteps;
+        return p;
+      }
+    }
     // many activation rows: the LDS-staged kernel (two stages, two blocks per
     // CU). Tile (128 x 128 or 128 x 64) and K ranges from a cost model fitted
     // to measured sweeps: K ranges until the blocks fill both slots of every
@@ -1063,6 +1091,20 @@ static void launch_staged(const GemmArgs& a0, const GemmPlan& p, const NormArgs*
   hipLaunchKernelGGL((gemm_stage_kernel<BN, BM, 2, MODE>), grid, dim3(256), 0, s, a);
 }
 
+template <int ST, int MODE>
+static void launch_staged128(const GemmArgs& a0, const GemmPlan& p, const NormArgs* fuse, hipStream_t s) {
+  GemmArgs a = a0;
+  a.ksplit = p.ksplit;
+  a.splits = p.splits;
+  dim3 grid((a.M + 63) / 64, (a.N + 63) / 64, a.splits);
+  if (a.splits > 1) {
+    hipLaunchKernelGGL((gemm_stage_kernel<64, 64, ST, EPI_STORE, 128>), grid, dim3(256), 0, s, a);
+    launch_reduce<MODE>(a, fuse, s);
+    return;
+  }
+  hipLaunchKernelGGL((gemm_stage_kernel<64, 64, ST, MODE, 128>), grid, dim3(256), 0, s, a);
+}
+
 template <int MODE, int NW = 8>
 static void launch_big(const GemmArgs& a, hipStream_t s) {
   dim3 grid((a.M + 255) / 256, (a.N + 255) / 256, 1);
@@ -1110,6 +1152,11 @@ static void launch_mode(const GemmArgs& a, const GemmPlan& p, const NormArgs* fu
   }
   if (p.kind == 3) {
     launch_big<MODE>(a, s);
+    return;
+  }
+  if (p.kind == 4) {
+    if (p.stages == 3) launch_staged128<3, MODE>(a, p, fuse, s);
+    else launch_staged128<2, MODE>(a, p, fuse, s);
     return;
   }
   if (p.kind == 2) {
