@@ -123,6 +123,10 @@ struct GemmArgs {
   // set by launch_gemm: every epilogue access of four consecutive columns is
   // a single aligned vector access (N % 4 == 0, aligned bases and strides)
   int epi_vec;
+  // planner hint: a row norm of this residual projection's output follows
+  // (launch_gemm_norm); with K ranges it runs inside the reduce, without
+  // them it costs a kernel of its own
+  int norm_follows;
 };
 
 void launch_gemm(const GemmArgs& a, hipStream_t s);

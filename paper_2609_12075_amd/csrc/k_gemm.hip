@@ -1002,6 +1002,7 @@ GemmPlan gemm_plan(const GemmArgs& a) {
         const int ksteps = (nk128 + sp - 1) / sp;
         double t = ksteps * (t64 * sp <= 256 ? 0.55 : 0.75);
         if (sp > 1) t += 1.0 + 8.0 * a.M * (double)a.N * sp / 5e6;
+        else if (a.norm_follows) t += 4.0;     // the norm kernel the reduce would have absorbed
         if (t < best_t) { best_t = t; best_s = sp; }
       }
       if (best_s > 0) {
@@ -1039,6 +1040,7 @@ GemmPlan gemm_plan(const GemmArgs& a) {
         const long rounds = (tiles * sp + 511) / 512;
         double t = rounds * ksteps * (bm == 128 ? 0.87 : 0.59);
         if (sp > 1) t += 4.0 * sp * a.M * ldp / 5e6 + 3.0;
+        else if (a.norm_follows) t += 4.0;
         if (t < best_t) {
           best_t = t;
           p.bn = 128; p.bm = bm; p.kind = 1; p.splits = sp; p.ksplit = ksteps * BK;
@@ -1223,13 +1225,13 @@ void launch_gemm_norm(const GemmArgs& a, const NormArgs& n, hipStream_t s) {
                        n.skip == 0 && n.rows == a.M && n.d == a.N && n.in == a.out && n.ld_in == a.ldo &&
                        a.N % 4 == 0 && a.ldo % 4 == 0 && n.ld_out % 4 == 0 && a.N <= 2048;
   if (fusable) {
-    const GemmPlan p = gemm_plan(a);
-    if (p.splits > 1) {
-      GemmArgs av = a;
-      av.epi_vec = epi_vec_ok(av) ? 1 : 0;
-      launch_mode<EPI_RESID>(av, p, &n, s);
-      return;
-    }
+    GemmArgs av = a;
+    av.norm_follows = 1;
+    av.epi_vec = epi_vec_ok(av) ? 1 : 0;
+    const GemmPlan p = gemm_plan(av);
+    launch_mode<EPI_RESID>(av, p, p.splits > 1 ? &n : nullptr, s);
+    if (p.splits == 1) launch_norm(n, s);
+    return;
   }
   launch_gemm(a, s);
   launch_norm(n, s);

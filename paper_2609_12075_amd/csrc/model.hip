@@ -787,6 +787,7 @@ GemmArgs vla_model_s::stage_gemm(int which, int B, int layer) const {
     case 1:   // VLM stage: LLM layer MLP down projection (+ residual)
       g = gm(*this, ST,llm[ll].wd, B * P, gu, c.llm_mlp, et);
       g.mode = EPI_RESID; g.out = h; g.ldo = D; g.out_type = ET_F32;
+      g.norm_follows = 1;     // the stage runs it with the next layer's norm fused
       break;
     case 2:   // action stage: layer MLP up (GeGLU for the joint expert, GELU for the DiT)
       if (c.head_kind == VLA_HEAD_JOINT) {
@@ -805,6 +806,7 @@ GemmArgs vla_model_s::stage_gemm(int which, int B, int layer) const {
         g = gm(*this, ST,dit[la].w2, B * Ltok, mlp, c.act_mlp, et);
         g.mode = EPI_RESID; g.bias = dit[la].b2; g.out = X; g.ldo = Da; g.out_type = ET_F32;
       }
+      g.norm_follows = 1;
       break;
     case 4:   // VLM stage: ViT layer MLP up (GELU)
       VLA_REQUIRE(c.vit_layers > 0, "model has no ViT");
