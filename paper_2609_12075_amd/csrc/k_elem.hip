@@ -21,13 +21,14 @@ __global__ void __launch_bounds__(256) norm_kernel(NormArgs a) {
   if (r >= a.rows) return;
   const int rin = a.skip > 0 ? r + (r / a.skip_group + 1) * a.skip : r;
   const float* x = a.in + (long)rin * a.ld_in;
-  rownorm::f4 v[NV];
+  rownorm::f4 v[NV], g[NV], b[NV];
 #pragma unroll
   for (int j = 0; j < NV; ++j) {
     const int i = (j * 64 + lane) * 4;
     v[j] = i < a.d ? *reinterpret_cast<const rownorm::f4*>(x + i) : rownorm::f4{0.f, 0.f, 0.f, 0.f};
   }
-  rownorm::store_row<NV>(a, r, v, lane);
+  rownorm::load_params<NV>(a, lane, g, b);
+  rownorm::store_row<NV>(a, r, v, lane, g, b);
 }
 
 // ---------------------------------------------------------------- staging

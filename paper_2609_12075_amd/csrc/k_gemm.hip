@@ -499,24 +499,38 @@ __global__ void __launch_bounds__(256) splitk_reduce_norm_kernel(GemmArgs a, Nor
   const long stride = (long)a.M * ldp;
   const float* p = a.ws + (long)r * ldp;
   float* x = reinterpret_cast<float*>(a.out) + (long)r * a.ldo;
-  // every load of the row (partials in split order, old x) before the first
-  // store, so they share one memory round trip
-  rownorm::f4 v[NV];
+  // every load of the row (partials in split order, old x, the residual's
+  // bias and gate, the norm's parameters) before the first store, so they
+  // share one memory round trip per four K ranges
+  rownorm::f4 v[NV], g[NV], b[NV];
   f32x4 t[NV], bs[NV], gt[NV];
   const bool has_bias = a.bias != nullptr, has_gate = a.gate != nullptr;
 #pragma unroll
   for (int j = 0; j < NV; ++j) {
     const int i = min((j * 64 + lane) * 4, a.N - 4);
-    f32x4 part[16];
-#pragma unroll
-    for (int z = 0; z < 16; ++z)
-      part[z] = z < a.splits ? *reinterpret_cast<const f32x4*>(p + z * stride + i) : f32x4{0.f, 0.f, 0.f, 0.f};
-    t[j] = part[0];
-#pragma unroll
-    for (int z = 1; z < 16; ++z) t[j] += part[z];
     v[j] = *reinterpret_cast<const f32x4*>(x + i);
     bs[j] = has_bias ? *reinterpret_cast<const f32x4*>(a.bias + i) : f32x4{0.f, 0.f, 0.f, 0.f};
     gt[j] = has_gate ? *reinterpret_cast<const f32x4*>(a.gate + i) : f32x4{1.f, 1.f, 1.f, 1.f};
+  }
+  rownorm::load_params<NV>(n, lane, g, b);
+  for (int z0 = 0; z0 < a.splits; z0 += 4) {
+    f32x4 part[NV][4];
+#pragma unroll
+    for (int j = 0; j < NV; ++j) {
+      const int i = min((j * 64 + lane) * 4, a.N - 4);
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        part[j][q] = z0 + q < a.splits ? *reinterpret_cast<const f32x4*>(p + (z0 + q) * stride + i)
+                                       : f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+#pragma unroll
+    for (int j = 0; j < NV; ++j) {
+      // partials summed in split order
+      if (z0 == 0) t[j] = part[j][0];
+      else t[j] += part[j][0];
+#pragma unroll
+      for (int q = 1; q < 4; ++q) t[j] += part[j][q];
+    }
   }
 #pragma unroll
   for (int j = 0; j < NV; ++j) {
@@ -529,7 +543,7 @@ __global__ void __launch_bounds__(256) splitk_reduce_norm_kernel(GemmArgs a, Nor
     v[j] += (t[j] + bs[j]) * gt[j];
     *reinterpret_cast<f32x4*>(x + i) = v[j];
   }
-  rownorm::store_row<NV>(n, r, v, lane);
+  rownorm::store_row<NV>(n, r, v, lane, g, b);
 }
 
 // ---------------------------------------------------------------- small-M kernel

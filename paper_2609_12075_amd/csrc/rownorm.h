@@ -15,12 +15,28 @@ __device__ __forceinline__ float wave_sum(float v) {
   return v;
 }
 
+// The norm's per-column parameters for this lane's columns: g (gain or
+// adaLN scale, 1 when absent) and b (bias or adaLN shift, 0 when absent).
+// Loaded together with the row itself, so both share one memory round trip.
+template <int NV>
+__device__ __forceinline__ void load_params(const NormArgs& a, int lane, f4 (&g)[NV], f4 (&b)[NV]) {
+#pragma unroll
+  for (int j = 0; j < NV; ++j) {
+    const int i = (j * 64 + lane) * 4;
+    const bool ok = i < a.d;
+    g[j] = (ok && a.g) ? *reinterpret_cast<const f4*>(a.g + i) : f4{a.kind == 2 ? 0.f : 1.f, a.kind == 2 ? 0.f : 1.f,
+                                                                    a.kind == 2 ? 0.f : 1.f, a.kind == 2 ? 0.f : 1.f};
+    b[j] = (ok && a.b) ? *reinterpret_cast<const f4*>(a.b + i) : f4{0.f, 0.f, 0.f, 0.f};
+  }
+}
+
 // Statistics of the row (two passes over registers: mean for the LayerNorm
 // kinds, then the centred second moment), then output row r of a:
 // kind 0 RMSNorm * g; kind 1 LayerNorm * g + b (each optional);
 // kind 2 LayerNorm * (1 + g) + b (adaLN modulation: g = scale, b = shift).
 template <int NV>
-__device__ __forceinline__ void store_row(const NormArgs& a, int r, const f4 (&v)[NV], int lane) {
+__device__ __forceinline__ void store_row(const NormArgs& a, int r, const f4 (&v)[NV], int lane, const f4 (&g)[NV],
+                                          const f4 (&b)[NV]) {
   const int d = a.d;
   float mean = 0.f;
   if (a.kind != 0) {
@@ -46,12 +62,11 @@ __device__ __forceinline__ void store_row(const NormArgs& a, int r, const f4 (&v
 #pragma unroll
     for (int e = 0; e < 4; ++e) y[e] = (v[j][e] - mean) * rstd;
     if (a.kind == 2) {
-      const f4 sc = *reinterpret_cast<const f4*>(a.g + i), sh = *reinterpret_cast<const f4*>(a.b + i);
 #pragma unroll
-      for (int e = 0; e < 4; ++e) y[e] = y[e] * (1.0f + sc[e]) + sh[e];
+      for (int e = 0; e < 4; ++e) y[e] = y[e] * (1.0f + g[j][e]) + b[j][e];
     } else {
-      if (a.g) { const f4 g = *reinterpret_cast<const f4*>(a.g + i); y *= g; }
-      if (a.b) { const f4 b = *reinterpret_cast<const f4*>(a.b + i); y += b; }
+      if (a.g) y *= g[j];
+      if (a.b) y += b[j];
     }
     if (a.out_type == ET_BF16) {
       *reinterpret_cast<b4*>(reinterpret_cast<bf16*>(a.out) + (long)r * a.ld_out + i) =
