@@ -308,21 +308,26 @@ def main():
     # The VLM stream's CU restriction for this (VLM batch, action batch)
     # combination: the fastest candidate in a short profile (the paper's
     # offline restriction table, for the one combination the benchmark runs).
+    # Two passes over the candidates, 6 timed locksteps each, averaged, so a
+    # momentary slowdown does not decide the choice.
     cu_profile = None
     if auto_cu:
-        cu_profile = {}
-        for cu in [int(x) for x in args.cu_candidates.split(",")]:
-            args.cu = cu
-            for k in range(1, 3):
-                lockstep(k)
-            torch.cuda.synchronize()
-            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            a.record(stream)
-            for k in range(1, 5):
-                lockstep(k)
-            b.record(stream)
-            torch.cuda.synchronize()
-            cu_profile[cu] = round(a.elapsed_time(b) / 4, 4)
+        cands = [int(x) for x in args.cu_candidates.split(",")]
+        sums = {cu: 0.0 for cu in cands}
+        for _ in range(2):
+            for cu in cands:
+                args.cu = cu
+                for k in range(1, 3):
+                    lockstep(k)
+                torch.cuda.synchronize()
+                a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                a.record(stream)
+                for k in range(1, 7):
+                    lockstep(k)
+                b.record(stream)
+                torch.cuda.synchronize()
+                sums[cu] += a.elapsed_time(b) / 6
+        cu_profile = {cu: round(sums[cu] / 2, 4) for cu in cands}
         args.cu = min(cu_profile, key=cu_profile.get)
         log(f"[bench] lockstep ms by VLM CU count {cu_profile}: using {args.cu}")
 

@@ -134,8 +134,9 @@ void launch_gemm(const GemmArgs& a, hipStream_t s);
 // Launch plan of a bf16 projection: tile (bn weight rows x bm activation
 // rows), number of K ranges and the K length per range.
 // kind 0: register-pipelined, 1: multi-stage (K-steps of 64), 2: small-M,
-// 3: large-tile, 4: multi-stage 64 x 64 tiles with K-steps of 128 (stages 2 or 3)
-struct GemmPlan { int bn, bm, splits, ksplit, kind, stages = 2, bk = 64; };
+// 3: large-tile, 4: multi-stage 64 x 64 or 128 x 128 tiles with K-steps of 128
+// (stages 2 or 3); kg: wave groups sharing each K-step (4 waves each)
+struct GemmPlan { int bn, bm, splits, ksplit, kind, stages = 2, bk = 64, kg = 1; };
 GemmPlan gemm_plan(const GemmArgs& a);
 
 // Attention: O = softmax(Q K^T * scale) V with grouped KV heads, keys drawn

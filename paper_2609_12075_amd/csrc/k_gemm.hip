@@ -302,9 +302,10 @@ __device__ __forceinline__ void tile_epilogue(const GemmArgs& a, const float* Cs
   }
 }
 
-// Epilogue of the split-K partial pass: the fp32 tile goes to the workspace
-// slice of K range bz unchanged (the reduce kernel runs the epilogue).
-template <int BN, int ROWS, int NT, int LDC>
+// Epilogue of the split-K partial pass: the fp32 tile (the sum of NSUM
+// planes, in plane order) goes to the workspace slice of K range bz (the
+// reduce kernel runs the epilogue).
+template <int BN, int ROWS, int NT, int LDC, int NSUM = 1>
 __device__ __forceinline__ void tile_store_partial(const GemmArgs& a, const float* Cs, int m_blk, int n_blk, int bz,
                                                    int tid) {
   constexpr int CPT = BN / 4, RS = NT / CPT, NIT = (ROWS + RS - 1) / RS;
@@ -315,8 +316,12 @@ __device__ __forceinline__ void tile_store_partial(const GemmArgs& a, const floa
 #pragma unroll
   for (int it = 0; it < NIT; ++it) {
     const int mr = r0 + it * RS, m = m_blk + mr;
-    if ((ROWS % RS == 0 || mr < ROWS) && m < a.M)
-      *reinterpret_cast<f32x4*>(part + (long)m * ldp + n) = *reinterpret_cast<const f32x4*>(Cs + mr * LDC + nc);
+    if ((ROWS % RS == 0 || mr < ROWS) && m < a.M) {
+      f32x4 t = *reinterpret_cast<const f32x4*>(Cs + mr * LDC + nc);
+#pragma unroll
+      for (int z = 1; z < NSUM; ++z) t += *reinterpret_cast<const f32x4*>(Cs + z * ROWS * LDC + mr * LDC + nc);
+      *reinterpret_cast<f32x4*>(part + (long)m * ldp + n) = t;
+    }
   }
 }
 
@@ -653,28 +658,38 @@ __global__ void __launch_bounds__(256) gemm_skinny_kernel(GemmArgs a) {
 // stored in slot c ^ swz(r) (BK 128: r & 15; BK 64: (r >> 1) & 7; BK 32: (r >> 2) & 3), which
 // makes the matrix-core fragment reads (16 rows, one chunk) conflict-free.
 // Chunks outside the operand (rows >= M or N, columns >= K) are read from a
-// zero buffer, which zero-fills K tails exactly. Block: 4 waves in a 2 x 2
-// grid, wave tile (BN/2) x (BM/2) of 16 x 16 x 32 products. BK 32 with more
-// stages keeps the same LDS per block but more K-steps of loads in flight.
-template <int BN, int BM, int STAGES, int MODE, int BK = 64>
-__global__ void __launch_bounds__(256)
+// zero buffer, which zero-fills K tails exactly. Block: KG groups of 4 waves;
+// the waves of a group form a 2 x 2 grid of (BN/2) x (BM/2) wave tiles of
+// 16 x 16 x 32 products, and group g takes K chunks g, g + KG, ... of every
+// K-step's BK / 32 (a second group doubles the waves that issue loads and
+// fragment reads per CU: with one wave per SIMD, LDS reads stay
+// latency-bound at ~100 B/clk per CU, with two they reach ~280). The groups'
+// tiles are summed in a fixed order in the epilogue. BK 32 with more stages
+// keeps the same LDS per block but more K-steps of loads in flight.
+template <int BN, int BM, int STAGES, int MODE, int BK = 64, int KG = 1>
+__global__ void __launch_bounds__(256 * KG)
 gemm_stage_kernel(GemmArgs a) {
+  constexpr int NT = 256 * KG, NWV = 4 * KG;            // threads, waves
   constexpr int ROWB = BK * 2;                          // bytes per LDS row
   constexpr int CPR = BK / 8;                           // 16-byte chunks per row
   constexpr int RPI = 64 / CPR;                         // rows per wave load instruction
   constexpr int SWS = BK == 128 ? 0 : (BK == 64 ? 1 : 2);   // swizzle: slot = c ^ ((r >> SWS) & (CPR - 1))
   constexpr int TN = BN / 32, TM = BM / 32;
   constexpr int STAGE_BYTES = (BN + BM) * ROWB;
-  constexpr int WG = BN / RPI / 4, AG = BM / RPI / 4;   // row groups per wave (W, A)
+  constexpr int WG = BN / RPI / NWV, AG = BM / RPI / NWV;   // row groups per wave (W, A)
   constexpr int LOADS = WG + AG;                        // direct loads per thread per stage
+  constexpr int KC = BK / 32, KCG = KC / KG;            // K chunks per step, per wave group
   static_assert(BK == 128 || BK == 64 || BK == 32, "BK must be 32, 64 or 128");
+  static_assert(WG * RPI * NWV == BN && AG * RPI * NWV == BM, "row groups must divide among the waves");
+  static_assert(KCG * KG == KC, "K chunks must divide among the wave groups");
   constexpr int LDC = BN + 4;
-  constexpr int SMEM = STAGES * STAGE_BYTES > BM * LDC * 4 ? STAGES * STAGE_BYTES : BM * LDC * 4;
+  constexpr int CS_BYTES = KG * BM * LDC * 4;           // one fp32 tile plane per wave group
+  constexpr int SMEM = STAGES * STAGE_BYTES > CS_BYTES ? STAGES * STAGE_BYTES : CS_BYTES;
   __shared__ __attribute__((aligned(1024))) char smem[SMEM];
-  auto Cs = reinterpret_cast<float (*)[LDC]>(smem);
+  float* Cs = reinterpret_cast<float*>(smem);
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wn0 = (wave >> 1) * (BN / 2), wm0 = (wave & 1) * (BM / 2);
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, kg = wave >> 2, w4 = wave & 3;
+  const int wn0 = (w4 >> 1) * (BN / 2), wm0 = (w4 & 1) * (BM / 2);
   int bx, by, bz;
   xcd_remap_grouped(bx, by, bz, 8);
   const int n_blk = by * BN, m_blk = bx * BM;
@@ -693,14 +708,14 @@ gemm_stage_kernel(GemmArgs a) {
     char* st = smem + buf * STAGE_BYTES;
 #pragma unroll
     for (int j = 0; j < WG; ++j) {
-      const int grp = j * 4 + wave, r = grp * RPI + lrow;
+      const int grp = j * NWV + wave, r = grp * RPI + lrow;
       const int c = slot ^ ((r >> SWS) & (CPR - 1)), k = kbeg + kt * BK + c * 8, n = n_blk + r;
       const bf16* src = (n < a.N && k < K) ? W + (long)n * a.ldw + k : Z;
       __builtin_amdgcn_global_load_lds(src, st + grp * RPI * ROWB, 16, 0, 0);
     }
 #pragma unroll
     for (int j = 0; j < AG; ++j) {
-      const int grp = j * 4 + wave, r = grp * RPI + lrow;
+      const int grp = j * NWV + wave, r = grp * RPI + lrow;
       const int c = slot ^ ((r >> SWS) & (CPR - 1)), k = kbeg + kt * BK + c * 8, m = m_blk + r;
       const bf16* src = (m < a.M && k < K) ? A + (long)m * a.lda + k : Z;
       __builtin_amdgcn_global_load_lds(src, st + BN * ROWB + grp * RPI * ROWB, 16, 0, 0);
@@ -729,33 +744,33 @@ gemm_stage_kernel(GemmArgs a) {
     }
     if (kt + STAGES - 1 < nk) issue(kt + STAGES - 1, (kt + STAGES - 1) % STAGES);
     const char* st = smem + (kt % STAGES) * STAGE_BYTES;
-    // all fragments of the K-step, then the products; the scheduler is told
-    // to interleave the second chunk's fragment reads with the first chunk's
-    // matrix instructions, so LDS latency hides behind matrix work
-    constexpr int KC = BK / 32;
-    bf16x8 wf[KC][TN], af[KC][TM];
+    // all of the group's fragments of the K-step, then the products; the
+    // scheduler is told to interleave the second chunk's fragment reads with
+    // the first chunk's matrix instructions, so LDS latency hides behind
+    // matrix work
+    bf16x8 wf[KCG][TN], af[KCG][TM];
 #pragma unroll
-    for (int kc = 0; kc < KC; ++kc) {
-      const int c = kc * 4 + lq;
+    for (int q = 0; q < KCG; ++q) {
+      const int c = (q * KG + kg) * 4 + lq;
 #pragma unroll
       for (int i = 0; i < TN; ++i) {
         const int r = wn0 + 16 * i + lr;
-        wf[kc][i] = *reinterpret_cast<const bf16x8*>(st + r * ROWB + ((c ^ ((r >> SWS) & (CPR - 1))) << 4));
+        wf[q][i] = *reinterpret_cast<const bf16x8*>(st + r * ROWB + ((c ^ ((r >> SWS) & (CPR - 1))) << 4));
       }
 #pragma unroll
       for (int j = 0; j < TM; ++j) {
         const int r = wm0 + 16 * j + lr;
-        af[kc][j] = *reinterpret_cast<const bf16x8*>(st + BN * ROWB + r * ROWB + ((c ^ ((r >> SWS) & (CPR - 1))) << 4));
+        af[q][j] = *reinterpret_cast<const bf16x8*>(st + BN * ROWB + r * ROWB + ((c ^ ((r >> SWS) & (CPR - 1))) << 4));
       }
     }
 #pragma unroll
-    for (int kc = 0; kc < KC; ++kc)
+    for (int q = 0; q < KCG; ++q)
 #pragma unroll
       for (int i = 0; i < TN; ++i)
 #pragma unroll
         for (int j = 0; j < TM; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[kc][i], af[kc][j], acc[i][j], 0, 0, 0);
-    if constexpr (KC == 2) {
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[q][i], af[q][j], acc[i][j], 0, 0, 0);
+    if constexpr (KCG == 2) {
       constexpr int NRD = TN + TM, NMF = TN * TM, R = NMF / NRD > 0 ? NMF / NRD : 1;
       __builtin_amdgcn_sched_group_barrier(0x100, NRD, 0);      // chunk 0 reads
 #pragma unroll
@@ -766,26 +781,31 @@ gemm_stage_kernel(GemmArgs a) {
       __builtin_amdgcn_sched_group_barrier(0x008, 2 * NMF - NRD * R, 0);
     }
   }
+  // each wave group's tile to its own fp32 plane; the epilogues add the
+  // planes in group order
   __syncthreads();
+  float* Cp = Cs + kg * BM * LDC;
 #pragma unroll
   for (int i = 0; i < TN; ++i)
 #pragma unroll
     for (int j = 0; j < TM; ++j)
-      *reinterpret_cast<f32x4*>(&Cs[wm0 + 16 * j + lr][wn0 + 16 * i + (lane >> 4) * 4]) = acc[i][j];
+      *reinterpret_cast<f32x4*>(&Cp[(wm0 + 16 * j + lr) * LDC + wn0 + 16 * i + (lane >> 4) * 4]) = acc[i][j];
   __syncthreads();
   if (a.splits > 1) {
     // split-K: store this K range's partial tile; the reduce kernel finishes
-    tile_store_partial<BN, BM, 256, LDC>(a, &Cs[0][0], m_blk, n_blk, bz, tid);
+    tile_store_partial<BN, BM, NT, LDC, KG>(a, Cs, m_blk, n_blk, bz, tid);
     return;
   }
   if (a.epi_vec) {
-    tile_epilogue<MODE, BN, BM, 256, LDC>(a, &Cs[0][0], m_blk, n_blk, tid);
+    tile_epilogue<MODE, BN, BM, NT, LDC, KG>(a, Cs, m_blk, n_blk, tid);
     return;
   }
 #pragma unroll 1
-  for (int c = tid; c < BM * (BN / 4); c += 256) {
+  for (int c = tid; c < BM * (BN / 4); c += NT) {
     const int mr = c / (BN / 4), nc = (c % (BN / 4)) * 4;
-    f32x4 t = *reinterpret_cast<const f32x4*>(&Cs[mr][nc]);
+    f32x4 t = *reinterpret_cast<const f32x4*>(&Cs[mr * LDC + nc]);
+#pragma unroll
+    for (int z = 1; z < KG; ++z) t += *reinterpret_cast<const f32x4*>(&Cs[z * BM * LDC + mr * LDC + nc]);
     float v[4] = {t[0], t[1], t[2], t[3]};
     epilogue4<MODE>(a, m_blk + mr, n_blk + nc, v);
   }
@@ -999,32 +1019,46 @@ GemmPlan gemm_plan(const GemmArgs& a) {
       p.ksplit = nk * BK;
       return p;
     }
-    // a few hundred activation rows (the action stage at batch 2-16, short
-    // prefills): 64 x 64 tiles with K-steps of 128 while they fit in one
-    // round of two blocks per CU (<= 512 blocks), three stages when one block
-    // per CU suffices; the number of K ranges s from a cost model fitted to
-    // measured sweeps: ceil(K-steps / s) x step time (0.55 us at one block
-    // per CU, 0.75 us at two) + for s > 1 the reduce (~1 us + its fp32
-    // partial traffic at ~5 TB/s, 8 M N s bytes)
+    // a few hundred activation rows (the action stage at batch 2-32, short
+    // prefills): K-steps of 128 shared by two wave groups (8 waves). 64 x 64
+    // tiles while they fit in one round of two blocks per CU (<= 512 blocks),
+    // three stages (96 KiB of LDS, one block per CU) when the blocks fit in
+    // kOneRoundCUs; the number of K ranges s from a cost model fitted to
+    // measured sweeps: ceil(K-steps / s) x step time (0.48 us at one block per
+    // CU, 0.9 us at two) + for s > 1 the reduce (~2.5 us + its fp32 partial
+    // traffic at ~5 TB/s, 8 M N s bytes), or for s = 1 the row norm's own
+    // kernel when one follows (~4 us). Wider products whose 128 x 128 tiles
+    // (135 KiB of LDS) fill 160 to kOneRoundCUs CUs once take those tiles
+    // (measured 10-15 % faster than 128 x 64 tiles with K-steps of 64 there).
+    // kOneRoundCUs is below the chip's 256 because the action stage shares
+    // the GPU with a VLM stage that holds some CUs' LDS: one-block-per-CU
+    // launches sized for all 256 CUs ran a second round there.
+    constexpr long kOneRoundCUs = 192;
     if (a.M <= 1024 && a.K <= 4096 && (a.M > 64 || (a.N < 1536 && a.K >= 2048))) {
-      const long t64 = blocks(64, 64);
+      const long t64 = blocks(64, 64), t128 = blocks(128, 128);
       const int nk128 = (a.K + 127) / 128;
       double best_t = 1e30;
       int best_s = 0;
       for (int sp = 1; sp <= 8; sp *= 2) {
         if (t64 * sp > 512 || (sp > 1 && (nk128 < 2 * sp || !a.ws || (long)sp * a.M * ldp > a.ws_floats))) continue;
         const int ksteps = (nk128 + sp - 1) / sp;
-        double t = ksteps * (t64 * sp <= 256 ? 0.55 : 0.75);
-        if (sp > 1) t += 1.0 + 8.0 * a.M * (double)a.N * sp / 5e6;
-        else if (a.norm_follows) t += 4.0;     // the norm kernel the reduce would have absorbed
+        double t = ksteps * (t64 * sp <= kOneRoundCUs ? 0.48 : 0.9);
+        if (sp > 1) t += 2.5 + 8.0 * a.M * (double)a.N * sp / 5e6;
+        else if (a.norm_follows) t += 4.0;
         if (t < best_t) { best_t = t; best_s = sp; }
       }
       if (best_s > 0) {
         const int ksteps = (nk128 + best_s - 1) / best_s;
-        p.bn = 64; p.bm = 64; p.kind = 4; p.bk = 128;
-        p.stages = t64 * best_s <= 256 ? 3 : 2;
+        p.bn = 64; p.bm = 64; p.kind = 4; p.bk = 128; p.kg = 2;
+        p.stages = t64 * best_s <= kOneRoundCUs ? 3 : 2;
         p.ksplit = ksteps * 128;
         p.splits = (nk128 + ksteps - 1) / ksteps;
+        return p;
+      }
+      if (a.M >= 256 && t128 >= 160 && t128 <= kOneRoundCUs) {
+        p.bn = 128; p.bm = 128; p.kind = 4; p.bk = 128; p.kg = 2; p.stages = 2;
+        p.ksplit = nk128 * 128;
+        p.splits = 1;
         return p;
       }
     }
@@ -1107,18 +1141,18 @@ static void launch_staged(const GemmArgs& a0, const GemmPlan& p, const NormArgs*
   hipLaunchKernelGGL((gemm_stage_kernel<BN, BM, 2, MODE>), grid, dim3(256), 0, s, a);
 }
 
-template <int ST, int MODE>
+template <int BT, int ST, int MODE>
 static void launch_staged128(const GemmArgs& a0, const GemmPlan& p, const NormArgs* fuse, hipStream_t s) {
   GemmArgs a = a0;
   a.ksplit = p.ksplit;
   a.splits = p.splits;
-  dim3 grid((a.M + 63) / 64, (a.N + 63) / 64, a.splits);
+  dim3 grid((a.M + BT - 1) / BT, (a.N + BT - 1) / BT, a.splits);
   if (a.splits > 1) {
-    hipLaunchKernelGGL((gemm_stage_kernel<64, 64, ST, EPI_STORE, 128>), grid, dim3(256), 0, s, a);
+    hipLaunchKernelGGL((gemm_stage_kernel<BT, BT, ST, EPI_STORE, 128, 2>), grid, dim3(512), 0, s, a);
     launch_reduce<MODE>(a, fuse, s);
     return;
   }
-  hipLaunchKernelGGL((gemm_stage_kernel<64, 64, ST, MODE, 128>), grid, dim3(256), 0, s, a);
+  hipLaunchKernelGGL((gemm_stage_kernel<BT, BT, ST, MODE, 128, 2>), grid, dim3(512), 0, s, a);
 }
 
 template <int MODE, int NW = 8>
@@ -1171,8 +1205,9 @@ static void launch_mode(const GemmArgs& a, const GemmPlan& p, const NormArgs* fu
     return;
   }
   if (p.kind == 4) {
-    if (p.stages == 3) launch_staged128<3, MODE>(a, p, fuse, s);
-    else launch_staged128<2, MODE>(a, p, fuse, s);
+    if (p.bn == 128) launch_staged128<128, 2, MODE>(a, p, fuse, s);
+    else if (p.stages == 3) launch_staged128<64, 3, MODE>(a, p, fuse, s);
+    else launch_staged128<64, 2, MODE>(a, p, fuse, s);
     return;
   }
   if (p.kind == 2) {

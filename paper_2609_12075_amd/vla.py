@@ -161,12 +161,12 @@ class Model:
 
     def replay_gemm(self, which: int, batch: int, iters: int, stream=None):
         """Enqueue `iters` launches of one stage projection. Returns (flops of
-        one launch, plan dict: tile_n, tile_m, splits, mode, kind, stages, bk)."""
+        one launch, plan dict: tile_n, tile_m, splits, mode, kind, stages, bk, kg)."""
         f = ctypes.c_double(0.0)
-        plan = (ctypes.c_int * 7)()
+        plan = (ctypes.c_int * 8)()
         _check(lib().vla_debug_replay_gemm(self.handle, which, batch, iters, _stream(stream), ctypes.byref(f), plan))
         return f.value, {"tile_n": plan[0], "tile_m": plan[1], "splits": plan[2], "mode": plan[3], "kind": plan[4],
-                         "stages": plan[5], "bk": plan[6]}
+                         "stages": plan[5], "bk": plan[6], "kg": plan[7]}
 
     @staticmethod
     def kernel_symbol(plan):
@@ -175,7 +175,7 @@ class Model:
         mode = plan["mode"] if plan["splits"] == 1 else 0
         if plan["kind"] in (1, 4):
             return (f"gemm_stage_kernelILi{plan['tile_n']}ELi{plan['tile_m']}ELi{plan['stages']}ELi{mode}"
-                    f"ELi{plan['bk']}E")
+                    f"ELi{plan['bk']}ELi{plan['kg']}E")
         if plan["kind"] == 2:
             return f"gemm_skinny_kernelILi{plan['tile_n'] // 16}ELi{mode}E"
         if plan["kind"] == 3:

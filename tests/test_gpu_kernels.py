@@ -35,6 +35,9 @@ GEMM_SHAPES = [
     (2600, 4100, 2056),
     # staged 64 x 64 tiles (short K, mid-sized M), ragged
     (800, 1600, 720), (431, 2500, 1000),
+    # two wave groups per K-step of 128: 128 x 128 tiles, ragged M, N and K;
+    # 64 x 64 tiles with two and four K ranges (two and three stages), ragged
+    (777, 3000, 1000), (390, 1000, 4000), (130, 700, 1800), (300, 700, 1800),
 ]
 
 
@@ -87,7 +90,7 @@ def test_gemm_f32(M, N, K):
 
 @pytest.mark.parametrize("M,N,K,kind", [(50, 720, 960, 0), (50, 720, 1920, 0), (800, 720, 1920, 0),
                                           (17, 1024, 4096, 2), (200, 1024, 2048, 1), (3840, 960, 960, 0),
-                                          (7, 36, 72, 1)])
+                                          (7, 36, 72, 1), (400, 720, 1920, 2)])
 def test_resid_norm(M, N, K, kind):
     """Residual projection + row norm (fused into the split-K reduce when
     the projection splits K) against fp64."""
