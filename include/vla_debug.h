@@ -44,6 +44,27 @@ vla_status vla_debug_resid_norm(int M, int N, int K, const void* A, const void* 
                                 hipStream_t stream);
 
 /*
+ * Projection with the RMSNorm of its input rows folded in (the action
+ * expert's QKV and MLP up projections read rows not yet normalised, with the
+ * norm's gain folded into the weight columns):
+ *   out[m][n] = rsqrt(sum_k A[m][k]^2 / K + eps) * sum_k A[m][k] Wt[n][k] + bias[n]
+ * A bf16 [M][K], Wt bf16 [N][K], bias fp32 [N] or NULL, out fp32 [M][N].
+ * K % 8 == 0. The sum of squares is taken from the bf16 A the product reads.
+ */
+vla_status vla_debug_gemm_rms(int M, int N, int K, const void* A, const void* Wt, const float* bias, float eps,
+                              float* out, hipStream_t stream);
+
+/*
+ * Residual projection that also writes a bf16 copy of the updated rows (the
+ * input of a projection with a folded RMSNorm):
+ *   x[m][n] += gate[n] * (sum_k A[m][k] Wt[n][k] + bias[n]);  xb[m][n] = bf16(x[m][n])
+ * A bf16 [M][K], Wt bf16 [N][K], bias/gate fp32 [N] or NULL, x fp32 [M][N],
+ * xb bf16 [M][N]. K % 8 == 0.
+ */
+vla_status vla_debug_resid_copy(int M, int N, int K, const void* A, const void* Wt, const float* bias,
+                                const float* gate, float* x, void* xb, hipStream_t stream);
+
+/*
  * o = softmax(q k^T / sqrt(hd)) v over the keys [k0 ; k1] (segment 1 may be
  * empty), grouped KV heads (query head h uses KV head h / (Hq / Hkv)).
  *  q  device [B][Hq][Lq][hd]; k0, v0 [B][Hkv][len0][hd]; k1, v1 [B][Hkv][len1][hd];

@@ -327,6 +327,38 @@ vla_status vla_debug_resid_norm(int M, int N, int K, const void* A, const void* 
   });
 }
 
+vla_status vla_debug_gemm_rms(int M, int N, int K, const void* A, const void* Wt, const float* bias, float eps,
+                              float* out, hipStream_t s) {
+  return guarded([&] {
+    VLA_REQUIRE(M >= 0 && N >= 0 && K >= 8 && A && Wt && out, "bad gemm_rms arguments");
+    VLA_REQUIRE(K % 8 == 0, "gemm_rms needs K % 8 == 0");
+    GemmArgs g{};
+    g.M = M; g.N = N; g.K = K; g.A = A; g.lda = K; g.a_type = ET_BF16; g.W = Wt; g.ldw = K; g.w_type = ET_BF16;
+    g.mode = EPI_STORE; g.bias = bias; g.tab_period = 1; g.out = out; g.ldo = N; g.out_type = ET_F32;
+    g.ws = debug_ws(0, vla_model_s::kSplitKFloats); g.ws_floats = vla_model_s::kSplitKFloats;
+    g.zeros = debug_ws(2, 64);
+    g.rms_in = K; g.rms_eps = eps;
+    launch_gemm(g, s);
+    VLA_HIP(hipGetLastError());
+  });
+}
+
+vla_status vla_debug_resid_copy(int M, int N, int K, const void* A, const void* Wt, const float* bias,
+                                const float* gate, float* x, void* xb, hipStream_t s) {
+  return guarded([&] {
+    VLA_REQUIRE(M >= 0 && N >= 0 && K >= 8 && A && Wt && x && xb, "bad resid_copy arguments");
+    VLA_REQUIRE(K % 8 == 0, "resid_copy needs K % 8 == 0");
+    GemmArgs a{};
+    a.M = M; a.N = N; a.K = K; a.A = A; a.lda = K; a.a_type = ET_BF16; a.W = Wt; a.ldw = K; a.w_type = ET_BF16;
+    a.mode = EPI_RESID; a.bias = bias; a.gate = gate; a.tab_period = 1; a.out = x; a.ldo = N; a.out_type = ET_F32;
+    a.out2 = xb; a.ldo2 = N;
+    a.ws = debug_ws(0, vla_model_s::kSplitKFloats); a.ws_floats = vla_model_s::kSplitKFloats;
+    a.zeros = debug_ws(2, 64);
+    launch_gemm(a, s);
+    VLA_HIP(hipGetLastError());
+  });
+}
+
 vla_status vla_debug_attention(int B, int Hq, int Hkv, int Lq, int hd, int et, const void* q, const void* k0,
                                const void* v0, int len0, const void* k1, const void* v1, int len1, void* o,
                                hipStream_t s) {

@@ -127,6 +127,15 @@ struct GemmArgs {
   // (launch_gemm_norm); with K ranges it runs inside the reduce, without
   // them it costs a kernel of its own
   int norm_follows;
+  // optional bf16 copy of an fp32 result (EPI_RESID, or EPI_STORE with fp32
+  // out, no row groups): out2[m * ldo2 + n] = bf16(out value)
+  void* out2; int ldo2;
+  // RMSNorm folded into this projection (rms_in = d > 0): A holds rows x not
+  // yet normalised and W the weights with the norm's gain folded into their
+  // columns; row m of the product is scaled by rsqrt(sum_k x[m][k]^2 / d +
+  // rms_eps) before the epilogue, the sum taken from the bf16 A tiles the
+  // product reads (bf16 A and W, no K ranges)
+  int rms_in; float rms_eps;
 };
 
 void launch_gemm(const GemmArgs& a, hipStream_t s);
@@ -220,6 +229,8 @@ void launch_transpose_convert(const float* src, int K, int N, void* dst, int ldk
                               const int* perm, hipStream_t s);
 void launch_convert(const float* src, long n, void* dst, int et, hipStream_t s);
 void launch_round_bf16_f32(const float* src, long n, float* dst, hipStream_t s);
+// W[n][k] = bf16(W[n][k] * g[k]) for n < N, k < K (bf16 rows of stride ldk)
+void launch_scale_cols_bf16(void* W, long N, int K, int ldk, const float* g, hipStream_t s);
 
 // Debug probe: each workgroup writes its hardware placement (XCC id, SE id,
 // CU id) to out[block] as one word: xcc << 16 | se << 8 | cu.

@@ -144,6 +144,18 @@ __global__ void round_bf16_kernel(const float* src, long n, float* dst) {
     dst[e] = round_bf16(src[e]);
 }
 
+// W[n][k] *= g[k] for the bf16 weight rows of a projection whose input row
+// norm is folded into it (k < K; row stride ldk), rounded back to bf16
+__global__ void scale_cols_bf16_kernel(bf16* W, long N, int K, int ldk, const float* g) {
+  const long total = N * (long)K;
+  for (long e = blockIdx.x * (long)blockDim.x + threadIdx.x; e < total; e += (long)gridDim.x * blockDim.x) {
+    const long n = e / K;
+    const int k = (int)(e % K);
+    bf16& w = W[n * ldk + k];
+    w = (bf16)((float)w * g[k]);
+  }
+}
+
 // ---------------------------------------------------------------- probe
 __global__ void cu_probe_kernel(uint32_t* out, int spin) {
   // HW_ID (hwreg 4) and XCC_ID (hwreg 20), read whole (size 32, offset 0)
@@ -213,6 +225,11 @@ void launch_transpose_convert(const float* src, int K, int N, void* dst, int ldk
 
 void launch_convert(const float* src, long n, void* dst, int et, hipStream_t s) {
   hipLaunchKernelGGL(convert_kernel, dim3(grid_for(n)), dim3(256), 0, s, src, n, dst, et);
+}
+
+void launch_scale_cols_bf16(void* W, long N, int K, int ldk, const float* g, hipStream_t s) {
+  hipLaunchKernelGGL(scale_cols_bf16_kernel, dim3(grid_for(N * (long)K)), dim3(256), 0, s, reinterpret_cast<bf16*>(W), N,
+                     K, ldk, g);
 }
 
 void launch_round_bf16_f32(const float* src, long n, float* dst, hipStream_t s) {

@@ -15,6 +15,18 @@
 #include "rownorm.h"
 
 typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
+typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2v;
+
+// s0 + v0^2 + v1^2 + v2^2 + v3^2 and s1 + v4^2 + ... + v7^2 with the bf16
+// pair dot instruction (two accumulators keep the chain short)
+__device__ __forceinline__ void sumsq8(const bf16x8& v, float& s0, float& s1) {
+  const bf16x2v p0 = __builtin_shufflevector(v, v, 0, 1), p1 = __builtin_shufflevector(v, v, 2, 3);
+  const bf16x2v p2 = __builtin_shufflevector(v, v, 4, 5), p3 = __builtin_shufflevector(v, v, 6, 7);
+  s0 = __builtin_amdgcn_fdot2_f32_bf16(p0, p0, s0, false);
+  s1 = __builtin_amdgcn_fdot2_f32_bf16(p2, p2, s1, false);
+  s0 = __builtin_amdgcn_fdot2_f32_bf16(p1, p1, s0, false);
+  s1 = __builtin_amdgcn_fdot2_f32_bf16(p3, p3, s1, false);
+}
 typedef __attribute__((ext_vector_type(4))) __bf16 bf16x4;
 typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2;
 typedef __attribute__((ext_vector_type(4))) float f32x4;
@@ -68,6 +80,10 @@ __device__ __forceinline__ void epilogue4(const GemmArgs& a, int m, int n0, floa
         } else {
           for (int j = 0; j < nv; ++j) o[j] = r[j];
         }
+        if (a.out2) {
+          bf16* o2 = reinterpret_cast<bf16*>(a.out2) + (long)m * a.ldo2 + n0;
+          for (int j = 0; j < nv; ++j) o2[j] = (bf16)r[j];
+        }
       }
       break;
     }
@@ -79,6 +95,7 @@ __device__ __forceinline__ void epilogue4(const GemmArgs& a, int m, int n0, floa
         float x = v[j] + (a.bias ? a.bias[n0 + j] : 0.0f);
         if (a.gate) x *= a.gate[n0 + j];
         o[j] += x;
+        if (a.out2) reinterpret_cast<bf16*>(a.out2)[(long)m * a.ldo2 + n0 + j] = (bf16)o[j];
       }
       break;
     }
@@ -180,10 +197,14 @@ __device__ __forceinline__ void epi_rows(const GemmArgs& a, const f32x4 (&t)[NIT
         for (int j = 0; j < 4; ++j) x[j] = act_apply(x[j], a.act);
       }
       const long o = row_off(ms[it]) + n0;
-      if (a.out_type == ET_BF16)
+      if (a.out_type == ET_BF16) {
         *reinterpret_cast<bf16x4*>(reinterpret_cast<bf16*>(a.out) + o) = bf16x4{(bf16)x[0], (bf16)x[1], (bf16)x[2], (bf16)x[3]};
-      else
+      } else {
         *reinterpret_cast<f32x4*>(reinterpret_cast<float*>(a.out) + o) = x;
+        if (a.out2)
+          *reinterpret_cast<bf16x4*>(reinterpret_cast<bf16*>(a.out2) + (long)ms[it] * a.ldo2 + n0) =
+              bf16x4{(bf16)x[0], (bf16)x[1], (bf16)x[2], (bf16)x[3]};
+      }
     }
   } else if constexpr (MODE == EPI_RESID || MODE == EPI_EULER) {
     float* out = reinterpret_cast<float*>(a.out);
@@ -202,6 +223,9 @@ __device__ __forceinline__ void epi_rows(const GemmArgs& a, const f32x4 (&t)[NIT
       if constexpr (MODE == EPI_RESID) r = old[it] + (t[it] + bias) * gate;
       else r = old[it] + a.dt * (t[it] + bias);
       *reinterpret_cast<f32x4*>(out + off[it]) = r;
+      if (MODE == EPI_RESID && a.out2)
+        *reinterpret_cast<bf16x4*>(reinterpret_cast<bf16*>(a.out2) + (long)ms[it] * a.ldo2 + n0) =
+            bf16x4{(bf16)r[0], (bf16)r[1], (bf16)r[2], (bf16)r[3]};
     }
   } else if constexpr (MODE == EPI_GEGLU) {
     // weight rows interleaved: column 2f = gate f, 2f + 1 = up f
@@ -271,9 +295,11 @@ __device__ __forceinline__ void epi_rows(const GemmArgs& a, const f32x4 (&t)[NIT
 // Thread tid of NT finishes the tile's rows r0 + it * RS of its four columns
 // (see above), GRP rows per memory round trip (GRP bounds the registers the
 // row loads hold); the tile is the sum of NSUM fp32 planes in LDS (plane
-// stride ROWS * LDC floats), added in plane order.
+// stride ROWS * LDC floats), added in plane order, times rsc[row] when rsc
+// (an LDS array of per-row scales) is given.
 template <int MODE, int BN, int ROWS, int NT, int LDC, int NSUM = 1, int GRP = 8>
-__device__ __forceinline__ void tile_epilogue(const GemmArgs& a, const float* Cs, int m_blk, int n_blk, int tid) {
+__device__ __forceinline__ void tile_epilogue(const GemmArgs& a, const float* Cs, int m_blk, int n_blk, int tid,
+                                              const float* rsc = nullptr) {
   // GeGLU has no row loads to overlap and its activation is long: two rows at
   // a time keep its registers within the kernels' budget
   constexpr int GR = MODE == EPI_GEGLU ? 2 : GRP;
@@ -296,6 +322,7 @@ __device__ __forceinline__ void tile_epilogue(const GemmArgs& a, const float* Cs
         t[it] = *reinterpret_cast<const f32x4*>(Cs + mr * LDC + nc);
 #pragma unroll
         for (int z = 1; z < NSUM; ++z) t[it] += *reinterpret_cast<const f32x4*>(Cs + z * ROWS * LDC + mr * LDC + nc);
+        if (rsc) t[it] *= rsc[mr];
       }
     }
     epi_rows<MODE, G>(a, t, ms, ok, n0);
@@ -562,10 +589,11 @@ __global__ void __launch_bounds__(256) splitk_reduce_norm_kernel(GemmArgs a, Nor
 // zeroed after the load), which keeps them all in flight together. The wave
 // partials are summed in LDS in wave order and the epilogue runs once per
 // output (no atomics: results do not depend on timing).
-template <int TN, int MODE>
+template <int TN, int MODE, int RMS = 0>
 __global__ void __launch_bounds__(256) gemm_skinny_kernel(GemmArgs a) {
   constexpr int BM = 64, BN = 16 * TN, CPW = 8;
   __shared__ __attribute__((aligned(16))) float red[4][BM][BN];
+  __shared__ float rsq[RMS ? 4 : 1][RMS ? BM : 1], rsc[RMS ? BM : 1];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   int bx, by, bz;
   xcd_remap_grouped(bx, by, bz, 8);
@@ -597,6 +625,7 @@ __global__ void __launch_bounds__(256) gemm_skinny_kernel(GemmArgs a) {
   for (int i = 0; i < TN; ++i)
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float rs[4] = {0.f, 0.f, 0.f, 0.f}, rs2[4] = {0.f, 0.f, 0.f, 0.f};   // RMS: sums of squares of this lane's A fragments
 
   for (int k0 = kbeg + wave * 32; k0 < kend; k0 += 4 * 32 * CPW) {
     bf16x8 wf[CPW][TN], af[CPW][4];
@@ -620,6 +649,10 @@ __global__ void __launch_bounds__(256) gemm_skinny_kernel(GemmArgs a) {
 #pragma unroll
       for (int j = 0; j < 4; ++j)
         if (!(kok && aok[j])) af[c][j] = bf16x8{};
+      if constexpr (RMS) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) sumsq8(af[c][j], rs[j], rs2[j]);
+      }
 #pragma unroll
       for (int i = 0; i < TN; ++i)
 #pragma unroll
@@ -633,16 +666,35 @@ __global__ void __launch_bounds__(256) gemm_skinny_kernel(GemmArgs a) {
 #pragma unroll
     for (int j = 0; j < 4; ++j)
       *reinterpret_cast<f32x4*>(&red[wave][j * 16 + lr][i * 16 + (lane >> 4) * 4]) = acc[i][j];
+  if constexpr (RMS) {
+    // every A element of the block's rows was read by exactly one lane: add
+    // the four K-chunk lanes of a row, then the waves, in wave order
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      rs[j] += rs2[j];
+      rs[j] += __shfl_xor(rs[j], 16);
+      rs[j] += __shfl_xor(rs[j], 32);
+    }
+    if (lane < 16) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) rsq[wave][j * 16 + lr] = rs[j];
+    }
+  }
   __syncthreads();
+  if constexpr (RMS) {
+    if (tid < BM) rsc[tid] = rsqrtf((rsq[0][tid] + rsq[1][tid] + rsq[2][tid] + rsq[3][tid]) / (float)a.rms_in + a.rms_eps);
+    __syncthreads();
+  }
   if (a.epi_vec) {
-    tile_epilogue<MODE, BN, BM, 256, BN, 4>(a, &red[0][0][0], m0, n0, tid);
+    tile_epilogue<MODE, BN, BM, 256, BN, 4>(a, &red[0][0][0], m0, n0, tid, RMS ? rsc : nullptr);
     return;
   }
 #pragma unroll
   for (int c = tid; c < BM * BN / 4; c += 256) {
     const int mr = c / (BN / 4), nc = (c % (BN / 4)) * 4;
-    const f32x4 t = *reinterpret_cast<const f32x4*>(&red[0][mr][nc]) + *reinterpret_cast<const f32x4*>(&red[1][mr][nc]) +
-                    *reinterpret_cast<const f32x4*>(&red[2][mr][nc]) + *reinterpret_cast<const f32x4*>(&red[3][mr][nc]);
+    f32x4 t = *reinterpret_cast<const f32x4*>(&red[0][mr][nc]) + *reinterpret_cast<const f32x4*>(&red[1][mr][nc]) +
+              *reinterpret_cast<const f32x4*>(&red[2][mr][nc]) + *reinterpret_cast<const f32x4*>(&red[3][mr][nc]);
+    if constexpr (RMS) t *= rsc[mr];
     float v[4] = {t[0], t[1], t[2], t[3]};
     epilogue4<MODE>(a, m0 + mr, n0 + nc, v);
   }
@@ -665,8 +717,12 @@ __global__ void __launch_bounds__(256) gemm_skinny_kernel(GemmArgs a) {
 // fragment reads per CU: with one wave per SIMD, LDS reads stay
 // latency-bound at ~100 B/clk per CU, with two they reach ~280). The groups'
 // tiles are summed in a fixed order in the epilogue. BK 32 with more stages
-// keeps the same LDS per block but more K-steps of loads in flight.
-template <int BN, int BM, int STAGES, int MODE, int BK = 64, int KG = 1>
+// keeps the same LDS per block but more K-steps of loads in flight. RMS: the
+// RMSNorm folded into the product (a.rms_in): every A element passes through
+// the fragment reads of the waves of weight-row half 0 exactly once, so those
+// lanes also sum the squares of their fragments; the row sums meet in LDS
+// and scale the tile rows in the epilogue.
+template <int BN, int BM, int STAGES, int MODE, int BK = 64, int KG = 1, int RMS = 0>
 __global__ void __launch_bounds__(256 * KG)
 gemm_stage_kernel(GemmArgs a) {
   constexpr int NT = 256 * KG, NWV = 4 * KG;            // threads, waves
@@ -684,9 +740,15 @@ gemm_stage_kernel(GemmArgs a) {
   static_assert(KCG * KG == KC, "K chunks must divide among the wave groups");
   constexpr int LDC = BN + 4;
   constexpr int CS_BYTES = KG * BM * LDC * 4;           // one fp32 tile plane per wave group
-  constexpr int SMEM = STAGES * STAGE_BYTES > CS_BYTES ? STAGES * STAGE_BYTES : CS_BYTES;
+  constexpr int MAIN = STAGES * STAGE_BYTES > CS_BYTES ? STAGES * STAGE_BYTES : CS_BYTES;
+  // RMS: per-(wave group, row) sums of squares and the row scales after the
+  // main buffer (one LDS object: a second one makes the compiler wait for
+  // every direct load before each fragment read)
+  constexpr int SMEM = MAIN + (RMS ? (KG + 1) * BM * 4 : 0);
   __shared__ __attribute__((aligned(1024))) char smem[SMEM];
   float* Cs = reinterpret_cast<float*>(smem);
+  float* rsq = reinterpret_cast<float*>(smem + MAIN);   // [KG][BM]
+  float* rsc = rsq + KG * BM;                           // [BM]
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, kg = wave >> 2, w4 = wave & 3;
   const int wn0 = (w4 >> 1) * (BN / 2), wm0 = (w4 & 1) * (BM / 2);
@@ -727,6 +789,9 @@ gemm_stage_kernel(GemmArgs a) {
   for (int i = 0; i < TN; ++i)
 #pragma unroll
     for (int j = 0; j < TM; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float rs[TM], rs2[TM];                                // RMS: this lane's sums of squares
+#pragma unroll
+  for (int j = 0; j < TM; ++j) rs[j] = rs2[j] = 0.f;
 
   const int lr = lane & 15, lq = lane >> 4;
 #pragma unroll
@@ -770,6 +835,12 @@ gemm_stage_kernel(GemmArgs a) {
 #pragma unroll
         for (int j = 0; j < TM; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[q][i], af[q][j], acc[i][j], 0, 0, 0);
+    if constexpr (RMS) {
+#pragma unroll
+      for (int q = 0; q < KCG; ++q)
+#pragma unroll
+        for (int j = 0; j < TM; ++j) sumsq8(af[q][j], rs[j], rs2[j]);
+    }
     if constexpr (KCG == 2) {
       constexpr int NRD = TN + TM, NMF = TN * TM, R = NMF / NRD > 0 ? NMF / NRD : 1;
       __builtin_amdgcn_sched_group_barrier(0x100, NRD, 0);      // chunk 0 reads
@@ -779,6 +850,20 @@ gemm_stage_kernel(GemmArgs a) {
         __builtin_amdgcn_sched_group_barrier(0x008, R, 0);      // R chunk-0 products
       }
       __builtin_amdgcn_sched_group_barrier(0x008, 2 * NMF - NRD * R, 0);
+    }
+  }
+  if constexpr (RMS) {
+    // the four lanes of a row (lq) hold disjoint K chunks: add them, then
+    // weight-row half 0's waves publish one sum per (wave group, row)
+#pragma unroll
+    for (int j = 0; j < TM; ++j) {
+      rs[j] += rs2[j];
+      rs[j] += __shfl_xor(rs[j], 16);
+      rs[j] += __shfl_xor(rs[j], 32);
+    }
+    if ((w4 >> 1) == 0 && lq == 0) {
+#pragma unroll
+      for (int j = 0; j < TM; ++j) rsq[kg * BM + wm0 + 16 * j + lr] = rs[j];
     }
   }
   // each wave group's tile to its own fp32 plane; the epilogues add the
@@ -791,13 +876,21 @@ gemm_stage_kernel(GemmArgs a) {
     for (int j = 0; j < TM; ++j)
       *reinterpret_cast<f32x4*>(&Cp[(wm0 + 16 * j + lr) * LDC + wn0 + 16 * i + (lane >> 4) * 4]) = acc[i][j];
   __syncthreads();
-  if (a.splits > 1) {
+  if constexpr (RMS) {
+    if (tid < BM) {
+      float t = rsq[tid];
+#pragma unroll
+      for (int z = 1; z < KG; ++z) t += rsq[z * BM + tid];
+      rsc[tid] = rsqrtf(t / (float)a.rms_in + a.rms_eps);
+    }
+    __syncthreads();
+  } else if (a.splits > 1) {
     // split-K: store this K range's partial tile; the reduce kernel finishes
     tile_store_partial<BN, BM, NT, LDC, KG>(a, Cs, m_blk, n_blk, bz, tid);
     return;
   }
   if (a.epi_vec) {
-    tile_epilogue<MODE, BN, BM, NT, LDC, KG>(a, Cs, m_blk, n_blk, tid);
+    tile_epilogue<MODE, BN, BM, NT, LDC, KG>(a, Cs, m_blk, n_blk, tid, RMS ? rsc : nullptr);
     return;
   }
 #pragma unroll 1
@@ -806,6 +899,7 @@ gemm_stage_kernel(GemmArgs a) {
     f32x4 t = *reinterpret_cast<const f32x4*>(&Cs[mr * LDC + nc]);
 #pragma unroll
     for (int z = 1; z < KG; ++z) t += *reinterpret_cast<const f32x4*>(&Cs[z * BM * LDC + mr * LDC + nc]);
+    if constexpr (RMS) t *= rsc[mr];
     float v[4] = {t[0], t[1], t[2], t[3]};
     epilogue4<MODE>(a, m_blk + mr, n_blk + nc, v);
   }
@@ -982,7 +1076,7 @@ __global__ void __launch_bounds__(256) gemm_f32_kernel(GemmArgs a) {
 // Kernels are specialised on tile shape, activation type and epilogue; fp32
 // activations (the Euler state, conditioning vectors, robot state) only feed
 // plain stores.
-GemmPlan gemm_plan(const GemmArgs& a) {
+static GemmPlan plan_base(const GemmArgs& a) {
   constexpr int BK = 64;
   GemmPlan p{64, 32, 1, 64, 0};
   if (a.w_type == ET_F32) {
@@ -1108,6 +1202,20 @@ GemmPlan gemm_plan(const GemmArgs& a) {
   return p;
 }
 
+// A product with a folded RMSNorm needs each row's whole K in one block: the
+// plan without K ranges, on a kernel that sums the squares (LDS-staged or
+// small-M).
+GemmPlan gemm_plan(const GemmArgs& a) {
+  if (!a.rms_in || a.w_type != ET_BF16) return plan_base(a);
+  GemmArgs b = a;
+  b.ws = nullptr;
+  b.ws_floats = 0;
+  GemmPlan p = plan_base(b);
+  if (p.kind == 1 || p.kind == 2 || p.kind == 4) return p;
+  const bool big = a.M >= 128 && (long)((a.M + 127) / 128) * ((a.N + 127) / 128) >= 128;
+  return GemmPlan{big ? 128 : 64, big ? 128 : 64, 1, (a.K + 63) / 64 * 64, 1};
+}
+
 // Second pass of a split product: the ordered reduce with the epilogue, or
 // for a residual projection with a following row norm, the fused reduce.
 template <int MODE>
@@ -1138,6 +1246,12 @@ static void launch_staged(const GemmArgs& a0, const GemmPlan& p, const NormArgs*
     launch_reduce<MODE>(a, fuse, s);
     return;
   }
+  if constexpr (MODE == EPI_STORE || MODE == EPI_QKV || MODE == EPI_GEGLU) {
+    if (a.rms_in) {
+      hipLaunchKernelGGL((gemm_stage_kernel<BN, BM, 2, MODE, 64, 1, 1>), grid, dim3(256), 0, s, a);
+      return;
+    }
+  }
   hipLaunchKernelGGL((gemm_stage_kernel<BN, BM, 2, MODE>), grid, dim3(256), 0, s, a);
 }
 
@@ -1152,6 +1266,12 @@ static void launch_staged128(const GemmArgs& a0, const GemmPlan& p, const NormAr
     launch_reduce<MODE>(a, fuse, s);
     return;
   }
+  if constexpr (MODE == EPI_STORE || MODE == EPI_QKV || MODE == EPI_GEGLU) {
+    if (a.rms_in) {
+      hipLaunchKernelGGL((gemm_stage_kernel<BT, BT, ST, MODE, 128, 2, 1>), grid, dim3(512), 0, s, a);
+      return;
+    }
+  }
   hipLaunchKernelGGL((gemm_stage_kernel<BT, BT, ST, MODE, 128, 2>), grid, dim3(512), 0, s, a);
 }
 
@@ -1164,6 +1284,12 @@ static void launch_big(const GemmArgs& a, hipStream_t s) {
 template <int TN, int MODE>
 static void launch_skinny(const GemmArgs& a, hipStream_t s) {
   dim3 grid((a.M + 63) / 64, (a.N + 16 * TN - 1) / (16 * TN), 1);
+  if constexpr (MODE == EPI_STORE || MODE == EPI_QKV || MODE == EPI_GEGLU) {
+    if (a.rms_in) {
+      hipLaunchKernelGGL((gemm_skinny_kernel<TN, MODE, 1>), grid, dim3(256), 0, s, a);
+      return;
+    }
+  }
   hipLaunchKernelGGL((gemm_skinny_kernel<TN, MODE>), grid, dim3(256), 0, s, a);
 }
 
@@ -1234,9 +1360,11 @@ static bool epi_vec_ok(const GemmArgs& a) {
   switch (a.mode) {
     case EPI_STORE:
       if (a.tab && (!al(a.tab, 16) || a.ldtab % 4 != 0 || a.tab_period <= 0)) return false;
+      if (a.out2 && (!al(a.out2, 8) || a.ldo2 % 4 != 0)) return false;
       return al(a.out, 16) && a.ldo % 4 == 0 && (a.row_group <= 0 || a.row_group_stride % 4 == 0);
     case EPI_RESID:
       if (a.gate && !al(a.gate, 16)) return false;
+      if (a.out2 && (!al(a.out2, 8) || a.ldo2 % 4 != 0)) return false;
       return al(a.out, 16) && a.ldo % 4 == 0 && (a.row_group <= 0 || a.row_group_stride % 4 == 0);
     case EPI_EULER:
       return al(a.out, 16) && a.ldo % 4 == 0;
@@ -1257,6 +1385,12 @@ void launch_gemm(const GemmArgs& a0, hipStream_t s) {
   if (a0.M <= 0 || a0.N <= 0) return;
   if (a0.a_type == ET_F32 && a0.w_type == ET_BF16 && a0.mode != EPI_STORE)
     throw VlaError{4, "fp32 activations with bf16 weights only feed plain stores"};
+  if (a0.rms_in && (a0.rms_in < 0 || a0.a_type != ET_BF16 || a0.w_type != ET_BF16 || !a0.zeros ||
+                    (a0.mode != EPI_STORE && a0.mode != EPI_QKV && a0.mode != EPI_GEGLU)))
+    throw VlaError{4, "a folded RMSNorm needs bf16 operands and a store, QKV or GeGLU epilogue"};
+  if (a0.out2 && (a0.row_group > 0 || a0.ldo2 < a0.N || a0.out_type != ET_F32 ||
+                  (a0.mode != EPI_STORE && a0.mode != EPI_RESID)))
+    throw VlaError{4, "a bf16 copy needs an fp32 store or residual epilogue without row groups"};
   GemmArgs a = a0;
   a.epi_vec = epi_vec_ok(a) ? 1 : 0;
   const GemmPlan p = a.w_type == ET_F32 ? GemmPlan{} : gemm_plan(a);
@@ -1270,7 +1404,7 @@ void launch_gemm(const GemmArgs& a0, hipStream_t s) {
 }
 
 void launch_gemm_norm(const GemmArgs& a, const NormArgs& n, hipStream_t s) {
-  const bool fusable = a.M > 0 && a.N > 0 && a.mode == EPI_RESID && a.w_type == ET_BF16 && a.row_group == 0 &&
+  const bool fusable = a.M > 0 && a.N > 0 && a.mode == EPI_RESID && a.w_type == ET_BF16 && a.row_group == 0 && !a.out2 &&
                        n.skip == 0 && n.rows == a.M && n.d == a.N && n.in == a.out && n.ld_in == a.ldo &&
                        a.N % 4 == 0 && a.ldo % 4 == 0 && n.ld_out % 4 == 0 && a.N <= 2048;
   if (fusable) {

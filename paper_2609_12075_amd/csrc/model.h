@@ -62,6 +62,10 @@ struct vla_model_s {
   // joint action expert
   Mat ain, t1a, t1t, t2, out; float *ain_b = nullptr, *t1_b = nullptr, *t2_b = nullptr, *lnf = nullptr, *out_b = nullptr;
   std::vector<LlmLayer> act;
+  // bf16 joint expert: each layer's RMSNorm gains are folded into the columns
+  // of the projection that reads the normalised rows (ln1 into qkv, ln2 into
+  // gu), and those projections normalise their input rows themselves
+  bool act_fold = false;
   // DiT head
   float* llm_lnf = nullptr; Mat vp; float* vp_b = nullptr; Mat xkv; float* xkv_b = nullptr;
   Mat state_w; float* state_b = nullptr;

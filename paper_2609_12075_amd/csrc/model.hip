@@ -290,6 +290,15 @@ void vla_model_s::init(const vla_config& c, const float* w, size_t n, int dev) {
       t1a = L.mat(Da, Da); t1t = L.mat(tdim, Da); t1_b = L.vec(Da);
       t2 = L.mat(Da, Da); t2_b = L.vec(Da);
       for (int l = 0; l < c.act_layers; ++l) act.push_back(gemma_layer(Da, Fa));
+      act_fold = et == ET_BF16;
+      if (act_fold) {
+        for (LlmLayer& y : act) {
+          launch_scale_cols_bf16(y.qkv.p, y.qkv.N, Da, y.qkv.ldk, y.ln1, L.s);
+          launch_scale_cols_bf16(y.gu.p, y.gu.N, Da, y.gu.ldk, y.ln2, L.s);
+        }
+        VLA_HIP(hipGetLastError());
+        VLA_HIP(hipStreamSynchronize(L.s));
+      }
       lnf = L.vec(Da);
       out = L.mat(Da, A); out_b = L.vec(A);
     } else {
@@ -614,13 +623,18 @@ void vla_model_s::enqueue_denoise(int B, const void* kv, const float* noise, int
     for (int k = 0; k < N; ++k) {
       store(gm(*this, ST,ain, M, x, A, ET_F32), e, Da, et, ain_b, ACT_NONE, s);
       store(gm(*this, ST,t1a, M, e, Da, et), u, Da, et, cc.tb + (size_t)k * Da, ACT_SILU, s);
-      store(gm(*this, ST,t2, M, u, Da, et), ha, Da, ET_F32, t2_b, ACT_NONE, s);
-      norm(M, Da, 0, ha, Da, za, Da, et, act[0].ln1, nullptr, eps, s);
+      // za holds RMSNorm(ha) with the next projection's gain, or with the
+      // gains folded into the projections (act_fold) bf16(ha), which the
+      // projection normalises row by row
+      GemmArgs g2 = gm(*this, ST,t2, M, u, Da, et);
+      if (act_fold) { g2.out2 = za; g2.ldo2 = Da; }
+      store(g2, ha, Da, ET_F32, t2_b, ACT_NONE, s);
+      if (!act_fold) norm(M, Da, 0, ha, Da, za, Da, et, act[0].ln1, nullptr, eps, s);
       for (int l = 0; l < c.act_layers; ++l) {
         const LlmLayer& y = act[l];
-        // za holds RMSNorm(ha) with this layer's gain
         GemmArgs q3 = gm(*this, ST,y.qkv, M, za, Da, et);
         q3.mode = EPI_QKV; q3.out_type = et;
+        if (act_fold) { q3.rms_in = Da; q3.rms_eps = eps; }
         QkvEpi& e3 = q3.qkv;
         e3.n_q = nq; e3.n_kv = nkv; e3.hd = hd; e3.seq = H; e3.pos0 = P; e3.rope_cs = rope_cs;
         e3.q = qa; e3.q_sb = (long)nq * H * hd; e3.q_sh = (long)H * hd; e3.q_si = hd;
@@ -635,15 +649,26 @@ void vla_model_s::enqueue_denoise(int B, const void* kv, const float* noise, int
         at.seg[1] = AttnSeg{ks, e3.k_sb, e3.k_sh, hd, vs, e3.v_sb, e3.v_sh, hd, H};
         at.o = oa; at.o_sb = (long)H * Hq; at.o_sh = hd; at.o_si = Hq;
         launch_attention(at, s);
-        resid_norm(gm(*this, ST,y.wo, M, oa, Hq, et), ha, Da, nullptr, nullptr,
-                   nargs(M, Da, 0, ha, Da, za, Da, et, y.ln2, nullptr, eps), s);
+        GemmArgs go = gm(*this, ST,y.wo, M, oa, Hq, et);
+        if (act_fold) {
+          go.out2 = za; go.ldo2 = Da;
+          resid(go, ha, Da, nullptr, nullptr, s);
+        } else {
+          resid_norm(go, ha, Da, nullptr, nullptr, nargs(M, Da, 0, ha, Da, za, Da, et, y.ln2, nullptr, eps), s);
+        }
         GemmArgs gg = gm(*this, ST,y.gu, M, za, Da, et);
         gg.mode = EPI_GEGLU; gg.out = gua; gg.ldo = Fa; gg.out_type = et;
+        if (act_fold) { gg.rms_in = Da; gg.rms_eps = eps; }
         launch_gemm(gg, s);
         // then the next layer's RMSNorm, or the final one
-        const float* gn = l + 1 < c.act_layers ? act[l + 1].ln1 : lnf;
-        resid_norm(gm(*this, ST,y.wd, M, gua, Fa, et), ha, Da, nullptr, nullptr,
-                   nargs(M, Da, 0, ha, Da, za, Da, et, gn, nullptr, eps), s);
+        GemmArgs gd = gm(*this, ST,y.wd, M, gua, Fa, et);
+        if (act_fold && l + 1 < c.act_layers) {
+          gd.out2 = za; gd.ldo2 = Da;
+          resid(gd, ha, Da, nullptr, nullptr, s);
+        } else {
+          const float* gn = l + 1 < c.act_layers ? act[l + 1].ln1 : lnf;
+          resid_norm(gd, ha, Da, nullptr, nullptr, nargs(M, Da, 0, ha, Da, za, Da, et, gn, nullptr, eps), s);
+        }
       }
       GemmArgs go = gm(*this, ST,out, M, za, Da, et);
       go.mode = EPI_EULER; go.out = x; go.ldo = A; go.out_type = ET_F32; go.bias = out_b; go.dt = dt;
@@ -793,6 +818,7 @@ GemmArgs vla_model_s::stage_gemm(int which, int B, int layer) const {
       if (c.head_kind == VLA_HEAD_JOINT) {
         g = gm(*this, ST,act[la].gu, B * H, za, Da, et);
         g.mode = EPI_GEGLU; g.out = gua; g.ldo = c.act_mlp; g.out_type = et;
+        if (act_fold) { g.rms_in = Da; g.rms_eps = c.norm_eps; }
       } else {
         g = gm(*this, ST,dit[la].w1, B * Ltok, zd, Da, et);
         g.mode = EPI_STORE; g.act = ACT_GELU; g.bias = dit[la].b1; g.out = mlp; g.ldo = c.act_mlp; g.out_type = et;
@@ -802,11 +828,15 @@ GemmArgs vla_model_s::stage_gemm(int which, int B, int layer) const {
       if (c.head_kind == VLA_HEAD_JOINT) {
         g = gm(*this, ST,act[la].wd, B * H, gua, c.act_mlp, et);
         g.mode = EPI_RESID; g.out = ha; g.ldo = Da; g.out_type = ET_F32;
+        // the stage's layers but the last write the bf16 copy the next
+        // layer's QKV normalises; without folded gains a norm follows
+        if (act_fold) { g.out2 = za; g.ldo2 = Da; }
+        else g.norm_follows = 1;
       } else {
         g = gm(*this, ST,dit[la].w2, B * Ltok, mlp, c.act_mlp, et);
         g.mode = EPI_RESID; g.bias = dit[la].b2; g.out = X; g.ldo = Da; g.out_type = ET_F32;
+        g.norm_follows = 1;
       }
-      g.norm_follows = 1;
       break;
     case 4:   // VLM stage: ViT layer MLP up (GELU)
       VLA_REQUIRE(c.vit_layers > 0, "model has no ViT");

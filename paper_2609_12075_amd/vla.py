@@ -24,7 +24,8 @@ VLA_OK, VLA_EINVAL, VLA_ENOMEM, VLA_EHIP, VLA_EUNSUPPORTED = range(5)
 # every exported symbol declared by include/vla.h and include/vla_debug.h
 EXPORTS = ["vla_weight_count", "vla_create_model", "vla_destroy_model", "vla_set_graphs", "vla_kv_bytes",
            "vla_prefill", "vla_prefill_ex", "vla_denoise", "vla_step", "vla_last_error",
-           "vla_debug_gemm", "vla_debug_resid_norm", "vla_debug_attention", "vla_debug_cu_probe", "vla_debug_replay_gemm"]
+           "vla_debug_gemm", "vla_debug_resid_norm", "vla_debug_gemm_rms", "vla_debug_resid_copy", "vla_debug_attention",
+           "vla_debug_cu_probe", "vla_debug_replay_gemm"]
 
 
 class VlaError(RuntimeError):
@@ -74,6 +75,10 @@ def lib():
         L.vla_debug_gemm.restype = ci
         L.vla_debug_resid_norm.argtypes = [ci, ci, ci, vp, vp, vp, vp, vp, ci, vp, vp, ctypes.c_float, vp, vp]
         L.vla_debug_resid_norm.restype = ci
+        L.vla_debug_gemm_rms.argtypes = [ci, ci, ci, vp, vp, vp, ctypes.c_float, vp, vp]
+        L.vla_debug_gemm_rms.restype = ci
+        L.vla_debug_resid_copy.argtypes = [ci, ci, ci, vp, vp, vp, vp, vp, vp, vp]
+        L.vla_debug_resid_copy.restype = ci
         L.vla_debug_attention.argtypes = [ci, ci, ci, ci, ci, ci, vp, vp, vp, ci, vp, vp, ci, vp, vp]
         L.vla_debug_attention.restype = ci
         L.vla_debug_cu_probe.argtypes = [ci, ci, ci, ci, ci, vp, vp]; L.vla_debug_cu_probe.restype = ci
@@ -227,6 +232,28 @@ def debug_resid_norm(A, Wt, x, kind, g=None, b=None, bias=None, gate=None, eps=1
     _check(lib().vla_debug_resid_norm(M, N, K, _ptr(A), _ptr(Wt), _ptr(bias), _ptr(gate), _ptr(x), kind, _ptr(g),
                                       _ptr(b), ctypes.c_float(eps), _ptr(z), _stream(stream)))
     return z
+
+
+def debug_gemm_rms(A, Wt, bias=None, eps=1e-6, stream=None):
+    """rsqrt(mean_k A^2 + eps) * (A Wt^T) + bias per row, fp32 (A, Wt bf16)."""
+    import torch
+    M, K = A.shape
+    N = Wt.shape[0]
+    out = torch.empty(M, N, dtype=torch.float32, device=A.device)
+    _check(lib().vla_debug_gemm_rms(M, N, K, _ptr(A), _ptr(Wt), _ptr(bias), ctypes.c_float(eps), _ptr(out),
+                                    _stream(stream)))
+    return out
+
+
+def debug_resid_copy(A, Wt, x, bias=None, gate=None, stream=None):
+    """x += gate * (A Wt^T + bias) in place; returns bf16(x)."""
+    import torch
+    M, K = A.shape
+    N = Wt.shape[0]
+    xb = torch.empty(M, N, dtype=torch.bfloat16, device=A.device)
+    _check(lib().vla_debug_resid_copy(M, N, K, _ptr(A), _ptr(Wt), _ptr(bias), _ptr(gate), _ptr(x), _ptr(xb),
+                                      _stream(stream)))
+    return xb
 
 
 def debug_attention(q, k0, v0, k1=None, v1=None, stream=None):

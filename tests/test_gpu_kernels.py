@@ -124,6 +124,61 @@ def test_resid_norm(M, N, K, kind):
     assert np.abs(zg - z_ref).max() < 2e-2 * np.abs(z_ref).max(), np.abs(zg - z_ref).max()
 
 
+RMS_SHAPES = [
+    # small-M kernel, ragged; 64 x 64 tiles with three and two stages; 128 x 128
+    # tiles with two wave groups, ragged; 128 x 64 and 128 x 128 tiles with
+    # K-steps of 64; shapes whose unfolded plan would split K or take the
+    # register-pipelined or large-tile kernel
+    (50, 3840, 720), (17, 1600, 1000), (100, 1600, 720), (400, 3840, 720), (777, 3000, 1000),
+    (800, 3840, 720), (1600, 3840, 720), (37, 33, 40), (200, 720, 1920), (2600, 4100, 2056),
+]
+
+
+@pytest.mark.parametrize("M,N,K", RMS_SHAPES)
+def test_gemm_rms(M, N, K):
+    """Projection with the RMSNorm of its input rows folded in, against fp64:
+    rows of different scales, one all-zero row (its scale is 1/sqrt(eps))."""
+    import torch
+    from paper_2609_12075_amd import vla
+    log(f"[gemm rms] M={M} N={N} K={K}")
+    eps = 1e-6
+    A = RNG.standard_normal((M, K)) * np.exp(RNG.uniform(-2, 2, (M, 1)))
+    A[M // 2] = 0.0
+    A = _bf16(A)
+    W = _bf16(RNG.standard_normal((N, K)) * 0.05)
+    bias = RNG.standard_normal(N).astype(np.float32)
+    A64 = A.astype(np.float64)
+    r = 1.0 / np.sqrt((A64 * A64).mean(axis=1) + eps)
+    ref = r[:, None] * (A64 @ W.astype(np.float64).T) + bias
+    out = vla.debug_gemm_rms(torch.from_numpy(A).to(torch.bfloat16).cuda(), torch.from_numpy(W).to(torch.bfloat16).cuda(),
+                             bias=torch.from_numpy(bias).cuda(), eps=eps)
+    torch.cuda.synchronize()
+    scale = np.sqrt(K) * 0.05 + 1.0
+    np.testing.assert_allclose(out.cpu().numpy(), ref, rtol=1e-4, atol=1e-5 * scale)
+
+
+@pytest.mark.parametrize("M,N,K", [(50, 720, 1920), (800, 720, 1920), (800, 720, 960), (37, 33, 40), (130, 202, 64)])
+def test_resid_copy(M, N, K):
+    """Residual projection with the bf16 copy of the updated rows: x against
+    fp64, the copy bit-identical to x rounded to bf16 (split and unsplit
+    plans, vector and per-element epilogues)."""
+    import torch
+    from paper_2609_12075_amd import vla
+    log(f"[resid copy] M={M} N={N} K={K}")
+    A = _bf16(RNG.standard_normal((M, K)))
+    W = _bf16(RNG.standard_normal((N, K)) * 0.05)
+    x0 = RNG.standard_normal((M, N)).astype(np.float32)
+    bias = RNG.standard_normal(N).astype(np.float32) * 0.1
+    gate = (1 + 0.1 * RNG.standard_normal(N)).astype(np.float32)
+    x_ref = x0.astype(np.float64) + (A.astype(np.float64) @ W.astype(np.float64).T + bias) * gate
+    x = torch.from_numpy(x0).cuda()
+    xb = vla.debug_resid_copy(torch.from_numpy(A).to(torch.bfloat16).cuda(), torch.from_numpy(W).to(torch.bfloat16).cuda(),
+                              x, bias=torch.from_numpy(bias).cuda(), gate=torch.from_numpy(gate).cuda())
+    torch.cuda.synchronize()
+    np.testing.assert_allclose(x.cpu().numpy(), x_ref, rtol=1e-4, atol=1e-4)
+    assert torch.equal(xb.cpu(), x.cpu().to(torch.bfloat16))
+
+
 ATTN_SHAPES = [
     # (B, Hq, Hkv, Lq, hd, len0, len1)
     (2, 8, 1, 50, 256, 816, 50),     # pi0-shaped action decode
