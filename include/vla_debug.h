@@ -96,12 +96,13 @@ vla_status vla_debug_cu_probe(int device, int cu_count, int from_top, int blocks
  * MLP down, 2 action-stage MLP up, 3 action-stage MLP down, 4 ViT MLP up;
  * launch i uses layer (i mod layer count)'s weights, so, as in a pass over
  * the stage, each launch reads weights the previous launches did not.
- * plan (may be NULL): int[8] set to
+ * plan (may be NULL): int[9] set to
  * the kernel's tile (weight rows, activation rows), number of K ranges
  * (1 = one kernel, > 1 = partial + reduce kernels), epilogue mode, kernel
  * kind (0 register-pipelined, 1 LDS-staged, 2 small-M, 3 large-tile,
- * 4 LDS-staged with K-steps of 128), LDS stages, K-step length and the
- * number of 4-wave groups that share each K-step.
+ * 4 LDS-staged with K-steps of 128), LDS stages, K-step length, the
+ * number of 4-wave groups that share each K-step, and 1 when the
+ * projection normalises its input rows (folded RMSNorm), else 0.
  */
 vla_status vla_debug_replay_gemm(vla_model m, int which, int batch, int iters, hipStream_t stream, double* flops,
                                  int* plan);

@@ -411,7 +411,7 @@ vla_status vla_debug_replay_gemm(vla_model m, int which, int batch, int iters, h
     if (plan) {
       const GemmPlan p = gemm_plan(a);
       plan[0] = p.bn; plan[1] = p.bm; plan[2] = p.splits; plan[3] = a.mode; plan[4] = p.kind;
-      plan[5] = p.stages; plan[6] = p.bk; plan[7] = p.kg;
+      plan[5] = p.stages; plan[6] = p.bk; plan[7] = p.kg; plan[8] = a.rms_in > 0 ? 1 : 0;
     }
     // launch i uses layer i's weights (cycling), so weights are re-read from
     // memory as in a pass over the stage rather than served from cache

@@ -166,12 +166,12 @@ class Model:
 
     def replay_gemm(self, which: int, batch: int, iters: int, stream=None):
         """Enqueue `iters` launches of one stage projection. Returns (flops of
-        one launch, plan dict: tile_n, tile_m, splits, mode, kind, stages, bk, kg)."""
+        one launch, plan dict: tile_n, tile_m, splits, mode, kind, stages, bk, kg, rms)."""
         f = ctypes.c_double(0.0)
-        plan = (ctypes.c_int * 8)()
+        plan = (ctypes.c_int * 9)()
         _check(lib().vla_debug_replay_gemm(self.handle, which, batch, iters, _stream(stream), ctypes.byref(f), plan))
         return f.value, {"tile_n": plan[0], "tile_m": plan[1], "splits": plan[2], "mode": plan[3], "kind": plan[4],
-                         "stages": plan[5], "bk": plan[6], "kg": plan[7]}
+                         "stages": plan[5], "bk": plan[6], "kg": plan[7], "rms": plan[8]}
 
     @staticmethod
     def kernel_symbol(plan):
@@ -180,9 +180,9 @@ class Model:
         mode = plan["mode"] if plan["splits"] == 1 else 0
         if plan["kind"] in (1, 4):
             return (f"gemm_stage_kernelILi{plan['tile_n']}ELi{plan['tile_m']}ELi{plan['stages']}ELi{mode}"
-                    f"ELi{plan['bk']}ELi{plan['kg']}E")
+                    f"ELi{plan['bk']}ELi{plan['kg']}ELi{plan['rms']}E")
         if plan["kind"] == 2:
-            return f"gemm_skinny_kernelILi{plan['tile_n'] // 16}ELi{mode}E"
+            return f"gemm_skinny_kernelILi{plan['tile_n'] // 16}ELi{mode}ELi{plan['rms']}E"
         if plan["kind"] == 3:
             return f"gemm_big_kernelILi{mode}E"
         return f"gemm_mfma_kernelILi{plan['tile_n']}ELi{plan['tile_m']}EDF16bLi{mode}E"
