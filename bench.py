@@ -85,8 +85,9 @@ def serve_main(args):
         m.prefill(mb, b["pixels"], b["text_ids"], b["kv0"], state=b.get("state"))
         m.prefill(mb, b["pixels"], b["text_ids"], b["kv1"], state=b.get("state"))
     torch.cuda.synchronize()
+    js = vla.nonblocking_stream(0)      # join stream of every lockstep (profile and executor alike)
     t0 = time.perf_counter()
-    prof = serve.profile_locksteps(models, bufs, mb, cus, reps=3, log=log)
+    prof = serve.profile_locksteps(models, bufs, mb, cus, reps=3, log=log, join_stream=js)
     log(f"[serve] profiled {prof.size} lockstep entries in {time.perf_counter() - t0:.1f} s")
     cu_table, dur_lut = serve.best_cu_table(prof, cus)
     dur_static = {cu: prof[i] for i, cu in enumerate(cus)}
@@ -109,7 +110,7 @@ def serve_main(args):
         if best > 0 and not args.serve_no_validate:
             for R in sorted({best, best + 1}):
                 s = serve.Scheduler(slo, mb, "esf")
-                s.set_gpu(models, bufs)
+                s.set_gpu(models, bufs, join_stream=js)
                 s.set_cu(256, cu_table)
                 arr = synth.poisson_arrivals(R, f, args.validate_seconds, epoch=100, n_models=len(cfgs))
                 req, ls = s.run(arr, drain_ns=int(1e9))
@@ -183,7 +184,7 @@ def serve_main(args):
                 m.prefill(mb, bb["pixels"], bb["text_ids"], bb["kv1"], state=bb.get("state"))
             torch.cuda.synchronize()
             sch = serve.Scheduler(vslo, mb, "esf")
-            sch.set_gpu(vmodels, vbufs)
+            sch.set_gpu(vmodels, vbufs, join_stream=js)
             sch.set_cu(256, vcu)
             arr = synth.poisson_arrivals(b, f0, args.validate_seconds, epoch=100, n_models=len(arch_of))
             req, ls = sch.run(arr, drain_ns=int(1e9))
@@ -288,13 +289,16 @@ def main():
     d = {k: torch.from_numpy(v).to(dev) for k, v in inp.items()}
     kv = [m.alloc_kv(B), m.alloc_kv(B)]
     act = [torch.empty_like(d["noise"]), torch.empty_like(d["noise"])]
-    stream = torch.cuda.current_stream()
+    # every timed launch goes to one non-blocking stream: vla_step runs the
+    # action half on it directly (no cross-queue wait pending during the graph)
+    torch.cuda.synchronize()
+    stream = vla.nonblocking_stream(0)
 
     def lockstep(k):
         # VLM stage of batch k into kv[k % 2] alongside the action stage of batch k - 1
         adit_b = B if k > 0 else 0
         vla.step(m, B, d["pixels"], d["text_ids"], kv[k % 2], m, adit_b, kv[(k - 1) % 2], d["noise"], N,
-                 act[(k - 1) % 2], vlm_cu_count=args.cu, state=d.get("state"))
+                 act[(k - 1) % 2], vlm_cu_count=args.cu, state=d.get("state"), join_stream=stream)
 
     auto_cu = args.cu == 0
     if auto_cu:
@@ -355,7 +359,7 @@ def main():
     attain = float(np.mean([x <= slo for x in lat]))
     log(f"[bench] {K} locksteps: {ms_per_step:.3f} ms/step, {value:.1f} chunks/s (wall {wall * 1e3 / K:.3f} ms/step)")
 
-    # ---- stages alone (graph replays on the current stream)
+    # ---- stages alone (graph replays on the same stream)
     def time_alone(fn, reps=10):
         fn()
         torch.cuda.synchronize()
@@ -367,18 +371,18 @@ def main():
         torch.cuda.synchronize()
         return a.elapsed_time(b) / reps
 
-    pre_ms = time_alone(lambda: m.prefill(B, d["pixels"], d["text_ids"], kv[0], state=d.get("state")))
-    den_ms = time_alone(lambda: m.denoise(B, kv[0], d["noise"], N, act[0]))
+    pre_ms = time_alone(lambda: m.prefill(B, d["pixels"], d["text_ids"], kv[0], state=d.get("state"), stream=stream))
+    den_ms = time_alone(lambda: m.denoise(B, kv[0], d["noise"], N, act[0], stream=stream))
     log(f"[bench] alone: prefill {pre_ms:.3f} ms, denoise {den_ms:.3f} ms ({den_ms / N:.3f} ms/step)")
 
     # ---- roofline of the projection kernels (HIP events around back-to-back launches)
     kern = {}
     for which in (0, 1, 2, 3):
-        m.replay_gemm(which, B, 3)
+        m.replay_gemm(which, B, 3, stream=stream)
         torch.cuda.synchronize()
         a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         a.record(stream)
-        flops, plan = m.replay_gemm(which, B, args.roofline_iters)
+        flops, plan = m.replay_gemm(which, B, args.roofline_iters, stream=stream)
         b.record(stream)
         torch.cuda.synchronize()
         us = a.elapsed_time(b) * 1e3 / args.roofline_iters

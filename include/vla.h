@@ -155,7 +155,11 @@ vla_status vla_denoise(vla_model m, int batch, const void* kv, const float* nois
  * with batch 0. Both halves wait for work already enqueued on `join_stream`,
  * and `join_stream` waits for both halves, so stream order is preserved.
  * vlm_cu_count: a multiple of 8 in [8, 256]; 256 means no restriction. The
- * restricted streams come from a per-device pool created on first use.
+ * restricted streams come from a per-device pool created on first use. When
+ * `join_stream` is a non-blocking stream (hipStreamNonBlocking) and the action
+ * half is unrestricted, the action half runs on `join_stream` itself (faster:
+ * no cross-queue wait is pending while its kernels run); otherwise it runs on
+ * a pool stream.
  */
 typedef struct {
   vla_model vlm_model;  int vlm_batch;

@@ -170,7 +170,7 @@ def alloc_io(models: Sequence[vla.Model], max_batch: int):
 
 
 def profile_locksteps(models: Sequence[vla.Model], bufs, max_batch: int, cu_counts: Sequence[int],
-                      reps: int = 3, warmup: int = 1, log=None):
+                      reps: int = 3, warmup: int = 1, log=None, join_stream=None):
     """Median duration (ns) of one lockstep for every (VLM model, VLM batch,
     action model, action batch) combination and every CU restriction of the
     VLM stream, timed with HIP events on the join stream. Returns
@@ -180,7 +180,7 @@ def profile_locksteps(models: Sequence[vla.Model], bufs, max_batch: int, cu_coun
     nm, nb = len(models), n_buckets(max_batch)
     bs = bucket_batches(max_batch)
     out = np.zeros((len(cu_counts), nm, nb, nm, nb), dtype=np.int64)
-    stream = torch.cuda.current_stream()
+    stream = join_stream if join_stream is not None else torch.cuda.current_stream()
     for ki, cu in enumerate(cu_counts):
         for mv in range(nm):
             for iv, bv in enumerate(bs):
@@ -199,7 +199,7 @@ def profile_locksteps(models: Sequence[vla.Model], bufs, max_batch: int, cu_coun
                         def one():
                             vla.step(models[mv] if bv else None, bv, xv["pixels"], xv["text_ids"], xv["kv0"],
                                      models[ma] if ba else None, ba, xa["kv1"], xa["noise"], models[ma].cfg.steps,
-                                     xa["act1"], vlm_cu_count=cu, state=xv.get("state"))
+                                     xa["act1"], vlm_cu_count=cu, state=xv.get("state"), join_stream=join_stream)
                         for _ in range(warmup):
                             one()
                         ts = []

@@ -192,6 +192,29 @@ class Model:
                                  _stream(stream)))
 
 
+_hip = None
+
+
+def nonblocking_stream(device: int = 0):
+    """A new non-blocking HIP stream on `device`, as a torch ExternalStream
+    (torch creates blocking streams only). Passed as vla_step's join stream it
+    lets the unrestricted action half run on it directly (see vla_step). The
+    stream lives until the process ends."""
+    global _hip
+    import torch
+    if _hip is None:
+        _hip = ctypes.CDLL("libamdhip64.so")
+    prev = torch.cuda.current_device()
+    torch.cuda.set_device(device)
+    try:
+        s = ctypes.c_void_p()
+        if _hip.hipStreamCreateWithFlags(ctypes.byref(s), ctypes.c_uint(1)) != 0:   # hipStreamNonBlocking
+            raise VlaError(VLA_EHIP, "hipStreamCreateWithFlags failed")
+    finally:
+        torch.cuda.set_device(prev)
+    return torch.cuda.ExternalStream(s.value, device=torch.device("cuda", device))
+
+
 def step(vlm_model: Optional[Model], vlm_batch: int, pixels, text_ids, kv_out,
          adit_model: Optional[Model], adit_batch: int, kv_in, noise, steps: int, actions_out,
          vlm_cu_count: int = 256, adit_cu_count: int = 0, state=None, join_stream=None):

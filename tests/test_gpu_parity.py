@@ -152,10 +152,12 @@ def test_prefix_kv_untouched_by_action_stage():
     np.testing.assert_array_equal(d["noise"].cpu().numpy(), synth.make_noise(cfg, 2))
 
 
-@pytest.mark.parametrize("cu", [256, 128, 64])
-def test_lockstep_matches_separate_stages(cu):
+@pytest.mark.parametrize("cu,join", [(256, "default"), (128, "default"), (64, "default"), (256, "nonblocking"),
+                                     (64, "nonblocking")])
+def test_lockstep_matches_separate_stages(cu, join):
     """vla_step(prefill of batch k on a CU-restricted stream, denoise of batch
-    k-1 on the action stream) gives the same bits as running them alone."""
+    k-1 on the action stream) gives the same bits as running them alone; with
+    a non-blocking join stream the action half runs on that stream itself."""
     import torch
     from paper_2609_12075_amd import vla
     cfg = SMOL_R
@@ -169,10 +171,15 @@ def test_lockstep_matches_separate_stages(cu):
     kv_prev, kv_cur = m.alloc_kv(2), m.alloc_kv(3)
     m.prefill(2, dp["pixels"], dp["text_ids"], kv_prev)
     act_prev = torch.empty_like(dp["noise"])
-    vla.step(m, 3, dc["pixels"], dc["text_ids"], kv_cur, m, 2, kv_prev, dp["noise"], cfg.steps, act_prev,
-             vlm_cu_count=cu)
     act_cur = torch.empty_like(dc["noise"])
-    vla.step(None, 0, None, None, None, m, 3, kv_cur, dc["noise"], cfg.steps, act_cur, vlm_cu_count=cu)
+    js = None
+    if join == "nonblocking":
+        torch.cuda.synchronize()        # a non-blocking stream does not wait for the default stream
+        js = vla.nonblocking_stream(0)
+    vla.step(m, 3, dc["pixels"], dc["text_ids"], kv_cur, m, 2, kv_prev, dp["noise"], cfg.steps, act_prev,
+             vlm_cu_count=cu, join_stream=js)
+    vla.step(None, 0, None, None, None, m, 3, kv_cur, dc["noise"], cfg.steps, act_cur, vlm_cu_count=cu,
+             join_stream=js)
     torch.cuda.synchronize()
     np.testing.assert_array_equal(act_prev.cpu().numpy(), ref_prev)
     np.testing.assert_array_equal(act_cur.cpu().numpy(), ref_cur)
