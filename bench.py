@@ -228,6 +228,96 @@ def counters_main(args):
     m.close()
 
 
+def stage_flops(c) -> tuple:
+    """Algorithmic flops per request of the two stages as the library computes
+    them (2 M N K per projection, 4 n_q hd Lq Lk per attention; the joint
+    expert's last LLM layer only projects K and V; the patch embedding and the
+    batch-independent time conditioning are left out). Returns (prefill,
+    action step)."""
+    from paper_2609_12075_amd import synth
+    hd, D, Hq, Hk = c.head_dim, c.llm_d, c.n_q * c.head_dim, c.n_kv * c.head_dim
+    T, P, F = c.tokens_per_img, c.prefix_len, c.llm_mlp
+    joint = c.head_kind == synth.HEAD_JOINT
+    pre = 0.0
+    if c.vit_layers > 0:
+        d, f, Ti = c.vit_d, c.vit_mlp, c.n_img * T
+        pre += c.vit_layers * (2 * Ti * d * 3 * d + 4 * c.n_img * d * T * T + 2 * Ti * d * d + 2 * 2 * Ti * d * f)
+        pre += 2 * Ti * d * D
+    full = c.llm_layers - (1 if joint else 0)
+    pre += full * (2 * P * D * (Hq + 2 * Hk) + 4 * c.n_q * hd * P * P + 2 * P * Hq * D + 2 * P * D * 2 * F + 2 * P * F * D)
+    if joint:
+        pre += 2 * P * D * 2 * Hk
+    else:
+        Da = c.act_d
+        pre += 2 * P * D * Da + 2 * P * Da * c.act_layers * 2 * Da
+    Da, Fa, H, A = c.act_d, c.act_mlp, c.horizon, c.action_dim
+    if joint:
+        step = 2 * H * A * Da + 2 * 2 * H * Da * Da + 2 * H * Da * A
+        step += c.act_layers * (2 * H * Da * (Hq + 2 * Hk) + 4 * c.n_q * hd * H * (P + H) + 2 * H * Hq * Da
+                                + 2 * H * Da * 2 * Fa + 2 * H * Fa * Da)
+    else:
+        L = H + 1
+        step = 2 * H * A * Da + 2 * H * Da * A
+        step += c.act_layers * (2 * L * Da * 3 * Da + 4 * Da * L * L + 2 * L * Da * Da + 2 * L * Da * Da
+                                + 4 * Da * L * P + 2 * L * Da * Da + 2 * 2 * L * Da * Fa)
+    return float(pre), float(step)
+
+
+def stages_main(args):
+    """Stage times per (config, batch): graph replays of prefill and of the
+    whole denoise (N Euler steps) on one stream, median of --stage-reps
+    replays after warm-ups, and the algorithmic TFLOP/s and share of the bf16
+    MFMA peak they imply."""
+    import numpy as np
+    import torch
+    from paper_2609_12075_amd import synth, vla
+    out = {}
+    for name in args.stage_configs.split(","):
+        base = synth.CONFIGS[name]
+        Bs = [int(b) for b in args.stage_batches.split(",") if int(b) <= max(base.max_batch, 1)]
+        cfg = base.with_(max_batch=max(Bs))
+        m = vla.Model(cfg, synth.make_weights(cfg), device=0)
+        torch.cuda.synchronize()
+        stream = vla.nonblocking_stream(0)
+        pre_f, step_f = stage_flops(cfg)
+        peak = PEAK["f32" if cfg.dtype == synth.DTYPE_F32 else "bf16"]
+        for B in Bs:
+            inp = synth.make_inputs(cfg, B)
+            d = {k: torch.from_numpy(v).to("cuda:0") for k, v in inp.items()}
+            kv = m.alloc_kv(B)
+            act = torch.empty_like(d["noise"])
+            torch.cuda.synchronize()
+
+            def med(fn):
+                for _ in range(args.stage_warmup):
+                    fn()
+                torch.cuda.synchronize()
+                evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.stage_reps + 1)]
+                evs[0].record(stream)
+                for i in range(args.stage_reps):
+                    fn()
+                    evs[i + 1].record(stream)
+                torch.cuda.synchronize()
+                return float(np.median([evs[i].elapsed_time(evs[i + 1]) for i in range(args.stage_reps)]))
+            pre = med(lambda: m.prefill(B, d["pixels"], d["text_ids"], kv, state=d.get("state"), stream=stream))
+            den = med(lambda: m.denoise(B, kv, d["noise"], cfg.steps, act, stream=stream))
+            step = den / cfg.steps
+            rec = {"prefill_ms": round(pre, 4), "adit_step_ms": round(step, 4), "denoise_ms": round(den, 4),
+                   "prefill_tflops": round(B * pre_f / pre / 1e9, 2), "adit_tflops": round(B * step_f / step / 1e9, 2)}
+            rec["prefill_mfma_frac"] = round(rec["prefill_tflops"] / peak, 4)
+            rec["adit_mfma_frac"] = round(rec["adit_tflops"] / peak, 4)
+            out[f"{name}:B{B}"] = rec
+            log(f"[stages] {name} B={B}: prefill {pre:.3f} ms ({rec['prefill_tflops']} TFLOP/s, "
+                f"{100 * rec['prefill_mfma_frac']:.1f} %), ADiT step {step:.4f} ms ({rec['adit_tflops']} TFLOP/s, "
+                f"{100 * rec['adit_mfma_frac']:.1f} %)")
+            del kv, act, d
+        m.close()
+        torch.cuda.empty_cache()
+    print(json.dumps({"metric": "stage times per config and batch", "reps": args.stage_reps, "warmup": args.stage_warmup,
+                      "flops_per_request": {n: stage_flops(synth.CONFIGS[n]) for n in args.stage_configs.split(",")},
+                      "stages": out}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -257,6 +347,11 @@ def main():
     ap.add_argument("--serve-variants", type=int, default=2, help="fine-tuned variants per architecture in the co-location study")
     ap.add_argument("--validate-seconds", type=float, default=8.0)
     ap.add_argument("--slo-ms", type=float, default=100.0)
+    ap.add_argument("--stages", action="store_true", help="stage times per config and batch instead of the lockstep bench")
+    ap.add_argument("--stage-configs", default="tiny,smolvla,pi0,gr00t")
+    ap.add_argument("--stage-batches", default="1,4,16")
+    ap.add_argument("--stage-reps", type=int, default=200)
+    ap.add_argument("--stage-warmup", type=int, default=20)
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -269,6 +364,9 @@ def main():
         return
     if args.counters:
         counters_main(args)
+        return
+    if args.stages:
+        stages_main(args)
         return
 
     import numpy as np
