@@ -328,7 +328,8 @@ def main():
     ap.add_argument("--cu", type=int, default=0,
                     help="compute units the VLM stream may use (multiple of 8); 0: the fastest of --cu-candidates, "
                          "profiled before the timed steps")
-    ap.add_argument("--cu-candidates", default="256,192,160,128,96,64,48,32")
+    ap.add_argument("--cu-candidates", default="256,224,192,160,128,96,64,32",
+                    help="VLM CU counts to profile (multiples of 32 keep every shader engine equally populated)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--roofline-iters", type=int, default=50)

@@ -154,7 +154,10 @@ vla_status vla_denoise(vla_model m, int batch, const void* kv, const float* nois
  * previous batch runs on an unrestricted stream. Either half may be skipped
  * with batch 0. Both halves wait for work already enqueued on `join_stream`,
  * and `join_stream` waits for both halves, so stream order is preserved.
- * vlm_cu_count: a multiple of 8 in [8, 256]; 256 means no restriction. The
+ * vlm_cu_count: a multiple of 8 in [8, 256]; 256 means no restriction (on
+ * MI355X multiples of 32 give every shader engine the same number of CUs; the
+ * dispatcher shares workgroups equally between shader engines, so other counts
+ * run at the speed of the next lower multiple of 32). The
  * restricted streams come from a per-device pool created on first use. When
  * `join_stream` is a non-blocking stream (hipStreamNonBlocking) and the action
  * half is unrestricted, the action half runs on `join_stream` itself (faster:
