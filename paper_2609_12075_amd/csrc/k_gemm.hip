@@ -720,8 +720,8 @@ __global__ void __launch_bounds__(256) gemm_skinny_kernel(GemmArgs a) {
 // keeps the same LDS per block but more K-steps of loads in flight. RMS: the
 // RMSNorm folded into the product (a.rms_in): every A element passes through
 // the fragment reads of the waves of weight-row half 0 exactly once, so those
-// lanes also sum the squares of their fragments; the row sums meet in LDS
-// and scale the tile rows in the epilogue.
+// waves' A_j A_j^T diagonals are the rows' sums of squares; the row sums
+// meet in LDS and scale the tile rows in the epilogue.
 template <int BN, int BM, int STAGES, int MODE, int BK = 64, int KG = 1, int RMS = 0>
 __global__ void __launch_bounds__(256 * KG)
 gemm_stage_kernel(GemmArgs a) {
@@ -789,9 +789,13 @@ gemm_stage_kernel(GemmArgs a) {
   for (int i = 0; i < TN; ++i)
 #pragma unroll
     for (int j = 0; j < TM; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-  float rs[TM], rs2[TM];                                // RMS: this lane's sums of squares
+  // RMS: A_j A_j^T over this wave's K chunks; its diagonal holds the rows'
+  // sums of squares (one extra matrix instruction per A fragment: these
+  // products are bound by the loads, not by the matrix pipe, and VALU
+  // dot products of the same fragments cost more)
+  f32x4 sq[TM];
 #pragma unroll
-  for (int j = 0; j < TM; ++j) rs[j] = rs2[j] = 0.f;
+  for (int j = 0; j < TM; ++j) sq[j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   const int lr = lane & 15, lq = lane >> 4;
 #pragma unroll
@@ -835,12 +839,6 @@ gemm_stage_kernel(GemmArgs a) {
 #pragma unroll
         for (int j = 0; j < TM; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wf[q][i], af[q][j], acc[i][j], 0, 0, 0);
-    if constexpr (RMS) {
-#pragma unroll
-      for (int q = 0; q < KCG; ++q)
-#pragma unroll
-        for (int j = 0; j < TM; ++j) sumsq8(af[q][j], rs[j], rs2[j]);
-    }
     if constexpr (KCG == 2) {
       constexpr int NRD = TN + TM, NMF = TN * TM, R = NMF / NRD > 0 ? NMF / NRD : 1;
       __builtin_amdgcn_sched_group_barrier(0x100, NRD, 0);      // chunk 0 reads
@@ -851,30 +849,27 @@ gemm_stage_kernel(GemmArgs a) {
       }
       __builtin_amdgcn_sched_group_barrier(0x008, 2 * NMF - NRD * R, 0);
     }
+    if constexpr (RMS) {
+#pragma unroll
+      for (int q = 0; q < KCG; ++q)
+#pragma unroll
+        for (int j = 0; j < TM; ++j) sq[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[q][j], af[q][j], sq[j], 0, 0, 0);
+    }
   }
   if constexpr (RMS) {
-    // the four lanes of a row (lq) hold disjoint K chunks: add them, then
-    // weight-row half 0's waves publish one sum per (wave group, row)
+    // lane l holds entries (4 (l / 16) + v, l % 16), v < 4, of each 16 x 16
+    // block: the diagonal entry of row c = l % 16 sits in v = c - 4 (l / 16).
+    // Weight-row half 0's waves publish one sum per (wave group, row).
+    const int c = lane & 15, v = c - 4 * lq;
+    if ((w4 >> 1) == 0 && v >= 0 && v < 4) {
 #pragma unroll
-    for (int j = 0; j < TM; ++j) {
-      rs[j] += rs2[j];
-      rs[j] += __shfl_xor(rs[j], 16);
-      rs[j] += __shfl_xor(rs[j], 32);
-    }
-    if ((w4 >> 1) == 0 && lq == 0) {
-#pragma unroll
-      for (int j = 0; j < TM; ++j) rsq[kg * BM + wm0 + 16 * j + lr] = rs[j];
+      for (int j = 0; j < TM; ++j)
+        rsq[kg * BM + wm0 + 16 * j + c] = v == 0 ? sq[j][0] : v == 1 ? sq[j][1] : v == 2 ? sq[j][2] : sq[j][3];
     }
   }
   // each wave group's tile to its own fp32 plane; the epilogues add the
-  // planes in group order
-  __syncthreads();
-  float* Cp = Cs + kg * BM * LDC;
-#pragma unroll
-  for (int i = 0; i < TN; ++i)
-#pragma unroll
-    for (int j = 0; j < TM; ++j)
-      *reinterpret_cast<f32x4*>(&Cp[(wm0 + 16 * j + lr) * LDC + wn0 + 16 * i + (lane >> 4) * 4]) = acc[i][j];
+  // planes in group order (the row scales, in their own LDS words, are
+  // formed while the planes are written)
   __syncthreads();
   if constexpr (RMS) {
     if (tid < BM) {
@@ -883,8 +878,15 @@ gemm_stage_kernel(GemmArgs a) {
       for (int z = 1; z < KG; ++z) t += rsq[z * BM + tid];
       rsc[tid] = rsqrtf(t / (float)a.rms_in + a.rms_eps);
     }
-    __syncthreads();
-  } else if (a.splits > 1) {
+  }
+  float* Cp = Cs + kg * BM * LDC;
+#pragma unroll
+  for (int i = 0; i < TN; ++i)
+#pragma unroll
+    for (int j = 0; j < TM; ++j)
+      *reinterpret_cast<f32x4*>(&Cp[(wm0 + 16 * j + lr) * LDC + wn0 + 16 * i + (lane >> 4) * 4]) = acc[i][j];
+  __syncthreads();
+  if (!RMS && a.splits > 1) {
     // split-K: store this K range's partial tile; the reduce kernel finishes
     tile_store_partial<BN, BM, NT, LDC, KG>(a, Cs, m_blk, n_blk, bz, tid);
     return;
