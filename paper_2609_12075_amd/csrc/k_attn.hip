@@ -397,6 +397,26 @@ __global__ void __launch_bounds__(64) attn_f32_kernel(AttnArgs a) {
 // the end in group order (as the split-KV combine does across blocks).
 typedef short v4s __attribute__((ext_vector_type(4)));
 
+// A row statistic combined with the value of lane l ^ 16 (l ^ 32): one CDNA4
+// permlane swap of a value with itself exchanges the 16-lane rows (32-lane
+// halves), and its two results hold the lane's own value and its partner's.
+__device__ __forceinline__ float max_x16(float v) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float max_x32(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float sum_x16(float v) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+__device__ __forceinline__ float sum_x32(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
 template <int HDP>
 struct V2 {
   static constexpr int BKV = HDP >= 256 ? 32 : 64;          // keys per tile
@@ -456,6 +476,30 @@ __global__ void __launch_bounds__(256 * KS) attn_v2_kernel(AttnArgs a) {
   const int nrounds = (nt + KS - 1) / KS;
   const bf16* Z = reinterpret_cast<const bf16*>(a.zeros);
 
+  // Loop-invariant addressing: the (request, KV head) base of each segment's
+  // K and V rows in bytes and, per lane and load, the byte offset of its row
+  // and chunk; per tile only the segment bases move (scalar work) and each
+  // lane picks its row's segment.
+  const long kbase0 = (long)a.seg[0].k + ((long)b * a.seg[0].k_sb + (long)g * a.seg[0].k_sh) * 2;
+  const long kbase1 = (long)a.seg[1].k + ((long)b * a.seg[1].k_sb + (long)g * a.seg[1].k_sh) * 2;
+  const long vbase0 = (long)a.seg[0].v + ((long)b * a.seg[0].v_sb + (long)g * a.seg[0].v_sh) * 2;
+  const long vbase1 = (long)a.seg[1].v + ((long)b * a.seg[1].v_sb + (long)g * a.seg[1].v_sh) * 2;
+  const long kst0 = a.seg[0].k_si * 2, kst1 = a.seg[1].k_si * 2, vst0 = a.seg[0].v_si * 2, vst1 = a.seg[1].v_si * 2;
+  // (head dim 256 with one key group keeps the per-tile computation: the
+  // hoisted offsets would cost it half its occupancy)
+  constexpr bool HOIST = !(HDP >= 256 && KS == 1);
+  constexpr int IWH = HOIST ? IW : 1;
+  int lrow[IWH], lok[IWH];
+  unsigned rk0[IWH], rk1[IWH], rv0[IWH], rv1[IWH];  // < 2^32 (checked by the launcher)
+#pragma unroll
+  for (int i = 0; i < IWH; ++i) {
+    const int u = (i * NW + wave) * 64 + lane, row = u / CR, c = (u % CR) ^ C::swz(row), d8 = c * 8;
+    lrow[i] = row;
+    lok[i] = d8 < hd;
+    rk0[i] = (unsigned)(row * kst0 + d8 * 2); rk1[i] = (unsigned)(row * kst1 + d8 * 2);
+    rv0[i] = (unsigned)(row * vst0 + d8 * 2); rv1[i] = (unsigned)(row * vst1 + d8 * 2);
+  }
+
   // round p holds tiles p KS .. p KS + KS - 1 in ring slot p % NR; each tile
   // is its K tile then its V tile. 16-byte unit u of a tile is (row u / CR,
   // slot u % CR); wave w loads units [(i NW + w) 64, + 64) for i < IW.
@@ -466,16 +510,28 @@ __global__ void __launch_bounds__(256 * KS) attn_v2_kernel(AttnArgs a) {
       const int t = p * KS + q;
       char* kt = base + q * 2 * TILE;
       const int k0 = kbeg + t * BKV;
+      // row k0 + r of segment 1 is its row k0 - len0 + r (used only for rows >= len0)
+      const long tk0 = kbase0 + k0 * kst0, tk1 = kbase1 + (long)(k0 - len0) * kst1;
+      const long tv0 = vbase0 + k0 * vst0, tv1 = vbase1 + (long)(k0 - len0) * vst1;
 #pragma unroll
       for (int i = 0; i < IW; ++i) {
-        const int u = (i * NW + wave) * 64 + lane, row = u / CR, c = (u % CR) ^ C::swz(row), d8 = c * 8;
-        const int kk = k0 + row;
         const bf16 *ks = Z, *vs = Z;
-        if (t < nt && kk < kend && d8 < hd) {
-          const int which = kk < len0 ? 0 : 1;
-          const int key = which ? kk - len0 : kk;
-          ks = seg_row(a, which, b, g, key, false) + d8;
-          vs = seg_row(a, which, b, g, key, true) + d8;
+        if constexpr (HOIST) {
+          const int kk = k0 + lrow[i];
+          if (t < nt && kk < kend && lok[i]) {
+            const bool s1 = kk >= len0;
+            ks = reinterpret_cast<const bf16*>(s1 ? tk1 + rk1[i] : tk0 + rk0[i]);
+            vs = reinterpret_cast<const bf16*>(s1 ? tv1 + rv1[i] : tv0 + rv0[i]);
+          }
+        } else {
+          const int u = (i * NW + wave) * 64 + lane, row = u / CR, c = (u % CR) ^ C::swz(row), d8 = c * 8;
+          const int kk = k0 + row;
+          if (t < nt && kk < kend && d8 < hd) {
+            const int which = kk < len0 ? 0 : 1;
+            const int key = which ? kk - len0 : kk;
+            ks = seg_row(a, which, b, g, key, false) + d8;
+            vs = seg_row(a, which, b, g, key, true) + d8;
+          }
         }
         __builtin_amdgcn_global_load_lds(ks, kt + (i * NW + wave) * 1024, 16, 0, 0);
         __builtin_amdgcn_global_load_lds(vs, kt + TILE + (i * NW + wave) * 1024, 16, 0, 0);
@@ -523,35 +579,34 @@ __global__ void __launch_bounds__(256 * KS) attn_v2_kernel(AttnArgs a) {
         sc[st] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[c], sc[st], 0, 0, 0);
       }
     }
-    // keys past the range exist only in a range's last tile; exp2 arguments
-    // are <= 0 (or -inf), so the plain hardware exp2 suffices and maps -inf
-    // to 0
-    float mx = -INFINITY;
-    const bool full = k0 + BKV <= kend;
+    // keys past the range exist only in a range's last tile (a block-uniform
+    // test): they get score -inf. The running max is kept in log2 units
+    // (scores times scale log2 e, positive), so each probability is one fused
+    // multiply-add and the hardware exp2, whose argument is <= 0 or -inf.
+    if (k0 + BKV > kend) {
 #pragma unroll
-    for (int st = 0; st < NST; ++st)
+      for (int st = 0; st < NST; ++st)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int kk = k0 + st * 16 + grp * 4 + i;
-        const float v = (full || kk < kend) ? sc[st][i] * sl2 : -INFINITY;
-        sc[st][i] = v;
-        mx = fmaxf(mx, v);
-      }
-    mx = fmaxf(mx, __shfl_xor(mx, 16));
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
-    const float m_new = fmaxf(m_run, mx);
+        for (int i = 0; i < 4; ++i)
+          if (k0 + st * 16 + grp * 4 + i >= kend) sc[st][i] = -INFINITY;
+    }
+    float mx = fmaxf(fmaxf(sc[0][0], sc[0][1]), fmaxf(sc[0][2], sc[0][3]));
+#pragma unroll
+    for (int st = 1; st < NST; ++st)
+      mx = fmaxf(mx, fmaxf(fmaxf(sc[st][0], sc[st][1]), fmaxf(sc[st][2], sc[st][3])));
+    mx = max_x32(max_x16(mx));
+    const float m_new = fmaxf(m_run, mx * sl2);
     const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-    float psum = 0.f;
+    float ps[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int st = 0; st < NST; ++st)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const float pv = __builtin_amdgcn_exp2f(sc[st][i] - m_new);
+        const float pv = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[st][i], sl2, -m_new));
         sc[st][i] = pv;
-        psum += pv;
+        ps[i] += pv;
       }
-    psum += __shfl_xor(psum, 16);
-    psum += __shfl_xor(psum, 32);
+    const float psum = sum_x32(sum_x16((ps[0] + ps[1]) + (ps[2] + ps[3])));
     l_run = l_run * alpha + psum;
     m_run = m_new;
 #pragma unroll
@@ -697,6 +752,12 @@ void launch_attention(const AttnArgs& a, hipStream_t s) {
     hipLaunchKernelGGL(attn_f32_kernel, dim3(a.Lq, a.Hq, a.B), dim3(64), 0, s, a);
     return;
   }
+  // the direct-load kernel keeps scores in log2 units scaled by a positive
+  // factor and 32-bit offsets of a tile's rows within a segment
+  VLA_REQUIRE(a.scale > 0.f, "attention scale must be positive");
+  for (const AttnSeg& sg : a.seg)
+    VLA_REQUIRE(64L * 2 * std::max(std::labs(sg.k_si), std::labs(sg.v_si)) + 2L * a.hd < (1L << 32),
+                "attention key row stride too large");
   AttnArgs b = a;
   int ks;
   attn_plan(a, b.splits, b.kchunk, ks);
