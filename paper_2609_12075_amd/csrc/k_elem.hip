@@ -97,7 +97,7 @@ __global__ void copy_f32_kernel(const float* src, float* dst, long n) {
 __global__ void silu_f32_kernel(const float* src, float* dst, long n) {
   for (long e = blockIdx.x * (long)blockDim.x + threadIdx.x; e < n; e += (long)gridDim.x * blockDim.x) {
     const float x = src[e];
-    dst[e] = x / (1.0f + __expf(-x));
+    dst[e] = x * __builtin_amdgcn_rcpf(1.0f + __expf(-x));
   }
 }
 

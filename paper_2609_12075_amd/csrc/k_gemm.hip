@@ -33,10 +33,15 @@ typedef __attribute__((ext_vector_type(4))) float f32x4;
 
 // ---------------------------------------------------------------- epilogue
 __device__ __forceinline__ float act_apply(float x, int act) {
-  if (act == ACT_SILU) return x / (1.0f + __expf(-x));
+  if (act == ACT_SILU) return x * __builtin_amdgcn_rcpf(1.0f + __expf(-x));   // -0 once e^-x overflows
   if (act == ACT_GELU) {
-    const float c = 0.7978845608028654f;   // sqrt(2/pi)
-    return 0.5f * x * (1.0f + tanhf(c * (x + 0.044715f * x * x * x)));
+    // tanh form: 0.5 x (1 + tanh u) with u = sqrt(2/pi) (x + 0.044715 x^3),
+    // evaluated through the identity 0.5 (1 + tanh u) = 1 / (1 + e^(-2u)):
+    // the hardware exp2 and reciprocal (about 1 ulp each) in place of the
+    // library tanh; e^(-2u) = +inf for very negative x gives -0, = 0 for very
+    // positive x gives x
+    const float u = 0.7978845608028654f * (x + 0.044715f * x * x * x);
+    return x * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(-2.8853900817779268f * u));   // 2 log2 e
   }
   return x;
 }
