@@ -1253,7 +1253,7 @@ static void launch_staged(const GemmArgs& a0, const GemmPlan& p, const NormArgs*
     launch_reduce<MODE>(a, fuse, s);
     return;
   }
-  if constexpr (MODE == EPI_STORE || MODE == EPI_QKV || MODE == EPI_GEGLU) {
+  if constexpr (MODE == EPI_STORE || MODE == EPI_QKV || MODE == EPI_GEGLU || MODE == EPI_EULER) {
     if (a.rms_in) {
       hipLaunchKernelGGL((gemm_stage_kernel<BN, BM, 2, MODE, 64, 1, 1>), grid, dim3(256), 0, s, a);
       return;
@@ -1273,7 +1273,7 @@ static void launch_staged128(const GemmArgs& a0, const GemmPlan& p, const NormAr
     launch_reduce<MODE>(a, fuse, s);
     return;
   }
-  if constexpr (MODE == EPI_STORE || MODE == EPI_QKV || MODE == EPI_GEGLU) {
+  if constexpr (MODE == EPI_STORE || MODE == EPI_QKV || MODE == EPI_GEGLU || MODE == EPI_EULER) {
     if (a.rms_in) {
       hipLaunchKernelGGL((gemm_stage_kernel<BT, BT, ST, MODE, 128, 2, 1>), grid, dim3(512), 0, s, a);
       return;
@@ -1291,7 +1291,7 @@ static void launch_big(const GemmArgs& a, hipStream_t s) {
 template <int TN, int MODE>
 static void launch_skinny(const GemmArgs& a, hipStream_t s) {
   dim3 grid((a.M + 63) / 64, (a.N + 16 * TN - 1) / (16 * TN), 1);
-  if constexpr (MODE == EPI_STORE || MODE == EPI_QKV || MODE == EPI_GEGLU) {
+  if constexpr (MODE == EPI_STORE || MODE == EPI_QKV || MODE == EPI_GEGLU || MODE == EPI_EULER) {
     if (a.rms_in) {
       hipLaunchKernelGGL((gemm_skinny_kernel<TN, MODE, 1>), grid, dim3(256), 0, s, a);
       return;
@@ -1393,8 +1393,8 @@ void launch_gemm(const GemmArgs& a0, hipStream_t s) {
   if (a0.a_type == ET_F32 && a0.w_type == ET_BF16 && a0.mode != EPI_STORE)
     throw VlaError{4, "fp32 activations with bf16 weights only feed plain stores"};
   if (a0.rms_in && (a0.rms_in < 0 || a0.a_type != ET_BF16 || a0.w_type != ET_BF16 || !a0.zeros ||
-                    (a0.mode != EPI_STORE && a0.mode != EPI_QKV && a0.mode != EPI_GEGLU)))
-    throw VlaError{4, "a folded RMSNorm needs bf16 operands and a store, QKV or GeGLU epilogue"};
+                    (a0.mode != EPI_STORE && a0.mode != EPI_QKV && a0.mode != EPI_GEGLU && a0.mode != EPI_EULER)))
+    throw VlaError{4, "a folded RMSNorm needs bf16 operands and a store, QKV, GeGLU or Euler epilogue"};
   if (a0.out2 && (a0.row_group > 0 || a0.ldo2 < a0.N || a0.out_type != ET_F32 ||
                   (a0.mode != EPI_STORE && a0.mode != EPI_RESID)))
     throw VlaError{4, "a bf16 copy needs an fp32 store or residual epilogue without row groups"};

@@ -301,6 +301,13 @@ void vla_model_s::init(const vla_config& c, const float* w, size_t n, int dev) {
       }
       lnf = L.vec(Da);
       out = L.mat(Da, A); out_b = L.vec(A);
+      if (act_fold) {
+        // the final RMSNorm's gain, folded like the layers' into the output
+        // projection's columns
+        launch_scale_cols_bf16(out.p, out.N, Da, out.ldk, lnf, L.s);
+        VLA_HIP(hipGetLastError());
+        VLA_HIP(hipStreamSynchronize(L.s));
+      }
     } else {
       llm_lnf = L.vec(D);
       vp = L.mat(D, Da); vp_b = L.vec(Da);
@@ -662,7 +669,7 @@ void vla_model_s::enqueue_denoise(int B, const void* kv, const float* noise, int
         launch_gemm(gg, s);
         // then the next layer's RMSNorm, or the final one
         GemmArgs gd = gm(*this, ST,y.wd, M, gua, Fa, et);
-        if (act_fold && l + 1 < c.act_layers) {
+        if (act_fold) {
           gd.out2 = za; gd.ldo2 = Da;
           resid(gd, ha, Da, nullptr, nullptr, s);
         } else {
@@ -672,6 +679,7 @@ void vla_model_s::enqueue_denoise(int B, const void* kv, const float* noise, int
       }
       GemmArgs go = gm(*this, ST,out, M, za, Da, et);
       go.mode = EPI_EULER; go.out = x; go.ldo = A; go.out_type = ET_F32; go.bias = out_b; go.dt = dt;
+      if (act_fold) { go.rms_in = Da; go.rms_eps = eps; }   // the final norm, folded
       launch_gemm(go, s);
     }
     return;
@@ -828,8 +836,9 @@ GemmArgs vla_model_s::stage_gemm(int which, int B, int layer) const {
       if (c.head_kind == VLA_HEAD_JOINT) {
         g = gm(*this, ST,act[la].wd, B * H, gua, c.act_mlp, et);
         g.mode = EPI_RESID; g.out = ha; g.ldo = Da; g.out_type = ET_F32;
-        // the stage's layers but the last write the bf16 copy the next
-        // layer's QKV normalises; without folded gains a norm follows
+        // with folded gains the layers write the bf16 copy that the next
+        // layer's QKV (the last: the output projection) normalises; without
+        // them a norm follows
         if (act_fold) { g.out2 = za; g.ldo2 = Da; }
         else g.norm_follows = 1;
       } else {
