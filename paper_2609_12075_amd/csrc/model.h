@@ -61,6 +61,9 @@ struct vla_model_s {
   std::vector<LlmLayer> llm;
   // joint action expert
   Mat ain, t1a, t1t, t2, out; float *ain_b = nullptr, *t1_b = nullptr, *t2_b = nullptr, *lnf = nullptr, *out_b = nullptr;
+  // bf16 joint expert: the action-in projection composed with the time MLP's
+  // action half (W_ain W_t1a, [A] -> [Da]) and the bias that absorbs b_ain
+  Mat ain_t1; float* t1_b1 = nullptr;
   std::vector<LlmLayer> act;
   // bf16 joint expert: each layer's RMSNorm gains are folded into the columns
   // of the projection that reads the normalised rows (ln1 into qkv, ln2 into

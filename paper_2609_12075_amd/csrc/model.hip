@@ -197,7 +197,29 @@ struct Loader {
     mat_into(w, K, N, iota(N, 0));
     return w;
   }
+  // matrix [K][N] computed on the host (not read from the parameter buffer)
+  Mat mat_host(int K, int N, const float* h) {
+    Mat w = alloc_mat(N, K);
+    float* d = upload(h, (size_t)K * N);
+    const std::vector<int> rows = iota(N, 0);
+    if (rows.size() > rowmap_cap) throw VlaError{1, "internal: rowmap staging too small"};
+    VLA_HIP(hipMemcpyAsync(rowmap, rows.data(), rows.size() * sizeof(int), hipMemcpyHostToDevice, s));
+    launch_transpose_convert(d, K, N, w.p, w.ldk, m->et, rowmap, s);
+    VLA_HIP(hipGetLastError());
+    VLA_HIP(hipStreamSynchronize(s));
+    return w;
+  }
 };
+
+// round-to-nearest-even to bf16, kept in an fp32 (host side; finite inputs)
+static double host_bf16(float x) {
+  uint32_t u;
+  std::memcpy(&u, &x, 4);
+  u = (u + 0x7fffu + ((u >> 16) & 1u)) & 0xffff0000u;
+  float y;
+  std::memcpy(&y, &u, 4);
+  return y;
+}
 
 }  // namespace
 
@@ -286,8 +308,40 @@ void vla_model_s::init(const vla_config& c, const float* w, size_t n, int dev) {
     // ---- action stage
     const int Fa = c.act_mlp;
     if (!dit_head) {
-      ain = L.mat(A, Da); ain_b = L.vec(Da);
-      t1a = L.mat(Da, Da); t1t = L.mat(tdim, Da); t1_b = L.vec(Da);
+      const float* h_ain = L.host + L.off;
+      ain = L.mat(A, Da);
+      const float* h_ain_b = L.host + L.off;
+      ain_b = L.vec(Da);
+      const float* h_t1a = L.host + L.off;
+      t1a = L.mat(Da, Da); t1t = L.mat(tdim, Da);
+      const float* h_t1_b = L.host + L.off;
+      t1_b = L.vec(Da);
+      if (et == ET_BF16) {
+        // no nonlinearity between the action-in projection and the time MLP's
+        // action half: u = SiLU((x W_ain + b_ain) W_t1a + tau-part + b_t1)
+        // = SiLU(x (W_ain W_t1a) + tau-part + (b_ain W_t1a + b_t1)), composed
+        // once from the bf16 parameters in double precision (one projection
+        // per Euler step instead of two)
+        std::vector<double> w((size_t)A * Da, 0.0), bb(Da, 0.0);
+        std::vector<double> t1r((size_t)Da * Da);
+        for (size_t i = 0; i < t1r.size(); ++i) t1r[i] = host_bf16(h_t1a[i]);
+        for (int a = 0; a < A; ++a)
+          for (int k = 0; k < Da; ++k) {
+            const double v = host_bf16(h_ain[(size_t)a * Da + k]);
+            const double* row = &t1r[(size_t)k * Da];
+            double* o = &w[(size_t)a * Da];
+            for (int n = 0; n < Da; ++n) o[n] += v * row[n];
+          }
+        for (int k = 0; k < Da; ++k) {
+          const double v = host_bf16(h_ain_b[k]);
+          for (int n = 0; n < Da; ++n) bb[n] += v * t1r[(size_t)k * Da + n];
+        }
+        std::vector<float> wf(w.begin(), w.end()), bf(Da);
+        for (int n = 0; n < Da; ++n) bf[n] = (float)(bb[n] + host_bf16(h_t1_b[n]));
+        ain_t1 = L.mat_host(A, Da, wf.data());
+        t1_b1 = (float*)dalloc((size_t)Da * 4);
+        VLA_HIP(hipMemcpy(t1_b1, bf.data(), (size_t)Da * 4, hipMemcpyHostToDevice));
+      }
       t2 = L.mat(Da, Da); t2_b = L.vec(Da);
       for (int l = 0; l < c.act_layers; ++l) act.push_back(gemma_layer(Da, Fa));
       act_fold = et == ET_BF16;
@@ -596,7 +650,7 @@ const CondCache& vla_model_s::cond_for(int N, hipStream_t s) {
   launch_time_embed(N, tdim, cc.phi, s);
   if (!dit_head) {
     cc.tb = (float*)dalloc((size_t)N * Da * 4);
-    store(gm(*this, ST,t1t, N, cc.phi, tdim, ET_F32), cc.tb, Da, ET_F32, t1_b, ACT_NONE, s);
+    store(gm(*this, ST,t1t, N, cc.phi, tdim, ET_F32), cc.tb, Da, ET_F32, ain_t1.p ? t1_b1 : t1_b, ACT_NONE, s);
   } else {
     const int NL = cfg.act_layers;
     cc.c1 = (float*)dalloc((size_t)N * Da * 4);
@@ -628,8 +682,12 @@ void vla_model_s::enqueue_denoise(int B, const void* kv, const float* noise, int
     const int M = B * H, nq = c.n_q, nkv = c.n_kv, Fa = c.act_mlp;
     const size_t per = (size_t)B * nkv * P * hd * es;
     for (int k = 0; k < N; ++k) {
-      store(gm(*this, ST,ain, M, x, A, ET_F32), e, Da, et, ain_b, ACT_NONE, s);
-      store(gm(*this, ST,t1a, M, e, Da, et), u, Da, et, cc.tb + (size_t)k * Da, ACT_SILU, s);
+      if (ain_t1.p) {
+        store(gm(*this, ST,ain_t1, M, x, A, ET_F32), u, Da, et, cc.tb + (size_t)k * Da, ACT_SILU, s);
+      } else {
+        store(gm(*this, ST,ain, M, x, A, ET_F32), e, Da, et, ain_b, ACT_NONE, s);
+        store(gm(*this, ST,t1a, M, e, Da, et), u, Da, et, cc.tb + (size_t)k * Da, ACT_SILU, s);
+      }
       // za holds RMSNorm(ha) with the next projection's gain, or with the
       // gains folded into the projections (act_fold) bf16(ha), which the
       // projection normalises row by row
