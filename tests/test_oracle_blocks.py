@@ -1,0 +1,314 @@
+"""Pins for the oracle's block compositions (CPU).
+
+Each test rebuilds a whole block or stage from library modules or from a
+closed form and compares the oracle's function with it, so that a swapped
+operand (gate/up), a dropped residual, a wrong norm gain, a wrong split order
+of the adaLN modulation, or a wrong key/value concatenation fails:
+
+* ``llm_layer`` / ``prefill_row`` against a stack of ``transformers``'
+  Gemma decoder layers (RMSNorm with gain 1 + w, half-split RoPE, grouped
+  KV heads, tanh-GELU GeGLU), run bidirectionally over the prefix;
+* the action-expert layers of ``joint_velocity`` against the same Gemma
+  layers with the prefix keys/values in the layer's cache (queries of the
+  action tokens see [prefix ; own] keys at positions P .. P+H-1);
+* ``image_tokens`` against ``conv2d`` + position table + torch's pre-LN
+  ``TransformerEncoderLayer`` stack + ``LayerNorm`` + ``Linear``;
+* ``dit_velocity``'s gated branches in closed form: with 1 + scale = 0 every
+  token's modulated input equals the shift, self-attention over identical
+  tokens returns that token's value row, and cross-attention over identical
+  keys returns the mean of the values.
+
+The transformers pins run its eager attention, whose softmax and rotary
+angles are fp32: agreement is ~1e-6 relative, against O(1) for any of the
+structural mistakes above."""
+import math
+
+import numpy as np
+import pytest
+import torch
+import torch.nn.functional as F
+
+from oracle import vla as O
+from paper_2609_12075_amd import synth as S
+
+transformers = pytest.importorskip("transformers")
+from transformers import GemmaConfig  # noqa: E402
+from transformers.cache_utils import DynamicCache  # noqa: E402
+from transformers.models.gemma import modeling_gemma as MG  # noqa: E402
+
+RNG = np.random.default_rng(2609)
+T = lambda a: torch.from_numpy(np.ascontiguousarray(a, dtype=np.float64))
+
+
+def rel(a, b):
+    return float(np.linalg.norm(np.asarray(a) - np.asarray(b)) / np.linalg.norm(np.asarray(b)))
+
+
+def _rand_joint(cfg, scale=0.15, seed=0):
+    """Parameters of a joint-head model with larger spread than the
+    benchmark's N(0, 0.02) so every nonlinearity is exercised."""
+    r = np.random.default_rng(seed)
+    W = {}
+    for name, shape, kind in S.weight_schema(cfg):
+        v = r.standard_normal(shape) * scale
+        W[name] = 1.0 + v if kind == S.GAIN else v
+    return W
+
+
+def _gemma_layer(d, mlp, n_q, n_kv, hd, W, p, idx, eps=1e-6):
+    """transformers' Gemma decoder layer loaded with the oracle's parameters
+    (matrices stored [in, out] -> nn.Linear weight [out, in]; the Gemma norm
+    multiplies by 1 + weight)."""
+    c = GemmaConfig(vocab_size=16, hidden_size=d, intermediate_size=mlp, num_hidden_layers=idx + 1,
+                    num_attention_heads=n_q, num_key_value_heads=n_kv, head_dim=hd,
+                    hidden_act="gelu_pytorch_tanh", rms_norm_eps=eps,
+                    rope_parameters={"rope_type": "default", "rope_theta": 10000.0}, attention_bias=False)
+    c._attn_implementation = "eager"
+    layer = MG.GemmaDecoderLayer(c, idx).double().eval()
+    with torch.no_grad():
+        layer.self_attn.q_proj.weight.copy_(T(W[p + "wq"].T))
+        layer.self_attn.k_proj.weight.copy_(T(W[p + "wk"].T))
+        layer.self_attn.v_proj.weight.copy_(T(W[p + "wv"].T))
+        layer.self_attn.o_proj.weight.copy_(T(W[p + "wo"].T))
+        layer.mlp.gate_proj.weight.copy_(T(W[p + "wg"].T))
+        layer.mlp.up_proj.weight.copy_(T(W[p + "wu"].T))
+        layer.mlp.down_proj.weight.copy_(T(W[p + "wd"].T))
+        layer.input_layernorm.weight.copy_(T(W[p + "ln1.g"] - 1.0))
+        layer.post_attention_layernorm.weight.copy_(T(W[p + "ln2.g"] - 1.0))
+    return c, layer
+
+
+def _rotary(c, pos):
+    rot = MG.GemmaRotaryEmbedding(c)
+    dummy = torch.zeros(1, dtype=torch.float64)
+    return rot(dummy, torch.as_tensor(pos, dtype=torch.long)[None])
+
+
+def _hf_prefill(cfg, W, h0):
+    """Bidirectional Gemma stack over the prefix; returns (h, keys, values)
+    with keys after RoPE, as the layers' cache holds them."""
+    P = h0.shape[0]
+    cache = DynamicCache()
+    h = T(h0)[None]
+    mask = torch.zeros(1, 1, P, P, dtype=torch.float64)
+    for l in range(cfg.llm_layers):
+        c, layer = _gemma_layer(cfg.llm_d, cfg.llm_mlp, cfg.n_q, cfg.n_kv, cfg.head_dim, W, f"llm.{l}.", l,
+                                cfg.norm_eps)
+        with torch.no_grad():
+            h = layer(h, attention_mask=mask, position_ids=torch.arange(P)[None], past_key_values=cache,
+                      use_cache=True, position_embeddings=_rotary(c, np.arange(P)))
+    ks = [cache.layers[l].keys[0].numpy() for l in range(cfg.llm_layers)]
+    vs = [cache.layers[l].values[0].numpy() for l in range(cfg.llm_layers)]
+    return h[0].numpy(), ks, vs
+
+
+JOINT_SHAPES = [
+    # (llm_d, n_q, n_kv, hd, mlp, act_d, act_mlp): grouped KV 3:1 and one KV head (as in pi0)
+    (48, 6, 2, 8, 72, 40, 56),
+    (64, 4, 1, 16, 96, 24, 40),
+]
+
+
+def _joint_cfg(shape, layers=2):
+    D, nq, nkv, hd, mlp, da, fa = shape
+    return S.CONFIGS["tiny"].with_(name="blockpin", img_hw=16, patch=4, n_text=5, vocab=50, llm_layers=layers,
+                                   llm_d=D, n_q=nq, n_kv=nkv, head_dim=hd, llm_mlp=mlp, act_layers=layers,
+                                   act_d=da, act_heads=nq, act_mlp=fa, horizon=6, action_dim=5)
+
+
+@pytest.mark.parametrize("shape", JOINT_SHAPES)
+def test_llm_layer_against_gemma_decoder_layer(shape):
+    cfg = _joint_cfg(shape, layers=1)
+    W = _rand_joint(cfg, seed=1)
+    h0 = RNG.standard_normal((9, cfg.llm_d))
+    pos = np.arange(9)
+    h, k, v = O.llm_layer(cfg, W, 0, h0, pos)
+    ref_h, ref_k, ref_v = _hf_prefill(cfg, W, h0)
+    assert rel(h, ref_h) < 2e-6, rel(h, ref_h)
+    assert rel(k, ref_k[0]) < 2e-6 and rel(v, ref_v[0]) < 2e-6
+    # the KV-only form of the last layer gives the same keys and values
+    none, k2, v2 = O.llm_layer(cfg, W, 0, h0, pos, need_out=False)
+    assert none is None
+    np.testing.assert_array_equal(k2, k)
+    np.testing.assert_array_equal(v2, v)
+
+
+@pytest.mark.parametrize("shape", JOINT_SHAPES)
+def test_prefill_row_against_gemma_stack(shape):
+    """The whole VLM stage of a joint model: image tokens and embedded text,
+    then the decoder stack; every layer's post-RoPE keys and values."""
+    cfg = _joint_cfg(shape, layers=3)
+    W = _rand_joint(cfg, seed=2)
+    pix = RNG.random((cfg.n_img, 3, cfg.img_hw, cfg.img_hw))
+    ids = RNG.integers(0, cfg.vocab, cfg.n_text)
+    pre = O.prefill_row(cfg, W, pix, ids)
+    # the prefix: conv patch embedding + bias + positions, then the text rows
+    img = F.conv2d(T(pix), T(W["patch.w"].T.reshape(cfg.llm_d, 3, cfg.patch, cfg.patch)), T(W["patch.b"]),
+                   stride=cfg.patch)
+    img = img.flatten(2).transpose(1, 2).reshape(-1, cfg.llm_d).numpy() + np.tile(W["patch.pos"], (cfg.n_img, 1))
+    h0 = np.concatenate([img, W["embed"][ids]])
+    _, ks, vs = _hf_prefill(cfg, W, h0)
+    for l in range(cfg.llm_layers):
+        assert rel(pre["k"][l], ks[l]) < 2e-6, (l, rel(pre["k"][l], ks[l]))
+        assert rel(pre["v"][l], vs[l]) < 2e-6, (l, rel(pre["v"][l], vs[l]))
+
+
+@pytest.mark.parametrize("shape", JOINT_SHAPES)
+def test_joint_velocity_against_gemma_layers_with_prefix_cache(shape):
+    """Action-expert layers = Gemma layers of width act_d in the LLM's head
+    layout whose cache already holds LLM layer l's prefix keys and values;
+    the action tokens sit at positions P .. P+H-1 and see every key."""
+    cfg = _joint_cfg(shape, layers=2)
+    W = _rand_joint(cfg, seed=3)
+    P, H = 11, cfg.horizon
+    pre = {"k": [RNG.standard_normal((cfg.n_kv, P, cfg.head_dim)) for _ in range(cfg.llm_layers)],
+           "v": [RNG.standard_normal((cfg.n_kv, P, cfg.head_dim)) for _ in range(cfg.llm_layers)]}
+    x = RNG.standard_normal((H, cfg.action_dim))
+    for t in (1.0, 0.3):
+        got = O.joint_velocity(cfg, W, pre, x, t)
+        # time-conditioned action embedding (concat MLP), as torch modules
+        lin = lambda a, w, b=None: F.linear(a, T(w.T), None if b is None else T(b))
+        e = lin(T(x), W["act.in.w"], W["act.in.b"])
+        phi = T(O.timestep_embedding(t, cfg.tdim))
+        cat = torch.cat([e, phi.expand(H, -1)], -1)
+        w1 = np.concatenate([W["act.t1a.w"], W["act.t1t.w"]], 0)
+        h = lin(F.silu(lin(cat, w1, W["act.t1.b"])), W["act.t2.w"], W["act.t2.b"])[None]
+        mask = torch.zeros(1, 1, H, P + H, dtype=torch.float64)
+        posn = P + np.arange(H)
+        for l in range(cfg.act_layers):
+            c, layer = _gemma_layer(cfg.act_d, cfg.act_mlp, cfg.n_q, cfg.n_kv, cfg.head_dim, W, f"act.{l}.", 0,
+                                    cfg.norm_eps)
+            cache = DynamicCache()
+            cache.update(T(pre["k"][l])[None], T(pre["v"][l])[None], 0)
+            with torch.no_grad():
+                h = layer(h, attention_mask=mask, position_ids=torch.as_tensor(posn)[None], past_key_values=cache,
+                          use_cache=True, position_embeddings=_rotary(c, posn))
+        fn = MG.GemmaRMSNorm(cfg.act_d, eps=cfg.norm_eps).double()
+        with torch.no_grad():
+            fn.weight.copy_(T(W["act.lnf.g"] - 1.0))
+            ref = lin(fn(h[0]), W["act.out.w"], W["act.out.b"]).numpy()
+        assert rel(got, ref) < 2e-6, (t, rel(got, ref))
+
+
+def _vit_cfg(vit_layers, n_img=2):
+    return S.CONFIGS["pi0"].with_(name="vitpin", n_img=n_img, img_hw=28, patch=7, vit_layers=vit_layers, vit_d=32,
+                                  vit_heads=4, vit_mlp=48, n_text=3, vocab=20, llm_layers=1, llm_d=24, n_q=2, n_kv=1,
+                                  head_dim=8, llm_mlp=32, act_layers=1, act_d=16, act_heads=2, act_mlp=24)
+
+
+@pytest.mark.parametrize("vit_layers", [0, 2])
+def test_image_tokens_against_torch_modules(vit_layers):
+    """image_tokens = per image: conv2d patch embedding (+ bias) + position
+    table, then (with a vision encoder) pre-LN TransformerEncoderLayers with
+    tanh-GELU, a final LayerNorm and the projector to the LLM width; images
+    concatenated in order."""
+    cfg = _vit_cfg(vit_layers)
+    W = _rand_joint(cfg, scale=0.2, seed=4)
+    pix = RNG.random((cfg.n_img, 3, cfg.img_hw, cfg.img_hw))
+    got = O.image_tokens(cfg, W, pix)
+    E = cfg.embed_d
+    x = F.conv2d(T(pix), T(W["patch.w"].T.reshape(E, 3, cfg.patch, cfg.patch)), T(W["patch.b"]), stride=cfg.patch)
+    x = x.flatten(2).transpose(1, 2) + T(W["patch.pos"])[None]          # [n_img, tokens, E]
+    if vit_layers:
+        d = cfg.vit_d
+        for l in range(vit_layers):
+            p = f"vit.{l}."
+            layer = torch.nn.TransformerEncoderLayer(d, cfg.vit_heads, cfg.vit_mlp, dropout=0.0,
+                                                     activation=lambda a: F.gelu(a, approximate="tanh"),
+                                                     layer_norm_eps=cfg.norm_eps, batch_first=True,
+                                                     norm_first=True).double().eval()
+            with torch.no_grad():
+                layer.self_attn.in_proj_weight.copy_(T(np.concatenate([W[p + "wq"], W[p + "wk"], W[p + "wv"]], 1).T))
+                layer.self_attn.in_proj_bias.copy_(T(np.concatenate([W[p + "bq"], W[p + "bk"], W[p + "bv"]])))
+                layer.self_attn.out_proj.weight.copy_(T(W[p + "wo"].T))
+                layer.self_attn.out_proj.bias.copy_(T(W[p + "bo"]))
+                layer.linear1.weight.copy_(T(W[p + "w1"].T)); layer.linear1.bias.copy_(T(W[p + "b1"]))
+                layer.linear2.weight.copy_(T(W[p + "w2"].T)); layer.linear2.bias.copy_(T(W[p + "b2"]))
+                layer.norm1.weight.copy_(T(W[p + "ln1.g"])); layer.norm1.bias.copy_(T(W[p + "ln1.b"]))
+                layer.norm2.weight.copy_(T(W[p + "ln2.g"])); layer.norm2.bias.copy_(T(W[p + "ln2.b"]))
+                x = layer(x)
+        ln = torch.nn.LayerNorm(d, eps=cfg.norm_eps).double()
+        proj = torch.nn.Linear(d, cfg.llm_d).double()
+        with torch.no_grad():
+            ln.weight.copy_(T(W["vit.lnf.g"])); ln.bias.copy_(T(W["vit.lnf.b"]))
+            proj.weight.copy_(T(W["vit.proj.w"].T)); proj.bias.copy_(T(W["vit.proj.b"]))
+            x = proj(ln(x))
+    ref = x.reshape(-1, cfg.llm_d).detach().numpy()
+    assert got.shape == (cfg.n_img_tokens, cfg.llm_d)
+    assert rel(got, ref) < 1e-11, rel(got, ref)
+
+
+# ---------------------------------------------------------------- DiT gated branches, closed form
+def _dit_cfg():
+    return S.CONFIGS["gr00t"].with_(name="dit-closed", img_hw=28, patch=7, vit_layers=1, vit_d=32, vit_heads=4,
+                                    vit_mlp=48, n_text=3, vocab=20, llm_layers=1, llm_d=24, n_q=2, n_kv=1,
+                                    head_dim=8, llm_mlp=32, act_layers=3, act_d=32, act_heads=4, act_mlp=40,
+                                    horizon=5, action_dim=6, state_dim=4, time_dim=16)
+
+
+@pytest.mark.parametrize("t", [1.0, 0.5])
+def test_dit_gated_branches_closed_form(t):
+    """Modulation weights 0 and biases with scale1 = scale2 = -1: the
+    modulated LayerNorm outputs equal shift1 (before self-attention) and
+    shift2 (before the MLP) for every token. Self-attention over identical
+    tokens returns their common value row, so the SA branch adds
+    gate1 * ((shift1 Wv + bv) Wo + bo); the MLP branch adds
+    gate2 * (GELU(shift2 W1 + b1) W2 + b2). With every cross key row equal,
+    cross-attention returns the mean of the value rows. Shift, scale and gate
+    chunks get different values, so a wrong split order or a missing gate
+    breaks the closed form."""
+    cfg = _dit_cfg()
+    W = _rand_joint(cfg, scale=0.2, seed=5)
+    d, L = cfg.act_d, cfg.act_layers
+    r = np.random.default_rng(6)
+    mods = []
+    for l in range(L):
+        sh1, g1, sh2, g2 = (r.standard_normal(d) for _ in range(4))
+        W[f"dit.{l}.mod.w"] = np.zeros((d, 6 * d))
+        W[f"dit.{l}.mod.b"] = np.concatenate([sh1, -np.ones(d), g1, sh2, -np.ones(d), g2])
+        mods.append((sh1, g1, sh2, g2))
+    P = 7
+    kc = [np.tile(r.standard_normal(d), (P, 1)) for _ in range(L)]      # identical keys
+    vc = [r.standard_normal((P, d)) for _ in range(L)]
+    state = r.standard_normal(d)
+    pre = {"kc": kc, "vc": vc, "state": state}
+    x = r.standard_normal((cfg.horizon, cfg.action_dim))
+    got = O.dit_velocity(cfg, W, pre, x, t)
+
+    X = np.concatenate([state[None], x @ W["dit.ain.w"] + W["dit.ain.b"]]) + W["dit.pos"]
+    for l in range(L):
+        p = f"dit.{l}."
+        sh1, g1, sh2, g2 = mods[l]
+        X = X + g1 * ((sh1 @ W[p + "wv"] + W[p + "bv"]) @ W[p + "wo"] + W[p + "bo"])
+        X = X + vc[l].mean(0) @ W[p + "co.w"] + W[p + "co.b"]
+        X = X + g2 * (F.gelu(T(sh2 @ W[p + "w1"] + W[p + "b1"]), approximate="tanh").numpy() @ W[p + "w2"]
+                      + W[p + "b2"])
+    # final adaLN: (shift, scale) from the time conditioning, then the action rows
+    phi = T(O.timestep_embedding(t, cfg.tdim))
+    c = F.linear(F.silu(F.linear(phi, T(W["dit.t1.w"].T), T(W["dit.t1.b"]))), T(W["dit.t2.w"].T), T(W["dit.t2.b"]))
+    modf = F.linear(F.silu(c), T(W["dit.modf.w"].T), T(W["dit.modf.b"])).numpy()
+    z = F.layer_norm(T(X), (d,), eps=cfg.norm_eps).numpy() * (1 + modf[d:]) + modf[:d]
+    ref = z[1:] @ W["dit.out.w"] + W["dit.out.b"]
+    assert rel(got, ref) < 1e-12, rel(got, ref)
+
+
+def test_dit_closed_form_detects_split_order():
+    """The closed form above is sensitive to the chunk order: exchanging the
+    shift1 and gate1 chunks changes the velocity by O(1)."""
+    cfg = _dit_cfg()
+    W = _rand_joint(cfg, scale=0.2, seed=5)
+    d = cfg.act_d
+    r = np.random.default_rng(7)
+    a, g = r.standard_normal(d), r.standard_normal(d)
+    for l in range(cfg.act_layers):
+        W[f"dit.{l}.mod.w"] = np.zeros((d, 6 * d))
+    pre = {"kc": [np.tile(r.standard_normal(d), (4, 1)) for _ in range(cfg.act_layers)],
+           "vc": [r.standard_normal((4, d)) for _ in range(cfg.act_layers)], "state": r.standard_normal(d)}
+    x = r.standard_normal((cfg.horizon, cfg.action_dim))
+    outs = []
+    for b in (np.concatenate([a, -np.ones(d), g, a, -np.ones(d), g]),
+              np.concatenate([g, -np.ones(d), a, g, -np.ones(d), a])):
+        for l in range(cfg.act_layers):
+            W[f"dit.{l}.mod.b"] = b
+        outs.append(O.dit_velocity(cfg, W, pre, x, 0.5))
+    assert rel(outs[0], outs[1]) > 1e-2
