@@ -178,6 +178,19 @@ vla_status vla_step(const vla_step_args* args, hipStream_t join_stream);
 /* Message of the last failed call on this thread ("" if none). */
 const char* vla_last_error(void);
 
+/*
+ * Orderly teardown, for the end of a process (or before unloading the
+ * library): waits for all work on every device the library used, then
+ * releases every model still alive (its graphs, capture streams and device
+ * memory; those handles become invalid and vla_destroy_model ignores them),
+ * the CU-restricted stream pool and its events, and the workspaces of the
+ * test hooks. Callers must not use the library concurrently with it. The
+ * library stays usable afterwards (pools are re-created on demand). Call it
+ * before the HIP runtime unloads, e.g. from an exit handler that runs before
+ * the host framework's own teardown.
+ */
+void vla_shutdown(void);
+
 #ifdef __cplusplus
 }
 #endif

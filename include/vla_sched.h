@@ -14,11 +14,14 @@
  * pre-captured graph (Section 4.1.2). A request meets its SLO when its
  * completion time minus its arrival time is at most the model's SLO.
  *
- * The scheduler runs a whole arrival trace against an executor: either the
- * GPU (vla_step on caller-provided buffers, wall-clock time) or a table of
- * lockstep durations (simulated time, deterministic, no GPU needed).
- * All calls are host calls; only vla_sched_run with the GPU executor touches
- * the device. Errors follow vla.h (status + vla_last_error).
+ * The scheduler serves requests online (submit / run_lockstep / poll) or
+ * runs a whole arrival trace, against an executor: the GPU (vla_step, wall
+ * clock) with per-request inputs gathered into library-owned stage buffers,
+ * the GPU on fixed caller buffers (every batch reads rows 0 .. b-1), or a
+ * table of lockstep durations (simulated time, deterministic, no GPU).
+ * All calls are host calls; only locksteps of a GPU executor touch the
+ * device. A scheduler is used by one host thread at a time. Errors follow
+ * vla.h (status + vla_last_error).
  */
 #ifndef VLA_SCHED_H
 #define VLA_SCHED_H
@@ -107,8 +110,9 @@ vla_status vla_sched_set_mode(vla_sched s, int mode);
 vla_status vla_sched_set_cu(vla_sched s, int default_cu, const int* cu_table);
 
 /*
- * Run an arrival trace: n requests with arrival times t_arrival_ns (sorted
- * ascending, relative to the run start) and model indices. Requests still
+ * Run an arrival trace (vla_sched_run_trace without per-request inputs): n
+ * requests with arrival times t_arrival_ns (sorted ascending, relative to the
+ * run start) and model indices. Requests still
  * unfinished `drain_ns` after the last arrival are reported unfinished.
  * Writes req_out[n] and up to ls_cap lockstep records (*n_ls_out = count
  * executed, which may exceed ls_cap; records beyond it are dropped).
@@ -116,6 +120,92 @@ vla_status vla_sched_set_cu(vla_sched s, int default_cu, const int* cu_table);
 vla_status vla_sched_run(vla_sched s, const int64_t* t_arrival_ns, const int32_t* model, int n,
                          int64_t drain_ns, vla_request_rec* req_out, vla_lockstep_rec* ls_out, int ls_cap,
                          int* n_ls_out);
+
+/*
+ * Online serving (Sections 4.1.2 and 4.1.3): requests arrive one at a time
+ * with their own inputs, each lockstep admits a batch, and finished action
+ * chunks are handed back per request.
+ *
+ * vla_sched_set_gpu_online selects the online GPU executor: for every model
+ * the library allocates stage buffers of max_batch rows (pixels, text ids,
+ * state, two noise slots, two hand-off slots, two action slots) and keeps
+ * them until vla_sched_destroy. A lockstep then runs on `join`:
+ *   1. one batched-copy kernel gathers the admitted requests' pixels, text
+ *      ids, state (zeros when NULL) and noise into rows 0 .. b-1 of the VLM
+ *      model's stage buffers (noise into the slot the next lockstep's action
+ *      half reads);
+ *   2. vla_step runs the VLM half on those rows, restricted by the CU table,
+ *      beside the action half of the batch admitted one lockstep earlier;
+ *   3. one batched-copy kernel scatters row i of that action batch to the
+ *      actions_out buffer of the request that sat in row i;
+ *   4. the host waits for `join`; the finished requests become completions.
+ * steps[m]: Euler steps of model m's action stage.
+ */
+typedef struct {
+  const float* pixels;     /* device fp32 [n_img][3][img_hw][img_hw] */
+  const int32_t* text_ids; /* device int32 [n_text] */
+  const float* state;      /* device fp32 [state_dim] (DiT models) or NULL for a zero state */
+  const float* noise;      /* device fp32 [horizon][action_dim], read only */
+  float* actions_out;      /* device fp32 [horizon][action_dim], written when the request completes */
+} vla_request_io;
+
+typedef struct {           /* a finished request, as returned by vla_sched_poll */
+  int64_t id;
+  int model;
+  int met_slo;
+  int64_t t_arrival_ns, t_vlm_start_ns, t_done_ns;
+} vla_completion;
+
+vla_status vla_sched_set_gpu_online(vla_sched s, const vla_model* models, const int* steps, hipStream_t join);
+
+/* Scheduler clock in ns: wall time since the executor was set (or since the
+ * last vla_sched_reset) for the GPU executors, the simulated time for the
+ * simulated one. Arrival times passed to vla_sched_submit use this clock. */
+int64_t vla_sched_clock_ns(vla_sched s);
+
+/* Drop every queued, in-flight and unpolled request and restart the clock at
+ * 0 (the lockstep counter restarts too). */
+vla_status vla_sched_reset(vla_sched s);
+
+/*
+ * Queue a request of `model` that arrived at t_arrival_ns (scheduler clock)
+ * at the tail of that model's FIFO. `io` is copied; the buffers it names
+ * must stay valid until the request's completion has been polled. With the
+ * online GPU executor io (pixels, text_ids, noise, actions_out) is required;
+ * the simulated executor and the fixed-buffer GPU executor accept NULL.
+ */
+vla_status vla_sched_submit(vla_sched s, int64_t id, int model, int64_t t_arrival_ns, const vla_request_io* io);
+
+/* Requests queued or waiting for the action stage. */
+int vla_sched_pending(vla_sched s);
+
+/*
+ * Run one lockstep now (a whole batch in Monolithic mode): choose the queue,
+ * admit a power-of-two batch, execute, and turn the batch whose action stage
+ * finished into completions. With nothing queued and nothing waiting for the
+ * action stage it does nothing and sets *ran = 0. rec (may be NULL) receives
+ * the lockstep's record. The simulated clock advances by the lockstep's
+ * duration; the GPU executors block until the lockstep has finished.
+ */
+vla_status vla_sched_run_lockstep(vla_sched s, vla_lockstep_rec* rec, int* ran);
+
+/* Let the clock reach t_ns when idle: the simulated clock jumps there, the
+ * GPU executors sleep until then. Earlier times do nothing. */
+vla_status vla_sched_wait_until(vla_sched s, int64_t t_ns);
+
+/* Move up to `cap` completions (oldest first) into out; returns how many. */
+int vla_sched_poll(vla_sched s, vla_completion* out, int cap);
+
+/*
+ * Trace driver on the calls above: resets the scheduler, submits request i
+ * (id i, io[i] when io is not NULL) once the clock reaches t_arrival_ns[i],
+ * runs locksteps while work is pending, idles until the next arrival
+ * otherwise, and stops drain_ns after the last arrival. Outputs as for
+ * vla_sched_run.
+ */
+vla_status vla_sched_run_trace(vla_sched s, const int64_t* t_arrival_ns, const int32_t* model,
+                               const vla_request_io* io, int n, int64_t drain_ns, vla_request_rec* req_out,
+                               vla_lockstep_rec* ls_out, int ls_cap, int* n_ls_out);
 
 /*
  * Adaptive traffic controller (Section 4.2.2): robot-to-GPU assignment for a

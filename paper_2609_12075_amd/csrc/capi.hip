@@ -7,6 +7,7 @@
 #include <list>
 #include <map>
 #include <mutex>
+#include <set>
 
 #include "../../include/vla.h"
 #include "../../include/vla_debug.h"
@@ -60,6 +61,11 @@ constexpr int kMaxMaskedStreams = 3;
 
 std::mutex g_pool_mu;
 std::map<int, DevicePool> g_pools;
+
+// Models alive (created and not yet destroyed), so that vla_shutdown can
+// release them and vla_destroy_model ignores handles it already released.
+std::mutex g_models_mu;
+std::set<vla_model_s*> g_models;
 
 int device_cu_count(int dev) {
   hipDeviceProp_t p;
@@ -137,10 +143,13 @@ hipStream_t adit_stream(int dev, int count) { return pool_stream(dev, count <= 0
 void check_model(vla_model m) { VLA_REQUIRE(m != nullptr, "null model"); }
 
 // Split workspaces of the single-kernel test hooks: one per (device, kind),
-// allocated on first use and kept until the process ends.
+// allocated on first use and kept until vla_shutdown.
+std::mutex g_ws_mu;
+std::map<std::pair<int, int>, float*> g_ws;
+
 float* debug_ws(int kind, long floats) {
-  static std::mutex mu;
-  static std::map<std::pair<int, int>, float*> ws;
+  auto& mu = g_ws_mu;
+  auto& ws = g_ws;
   std::lock_guard<std::mutex> lk(mu);
   int dev = 0;
   VLA_HIP(hipGetDevice(&dev));
@@ -202,14 +211,64 @@ vla_status vla_create_model(const vla_config* cfg, const float* weights_host, si
       delete m;
       throw;
     }
+    {
+      std::lock_guard<std::mutex> lk(g_models_mu);
+      g_models.insert(m);
+    }
     *out = m;
   });
 }
 
 void vla_destroy_model(vla_model m) {
   if (!m) return;
+  {
+    std::lock_guard<std::mutex> lk(g_models_mu);
+    if (!g_models.erase(m)) return;     // already released by vla_shutdown
+  }
   try { m->destroy(); } catch (...) {}
   delete m;
+}
+
+void vla_shutdown(void) {
+  std::set<int> devices;
+  std::set<vla_model_s*> models;
+  {
+    std::lock_guard<std::mutex> lk(g_models_mu);
+    models.swap(g_models);
+  }
+  for (vla_model_s* m : models) {
+    devices.insert(m->device);
+    try { m->destroy(); } catch (...) {}
+    delete m;
+  }
+  std::lock_guard<std::mutex> lk(g_pool_mu);
+  for (auto& kv : g_pools) devices.insert(kv.first);
+  {
+    std::lock_guard<std::mutex> wl(g_ws_mu);
+    for (auto& kv : g_ws) devices.insert(kv.first.first);
+  }
+  int cur = -1;
+  const bool have_cur = hipGetDevice(&cur) == hipSuccess;
+  for (int d : devices) {
+    if (hipSetDevice(d) == hipSuccess) (void)hipDeviceSynchronize();
+  }
+  for (auto& kv : g_pools) {
+    if (hipSetDevice(kv.first) != hipSuccess) continue;
+    DevicePool& p = kv.second;
+    for (auto& s : p.vlm) (void)hipStreamDestroy(s.second);
+    for (auto& s : p.adit) (void)hipStreamDestroy(s.second);
+    for (hipEvent_t e : {p.ev_start, p.ev_v, p.ev_a})
+      if (e) (void)hipEventDestroy(e);
+  }
+  g_pools.clear();
+  {
+    std::lock_guard<std::mutex> wl(g_ws_mu);
+    for (auto& kv : g_ws) {
+      if (hipSetDevice(kv.first.first) == hipSuccess) (void)hipFree(kv.second);
+    }
+    g_ws.clear();
+  }
+  if (have_cur) (void)hipSetDevice(cur);
 }
 
 vla_status vla_set_graphs(vla_model m, int enabled) {

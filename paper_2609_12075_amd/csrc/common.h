@@ -235,3 +235,12 @@ void launch_scale_cols_bf16(void* W, long N, int K, int ldk, const float* g, hip
 // Debug probe: each workgroup writes its hardware placement (XCC id, SE id,
 // CU id) to out[block] as one word: xcc << 16 | se << 8 | cu.
 void launch_cu_probe(uint32_t* out, int blocks, int spin, hipStream_t s);
+
+// One segment of a batched copy: `bytes` bytes from src to dst (src NULL:
+// zero fill). Used by the serving scheduler to gather admitted requests'
+// inputs into a model's stage rows and to scatter finished action chunks.
+struct CopySeg { const void* src; void* dst; long long bytes; };
+// Copies n segments whose descriptors sit in device memory (segs), each cut
+// into chunks of kCopyChunk bytes; max_bytes bounds every segment's size.
+constexpr long long kCopyChunk = 65536;
+void launch_batched_copy(const CopySeg* segs, int n, long long max_bytes, hipStream_t s);

@@ -175,6 +175,30 @@ inline int grid_for(long n, int block = 256) {
 
 }  // namespace
 
+// Batched copy: block (x, y) copies chunk x of segment y. 16-byte vector
+// accesses when source, destination and size allow them, else 4-byte, else
+// single bytes; a null source writes zeros.
+__global__ void __launch_bounds__(256) batched_copy_kernel(const CopySeg* segs) {
+  const CopySeg sg = segs[blockIdx.y];
+  const long long off = (long long)blockIdx.x * kCopyChunk;
+  if (off >= sg.bytes) return;
+  const long long n = sg.bytes - off < kCopyChunk ? sg.bytes - off : kCopyChunk;
+  const char* src = (const char*)sg.src;
+  char* dst = (char*)sg.dst + off;
+  const uintptr_t al = (uintptr_t)dst | (uintptr_t)(src ? src + off : nullptr) | (uintptr_t)n;
+  if ((al & 15) == 0) {
+    uint4* d = (uint4*)dst;
+    const uint4* s4 = src ? (const uint4*)(src + off) : nullptr;
+    for (long long i = threadIdx.x; i < n / 16; i += blockDim.x) d[i] = s4 ? s4[i] : make_uint4(0, 0, 0, 0);
+  } else if ((al & 3) == 0) {
+    uint32_t* d = (uint32_t*)dst;
+    const uint32_t* s1 = src ? (const uint32_t*)(src + off) : nullptr;
+    for (long long i = threadIdx.x; i < n / 4; i += blockDim.x) d[i] = s1 ? s1[i] : 0u;
+  } else {
+    for (long long i = threadIdx.x; i < n; i += blockDim.x) dst[i] = src ? src[off + i] : (char)0;
+  }
+}
+
 void launch_norm(const NormArgs& a, hipStream_t s) {
   if (a.rows <= 0) return;
   if (a.d % 4 || a.ld_in % 4 || a.ld_out % 4 || a.d > 2048) throw VlaError{4, "norm: d, ld must be multiples of 4, d <= 2048"};
@@ -234,6 +258,13 @@ void launch_scale_cols_bf16(void* W, long N, int K, int ldk, const float* g, hip
 
 void launch_round_bf16_f32(const float* src, long n, float* dst, hipStream_t s) {
   hipLaunchKernelGGL(round_bf16_kernel, dim3(grid_for(n)), dim3(256), 0, s, src, n, dst);
+}
+
+void launch_batched_copy(const CopySeg* segs, int n, long long max_bytes, hipStream_t s) {
+  if (n <= 0 || max_bytes <= 0) return;
+  const long long chunks = (max_bytes + kCopyChunk - 1) / kCopyChunk;
+  VLA_REQUIRE(n <= 65535 && chunks <= (1LL << 31) - 1, "batched copy too large");
+  batched_copy_kernel<<<dim3((unsigned)chunks, (unsigned)n), 256, 0, s>>>(segs);
 }
 
 void launch_cu_probe(uint32_t* out, int blocks, int spin, hipStream_t s) {

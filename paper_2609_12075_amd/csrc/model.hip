@@ -452,12 +452,16 @@ void vla_model_s::init(const vla_config& c, const float* w, size_t n, int dev) {
 
 void vla_model_s::destroy() {
   DeviceGuard g(device);
+  // every launch of this model's graphs and kernels must have finished before
+  // the executables, the capture streams and the memory they use go away
+  (void)hipDeviceSynchronize();
   for (int st = 0; st < 2; ++st) {
     for (auto& kv : graph_cache[st]) (void)hipGraphExecDestroy(kv.second);
     graph_cache[st].clear();
+    graph_lru[st].clear();
     if (cap_stream[st]) (void)hipStreamDestroy(cap_stream[st]);
+    cap_stream[st] = nullptr;
   }
-  (void)hipDeviceSynchronize();
   for (void* p : allocs) (void)hipFree(p);
   allocs.clear();
 }

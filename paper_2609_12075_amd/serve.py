@@ -29,6 +29,15 @@ class _Cfg(ctypes.Structure):
                 ("max_batch", ctypes.c_int), ("policy", ctypes.c_int)]
 
 
+class _ReqIO(ctypes.Structure):
+    _fields_ = [("pixels", ctypes.c_void_p), ("text_ids", ctypes.c_void_p), ("state", ctypes.c_void_p),
+                ("noise", ctypes.c_void_p), ("actions_out", ctypes.c_void_p)]
+
+
+COMP_DTYPE = np.dtype([("id", np.int64), ("model", np.int32), ("met_slo", np.int32), ("t_arrival_ns", np.int64),
+                       ("t_vlm_start_ns", np.int64), ("t_done_ns", np.int64)])
+
+
 class _IO(ctypes.Structure):
     _fields_ = [("model", ctypes.c_void_p), ("pixels", ctypes.c_void_p), ("text_ids", ctypes.c_void_p),
                 ("state", ctypes.c_void_p), ("noise", ctypes.c_void_p), ("kv", ctypes.c_void_p * 2),
@@ -47,6 +56,16 @@ def _lib():
         L.vla_sched_set_mode.argtypes = [vp, ci]; L.vla_sched_set_mode.restype = ci
         L.vla_sched_run.argtypes = [vp, vp, vp, ci, i64, vp, vp, ci, ctypes.POINTER(ci)]
         L.vla_sched_run.restype = ci
+        L.vla_sched_set_gpu_online.argtypes = [vp, vp, vp, vp]; L.vla_sched_set_gpu_online.restype = ci
+        L.vla_sched_clock_ns.argtypes = [vp]; L.vla_sched_clock_ns.restype = i64
+        L.vla_sched_reset.argtypes = [vp]; L.vla_sched_reset.restype = ci
+        L.vla_sched_submit.argtypes = [vp, i64, ci, i64, vp]; L.vla_sched_submit.restype = ci
+        L.vla_sched_pending.argtypes = [vp]; L.vla_sched_pending.restype = ci
+        L.vla_sched_run_lockstep.argtypes = [vp, vp, ctypes.POINTER(ci)]; L.vla_sched_run_lockstep.restype = ci
+        L.vla_sched_wait_until.argtypes = [vp, i64]; L.vla_sched_wait_until.restype = ci
+        L.vla_sched_poll.argtypes = [vp, vp, ci]; L.vla_sched_poll.restype = ci
+        L.vla_sched_run_trace.argtypes = [vp, vp, vp, vp, ci, i64, vp, vp, ci, ctypes.POINTER(ci)]
+        L.vla_sched_run_trace.restype = ci
         L.vla_traffic_assign.argtypes = [ci, ci, vp, vp, vp, ctypes.c_longlong, vp, ctypes.POINTER(ctypes.c_longlong),
                                          ctypes.POINTER(ci)]
         L.vla_traffic_assign.restype = ci
@@ -79,7 +98,9 @@ class Scheduler:
         vla._check(_lib().vla_sched_create(ctypes.byref(cfg), ctypes.byref(h)))
         self.handle = h
         self._keep = []
+        self.online = False
         vla._check(_lib().vla_sched_set_mode(self.handle, MODES[mode]))
+        vla.register(self)
 
     def close(self):
         if getattr(self, "handle", None):
@@ -124,18 +145,70 @@ class Scheduler:
         self._keep.append((models, bufs))
         vla._check(_lib().vla_sched_set_gpu_executor(self.handle, ctypes.addressof(ios), vla._stream(join_stream)))
 
-    def run(self, arrivals: np.ndarray, drain_ns: int, ls_cap: int = 1 << 20):
-        """arrivals: structured array with t_ns (sorted) and model. Returns
-        (request records, lockstep records) as numpy structured arrays."""
+    def set_gpu_online(self, models: Sequence[vla.Model], join_stream=None):
+        """Online GPU executor: the library allocates max_batch stage rows per
+        model; requests bring their own device inputs (see submit)."""
+        hs = (ctypes.c_void_p * self.n_models)(*[m.handle.value for m in models])
+        st = (ctypes.c_int * self.n_models)(*[m.cfg.steps for m in models])
+        self._keep.append((models, join_stream))
+        vla._check(_lib().vla_sched_set_gpu_online(self.handle, hs, st, vla._stream(join_stream)))
+        self.online = True
+
+    @staticmethod
+    def request_io(pixels, text_ids, noise, actions_out, state=None) -> _ReqIO:
+        """Per-request device buffers: pixels [n_img,3,H,W] fp32, text_ids
+        [n_text] int32, noise and actions_out [horizon, action_dim] fp32,
+        state [state_dim] fp32 or None. Views of larger tensors are fine."""
+        return _ReqIO(vla._ptr(pixels), vla._ptr(text_ids), vla._ptr(state), vla._ptr(noise), vla._ptr(actions_out))
+
+    def clock_ns(self) -> int:
+        return int(_lib().vla_sched_clock_ns(self.handle))
+
+    def reset(self):
+        vla._check(_lib().vla_sched_reset(self.handle))
+
+    def submit(self, rid: int, model: int, t_arrival_ns: int, io: Optional[_ReqIO] = None):
+        vla._check(_lib().vla_sched_submit(self.handle, int(rid), int(model), int(t_arrival_ns),
+                                           ctypes.byref(io) if io is not None else None))
+
+    def pending(self) -> int:
+        return int(_lib().vla_sched_pending(self.handle))
+
+    def run_lockstep(self):
+        """One lockstep now; returns its record, or None when idle."""
+        rec = np.zeros(1, dtype=LS_DTYPE)
+        ran = ctypes.c_int(0)
+        vla._check(_lib().vla_sched_run_lockstep(self.handle, rec.ctypes.data, ctypes.byref(ran)))
+        return rec[0] if ran.value else None
+
+    def wait_until(self, t_ns: int):
+        vla._check(_lib().vla_sched_wait_until(self.handle, int(t_ns)))
+
+    def poll(self, cap: int = 4096) -> np.ndarray:
+        out = np.zeros(cap, dtype=COMP_DTYPE)
+        n = int(_lib().vla_sched_poll(self.handle, out.ctypes.data, cap))
+        return out[:n]
+
+    def run(self, arrivals: np.ndarray, drain_ns: int, ls_cap: int = 1 << 20, ios=None):
+        """arrivals: structured array with t_ns (sorted) and model. ios: array
+        of per-request inputs (request_io, one per arrival; required with the
+        online executor). Returns (request records, lockstep records) as numpy
+        structured arrays."""
         t = np.ascontiguousarray(arrivals["t_ns"], dtype=np.int64)
         mo = np.ascontiguousarray(arrivals["model"], dtype=np.int32)
         n = len(t)
         req = np.zeros(n, dtype=REQ_DTYPE)
         ls = np.zeros(ls_cap, dtype=LS_DTYPE)
         nls = ctypes.c_int(0)
-        vla._check(_lib().vla_sched_run(self.handle, t.ctypes.data if n else None, mo.ctypes.data if n else None, n,
-                                        int(drain_ns), req.ctypes.data if n else None, ls.ctypes.data, ls_cap,
-                                        ctypes.byref(nls)))
+        io_arr = None
+        if ios is not None:
+            assert len(ios) == n, "one request_io per arrival"
+            io_arr = (_ReqIO * n)(*ios)
+        vla._check(_lib().vla_sched_run_trace(self.handle, t.ctypes.data if n else None,
+                                              mo.ctypes.data if n else None,
+                                              ctypes.addressof(io_arr) if io_arr is not None else None, n,
+                                              int(drain_ns), req.ctypes.data if n else None, ls.ctypes.data, ls_cap,
+                                              ctypes.byref(nls)))
         return req, ls[:min(nls.value, ls_cap)]
 
 

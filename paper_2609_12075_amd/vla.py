@@ -8,8 +8,10 @@ is no fallback path.
 """
 from __future__ import annotations
 
+import atexit
 import ctypes
 import os
+import weakref
 from typing import Optional
 
 import numpy as np
@@ -23,7 +25,7 @@ VLA_OK, VLA_EINVAL, VLA_ENOMEM, VLA_EHIP, VLA_EUNSUPPORTED = range(5)
 
 # every exported symbol declared by include/vla.h and include/vla_debug.h
 EXPORTS = ["vla_weight_count", "vla_create_model", "vla_destroy_model", "vla_set_graphs", "vla_kv_bytes",
-           "vla_prefill", "vla_prefill_ex", "vla_denoise", "vla_step", "vla_last_error",
+           "vla_prefill", "vla_prefill_ex", "vla_denoise", "vla_step", "vla_last_error", "vla_shutdown",
            "vla_debug_gemm", "vla_debug_resid_norm", "vla_debug_gemm_rms", "vla_debug_resid_copy", "vla_debug_attention",
            "vla_debug_cu_probe", "vla_debug_replay_gemm"]
 
@@ -85,8 +87,54 @@ def lib():
         L.vla_debug_replay_gemm.argtypes = [vp, ci, ci, ci, vp, ctypes.POINTER(ctypes.c_double),
                                             ctypes.POINTER(ctypes.c_int)]
         L.vla_debug_replay_gemm.restype = ci
+        L.vla_shutdown.argtypes = []; L.vla_shutdown.restype = None
         _lib = L
+        # atexit handlers run last-registered-first: importing torch before
+        # registering puts this teardown ahead of torch's own
+        import torch  # noqa: F401
+        atexit.register(shutdown)
     return _lib
+
+
+# objects holding library resources (models, schedulers), closed by shutdown()
+_live = weakref.WeakSet()
+# non-blocking streams created by nonblocking_stream(), destroyed by shutdown()
+_streams = []
+
+
+def register(obj):
+    """Track an object with a close() method so shutdown() releases it."""
+    _live.add(obj)
+
+
+def shutdown():
+    """Orderly teardown before the runtime unloads: wait for the GPU, close
+    live schedulers and models, destroy the streams this module created, then
+    vla_shutdown() (stream pool, events, hook workspaces)."""
+    global _streams
+    if _lib is None:
+        return
+    try:
+        import torch
+        if torch.cuda.is_available() and torch.cuda.is_initialized():
+            torch.cuda.synchronize()
+    except Exception:
+        pass
+    for obj in sorted(list(_live), key=lambda o: 0 if hasattr(o, "n_models") else 1):
+        try:
+            obj.close()
+        except Exception:
+            pass
+    if _streams:
+        for dev, s in _streams:
+            try:
+                _hip.hipSetDevice(ctypes.c_int(dev))
+                _hip.hipStreamSynchronize(ctypes.c_void_p(s))
+                _hip.hipStreamDestroy(ctypes.c_void_p(s))
+            except Exception:
+                pass
+        _streams = []
+    _lib.vla_shutdown()
 
 
 def _check(status: int):
@@ -135,6 +183,7 @@ class Model:
         _check(lib().vla_create_model(ctypes.byref(s), w.ctypes.data, w.size, device, ctypes.byref(h)))
         self.handle = h
         self.device = device
+        register(self)
 
     def close(self):
         if getattr(self, "handle", None):
@@ -199,7 +248,7 @@ def nonblocking_stream(device: int = 0):
     """A new non-blocking HIP stream on `device`, as a torch ExternalStream
     (torch creates blocking streams only). Passed as vla_step's join stream it
     lets the unrestricted action half run on it directly (see vla_step). The
-    stream lives until the process ends."""
+    stream lives until shutdown() (registered to run at interpreter exit)."""
     global _hip
     import torch
     if _hip is None:
@@ -210,6 +259,7 @@ def nonblocking_stream(device: int = 0):
         s = ctypes.c_void_p()
         if _hip.hipStreamCreateWithFlags(ctypes.byref(s), ctypes.c_uint(1)) != 0:   # hipStreamNonBlocking
             raise VlaError(VLA_EHIP, "hipStreamCreateWithFlags failed")
+        _streams.append((device, s.value))
     finally:
         torch.cuda.set_device(prev)
     return torch.cuda.ExternalStream(s.value, device=torch.device("cuda", device))

@@ -4,7 +4,7 @@ import numpy as np
 import pytest
 
 from oracle import sched as REF
-from paper_2609_12075_amd import serve, synth
+from paper_2609_12075_amd import serve, synth, vla
 
 MS = 1_000_000
 
@@ -234,3 +234,56 @@ def test_variant_tables_reuse_the_architecture_profile():
     req, ls = run(items, [100.0] * 4, mb, vd * (MS // 20), drain=10 ** 10)
     assert (req["t_done_ns"] > 0).all()
     assert {int(x["vlm_model"]) for x in ls if x["vlm_batch"] > 0} == {0, 1, 2, 3}
+
+
+@pytest.mark.parametrize("seed", range(16))
+def test_online_calls_match_reference(seed):
+    """The online calls (submit as the clock passes each arrival, one
+    run_lockstep at a time, wait_until when idle, poll for completions)
+    reproduce the reference scheduler's locksteps and per-request times, with
+    completions identified by the ids given at submission."""
+    items, slo, mb, table, policy, overhead = _random_case(seed + 200)
+    mode = "monolithic" if seed % 5 == 4 else "lockstep"
+    rreq, rls = REF.simulate(items, slo, mb, table.tolist(), policy=policy, overhead_ns=overhead, mode=mode)
+    s = serve.Scheduler(slo, mb, policy, mode)
+    s.set_sim(table, overhead)
+    ids = [1000 + 7 * i for i in range(len(items))]
+    nxt, recs, comps = 0, [], []
+    while True:
+        now = s.clock_ns()
+        while nxt < len(items) and items[nxt][0] <= now:
+            s.submit(ids[nxt], items[nxt][1], items[nxt][0])
+            nxt += 1
+        if s.pending() == 0:
+            if nxt >= len(items):
+                break
+            s.wait_until(items[nxt][0])
+            continue
+        r = s.run_lockstep()
+        assert r is not None
+        recs.append(tuple(int(v) for v in r))
+        comps.extend(s.poll(3))          # small cap: the rest stays queued for the next poll
+    comps.extend(s.poll())
+    assert s.run_lockstep() is None and s.pending() == 0
+    assert recs == [tuple(b) for b in rls]
+    assert len(comps) == len(items)
+    by_id = {int(c["id"]): c for c in comps}
+    for i, b in enumerate(rreq):
+        c = by_id[ids[i]]
+        assert (int(c["t_arrival_ns"]), int(c["t_vlm_start_ns"]), int(c["t_done_ns"]), int(c["model"]),
+                int(c["met_slo"])) == (b["t_arrival"], b["t_vlm_start"], b["t_done"], b["model"], b["met"])
+    s.close()
+
+
+def test_online_submit_rejects_bad_requests():
+    s = serve.Scheduler([50.0, 80.0], 4)
+    s.set_sim(const_table(2, 4, MS), 0)
+    with pytest.raises(vla.VlaError):
+        s.submit(1, 2, 0)               # model index out of range
+    with pytest.raises(vla.VlaError):
+        s.submit(1, 0, -5)              # negative arrival
+    s.submit(1, 0, 0)
+    assert s.pending() == 1
+    s.reset()
+    assert s.pending() == 0 and s.clock_ns() == 0 and s.run_lockstep() is None
+    s.close()
