@@ -242,21 +242,40 @@ def weight_count(c: VLAConfig) -> int:
     return int(sum(int(np.prod(sh)) for _, sh, _ in weight_schema(c)))
 
 
-def make_weights(c: VLAConfig) -> np.ndarray:
-    """Flat fp32 parameter buffer in canonical order (seed 1000 + cfg.seed)."""
+def make_weights(c: VLAConfig, threads: int = 0) -> np.ndarray:
+    """Flat fp32 parameter buffer in canonical order (seed 1000 + cfg.seed).
+    Tensor i draws from its own stream, so tensors are filled by a thread
+    pool (numpy releases the GIL while it draws) with the same values as a
+    serial fill."""
+    import concurrent.futures as cf
+    import os
     sch = weight_schema(c)
     out = np.empty(weight_count(c), dtype=np.float32)
-    off = 0
-    for i, (_, shape, kind) in enumerate(sch):
+    offs, off = [], 0
+    for _, shape, _ in sch:
+        offs.append(off)
+        off += int(np.prod(shape))
+
+    def fill(i):
+        _, shape, kind = sch[i]
         n = int(np.prod(shape))
         rng = np.random.Generator(np.random.PCG64(
             np.random.SeedSequence(1000 + c.seed, spawn_key=(i,))))
-        v = out[off:off + n]
+        v = out[offs[i]:offs[i] + n]
         rng.standard_normal(out=v, dtype=np.float32)
         v *= np.float32(0.02)
         if kind == GAIN:
             v += np.float32(1.0)
-        off += n
+
+    nt = threads or min(16, os.cpu_count() or 1)
+    if nt <= 1 or out.size < (1 << 22):
+        for i in range(len(sch)):
+            fill(i)
+    else:
+        # largest tensors first so the pool stays busy to the end
+        order = sorted(range(len(sch)), key=lambda i: -int(np.prod(sch[i][1])))
+        with cf.ThreadPoolExecutor(max_workers=nt) as ex:
+            list(ex.map(fill, order))
     return out
 
 
