@@ -1,20 +1,37 @@
 #!/usr/bin/env python3
 """Benchmark of the VLA serving hot path on one MI355X.
 
-A step is one lockstep of the serving pipeline (paper Section 4.1.2): the VLM
-stage (patch embedding, LLM prefill writing the per-layer prefix KV) of batch
-k runs on a stream restricted to `--cu` compute units while the action stage
-(the flow-matching Euler loop) of batch k-1 runs on the unrestricted stream,
-both as replayed HIP graphs through the C ABI's vla_step. Each step therefore
-completes one batch of action chunks; `value` is action chunks per second over
-the timed steps, with every input resident in HBM.
+Default: the co-located serving workload, a pi0-shaped and a SmolVLA-shaped
+model sharing one GPU (robot i -> model i mod 2), Poisson requests at
+--rate Hz per robot, a --slo-ms deadline, earliest-SLO-first queues and
+power-of-two batches up to --serve-batch (paper Sections 4.1.2-4.1.3). The
+metric is the paper's robot-limit method (Section 4.2.2, Section 5.1): the
+largest robot count whose SLO attainment is >= 98 %, times the rate, in
+action chunks/s. It is found in three steps:
 
-Also reported: the stage times alone (VLM prefill ms, ADiT step ms), the
-per-chunk latency in the saturated pipeline against the model's SLO, a
-roofline entry for the dominant kernel (timed with HIP events on the stream it
-runs on), and the CPU oracle timed on a bounded sample of the same workload.
+1. profile every lockstep combination (VLM model, batch, action model,
+   batch) under each VLM CU restriction and keep the fastest restriction per
+   combination (the lookup table of Section 4.1.2);
+2. sweep the robot count on those durations in the simulated executor;
+3. serve in real time on the GPU through the online scheduler (every request
+   gathers its own robot's inputs into the stage rows and gets its chunk
+   scattered back) at the simulated limit, then one robot more or fewer until
+   the largest count with >= 98 % attainment is confirmed. ``value`` is that
+   GPU-validated count times the rate.
 
-    python bench.py [--steps K] [--warmup W] [--config smolvla] [--batch B] [--cu 256]
+A step (``--steps``/``--warmup``) is one lockstep of the saturated pipeline
+at the serving batch, alternating (pi0 VLM || SmolVLA action stage) and
+(SmolVLA VLM || pi0 action stage) at the table's CU restriction;
+``ms_per_step`` is their mean. Also reported: stage times alone, ADiT step
+ms and MFMA fractions, a roofline entry for the kernel with the most time in
+this workload (timed with HIP events on the stream it runs on), and the CPU
+oracle on a bounded sample of the same workload.
+
+Other modes: --lockstep (one model, saturated locksteps), --serve (studies:
+controls, policies, periodic traffic, traffic controller), --stages (stage
+times per config and batch), --counters (hardware counter passes).
+
+    python bench.py [--steps K] [--warmup W] [--rate 10] [--serve-batch 4]
 """
 import argparse
 import json
@@ -318,6 +335,347 @@ def stages_main(args):
                       "stages": out}), flush=True)
 
 
+def _layer_params(cfg, flat, dtype, prefixes):
+    """Oracle parameters (bf16-rounded for bf16 models) of the tensors whose
+    names start with one of `prefixes`, in `dtype`."""
+    import numpy as np
+    from oracle import vla as O
+    from paper_2609_12075_amd import synth
+    W = {}
+    for k, v in synth.weight_views(cfg, flat).items():
+        if k.startswith(prefixes):
+            src = O.bf16_round(v) if cfg.dtype == synth.DTYPE_BF16 else np.asarray(v, np.float32)
+            W[k] = src.astype(dtype)
+    return W
+
+
+def oracle_request_seconds(cfg, flat, dtype):
+    """Seconds the CPU oracle needs for one request of `cfg` (batch 1):
+    prefill and denoise, each from timed samples scaled by layer counts (one
+    ViT block per image, one full LLM block, one action-stage layer per Euler
+    step), so a pi0-shaped request costs a few seconds of CPU instead of a
+    minute. Inputs are seeded; the oracle's arithmetic does not depend on
+    their values."""
+    import numpy as np
+    from oracle import vla as O
+    from paper_2609_12075_amd import synth
+    rng = np.random.default_rng(0)
+    joint = cfg.head_kind == synth.HEAD_JOINT
+    pre_s = 0.0
+    if cfg.vit_layers > 0:
+        W = _layer_params(cfg, flat, dtype, ("vit.0.",))
+        x = rng.standard_normal((cfg.tokens_per_img, cfg.vit_d)).astype(dtype)
+        t = time.perf_counter()
+        O.vit_layer(cfg, W, 0, x)
+        pre_s += cfg.n_img * cfg.vit_layers * (time.perf_counter() - t)
+    W = _layer_params(cfg, flat, dtype, ("llm.0.",))
+    h = rng.standard_normal((cfg.prefix_len, cfg.llm_d)).astype(dtype)
+    t = time.perf_counter()
+    O.llm_layer(cfg, W, 0, h, np.arange(cfg.prefix_len))
+    pre_s += cfg.llm_layers * (time.perf_counter() - t)
+    one = cfg.with_(act_layers=1, llm_layers=1)
+    if joint:
+        W = _layer_params(cfg, flat, dtype, ("act.0.", "act.in", "act.t1", "act.t2", "act.lnf", "act.out"))
+        pre = {"k": [rng.standard_normal((cfg.n_kv, cfg.prefix_len, cfg.head_dim)).astype(dtype)],
+               "v": [rng.standard_normal((cfg.n_kv, cfg.prefix_len, cfg.head_dim)).astype(dtype)]}
+        fn = O.joint_velocity
+    else:
+        W = _layer_params(cfg, flat, dtype, ("dit.0.", "dit.t", "dit.ain", "dit.pos", "dit.modf", "dit.out"))
+        pre = {"kc": [rng.standard_normal((cfg.prefix_len, cfg.act_d)).astype(dtype)],
+               "vc": [rng.standard_normal((cfg.prefix_len, cfg.act_d)).astype(dtype)],
+               "state": rng.standard_normal(cfg.act_d).astype(dtype)}
+        fn = O.dit_velocity
+    x = rng.standard_normal((cfg.horizon, cfg.action_dim)).astype(dtype)
+    fn(one, W, pre, x, 1.0)
+    t = time.perf_counter()
+    fn(one, W, pre, x, 0.5)
+    den_s = cfg.steps * cfg.act_layers * (time.perf_counter() - t)
+    return pre_s, den_s
+
+
+def cpu_baseline_colocated(cfgs, flats, budget_s):
+    """The CPU oracle on the co-located workload: per model, seconds per
+    request (prefill, denoise) in fp64 (the parity precision) and fp32 with
+    all BLAS threads, and in fp64 on one core for the SmolVLA-shaped model;
+    plus one whole SmolVLA-shaped request end to end as a check of the
+    layer-scaled estimate. CPU chunks/s = 2 / (s_pi0 + s_smolvla) (robots
+    alternate between the two models)."""
+    import numpy as np
+    from oracle import vla as O
+    from paper_2609_12075_amd import synth
+    blas, threads = "unknown", os.cpu_count() or 1
+    try:
+        from threadpoolctl import threadpool_info, threadpool_limits
+        info = [i for i in threadpool_info() if i.get("user_api") == "blas"]
+        if info:
+            blas = f"{info[0].get('internal_api')} {info[0].get('version')} ({info[0].get('threading_layer', '')})"
+            threads = int(info[0].get("num_threads", threads))
+    except Exception:
+        threadpool_limits = None
+    cpu_model = "unknown"
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                cpu_model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    t0 = time.perf_counter()
+    # repeat the sampled timings (median of each) until about budget_s of CPU work
+    samples = {(c.name, d): [] for c in cfgs for d in ("f64", "f32")}
+    reps = 0
+    while reps < 1 or (time.perf_counter() - t0 < 0.7 * budget_s and reps < 9):
+        for c, f in zip(cfgs, flats):
+            for dname, dt in (("f64", np.float64), ("f32", np.float32)):
+                samples[(c.name, dname)].append(oracle_request_seconds(c, f, dt))
+        reps += 1
+    per = {}
+    for c in cfgs:
+        e = {}
+        for dname in ("f64", "f32"):
+            pre_s = float(np.median([x[0] for x in samples[(c.name, dname)]]))
+            den_s = float(np.median([x[1] for x in samples[(c.name, dname)]]))
+            e[dname] = {"prefill_s": round(pre_s, 3), "denoise_s": round(den_s, 3), "request_s": round(pre_s + den_s, 3)}
+        per[c.name] = e
+    single = None
+    smol = [(c, f) for c, f in zip(cfgs, flats) if c.name == "smolvla"]
+    if smol and threadpool_limits is not None:
+        c, f = smol[0]
+        with threadpool_limits(limits=1, user_api="blas"):
+            pre_s, den_s = oracle_request_seconds(c, f, np.float64)
+        single = {"model": c.name, "request_s": round(pre_s + den_s, 3), "cores": 1}
+    check = None
+    if smol:
+        c, f = smol[0]
+        W = O.params(c, f)
+        t = time.perf_counter()
+        O.run(c, W, synth.make_inputs(c, 1))
+        check = {"model": c.name, "measured_request_s": round(time.perf_counter() - t, 3),
+                 "estimated_request_s": per[c.name]["f64"]["request_s"]}
+        del W
+    el = time.perf_counter() - t0
+    tot = {d: sum(per[c.name][d]["request_s"] for c in cfgs) for d in ("f64", "f32")}
+    n = len(cfgs)
+    return {"value": round(n / tot["f64"], 5), "unit": "action chunks/s", "cores": threads, "kind": "oracle",
+            "sample": (f"co-located {' + '.join(c.name for c in cfgs)} at batch 1, numpy fp64 on {threads} BLAS "
+                       f"threads: one ViT block per image, one LLM block and one action-stage layer per model timed "
+                       f"(median of {reps}) and scaled by layer and Euler-step counts, plus one whole "
+                       f"SmolVLA-shaped request as a check; {el:.1f} s of CPU"),
+            "f32_value": round(n / tot["f32"], 5), "per_model_s": per,
+            "single_core": single, "whole_request_check": check, "cpu_model": cpu_model, "blas": blas,
+            "host_cpus": os.cpu_count()}
+
+
+def flops_per_request(c):
+    """(prefill, all Euler steps) algorithmic flops of one request."""
+    pre, step = stage_flops(c)
+    return pre, step * c.steps
+
+
+def colocated_main(args):
+    """The metric: action chunks/s at >= 98 % SLO attainment for the
+    co-located pi0-shaped + SmolVLA-shaped workload (see the module
+    docstring). Prints one JSON line."""
+    import numpy as np
+    import torch
+    from paper_2609_12075_amd import serve, synth, vla
+
+    names = args.serve_models.split(",")
+    mb, f, K = args.serve_batch, args.rate, args.steps
+    cfgs = [synth.CONFIGS[n].with_(max_batch=mb) for n in names]
+    slo = [args.slo_ms] * len(cfgs)
+    cus = [int(x) for x in args.serve_cus.split(",")]
+    t_all = time.perf_counter()
+    flats = [synth.make_weights(c) for c in cfgs]
+    models = [vla.Model(c, w, device=0) for c, w in zip(cfgs, flats)]
+    log(f"[bench] models {names} (max_batch {mb}) created in {time.perf_counter() - t_all:.1f} s")
+    bufs = serve.alloc_io(models, mb)
+    for m, b in zip(models, bufs):          # both hand-off slots hold real prefixes
+        m.prefill(mb, b["pixels"], b["text_ids"], b["kv0"], state=b.get("state"))
+        m.prefill(mb, b["pixels"], b["text_ids"], b["kv1"], state=b.get("state"))
+    torch.cuda.synchronize()
+    js = vla.nonblocking_stream(0)          # join stream of every lockstep
+
+    # ---- 1. lockstep table under each VLM CU restriction -> lookup table
+    t0 = time.perf_counter()
+    prof = serve.profile_locksteps(models, bufs, mb, cus, reps=3, log=log, join_stream=js)
+    cu_table, dur_lut = serve.best_cu_table(prof, cus)
+    log(f"[bench] profiled {prof.size} lockstep entries in {time.perf_counter() - t0:.1f} s")
+    nb = serve.n_buckets(mb)
+    full = nb - 1                            # bucket of the serving batch
+
+    # ---- timed steps: saturated locksteps alternating the two model pairings
+    def lockstep(k):
+        mv, ma = k % 2, (k + 1) % 2
+        xv, xa = bufs[mv], bufs[ma]
+        vla.step(models[mv], mb, xv["pixels"], xv["text_ids"], xv["kv0"], models[ma], mb, xa["kv1"], xa["noise"],
+                 cfgs[ma].steps, xa["act1"], vlm_cu_count=int(cu_table[mv, full, ma, full]), state=xv.get("state"),
+                 join_stream=js)
+    for k in range(args.warmup):
+        lockstep(k)
+    torch.cuda.synchronize()
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(K + 1)]
+    t_wall = time.perf_counter()
+    evs[0].record(js)
+    for i in range(K):
+        lockstep(args.warmup + i)
+        evs[i + 1].record(js)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_wall
+    ms_per_step = evs[0].elapsed_time(evs[K]) / K
+    log(f"[bench] {K} saturated locksteps: {ms_per_step:.3f} ms/step (wall {wall * 1e3 / K:.3f}), "
+        f"{mb * 1e3 / ms_per_step:.1f} chunks/s")
+
+    # ---- 2. simulated sweep on the table
+    robots = list(range(1, args.serve_max_robots + 1))
+    rows, r_sim = serve.sweep_robots(dur_lut, slo, mb, robots, f, args.serve_seconds, args.serve_epochs)
+    log(f"[bench] simulated: {r_sim} robots at >= 98 % ({args.serve_epochs} x {args.serve_seconds:.0f} s traces)")
+
+    # ---- 3. real-time validation on the GPU (online executor, per-robot inputs)
+    sch = serve.Scheduler(slo, mb, "esf")
+    sch.set_gpu_online(models, join_stream=js)
+    sch.set_cu(256, cu_table)
+    n_rob_max = args.serve_max_robots + 2
+    rob_in = []
+    for i, c in enumerate(cfgs):
+        n = (n_rob_max + len(cfgs) - 1 - i) // len(cfgs)
+        inp = synth.make_inputs(c, n, first_row=100)
+        rob_in.append({k: torch.from_numpy(v).to("cuda:0") for k, v in inp.items()})
+
+    def validate(R, epoch):
+        arr = synth.poisson_arrivals(R, f, args.validate_seconds, epoch=epoch, n_models=len(cfgs))
+        outs = [torch.full((int((arr["model"] == i).sum()), c.horizon, c.action_dim), float("nan"), device="cuda:0")
+                for i, c in enumerate(cfgs)]
+        cnt = [0] * len(cfgs)
+        ios = []
+        for j in range(len(arr)):
+            mi, r = int(arr["model"][j]), int(arr["robot"][j]) // len(cfgs)
+            d = rob_in[mi]
+            ios.append(serve.Scheduler.request_io(d["pixels"][r], d["text_ids"][r], d["noise"][r], outs[mi][cnt[mi]],
+                                                  d["state"][r] if "state" in d else None))
+            cnt[mi] += 1
+        torch.cuda.synchronize()
+        req, ls = sch.run(arr, drain_ns=int(1e9), ios=ios)
+        done = req["t_done_ns"] >= 0
+        finite = all(bool(torch.isfinite(o).all()) for o, c in zip(outs, cnt) if c) if done.all() else None
+        dur = (ls["t_end_ns"] - ls["t_start_ns"]) / 1e6
+        rec = {"robots": int(R), "requests": int(len(req)), "attainment": round(serve.attainment(req), 4),
+               "p99_ms": round(serve.p99_ms(req), 2), "locksteps": int(len(ls)),
+               "lockstep_ms_mean": round(float(dur.mean()), 3) if len(dur) else None,
+               "outputs_finite": finite, "seconds": args.validate_seconds}
+        log(f"[bench] GPU R={R}: attainment {rec['attainment']:.4f}, p99 {rec['p99_ms']} ms, "
+            f"{rec['requests']} requests, {rec['locksteps']} locksteps")
+        return rec
+
+    t0 = time.perf_counter()
+    checks = []
+    R = max(1, min(r_sim, args.serve_max_robots))
+    rec = validate(R, 100)
+    checks.append(rec)
+    ok = rec["attainment"] >= 0.98
+    best = R if ok else 0
+    while ok and R < args.serve_max_robots:             # one more robot
+        R += 1
+        rec = validate(R, 100 + R)
+        checks.append(rec)
+        ok = rec["attainment"] >= 0.98
+        if ok:
+            best = R
+    R = checks[0]["robots"]
+    while best == 0 and R > 1:                          # or fewer, until one passes
+        R -= 1
+        rec = validate(R, 100 + R)
+        checks.append(rec)
+        if rec["attainment"] >= 0.98:
+            best = R
+    sch.close()
+    value = best * f
+    log(f"[bench] GPU-validated: {best} robots at >= 98 % -> {value} action chunks/s "
+        f"({time.perf_counter() - t0:.1f} s of validation)")
+
+    # ---- stage times alone at the serving batch (table entries with one half empty, unrestricted)
+    ki = cus.index(256) if 256 in cus else len(cus) - 1
+    stages = {}
+    for i, c in enumerate(cfgs):
+        pre_ms = prof[ki, i, full, 0, 0] / 1e6
+        den_ms = prof[ki, 0, 0, i, full] / 1e6
+        pf, df = flops_per_request(c)
+        stages[c.name] = {"batch": mb, "prefill_ms": round(pre_ms, 3), "denoise_ms": round(den_ms, 3),
+                          "adit_step_ms": round(den_ms / c.steps, 4),
+                          "prefill_mfma_frac": round(mb * pf / (pre_ms * 1e-3) / 1e12 / PEAK["bf16"], 4),
+                          "adit_mfma_frac": round(mb * df / (den_ms * 1e-3) / 1e12 / PEAK["bf16"], 4)}
+
+    # ---- roofline: the replayable projection with the most time per served pair of batches
+    kern = {}
+    for i, (c, m) in enumerate(zip(cfgs, models)):
+        for which in (0, 1, 2, 3, 4):
+            if which == 4 and c.vit_layers == 0:
+                continue
+            m.replay_gemm(which, mb, 3, stream=js)
+            torch.cuda.synchronize()
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(js)
+            flops, plan = m.replay_gemm(which, mb, args.roofline_iters, stream=js)
+            b.record(js)
+            torch.cuda.synchronize()
+            us = a.elapsed_time(b) * 1e3 / args.roofline_iters
+            joint = c.head_kind == synth.HEAD_JOINT
+            n_launch = {0: c.llm_layers - (1 if joint else 0), 1: c.llm_layers - (1 if joint else 0),
+                        2: c.act_layers * c.steps, 3: c.act_layers * c.steps, 4: c.vit_layers}[which]
+            kern[(c.name, which)] = {"flops": flops, "us": us, "plan": plan, "launches": n_launch,
+                                     "symbol": vla.Model.kernel_symbol(plan)}
+            log(f"[bench] kernel {c.name} {GEMM_NAMES[which]}: {us:.2f} us/launch, {flops / us / 1e6:.1f} TFLOP/s, "
+                f"{n_launch} launches per batch, plan {plan}")
+    dom = max(kern, key=lambda k: kern[k]["us"] * kern[k]["launches"])
+    kd = kern[dom]
+    achieved = kd["flops"] / kd["us"] / 1e6
+    traffic = None
+    tf = os.path.join(ROOT, "profiles", "traffic.json")
+    if os.path.exists(tf):
+        from paper_2609_12075_amd import profsum
+        trec = json.load(open(tf)).get(f"{dom[0]}:B{mb}:{kd['symbol']}")
+        if trec and trec.get("source_hash") == profsum.source_hash():
+            traffic = trec["traffic_bytes"]
+    roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK["bf16"], "unit": "TFLOP/s",
+                "frac": round(achieved / PEAK["bf16"], 4), "traffic": traffic,
+                "kernel": f"{dom[0]}-shaped {GEMM_NAMES[dom[1]]}", "kernel_symbol": kd["symbol"],
+                "flops_per_launch": kd["flops"], "us_per_launch": round(kd["us"], 3),
+                "launches_per_batch": kd["launches"], "batch": mb}
+
+    out = {
+        "metric": METRIC, "value": float(value), "unit": "action chunks/s", "n_gpus": 1, "steps": K,
+        "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16",
+        "data": ("synthetic: seeded Poisson robot traffic, per-robot U[0,1) pixels, U[0,1000) text ids, N(0,1) "
+                 "noise; random-init N(0,0.02) weights"),
+        "config": {"workload": "co-located " + " + ".join(f"{n}-shaped" for n in names) +
+                               f", Poisson {f:g} Hz per robot, {args.slo_ms:g} ms SLO, robots at >= 98 % attainment",
+                   "models": names, "rate_hz": f, "slo_ms": args.slo_ms, "max_batch": mb, "policy": "esf",
+                   "vlm_cu_candidates": cus, "parallelism": "single GPU, two streams (VLM CU-restricted)"},
+        "robots_at_98": best, "gpu_validation": checks,
+        "robots_at_98_sim": r_sim, "sim": {"epochs": args.serve_epochs, "trace_s": args.serve_seconds,
+                                           "sweep": rows},
+        "saturated_lockstep_chunks_per_s": round(mb * 1e3 / ms_per_step, 2),
+        "stages": stages,
+        "adit_step_ms": {n: stages[n]["adit_step_ms"] for n in stages},
+        "cu_table": cu_table.tolist(), "lockstep_ms_lut": (dur_lut / 1e6).round(3).tolist(),
+        "roofline": roofline,
+        "kernels": {f"{k[0]}:{GEMM_NAMES[k[1]]}": {"us": round(v["us"], 3), "launches_per_batch": v["launches"],
+                                                    "tflops": round(v["flops"] / v["us"] / 1e6, 2),
+                                                    "mfma_frac": round(v["flops"] / v["us"] / 1e6 / PEAK["bf16"], 4),
+                                                    "symbol": v["symbol"]}
+                    for k, v in kern.items()},
+    }
+    for m in models:
+        m.close()
+    torch.cuda.empty_cache()
+    if not args.no_cpu_baseline:
+        log("[bench] CPU oracle baseline")
+        out["cpu_baseline"] = cpu_baseline_colocated(cfgs, flats, args.cpu_seconds)
+    out["bench_wall_s"] = round(time.perf_counter() - t_all, 1)
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -328,7 +686,7 @@ def main():
     ap.add_argument("--cu", type=int, default=0,
                     help="compute units the VLM stream may use (multiple of 8); 0: the fastest of --cu-candidates, "
                          "profiled before the timed steps")
-    ap.add_argument("--cu-candidates", default="256,224,192,160,128,96,64,32",
+    ap.add_argument("--cu-candidates", default="256,192,128,64",
                     help="VLM CU counts to profile (multiples of 32 keep every shader engine equally populated)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -336,7 +694,10 @@ def main():
     ap.add_argument("--copy-probe", action="store_true", help="also run a 256 MiB device copy (counter scaling)")
     ap.add_argument("--counters", action="store_true", help="launch only the roofline kernel and a copy (PMC passes)")
     ap.add_argument("--which", type=int, default=2, help="projection for --counters (see vla_debug.h)")
-    ap.add_argument("--serve", action="store_true", help="co-located serving sweep instead of the lockstep bench")
+    ap.add_argument("--lockstep", action="store_true",
+                    help="one model's saturated locksteps (--config, --batch, --cu) instead of the serving metric")
+    ap.add_argument("--rate", type=float, default=10.0, help="requests per second per robot (default workload)")
+    ap.add_argument("--serve", action="store_true", help="co-located serving studies (controls, policies, traffic)")
     ap.add_argument("--serve-models", default="pi0,smolvla")
     ap.add_argument("--serve-batch", type=int, default=4)
     ap.add_argument("--serve-cus", default="64,128,192,256")
@@ -346,7 +707,7 @@ def main():
     ap.add_argument("--serve-epochs", type=int, default=5)
     ap.add_argument("--serve-no-validate", action="store_true")
     ap.add_argument("--serve-variants", type=int, default=2, help="fine-tuned variants per architecture in the co-location study")
-    ap.add_argument("--validate-seconds", type=float, default=8.0)
+    ap.add_argument("--validate-seconds", type=float, default=20.0)
     ap.add_argument("--slo-ms", type=float, default=100.0)
     ap.add_argument("--stages", action="store_true", help="stage times per config and batch instead of the lockstep bench")
     ap.add_argument("--stage-configs", default="tiny,smolvla,pi0,gr00t")
@@ -368,6 +729,9 @@ def main():
         return
     if args.stages:
         stages_main(args)
+        return
+    if not args.lockstep:
+        colocated_main(args)
         return
 
     import numpy as np

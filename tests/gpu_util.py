@@ -76,3 +76,32 @@ def rel_l2(a, b):
 
 def oracle_run(cfg, inputs, steps=None, rows=None):
     return O.run(cfg, oracle_params(cfg), inputs, steps=steps, rows=rows)
+
+
+def check_chunk(got, ref, noise, tol, what=""):
+    """Assert the parity bounds on action chunks [.., H, A]:
+    rel-L2 of the actions and of the displacement (actions - noise; the
+    noise itself is exact and would dilute errors) within tol, and no element
+    off by more than 5*tol times the RMS of the reference displacement.
+    Returns (actions rel-L2, displacement rel-L2, max element error / RMS)."""
+    got = np.asarray(got, np.float64)
+    ref = np.asarray(ref, np.float64)
+    noise = np.asarray(noise, np.float64)
+    assert np.isfinite(got).all(), what
+    r = rel_l2(got, ref)
+    rd = rel_l2(got - noise, ref - noise)
+    rms = float(np.sqrt(np.mean((ref - noise) ** 2)))
+    me = float(np.abs(got - ref).max()) / rms
+    log(f"[parity] {what}: actions rel-L2 {r:.3e}, displacement rel-L2 {rd:.3e}, max elem err / rms {me:.3e}")
+    assert r <= tol, (what, r)
+    assert rd <= tol, (what, rd)
+    assert me <= 5 * tol, (what, me)
+    return r, rd, me
+
+
+def drop_model(cfg):
+    """Destroy a cached model (and forget its parameters) to free memory."""
+    m = _models.pop(cfg, None)
+    if m is not None:
+        m.close()
+    _weights.pop(cfg, None)
