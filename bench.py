@@ -4,7 +4,8 @@
 Default: the co-located serving workload, a pi0-shaped and a SmolVLA-shaped
 model sharing one GPU (robot i -> model i mod 2), Poisson requests at
 --rate Hz per robot, a --slo-ms deadline, earliest-SLO-first queues and
-power-of-two batches up to --serve-batch (paper Sections 4.1.2-4.1.3). The
+power-of-two batches up to a cap of 2, 4 or 8 (--serve-batches; paper
+Sections 4.1.2-4.1.3). The
 metric is the paper's robot-limit method (Section 4.2.2, Section 5.1): the
 largest robot count whose SLO attainment is >= 98 %, times the rate, in
 action chunks/s. It is found in three steps:
@@ -12,7 +13,8 @@ action chunks/s. It is found in three steps:
 1. profile every lockstep combination (VLM model, batch, action model,
    batch) under each VLM CU restriction and keep the fastest restriction per
    combination (the lookup table of Section 4.1.2);
-2. sweep the robot count on those durations in the simulated executor;
+2. sweep the robot count on those durations in the simulated executor, for
+   each batch cap, and keep the cap that sustains the most robots;
 3. serve in real time on the GPU through the online scheduler (every request
    gathers its own robot's inputs into the stage rows and gets its chunk
    scattered back) at the simulated limit, then one robot more or fewer until
@@ -257,9 +259,10 @@ def stage_flops(c) -> tuple:
     joint = c.head_kind == synth.HEAD_JOINT
     pre = 0.0
     if c.vit_layers > 0:
-        d, f, Ti = c.vit_d, c.vit_mlp, c.n_img * T
-        pre += c.vit_layers * (2 * Ti * d * 3 * d + 4 * c.n_img * d * T * T + 2 * Ti * d * d + 2 * 2 * Ti * d * f)
-        pre += 2 * Ti * d * D
+        Tv = c.patch_tokens                      # the encoder's sequence per image
+        d, f, Ti = c.vit_d, c.vit_mlp, c.n_img * Tv
+        pre += c.vit_layers * (2 * Ti * d * 3 * d + 4 * c.n_img * d * Tv * Tv + 2 * Ti * d * d + 2 * 2 * Ti * d * f)
+        pre += 2 * (c.n_img * T) * (d * c.pix_shuffle ** 2) * D
     full = c.llm_layers - (1 if joint else 0)
     pre += full * (2 * P * D * (Hq + 2 * Hk) + 4 * c.n_q * hd * P * P + 2 * P * Hq * D + 2 * P * D * 2 * F + 2 * P * F * D)
     if joint:
@@ -481,26 +484,44 @@ def colocated_main(args):
     from paper_2609_12075_amd import serve, synth, vla
 
     names = args.serve_models.split(",")
-    mb, f, K = args.serve_batch, args.rate, args.steps
-    cfgs = [synth.CONFIGS[n].with_(max_batch=mb) for n in names]
+    f, K = args.rate, args.steps
+    mbs = sorted(int(x) for x in args.serve_batches.split(","))
+    mb_prof = mbs[-1]
+    cfgs = [synth.CONFIGS[n].with_(max_batch=mb_prof) for n in names]
     slo = [args.slo_ms] * len(cfgs)
     cus = [int(x) for x in args.serve_cus.split(",")]
     t_all = time.perf_counter()
     flats = [synth.make_weights(c) for c in cfgs]
     models = [vla.Model(c, w, device=0) for c, w in zip(cfgs, flats)]
-    log(f"[bench] models {names} (max_batch {mb}) created in {time.perf_counter() - t_all:.1f} s")
-    bufs = serve.alloc_io(models, mb)
+    log(f"[bench] models {names} (max_batch {mb_prof}) created in {time.perf_counter() - t_all:.1f} s")
+    bufs = serve.alloc_io(models, mb_prof)
     for m, b in zip(models, bufs):          # both hand-off slots hold real prefixes
-        m.prefill(mb, b["pixels"], b["text_ids"], b["kv0"], state=b.get("state"))
-        m.prefill(mb, b["pixels"], b["text_ids"], b["kv1"], state=b.get("state"))
+        m.prefill(mb_prof, b["pixels"], b["text_ids"], b["kv0"], state=b.get("state"))
+        m.prefill(mb_prof, b["pixels"], b["text_ids"], b["kv1"], state=b.get("state"))
     torch.cuda.synchronize()
     js = vla.nonblocking_stream(0)          # join stream of every lockstep
 
-    # ---- 1. lockstep table under each VLM CU restriction -> lookup table
+    # ---- 1. lockstep table under each VLM CU restriction, profiled once at the
+    # largest batch cap; a smaller cap's table is the leading buckets of it
     t0 = time.perf_counter()
-    prof = serve.profile_locksteps(models, bufs, mb, cus, reps=3, log=log, join_stream=js)
-    cu_table, dur_lut = serve.best_cu_table(prof, cus)
-    log(f"[bench] profiled {prof.size} lockstep entries in {time.perf_counter() - t0:.1f} s")
+    prof_all = serve.profile_locksteps(models, bufs, mb_prof, cus, reps=3, log=log, join_stream=js)
+    log(f"[bench] profiled {prof_all.size} lockstep entries in {time.perf_counter() - t0:.1f} s")
+
+    # ---- 2. simulated sweep per batch cap (max_batch of the scheduler)
+    robots = list(range(1, args.serve_max_robots + 1))
+    by_mb = {}
+    for mbx in mbs:
+        nbx = serve.n_buckets(mbx)
+        sub = np.ascontiguousarray(prof_all[:, :, :nbx, :, :nbx])
+        ct, dl = serve.best_cu_table(sub, cus)
+        rows_x, r_x = serve.sweep_robots(dl, slo, mbx, robots, f, args.serve_seconds, args.serve_epochs)
+        by_mb[mbx] = {"robots_at_98_sim": r_x, "cu_table": ct, "dur": dl, "sub": sub, "sweep": rows_x}
+        log(f"[bench] max_batch {mbx}: simulated {r_x} robots at >= 98 % "
+            f"({args.serve_epochs} x {args.serve_seconds:.0f} s traces)")
+    mb = max(mbs, key=lambda x: (by_mb[x]["robots_at_98_sim"], -x))
+    prof, cu_table, dur_lut = by_mb[mb]["sub"], by_mb[mb]["cu_table"], by_mb[mb]["dur"]
+    rows, r_sim = by_mb[mb]["sweep"], by_mb[mb]["robots_at_98_sim"]
+    log(f"[bench] serving with max_batch {mb}")
     nb = serve.n_buckets(mb)
     full = nb - 1                            # bucket of the serving batch
 
@@ -525,11 +546,6 @@ def colocated_main(args):
     ms_per_step = evs[0].elapsed_time(evs[K]) / K
     log(f"[bench] {K} saturated locksteps: {ms_per_step:.3f} ms/step (wall {wall * 1e3 / K:.3f}), "
         f"{mb * 1e3 / ms_per_step:.1f} chunks/s")
-
-    # ---- 2. simulated sweep on the table
-    robots = list(range(1, args.serve_max_robots + 1))
-    rows, r_sim = serve.sweep_robots(dur_lut, slo, mb, robots, f, args.serve_seconds, args.serve_epochs)
-    log(f"[bench] simulated: {r_sim} robots at >= 98 % ({args.serve_epochs} x {args.serve_seconds:.0f} s traces)")
 
     # ---- 3. real-time validation on the GPU (online executor, per-robot inputs)
     sch = serve.Scheduler(slo, mb, "esf")
@@ -655,6 +671,7 @@ def colocated_main(args):
         "robots_at_98": best, "gpu_validation": checks,
         "robots_at_98_sim": r_sim, "sim": {"epochs": args.serve_epochs, "trace_s": args.serve_seconds,
                                            "sweep": rows},
+        "robots_at_98_sim_by_max_batch": {str(x): by_mb[x]["robots_at_98_sim"] for x in mbs},
         "saturated_lockstep_chunks_per_s": round(mb * 1e3 / ms_per_step, 2),
         "stages": stages,
         "adit_step_ms": {n: stages[n]["adit_step_ms"] for n in stages},
@@ -699,7 +716,9 @@ def main():
     ap.add_argument("--rate", type=float, default=10.0, help="requests per second per robot (default workload)")
     ap.add_argument("--serve", action="store_true", help="co-located serving studies (controls, policies, traffic)")
     ap.add_argument("--serve-models", default="pi0,smolvla")
-    ap.add_argument("--serve-batch", type=int, default=4)
+    ap.add_argument("--serve-batch", type=int, default=4, help="batch cap of the --serve studies")
+    ap.add_argument("--serve-batches", default="2,4,8",
+                    help="batch caps the default workload tries (simulated); the best is validated on the GPU")
     ap.add_argument("--serve-cus", default="64,128,192,256")
     ap.add_argument("--serve-rates", default="10,20,30")
     ap.add_argument("--serve-max-robots", type=int, default=32)
@@ -710,7 +729,7 @@ def main():
     ap.add_argument("--validate-seconds", type=float, default=20.0)
     ap.add_argument("--slo-ms", type=float, default=100.0)
     ap.add_argument("--stages", action="store_true", help="stage times per config and batch instead of the lockstep bench")
-    ap.add_argument("--stage-configs", default="tiny,smolvla,pi0,gr00t")
+    ap.add_argument("--stage-configs", default="tiny,smolvla,smolvla_vit,pi0,gr00t")
     ap.add_argument("--stage-batches", default="1,4,16")
     ap.add_argument("--stage-reps", type=int, default=200)
     ap.add_argument("--stage-warmup", type=int, default=20)

@@ -76,6 +76,9 @@ enum { VLA_HEAD_JOINT = 0, VLA_HEAD_DIT = 1 };
  *    action tokens], cross-attention to the projected final LLM states, and a
  *    tanh-GELU MLP of act_mlp; time enters through a sinusoid of width
  *    time_dim and an MLP.
+ *    With pix_shuffle = s > 1 the image contributes (img_hw/patch/s)^2
+ *    tokens to the prefix (P counts these), the ViT still runs over all
+ *    (img_hw/patch)^2 patch tokens, and the position table has that many rows.
  *  - horizon actions of action_dim per chunk; state_dim robot state (DiT).
  *  - max_batch: the largest batch any call may use (workspaces are sized for
  *    it). norm_eps applies to every RMSNorm / LayerNorm.
@@ -91,6 +94,11 @@ typedef struct {
   int horizon, action_dim, state_dim, time_dim;
   int max_batch;
   float rope_base, norm_eps;
+  int pix_shuffle;     /* s: after the ViT's final LayerNorm, each s x s block of
+                          patch tokens (raster order) is merged into one token of
+                          width s*s*vit_d (block rows then columns, channels
+                          innermost) before the projection to llm_d; 0 or 1: none.
+                          s > 1 needs vit_layers > 0 and s | img_hw/patch */
 } vla_config;
 
 /* Number of fp32 values the parameter buffer of this shape holds, 0 if the
@@ -116,7 +124,8 @@ vla_status vla_set_graphs(vla_model m, int enabled);
  * Bytes of the VLM -> action-stage hand-off for `batch` requests (0 on a bad
  * argument). Layout, element type = the model dtype:
  *  - VLA_HEAD_JOINT: the prefix KV cache [llm_layers][2][batch][n_kv][P][head_dim],
- *    index 0 = keys after RoPE, 1 = values; P = n_img*(img_hw/patch)^2 + n_text.
+ *    index 0 = keys after RoPE, 1 = values; P = n_img*(img_hw/patch/s)^2 + n_text
+ *    (s = pix_shuffle, 1 when unset).
  *  - VLA_HEAD_DIT: cross-attention keys/values [batch][P][act_layers][2][act_d]
  *    followed by the embedded state token [batch][act_d].
  */

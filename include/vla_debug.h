@@ -81,10 +81,12 @@ vla_status vla_debug_attention(int B, int Hq, int Hkv, int Lq, int hd, int et, c
  * mask counted from the top when from_top != 0). Each workgroup sleeps
  * `spin` x 64 cycles-ish and writes out[2*i] = HW_ID, out[2*i+1] = XCC_ID
  * hardware register words. out: device uint32 [2 * blocks]. The join stream
- * waits for the probe.
+ * waits for the probe. via_graph != 0: the launch is captured into a graph on
+ * an unrestricted stream and the graph replayed on the restricted stream (as
+ * vla_step replays the stages); the call then waits for the replay.
  */
-vla_status vla_debug_cu_probe(int device, int cu_count, int from_top, int blocks, int spin, uint32_t* out,
-                              hipStream_t join);
+vla_status vla_debug_cu_probe(int device, int cu_count, int from_top, int blocks, int spin, int via_graph,
+                              uint32_t* out, hipStream_t join);
 
 /*
  * Enqueue `iters` launches of one projection of a model's stage, exactly as

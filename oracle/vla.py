@@ -155,6 +155,16 @@ def patchify(img, p):
     return t.transpose(1, 3, 0, 2, 4).reshape((h // p) * (w // p), c * p * p)
 
 
+def pixel_shuffle(x, g, s):
+    """Merge s x s blocks of a g x g token grid (tokens in raster order,
+    x [g*g, d]) into (g/s)^2 tokens of width s*s*d: output token I*(g/s) + J
+    (raster order over the blocks) concatenates the block's tokens
+    (s*I + di, s*J + dj) in row-major (di, dj) order, channels innermost."""
+    d = x.shape[-1]
+    t = x.reshape(g // s, s, g // s, s, d)            # I, di, J, dj, c
+    return t.transpose(0, 2, 1, 3, 4).reshape((g // s) ** 2, s * s * d)
+
+
 def heads(x, n, hd):
     """[L, n*hd] -> [n, L, hd]."""
     return x.reshape(x.shape[0], n, hd).transpose(1, 0, 2)
@@ -183,7 +193,10 @@ def vit_layer(cfg, W, l, x):
 
 
 def image_tokens(cfg, W, pixels_row):
-    """pixels [n_img, 3, H, W] -> image tokens [n_img*T, llm_d]."""
+    """pixels [n_img, 3, H, W] -> image tokens [n_img*T, llm_d]: per image,
+    patch embedding + position table, the ViT blocks, the final LayerNorm,
+    the s x s token merge when the model has one, and the projection to the
+    LLM width."""
     dt = W["patch.w"].dtype
     toks = []
     for i in range(cfg.n_img):
@@ -191,7 +204,10 @@ def image_tokens(cfg, W, pixels_row):
         if cfg.vit_layers > 0:
             for l in range(cfg.vit_layers):
                 x = vit_layer(cfg, W, l, x)
-            x = layernorm(x, W["vit.lnf.g"], W["vit.lnf.b"], cfg.norm_eps) @ W["vit.proj.w"] + W["vit.proj.b"]
+            x = layernorm(x, W["vit.lnf.g"], W["vit.lnf.b"], cfg.norm_eps)
+            if cfg.pix_shuffle > 1:
+                x = pixel_shuffle(x, cfg.patch_grid, cfg.pix_shuffle)
+            x = x @ W["vit.proj.w"] + W["vit.proj.b"]
         toks.append(x)
     return np.concatenate(toks, axis=0)
 

@@ -36,13 +36,13 @@ static vla_status guarded(F&& f) {
   }
 }
 
-// ---------------------------------------------------------------- stream pool
-// Streams are created once per (device, mask) and live until the process
-// ends. Mask bit i selects one compute unit; the driver spreads consecutive
-// bits over the accelerator dies (XCDs) first, so the lowest k bits give
-// k/8 units on each of the 8 XCDs.
 namespace {
 
+// ---------------------------------------------------------------- stream pool
+// Streams are created once per (device, mask) and live until vla_shutdown.
+// Mask bit i selects one compute unit; the driver spreads consecutive bits
+// over the accelerator dies (XCDs) first, so the lowest k bits give k/8
+// units on each of the 8 XCDs.
 struct DevicePool {
   std::map<int, hipStream_t> vlm;     // key: cu count (256 = unrestricted)
   std::map<int, hipStream_t> adit;    // key: cu count from the top of the mask
@@ -451,8 +451,8 @@ vla_status vla_debug_attention(int B, int Hq, int Hkv, int Lq, int hd, int et, c
   });
 }
 
-vla_status vla_debug_cu_probe(int device, int cu_count, int from_top, int blocks, int spin, uint32_t* out,
-                              hipStream_t join) {
+vla_status vla_debug_cu_probe(int device, int cu_count, int from_top, int blocks, int spin, int via_graph,
+                              uint32_t* out, hipStream_t join) {
   return guarded([&] {
     VLA_REQUIRE(blocks >= 1 && blocks <= 65536 && spin >= 0 && spin <= 100000 && out, "bad probe arguments");
     VLA_REQUIRE(cu_count >= 8 && cu_count <= 256 && cu_count % 8 == 0, "cu_count must be a multiple of 8 in [8, 256]");
@@ -462,8 +462,29 @@ vla_status vla_debug_cu_probe(int device, int cu_count, int from_top, int blocks
     hipStream_t s = from_top ? adit_stream(device, cu_count) : vlm_stream(device, cu_count);
     VLA_HIP(hipEventRecord(p.ev_start, join));
     VLA_HIP(hipStreamWaitEvent(s, p.ev_start, 0));
-    launch_cu_probe(out, blocks, spin, s);
-    VLA_HIP(hipGetLastError());
+    if (!via_graph) {
+      launch_cu_probe(out, blocks, spin, s);
+      VLA_HIP(hipGetLastError());
+    } else {
+      // as the stages run: captured on an unrestricted stream, replayed on
+      // the restricted one
+      hipStream_t cs = nullptr;
+      hipGraph_t graph = nullptr;
+      hipGraphExec_t exec = nullptr;
+      VLA_HIP(hipStreamCreateWithFlags(&cs, hipStreamNonBlocking));
+      hipError_t e = hipStreamBeginCapture(cs, hipStreamCaptureModeThreadLocal);
+      if (e == hipSuccess) {
+        launch_cu_probe(out, blocks, spin, cs);
+        e = hipStreamEndCapture(cs, &graph);
+      }
+      if (e == hipSuccess) e = hipGraphInstantiate(&exec, graph, nullptr, nullptr, 0);
+      if (e == hipSuccess) e = hipGraphLaunch(exec, s);
+      if (e == hipSuccess) e = hipStreamSynchronize(s);
+      if (exec) (void)hipGraphExecDestroy(exec);
+      if (graph) (void)hipGraphDestroy(graph);
+      (void)hipStreamDestroy(cs);
+      VLA_HIP(e);
+    }
     VLA_HIP(hipEventRecord(p.ev_v, s));
     VLA_HIP(hipStreamWaitEvent(join, p.ev_v, 0));
   });

@@ -235,6 +235,10 @@ void launch_scale_cols_bf16(void* W, long N, int K, int ldk, const float* g, hip
 // Debug probe: each workgroup writes its hardware placement (XCC id, SE id,
 // CU id) to out[block] as one word: xcc << 16 | se << 8 | cu.
 void launch_cu_probe(uint32_t* out, int blocks, int spin, hipStream_t s);
+// Merge s x s blocks of each image's g x g patch tokens ([n_img][g*g][d],
+// raster order) into [n_img][(g/s)^2][s*s*d]: block (I, J) in raster order,
+// its tokens (s*I + di, s*J + dj) in (di, dj) order, channels innermost.
+void launch_pixel_shuffle(const void* src, int n_img, int g, int s, int d, int et, void* dst, hipStream_t st);
 
 // One segment of a batched copy: `bytes` bytes from src to dst (src NULL:
 // zero fill). Used by the serving scheduler to gather admitted requests'

@@ -175,6 +175,24 @@ inline int grid_for(long n, int block = 256) {
 
 }  // namespace
 
+// Token merge: thread i writes 16-byte chunk c of block slot k of merged token
+// r (destination order), read from the source token that slot holds.
+__global__ void pixel_shuffle_kernel(const uint4* src, uint4* dst, long total, int g, int s, int cpt) {
+  const int G = g / s, ss = s * s;
+  for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += (long)gridDim.x * blockDim.x) {
+    const int c = (int)(i % cpt);
+    const long t = i / cpt;
+    const int kk = (int)(t % ss);
+    const long r = t / ss;
+    const int J = (int)(r % G);
+    const long r2 = r / G;
+    const int I = (int)(r2 % G);
+    const long img = r2 / G;
+    const long sr = img * g * g + (long)(s * I + kk / s) * g + s * J + kk % s;
+    dst[i] = src[sr * cpt + c];
+  }
+}
+
 // Batched copy: block (x, y) copies chunk x of segment y. 16-byte vector
 // accesses when source, destination and size allow them, else 4-byte, else
 // single bytes; a null source writes zeros.
@@ -258,6 +276,15 @@ void launch_scale_cols_bf16(void* W, long N, int K, int ldk, const float* g, hip
 
 void launch_round_bf16_f32(const float* src, long n, float* dst, hipStream_t s) {
   hipLaunchKernelGGL(round_bf16_kernel, dim3(grid_for(n)), dim3(256), 0, s, src, n, dst);
+}
+
+void launch_pixel_shuffle(const void* src, int n_img, int g, int s, int d, int et, void* dst, hipStream_t st) {
+  const long row_bytes = (long)d * (et == ET_BF16 ? 2 : 4);
+  VLA_REQUIRE(row_bytes % 16 == 0 && g % s == 0, "token merge needs 16-byte rows and s | g");
+  const int cpt = (int)(row_bytes / 16);
+  const long total = (long)n_img * g * g * cpt;
+  const long blocks = std::min<long>((total + 255) / 256, 65536);
+  pixel_shuffle_kernel<<<(unsigned)blocks, 256, 0, st>>>((const uint4*)src, (uint4*)dst, total, g, s, cpt);
 }
 
 void launch_batched_copy(const CopySeg* segs, int n, long long max_bytes, hipStream_t s) {

@@ -49,7 +49,9 @@ struct vla_model_s {
   int et = ET_F32;
   int device = 0;
   // derived sizes
-  int T = 0, P = 0, E = 0, Kp = 0, D = 0, Hq = 0, Hk = 0, hd = 0, Da = 0, A = 0, H = 0;
+  // T: image tokens per image in the prefix; Tv: patch tokens per image (the
+  // ViT's sequence); S: side of the merged token blocks (1: no merge)
+  int T = 0, Tv = 0, S = 1, P = 0, E = 0, Kp = 0, D = 0, Hq = 0, Hk = 0, hd = 0, Da = 0, A = 0, H = 0;
   int vhd = 0, dhd = 0, tdim = 0, Ltok = 0;
 
   std::vector<void*> allocs;   // every device allocation, freed on destroy
@@ -79,6 +81,7 @@ struct vla_model_s {
 
   // ---- prefill workspace
   void* patches = nullptr;
+  void* vshuf = nullptr;      // merged image tokens [B*n_img*T][S*S*vit_d] (S > 1)
   float* vx = nullptr; void *vz = nullptr, *vq = nullptr, *vk = nullptr, *vv = nullptr, *vo = nullptr, *vmlp = nullptr;
   float* h = nullptr; void *z = nullptr, *q = nullptr, *o = nullptr, *gu = nullptr, *kbuf = nullptr, *vbuf = nullptr;
   void* feat = nullptr; float* zero_state = nullptr;

@@ -19,9 +19,10 @@ inline int round_up(int x, int m) { return (x + m - 1) / m * m; }
 template <typename Take>
 void walk_params(const vla_config& c, Take&& take) {
   const int E = c.vit_layers > 0 ? c.vit_d : c.llm_d;
-  const int T = (c.img_hw / c.patch) * (c.img_hw / c.patch);
+  const int Tv = (c.img_hw / c.patch) * (c.img_hw / c.patch);    // patch tokens per image
+  const long S = c.pix_shuffle > 1 ? c.pix_shuffle : 1;
   const long pd = 3L * c.patch * c.patch;
-  take(pd * E); take(E); take((long)T * E);
+  take(pd * E); take(E); take((long)Tv * E);
   for (int l = 0; l < c.vit_layers; ++l) {
     const long d = c.vit_d, f = c.vit_mlp;
     take(d); take(d);                       // ln1
@@ -30,7 +31,7 @@ void walk_params(const vla_config& c, Take&& take) {
     take(d); take(d);                       // ln2
     take(d * f); take(f); take(f * d); take(d);
   }
-  if (c.vit_layers > 0) { take(c.vit_d); take(c.vit_d); take((long)c.vit_d * c.llm_d); take(c.llm_d); }
+  if (c.vit_layers > 0) { take(c.vit_d); take(c.vit_d); take(S * S * c.vit_d * c.llm_d); take(c.llm_d); }
   take((long)c.vocab * c.llm_d);
   const long D = c.llm_d, Hq = (long)c.n_q * c.head_dim, Hk = (long)c.n_kv * c.head_dim, F = c.llm_mlp;
   for (int l = 0; l < c.llm_layers; ++l) {
@@ -68,6 +69,9 @@ std::string vla_config_check(const vla_config& c) {
   if (c.vit_layers < 0 || (c.vit_layers > 0 && (!pos(c.vit_d) || !pos(c.vit_heads) || !pos(c.vit_mlp) || c.vit_d % c.vit_heads)))
     return "bad ViT shape";
   if (c.vit_layers > 0 && ((c.vit_d / c.vit_heads) % 8 || c.vit_d / c.vit_heads > 256)) return "ViT head dim must be a multiple of 8, <= 256";
+  if (c.pix_shuffle < 0) return "pix_shuffle must be >= 0";
+  if (c.pix_shuffle > 1 && (c.vit_layers == 0 || (c.img_hw / c.patch) % c.pix_shuffle))
+    return "pix_shuffle > 1 needs a ViT and must divide img_hw / patch";
   if (!pos(c.n_text) || !pos(c.vocab)) return "bad text shape";
   if (!pos(c.llm_layers) || !pos(c.llm_d) || !pos(c.n_q) || !pos(c.n_kv) || !pos(c.head_dim) || !pos(c.llm_mlp)) return "bad LLM shape";
   if (c.n_q % c.n_kv) return "n_q must be a multiple of n_kv";
@@ -227,7 +231,9 @@ void vla_model_s::init(const vla_config& c, const float* w, size_t n, int dev) {
   cfg = c;
   device = dev;
   et = c.dtype == VLA_BF16 ? ET_BF16 : ET_F32;
-  T = (c.img_hw / c.patch) * (c.img_hw / c.patch);
+  Tv = (c.img_hw / c.patch) * (c.img_hw / c.patch);
+  S = c.pix_shuffle > 1 ? c.pix_shuffle : 1;
+  T = Tv / (S * S);
   P = c.n_img * T + c.n_text;
   E = c.vit_layers > 0 ? c.vit_d : c.llm_d;
   const int pd = 3 * c.patch * c.patch;
@@ -259,7 +265,7 @@ void vla_model_s::init(const vla_config& c, const float* w, size_t n, int dev) {
     L.mat_into(patch, pd, E, Loader::iota(E, 0));
     patch.K = Kp;                     // the patch rows are zero-padded to Kp
     patch_b = L.vec(E);
-    pos = L.vec((size_t)T * E);
+    pos = L.vec((size_t)Tv * E);
     for (int l = 0; l < c.vit_layers; ++l) {
       VitLayer v{};
       const int d = c.vit_d, f = c.vit_mlp;
@@ -278,7 +284,7 @@ void vla_model_s::init(const vla_config& c, const float* w, size_t n, int dev) {
     }
     if (c.vit_layers > 0) {
       vit_lnf_g = L.vec(c.vit_d); vit_lnf_b = L.vec(c.vit_d);
-      proj = L.mat(c.vit_d, D); proj_b = L.vec(D);
+      proj = L.mat(S * S * c.vit_d, D); proj_b = L.vec(D);
     }
     {   // token embedding table, kept in the model dtype
       const size_t cnt = (size_t)c.vocab * D;
@@ -404,10 +410,11 @@ void vla_model_s::init(const vla_config& c, const float* w, size_t n, int dev) {
 
     // ---- workspaces (sized for max_batch)
     const size_t es = elem_size(et);
-    const size_t Mi = (size_t)Bm * c.n_img * T, Mp = (size_t)Bm * P;
+    const size_t Mi = (size_t)Bm * c.n_img * Tv, Mp = (size_t)Bm * P;
     patches = dalloc(Mi * Kp * es);
     if (c.vit_layers > 0) {
       const size_t d = c.vit_d;
+      if (S > 1) vshuf = dalloc(Mi * d * es);
       vx = (float*)dalloc(Mi * d * 4);
       vz = dalloc(Mi * d * es); vq = dalloc(Mi * d * es); vk = dalloc(Mi * d * es); vv = dalloc(Mi * d * es);
       vo = dalloc(Mi * d * es); vmlp = dalloc(Mi * c.vit_mlp * es);
@@ -530,7 +537,7 @@ void vla_model_s::enqueue_prefill(int B, const float* pix, const int32_t* ids, c
   constexpr int ST = STAGE_PREFILL;
   const vla_config& c = cfg;
   const size_t es = elem_size(et);
-  const int nimg = B * c.n_img, Mi = nimg * T, Mp = B * P;
+  const int nimg = B * c.n_img, Mi = nimg * Tv, Mp = B * P;
   const float eps = c.norm_eps;
   const bool dit_head = c.head_kind == VLA_HEAD_DIT;
 
@@ -544,7 +551,7 @@ void vla_model_s::enqueue_prefill(int B, const float* pix, const int32_t* ids, c
   } else {
     const int d = c.vit_d, nh = c.vit_heads;
     GemmArgs g = gm(*this, ST,patch, Mi, patches, Kp, et);
-    g.tab = pos; g.tab_period = T; g.ldtab = E;
+    g.tab = pos; g.tab_period = Tv; g.ldtab = E;
     store(g, vx, d, ET_F32, patch_b, ACT_NONE, s);
     norm(Mi, d, 1, vx, d, vz, d, et, vit[0].ln1g, vit[0].ln1b, eps, s);
     for (int l = 0; l < c.vit_layers; ++l) {
@@ -553,16 +560,16 @@ void vla_model_s::enqueue_prefill(int B, const float* pix, const int32_t* ids, c
       GemmArgs q3 = gm(*this, ST,y.qkv, Mi, vz, d, et);
       q3.mode = EPI_QKV; q3.bias = y.bqkv; q3.out_type = et;
       QkvEpi& e3 = q3.qkv;
-      e3.n_q = nh; e3.n_kv = nh; e3.hd = vhd; e3.n_off = 0; e3.seq = T; e3.pos0 = -1;
-      e3.q = vq; e3.q_sb = (long)nh * T * vhd; e3.q_sh = (long)T * vhd; e3.q_si = vhd;
+      e3.n_q = nh; e3.n_kv = nh; e3.hd = vhd; e3.n_off = 0; e3.seq = Tv; e3.pos0 = -1;
+      e3.q = vq; e3.q_sb = (long)nh * Tv * vhd; e3.q_sh = (long)Tv * vhd; e3.q_si = vhd;
       e3.k = vk; e3.k_sb = e3.q_sb; e3.k_sh = e3.q_sh; e3.k_si = vhd;
       e3.v = vv; e3.v_sb = e3.q_sb; e3.v_sh = e3.q_sh; e3.v_si = vhd;
       launch_gemm(q3, s);
-      AttnArgs at = attn(*this, ST,nimg, nh, nh, T, vhd, et);
+      AttnArgs at = attn(*this, ST,nimg, nh, nh, Tv, vhd, et);
       at.q = vq; at.q_sb = e3.q_sb; at.q_sh = e3.q_sh; at.q_si = vhd;
-      at.seg[0] = AttnSeg{vk, e3.k_sb, e3.k_sh, vhd, vv, e3.v_sb, e3.v_sh, vhd, T};
+      at.seg[0] = AttnSeg{vk, e3.k_sb, e3.k_sh, vhd, vv, e3.v_sb, e3.v_sh, vhd, Tv};
       at.seg[1].len = 0;
-      at.o = vo; at.o_sb = (long)T * d; at.o_sh = vhd; at.o_si = d;
+      at.o = vo; at.o_sb = (long)Tv * d; at.o_sh = vhd; at.o_si = d;
       launch_attention(at, s);
       resid_norm(gm(*this, ST,y.wo, Mi, vo, d, et), vx, d, y.bo, nullptr,
                  nargs(Mi, d, 1, vx, d, vz, d, et, y.ln2g, y.ln2b, eps), s);
@@ -573,7 +580,14 @@ void vla_model_s::enqueue_prefill(int B, const float* pix, const int32_t* ids, c
                  nargs(Mi, d, 1, vx, d, vz, d, et, last ? vit_lnf_g : vit[l + 1].ln1g,
                        last ? vit_lnf_b : vit[l + 1].ln1b, eps), s);
     }
-    GemmArgs gp = gm(*this, ST,proj, Mi, vz, d, et);
+    // vz holds the final LayerNorm of every patch token; with S > 1 each S x S
+    // block of them becomes one token of width S*S*d first
+    const void* pin = vz;
+    if (S > 1) {
+      launch_pixel_shuffle(vz, nimg, c.img_hw / c.patch, S, d, et, vshuf, s);
+      pin = vshuf;
+    }
+    GemmArgs gp = gm(*this, ST,proj, nimg * T, pin, S * S * d, et);
     gp.row_group = c.n_img * T; gp.row_group_stride = (long)P * D;
     store(gp, h, D, ET_F32, proj_b, ACT_NONE, s);
   }
@@ -911,7 +925,7 @@ GemmArgs vla_model_s::stage_gemm(int which, int B, int layer) const {
       break;
     case 4:   // VLM stage: ViT layer MLP up (GELU)
       VLA_REQUIRE(c.vit_layers > 0, "model has no ViT");
-      g = gm(*this, ST,vit[lv].w1, B * c.n_img * T, vz, c.vit_d, et);
+      g = gm(*this, ST,vit[lv].w1, B * c.n_img * Tv, vz, c.vit_d, et);
       g.mode = EPI_STORE; g.act = ACT_GELU; g.bias = vit[lv].b1; g.out = vmlp; g.ldo = c.vit_mlp; g.out_type = et;
       break;
     default:

@@ -1,7 +1,7 @@
 """Summaries of rocprofv3 output for the kernels of this library.
 
     python -m paper_2609_12075_amd.profsum stats <kernel_stats.csv> [--top N]
-    python -m paper_2609_12075_amd.profsum trace <kernel_trace.csv> --kernel REGEX
+    python -m paper_2609_12075_amd.profsum trace <kernel_trace.csv> --kernel REGEX [--last N]
     python -m paper_2609_12075_amd.profsum traffic --fetch <pmc.csv> --write <pmc.csv> \
         --kernel REGEX --copy-bytes N [--out traffic.json]
 
@@ -42,16 +42,26 @@ def stats(path: str, top: int = 20) -> str:
     return "\n".join(out)
 
 
-def trace(path: str, kernel: str) -> str:
+def trace(path: str, kernel: str, last: int = 0) -> str:
+    """Per (kernel, grid) dispatch durations; with last > 0 also the mean of
+    each group's last `last` dispatches in time order (a benchmark's final
+    replay phase of one projection, timed there with HIP events)."""
     rows = [r for r in csv.DictReader(open(path)) if re.search(kernel, r["Kernel_Name"])]
     g = collections.defaultdict(list)
     for r in rows:
         key = (r["Kernel_Name"][:100], r["Grid_Size_X"], r["Grid_Size_Y"], r["Grid_Size_Z"])
-        g[key].append(int(r["End_Timestamp"]) - int(r["Start_Timestamp"]))
-    out = [f"{'calls':>6} {'avg us':>9} {'median us':>10}  grid (threads)  kernel"]
-    for k, v in sorted(g.items(), key=lambda kv: -sum(kv[1])):
-        out.append(f"{len(v):6d} {sum(v) / len(v) / 1e3:9.2f} {statistics.median(v) / 1e3:10.2f}  "
-                   f"({k[1]},{k[2]},{k[3]})  {k[0]}")
+        g[key].append((int(r["Start_Timestamp"]), int(r["End_Timestamp"]) - int(r["Start_Timestamp"])))
+    head = f"{'calls':>6} {'avg us':>9} {'median us':>10}"
+    if last:
+        head += f" {'last ' + str(last) + ' avg us':>16}"
+    out = [head + "  grid (threads)  kernel"]
+    for k, v in sorted(g.items(), key=lambda kv: -sum(d for _, d in kv[1])):
+        d = [x for _, x in v]
+        line = f"{len(d):6d} {sum(d) / len(d) / 1e3:9.2f} {statistics.median(d) / 1e3:10.2f}"
+        if last:
+            tail = [x for _, x in sorted(v)[-last:]]
+            line += f" {sum(tail) / len(tail) / 1e3:16.2f}"
+        out.append(line + f"  ({k[1]},{k[2]},{k[3]})  {k[0]}")
     return "\n".join(out)
 
 
@@ -84,6 +94,7 @@ def main(argv=None):
     sub = ap.add_subparsers(dest="cmd", required=True)
     s = sub.add_parser("stats"); s.add_argument("csv"); s.add_argument("--top", type=int, default=20)
     t = sub.add_parser("trace"); t.add_argument("csv"); t.add_argument("--kernel", default=".")
+    t.add_argument("--last", type=int, default=0)
     f = sub.add_parser("traffic")
     f.add_argument("--fetch", required=True); f.add_argument("--write", required=True)
     f.add_argument("--kernel", required=True); f.add_argument("--copy-bytes", type=int, required=True)
@@ -92,7 +103,7 @@ def main(argv=None):
     if a.cmd == "stats":
         print(stats(a.csv, a.top))
     elif a.cmd == "trace":
-        print(trace(a.csv, a.kernel))
+        print(trace(a.csv, a.kernel, a.last))
     else:
         res = traffic(a.fetch, a.write, a.kernel, a.copy_bytes)
         js = json.dumps(res, indent=1)

@@ -64,11 +64,22 @@ class VLAConfig:
     rope_base: float = 10000.0
     norm_eps: float = 1e-6
     time_dim: int = 0          # sinusoid width for the DiT time MLP (0: act_d)
+    pix_shuffle: int = 1       # s x s blocks of encoder tokens merged into one image token (1: none)
 
     # ---- derived sizes (pure bookkeeping) ----
     @property
+    def patch_grid(self) -> int:
+        return self.img_hw // self.patch
+
+    @property
+    def patch_tokens(self) -> int:
+        """Patch tokens per image (the vision encoder's sequence)."""
+        return self.patch_grid ** 2
+
+    @property
     def tokens_per_img(self) -> int:
-        return (self.img_hw // self.patch) ** 2
+        """Image tokens per image in the LLM prefix."""
+        return self.patch_tokens // (self.pix_shuffle ** 2)
 
     @property
     def n_img_tokens(self) -> int:
@@ -121,6 +132,14 @@ CONFIGS["smolvla"] = VLAConfig(
     act_mlp=1920, horizon=50, action_dim=32, state_dim=0, max_batch=16, steps=10,
     seed=1)
 
+# SmolVLA-shaped with its whole vision encoder (a SigLIP-like ViT on 512 x 512
+# images, patch 16, whose 32 x 32 patch tokens are merged in 4 x 4 blocks into
+# 64 image tokens before the projection to the LLM width): the prefix keeps
+# 3 x 64 image tokens + 48 text tokens, as in the configuration above.
+CONFIGS["smolvla_vit"] = CONFIGS["smolvla"].with_(
+    name="smolvla_vit", img_hw=512, patch=16, vit_layers=12, vit_d=768, vit_heads=12, vit_mlp=3072,
+    pix_shuffle=4, seed=4)
+
 # pi0-shaped, bf16, batch 1-32.
 CONFIGS["pi0"] = VLAConfig(
     name="pi0", dtype=DTYPE_BF16, n_img=3, img_hw=224, patch=14,
@@ -163,7 +182,7 @@ def weight_schema(c: VLAConfig) -> List[Tuple[str, Tuple[int, ...], str]]:
     tensors concatenated in this order, each row-major fp32."""
     s: List[Tuple[str, Tuple[int, ...], str]] = []
     add = lambda n, sh, k: s.append((n, tuple(int(x) for x in sh), k))
-    E, T = c.embed_d, c.tokens_per_img
+    E, T = c.embed_d, c.patch_tokens
     # vision front-end
     add("patch.w", (c.patch_dim, E), MAT)
     add("patch.b", (E,), VEC)
@@ -181,7 +200,7 @@ def weight_schema(c: VLAConfig) -> List[Tuple[str, Tuple[int, ...], str]]:
         add(p + "w2", (f, d), MAT); add(p + "b2", (d,), VEC)
     if c.vit_layers > 0:
         add("vit.lnf.g", (c.vit_d,), GAIN); add("vit.lnf.b", (c.vit_d,), VEC)
-        add("vit.proj.w", (c.vit_d, c.llm_d), MAT); add("vit.proj.b", (c.llm_d,), VEC)
+        add("vit.proj.w", (c.vit_d * c.pix_shuffle ** 2, c.llm_d), MAT); add("vit.proj.b", (c.llm_d,), VEC)
     add("embed", (c.vocab, c.llm_d), VEC)
     D, Hq, Hk = c.llm_d, c.n_q * c.head_dim, c.n_kv * c.head_dim
     for l in range(c.llm_layers):

@@ -41,7 +41,7 @@ class VlaConfigC(ctypes.Structure):
         "dtype", "n_img", "img_hw", "patch", "vit_layers", "vit_d", "vit_heads", "vit_mlp", "n_text", "vocab",
         "llm_layers", "llm_d", "n_q", "n_kv", "head_dim", "llm_mlp", "head_kind", "act_layers", "act_d",
         "act_heads", "act_mlp", "horizon", "action_dim", "state_dim", "time_dim", "max_batch")] + [
-        ("rope_base", ctypes.c_float), ("norm_eps", ctypes.c_float)]
+        ("rope_base", ctypes.c_float), ("norm_eps", ctypes.c_float), ("pix_shuffle", ctypes.c_int)]
 
 
 class StepArgsC(ctypes.Structure):
@@ -60,6 +60,9 @@ def lib():
     if _lib is None:
         if not os.path.exists(_LIB_PATH):
             raise RuntimeError(f"{_LIB_PATH} not built: run `python -m paper_2609_12075_amd.build`")
+        # torch first: it loads the HIP runtime it ships, which the library's
+        # own dependency then resolves to, so the process has one runtime
+        import torch  # noqa: F401
         L = ctypes.CDLL(_LIB_PATH)
         vp, ci, sz = ctypes.c_void_p, ctypes.c_int, ctypes.c_size_t
         L.vla_weight_count.argtypes = [ctypes.POINTER(VlaConfigC)]; L.vla_weight_count.restype = sz
@@ -83,15 +86,14 @@ def lib():
         L.vla_debug_resid_copy.restype = ci
         L.vla_debug_attention.argtypes = [ci, ci, ci, ci, ci, ci, vp, vp, vp, ci, vp, vp, ci, vp, vp]
         L.vla_debug_attention.restype = ci
-        L.vla_debug_cu_probe.argtypes = [ci, ci, ci, ci, ci, vp, vp]; L.vla_debug_cu_probe.restype = ci
+        L.vla_debug_cu_probe.argtypes = [ci, ci, ci, ci, ci, ci, vp, vp]; L.vla_debug_cu_probe.restype = ci
         L.vla_debug_replay_gemm.argtypes = [vp, ci, ci, ci, vp, ctypes.POINTER(ctypes.c_double),
                                             ctypes.POINTER(ctypes.c_int)]
         L.vla_debug_replay_gemm.restype = ci
         L.vla_shutdown.argtypes = []; L.vla_shutdown.restype = None
         _lib = L
-        # atexit handlers run last-registered-first: importing torch before
-        # registering puts this teardown ahead of torch's own
-        import torch  # noqa: F401
+        # atexit handlers run last-registered-first: torch, imported above,
+        # registered its handlers already, so this teardown runs before them
         atexit.register(shutdown)
     return _lib
 
@@ -282,7 +284,7 @@ def step(vlm_model: Optional[Model], vlm_batch: int, pixels, text_ids, kv_out,
 
 
 # ---------------------------------------------------------------- test hooks
-def debug_gemm(A, Wt, bias=None, act=0, out=None, M=None, N=None, K=None, stream=None):
+def _gemm_call(fn, A, Wt, bias, act, out, M, N, K, stream):
     import torch
     M = A.shape[0] if M is None else M
     N = Wt.shape[0] if N is None else N
@@ -291,9 +293,13 @@ def debug_gemm(A, Wt, bias=None, act=0, out=None, M=None, N=None, K=None, stream
         out = torch.empty(M, N, dtype=torch.float32, device=A.device)
     at = 1 if A.dtype == torch.bfloat16 else 0
     wt = 1 if Wt.dtype == torch.bfloat16 else 0
-    _check(lib().vla_debug_gemm(M, N, K, _ptr(A), A.shape[1], at, _ptr(Wt), Wt.shape[1], wt, _ptr(bias), act,
-                                _ptr(out), out.shape[1], _stream(stream)))
+    _check(fn(M, N, K, _ptr(A), A.shape[1], at, _ptr(Wt), Wt.shape[1], wt, _ptr(bias), act, _ptr(out), out.shape[1],
+              _stream(stream)))
     return out
+
+
+def debug_gemm(A, Wt, bias=None, act=0, out=None, M=None, N=None, K=None, stream=None):
+    return _gemm_call(lib().vla_debug_gemm, A, Wt, bias, act, out, M, N, K, stream)
 
 
 def debug_resid_norm(A, Wt, x, kind, g=None, b=None, bias=None, gate=None, eps=1e-6, stream=None):
@@ -341,8 +347,10 @@ def debug_attention(q, k0, v0, k1=None, v1=None, stream=None):
     return o
 
 
-def debug_cu_probe(cu_count: int, blocks: int, spin: int = 200, from_top: bool = False, device: int = 0, stream=None):
+def debug_cu_probe(cu_count: int, blocks: int, spin: int = 200, from_top: bool = False, device: int = 0, stream=None,
+                   via_graph: bool = False):
     import torch
     out = torch.zeros(2 * blocks, dtype=torch.int32, device=f"cuda:{device}")
-    _check(lib().vla_debug_cu_probe(device, cu_count, int(from_top), blocks, spin, _ptr(out), _stream(stream)))
+    _check(lib().vla_debug_cu_probe(device, cu_count, int(from_top), blocks, spin, int(via_graph), _ptr(out),
+                                    _stream(stream)))
     return out

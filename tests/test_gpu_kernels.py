@@ -278,3 +278,23 @@ def test_cu_masked_streams_confine_work():
         assert len(got) <= k
         assert len(top) <= 256 - k
         assert not (got & top), "low and high masks must be disjoint"
+
+
+def test_cu_masked_streams_confine_graph_replays():
+    """The stages reach the restricted streams as graph replays (captured on an
+    unrestricted stream): the mask of the stream the graph is launched on
+    still confines the work, and the low and high masks stay disjoint."""
+    import torch
+    from paper_2609_12075_amd import vla
+    for k in (64, 128, 192):
+        got = _placements(vla.debug_cu_probe(k, 4096, spin=50, via_graph=True))
+        top = _placements(vla.debug_cu_probe(256 - k, 4096, spin=50, from_top=True, via_graph=True))
+        direct = _placements(vla.debug_cu_probe(k, 4096, spin=50))
+        torch.cuda.synchronize()
+        log(f"[cu probe] graph replay, mask {k}: {len(got)} CUs (direct launch {len(direct)}); top {256 - k}: "
+            f"{len(top)} CUs, overlap {len(got & top)}")
+        assert len(got) <= k and len(top) <= 256 - k
+        assert not (got & top)
+        assert len(got) >= k // 2, "a replayed graph spreads over the stream's CUs"
+        if len(direct) == k:          # the direct launch reached every CU of the mask
+            assert got <= direct

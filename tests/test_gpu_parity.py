@@ -18,6 +18,8 @@ SMOL_R = synth.reduced(synth.CONFIGS["smolvla"], max_batch=4)
 PI0_R = synth.reduced(synth.CONFIGS["pi0"], vit_layers=2, max_batch=3)
 GR00T_R = synth.reduced(synth.CONFIGS["gr00t"], vit_layers=2, max_batch=3)
 
+SMOLVIT_R = synth.reduced(synth.CONFIGS["smolvla_vit"], vit_layers=2, max_batch=3)
+
 TOL = {synth.DTYPE_F32: 1e-4, synth.DTYPE_BF16: 2e-2}
 
 
@@ -63,6 +65,26 @@ def test_pi0_reduced(B):
 @pytest.mark.parametrize("B,with_state", [(1, True), (2, True), (2, False)])
 def test_gr00t_reduced(B, with_state):
     check_parity(GR00T_R, B, with_state=with_state)
+
+
+@pytest.mark.parametrize("B", [1, 3])
+def test_smolvla_vision_encoder_reduced(B):
+    """SmolVLA-shaped model with its vision encoder (512 x 512 images, patch
+    16, 4 x 4 token merge), two ViT layers."""
+    check_parity(SMOLVIT_R, B)
+
+
+def test_smolvla_vision_encoder_full_size_sampled_rows():
+    """The whole 12-layer vision encoder with the 16-layer LLM and action
+    expert at batch 16; the oracle evaluates rows 0 and 15."""
+    cfg = synth.CONFIGS["smolvla_vit"]
+    B = cfg.max_batch
+    inp = synth.make_inputs(cfg, B)
+    act, _ = run(cfg, inp)
+    rows = [0, B - 1]
+    ref, _ = oracle_run(cfg, inp, rows=rows)
+    check_chunk(act[rows], ref, inp["noise"][rows], 2e-2, f"smolvla_vit full B={B} rows {rows}")
+    drop_model(cfg)
 
 
 def test_steps_one_and_max_batch():

@@ -196,13 +196,35 @@ def _vit_cfg(vit_layers, n_img=2):
                                   head_dim=8, llm_mlp=32, act_layers=1, act_d=16, act_heads=2, act_mlp=24)
 
 
-@pytest.mark.parametrize("vit_layers", [0, 2])
-def test_image_tokens_against_torch_modules(vit_layers):
+def _library_pixel_shuffle(x, s):
+    """The token merge of the SmolVLM connector in transformers (x [n, g*g, d])."""
+    from transformers.models.idefics3 import modeling_idefics3 as MI
+    return MI.Idefics3Connector.pixel_shuffle(None, x, scale_factor=s)
+
+
+@pytest.mark.parametrize("g,s,d", [(8, 4, 3), (12, 2, 5), (32, 4, 2)])
+def test_pixel_shuffle_against_library_and_definition(g, s, d):
+    x = RNG.standard_normal((g * g, d))
+    got = O.pixel_shuffle(x, g, s)
+    ref = _library_pixel_shuffle(T(x)[None], s)[0].numpy()
+    np.testing.assert_array_equal(got, ref)
+    # scalar definition: token (I, J) holds tokens (s I + di, s J + dj) in (di, dj) order
+    G = g // s
+    for I in range(G):
+        for J in range(G):
+            for di in range(s):
+                for dj in range(s):
+                    np.testing.assert_array_equal(got[I * G + J, (di * s + dj) * d:(di * s + dj + 1) * d],
+                                                  x[(s * I + di) * g + s * J + dj])
+
+
+@pytest.mark.parametrize("vit_layers,shuffle", [(0, 1), (2, 1), (2, 2)])
+def test_image_tokens_against_torch_modules(vit_layers, shuffle):
     """image_tokens = per image: conv2d patch embedding (+ bias) + position
     table, then (with a vision encoder) pre-LN TransformerEncoderLayers with
     tanh-GELU, a final LayerNorm and the projector to the LLM width; images
     concatenated in order."""
-    cfg = _vit_cfg(vit_layers)
+    cfg = _vit_cfg(vit_layers).with_(pix_shuffle=shuffle)
     W = _rand_joint(cfg, scale=0.2, seed=4)
     pix = RNG.random((cfg.n_img, 3, cfg.img_hw, cfg.img_hw))
     got = O.image_tokens(cfg, W, pix)
@@ -228,11 +250,14 @@ def test_image_tokens_against_torch_modules(vit_layers):
                 layer.norm2.weight.copy_(T(W[p + "ln2.g"])); layer.norm2.bias.copy_(T(W[p + "ln2.b"]))
                 x = layer(x)
         ln = torch.nn.LayerNorm(d, eps=cfg.norm_eps).double()
-        proj = torch.nn.Linear(d, cfg.llm_d).double()
+        proj = torch.nn.Linear(d * shuffle ** 2, cfg.llm_d).double()
         with torch.no_grad():
             ln.weight.copy_(T(W["vit.lnf.g"])); ln.bias.copy_(T(W["vit.lnf.b"]))
             proj.weight.copy_(T(W["vit.proj.w"].T)); proj.bias.copy_(T(W["vit.proj.b"]))
-            x = proj(ln(x))
+            x = ln(x)
+            if shuffle > 1:
+                x = _library_pixel_shuffle(x, shuffle)
+            x = proj(x)
     ref = x.reshape(-1, cfg.llm_d).detach().numpy()
     assert got.shape == (cfg.n_img_tokens, cfg.llm_d)
     assert rel(got, ref) < 1e-11, rel(got, ref)
