@@ -30,6 +30,22 @@ vla_status vla_debug_gemm(int M, int N, int K, const void* A, int lda, int a_typ
                           int w_type, const float* bias, int act, float* out, int ldo, hipStream_t stream);
 
 /*
+ * vla_debug_gemm without any allocation, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, hosts
+ * that forbid allocation). Same arguments, kernels, K ranges and results as
+ * vla_debug_gemm; its split-K partials and its zero block live in a static
+ * device array of 16 MiB + 256 bytes that every device the library runs on
+ * holds until the process ends. Returns VLA_EINVAL, enqueuing nothing, when
+ * the projection's K-split plan needs more than 16 MiB of partials
+ * (splits x M x round_up(N, 4) x 4 bytes; a plan without a K split needs
+ * none). Calls on one device share that array: calls that overlap on one
+ * device (different streams, or host threads) race and must be serialised
+ * by the caller. Each call first rewrites the zero block on `stream`.
+ */
+vla_status vla_gemm_noalloc(int M, int N, int K, const void* A, int lda, int a_type, const void* Wt, int ldw,
+                            int w_type, const float* bias, int act, float* out, int ldo, hipStream_t stream);
+
+/*
  * Residual projection followed by the row norm of its output (every
  * transformer block: x += o W_o, then the next sublayer's norm):
  *   x[m][n] += gate[n] * (sum_k A[m][k] Wt[n][k] + bias[n])   (x in place)

@@ -36,6 +36,19 @@ static vla_status guarded(F&& f) {
   }
 }
 
+// ---------------------------------------------------------------- static scratch
+// Scratch of the allocation-free projection entry point (vla_gemm_noalloc):
+// split-K partial products, then a block of zero bytes that the staged
+// kernels read for operand chunks past the end of K. Every device the library
+// runs on holds its own copy for the life of the process.
+constexpr long kScratchPartialBytes = 16L << 20;
+constexpr long kScratchZeroBytes = 256;
+static __device__ __align__(256) unsigned char scratch[kScratchPartialBytes + kScratchZeroBytes];
+
+__global__ void zero_bytes_kernel(uint4* p, int n16) {
+  for (int i = threadIdx.x; i < n16; i += blockDim.x) p[i] = make_uint4(0, 0, 0, 0);
+}
+
 namespace {
 
 // ---------------------------------------------------------------- stream pool
@@ -176,6 +189,25 @@ void check_denoise(vla_model m, int B, const void* kv, const float* noise, int s
   VLA_REQUIRE(steps >= 1 && steps <= 1000, "steps must be in [1, 1000]");
   VLA_REQUIRE(kv && noise && act, "null kv, noise or actions_out");
   VLA_REQUIRE((const void*)noise != (const void*)act, "actions_out may not alias noise");
+}
+
+// ---------------------------------------------------------------- static scratch address per device
+std::mutex g_scratch_mu;
+std::map<int, unsigned char*> g_scratch;     // device -> address of that device's scratch
+
+// The device address of `scratch` on the current device, looked up once per
+// device (the host-side name is not a device address).
+unsigned char* scratch_ptr() {
+  int dev = 0;
+  VLA_HIP(hipGetDevice(&dev));
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  auto it = g_scratch.find(dev);
+  if (it != g_scratch.end()) return it->second;
+  void* p = nullptr;
+  VLA_HIP(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+  VLA_REQUIRE(p != nullptr, "no device address for the static scratch");
+  g_scratch[dev] = (unsigned char*)p;
+  return (unsigned char*)p;
 }
 
 }  // namespace
@@ -372,6 +404,48 @@ vla_status vla_debug_gemm(int M, int N, int K, const void* A, int lda, int a_typ
     g.mode = EPI_STORE; g.act = act; g.bias = bias; g.tab_period = 1; g.out = out; g.ldo = ldo; g.out_type = ET_F32;
     g.ws = debug_ws(0, vla_model_s::kSplitKFloats); g.ws_floats = vla_model_s::kSplitKFloats;
     g.zeros = debug_ws(2, 64);
+    launch_gemm(g, s);
+    VLA_HIP(hipGetLastError());
+  });
+}
+
+vla_status vla_gemm_noalloc(int M, int N, int K, const void* A, int lda, int a_type, const void* Wt, int ldw,
+                            int w_type, const float* bias, int act, float* out, int ldo, hipStream_t s) {
+  return guarded([&] {
+    VLA_REQUIRE(M >= 0 && N >= 0 && K >= 0 && A && Wt && out, "bad gemm arguments");
+    VLA_REQUIRE(a_type == ET_F32 || a_type == ET_BF16, "bad a_type");
+    VLA_REQUIRE(w_type == ET_F32 || w_type == ET_BF16, "bad w_type");
+    VLA_REQUIRE(lda >= K && ldw >= K && ldo >= N, "leading dimensions too small");
+    if (w_type == ET_BF16) {
+      VLA_REQUIRE(K % 8 == 0 && lda % 8 == 0 && ldw % 8 == 0, "bf16 path needs K, lda, ldw % 8 == 0");
+    } else {
+      VLA_REQUIRE(a_type == ET_F32, "fp32 weights need fp32 activations");
+    }
+    VLA_REQUIRE(act >= ACT_NONE && act <= ACT_GELU, "bad act");
+    GemmArgs g{};
+    g.M = M; g.N = N; g.K = K; g.A = A; g.lda = lda; g.a_type = a_type; g.W = Wt; g.ldw = ldw; g.w_type = w_type;
+    g.mode = EPI_STORE; g.act = act; g.bias = bias; g.tab_period = 1; g.out = out; g.ldo = ldo; g.out_type = ET_F32;
+    // The plan vla_debug_gemm would choose (its workspace holds
+    // kSplitKFloats partials) must fit the static scratch: then this call
+    // launches the same kernels over the same K ranges, with the same results.
+    g.zeros = (const void*)&g;                 // planning only: any non-null address
+    g.ws = (float*)&g;
+    g.ws_floats = vla_model_s::kSplitKFloats;
+    const GemmPlan want = gemm_plan(g);
+    const long ldp = (N + 3) & ~3;
+    const long need = want.splits > 1 ? (long)want.splits * M * ldp * 4 : 0;
+    VLA_REQUIRE(need <= kScratchPartialBytes,
+                "projection needs " + std::to_string(need) + " bytes of split-K partials; the static scratch holds " +
+                    std::to_string(kScratchPartialBytes) + " (use vla_debug_gemm, which allocates)");
+    g.ws_floats = kScratchPartialBytes / 4;
+    const GemmPlan got = gemm_plan(g);
+    VLA_REQUIRE(got.splits == want.splits && got.kind == want.kind && got.bn == want.bn && got.bm == want.bm,
+                "projection plan does not fit the static scratch");
+    unsigned char* p = scratch_ptr();
+    g.ws = (float*)p;
+    g.zeros = p + kScratchPartialBytes;
+    zero_bytes_kernel<<<1, 64, 0, s>>>((uint4*)(p + kScratchPartialBytes), (int)(kScratchZeroBytes / 16));
+    VLA_HIP(hipGetLastError());
     launch_gemm(g, s);
     VLA_HIP(hipGetLastError());
   });

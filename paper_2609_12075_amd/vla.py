@@ -27,7 +27,7 @@ VLA_OK, VLA_EINVAL, VLA_ENOMEM, VLA_EHIP, VLA_EUNSUPPORTED = range(5)
 EXPORTS = ["vla_weight_count", "vla_create_model", "vla_destroy_model", "vla_set_graphs", "vla_kv_bytes",
            "vla_prefill", "vla_prefill_ex", "vla_denoise", "vla_step", "vla_last_error", "vla_shutdown",
            "vla_debug_gemm", "vla_debug_resid_norm", "vla_debug_gemm_rms", "vla_debug_resid_copy", "vla_debug_attention",
-           "vla_debug_cu_probe", "vla_debug_replay_gemm"]
+           "vla_debug_cu_probe", "vla_debug_replay_gemm", "vla_gemm_noalloc"]
 
 
 class VlaError(RuntimeError):
@@ -78,6 +78,8 @@ def lib():
         L.vla_last_error.argtypes = []; L.vla_last_error.restype = ctypes.c_char_p
         L.vla_debug_gemm.argtypes = [ci, ci, ci, vp, ci, ci, vp, ci, ci, vp, ci, vp, ci, vp]
         L.vla_debug_gemm.restype = ci
+        L.vla_gemm_noalloc.argtypes = [ci, ci, ci, vp, ci, ci, vp, ci, ci, vp, ci, vp, ci, vp]
+        L.vla_gemm_noalloc.restype = ci
         L.vla_debug_resid_norm.argtypes = [ci, ci, ci, vp, vp, vp, vp, vp, ci, vp, vp, ctypes.c_float, vp, vp]
         L.vla_debug_resid_norm.restype = ci
         L.vla_debug_gemm_rms.argtypes = [ci, ci, ci, vp, vp, vp, ctypes.c_float, vp, vp]
@@ -300,6 +302,12 @@ def _gemm_call(fn, A, Wt, bias, act, out, M, N, K, stream):
 
 def debug_gemm(A, Wt, bias=None, act=0, out=None, M=None, N=None, K=None, stream=None):
     return _gemm_call(lib().vla_debug_gemm, A, Wt, bias, act, out, M, N, K, stream)
+
+
+def gemm_noalloc(A, Wt, bias=None, act=0, out=None, M=None, N=None, K=None, stream=None):
+    """vla_gemm_noalloc: the projection of debug_gemm with its scratch in the
+    library's static device array (no allocation)."""
+    return _gemm_call(lib().vla_gemm_noalloc, A, Wt, bias, act, out, M, N, K, stream)
 
 
 def debug_resid_norm(A, Wt, x, kind, g=None, b=None, bias=None, gate=None, eps=1e-6, stream=None):
