@@ -81,21 +81,115 @@ def cpu_baseline(cfg, weights, budget_s):
                       f"steps), numpy fp64, {el:.1f} s"}
 
 
+class GpuValidator:
+    """Real-time serving runs on the GPU for the robot-limit search: the
+    online scheduler gathers each request's inputs from its robot's own
+    device buffers (robot i -> model i mod n) and scatters its chunk to a
+    buffer of its own; attainment counts unfinished requests as misses."""
+
+    def __init__(self, models, cfgs, slo, f, seconds, join_stream, n_rob_max, log_prefix="[bench]"):
+        import torch
+        from paper_2609_12075_amd import synth
+        self.models, self.cfgs, self.slo, self.f, self.seconds = models, cfgs, slo, f, seconds
+        self.js, self.lp = join_stream, log_prefix
+        self.rob_in = []
+        for i, c in enumerate(cfgs):
+            n = (n_rob_max + len(cfgs) - 1 - i) // len(cfgs)
+            inp = synth.make_inputs(c, max(n, 1), first_row=100)
+            self.rob_in.append({k: torch.from_numpy(v).to("cuda:0") for k, v in inp.items()})
+
+    def run(self, R, epoch, mb, cu_table=None, default_cu=256, mode="lockstep", disjoint=False, policy="esf",
+            traffic="poisson", slo=None):
+        import torch
+        from paper_2609_12075_amd import serve, synth
+        slo = self.slo if slo is None else slo
+        gen = synth.poisson_arrivals if traffic == "poisson" else synth.periodic_arrivals
+        arr = gen(R, self.f, self.seconds, epoch=epoch, n_models=len(self.cfgs))
+        outs = [torch.full((max(1, int((arr["model"] == i).sum())), c.horizon, c.action_dim), float("nan"),
+                           device="cuda:0") for i, c in enumerate(self.cfgs)]
+        cnt, ios = [0] * len(self.cfgs), []
+        for j in range(len(arr)):
+            mi, r = int(arr["model"][j]), int(arr["robot"][j]) // len(self.cfgs)
+            d = self.rob_in[mi]
+            ios.append(serve.Scheduler.request_io(d["pixels"][r], d["text_ids"][r], d["noise"][r], outs[mi][cnt[mi]],
+                                                  d["state"][r] if "state" in d else None))
+            cnt[mi] += 1
+        sch = serve.Scheduler(slo, mb, policy, mode)
+        sch.set_gpu_online(self.models, join_stream=self.js)
+        sch.set_cu(default_cu, cu_table)
+        sch.set_disjoint(disjoint)
+        torch.cuda.synchronize()
+        req, ls = sch.run(arr, drain_ns=int(1e9), ios=ios)
+        sch.close()
+        done = req["t_done_ns"] >= 0
+        finite = all(bool(torch.isfinite(o[:c]).all()) for o, c in zip(outs, cnt) if c) if done.all() else None
+        dur = (ls["t_end_ns"] - ls["t_start_ns"]) / 1e6
+        rec = {"robots": int(R), "requests": int(len(req)), "attainment": round(serve.attainment(req), 4),
+               "p99_ms": round(serve.p99_ms(req), 2), "locksteps": int(len(ls)),
+               "lockstep_ms_mean": round(float(dur.mean()), 3) if len(dur) else None,
+               "outputs_finite": finite, "seconds": self.seconds}
+        log(f"{self.lp} GPU R={R}: attainment {rec['attainment']:.4f}, p99 {rec['p99_ms']} ms, "
+            f"{rec['requests']} requests, {rec['locksteps']} locksteps")
+        return rec
+
+    def search(self, R0, r_max, epoch0=100, target=0.98, **kw):
+        """Largest robot count with GPU attainment >= target, starting from
+        the simulated limit R0: up while it holds, else down until it does.
+        Returns (robots, checks)."""
+        checks, R = [], max(1, min(R0, r_max))
+        rec = self.run(R, epoch0, **kw)
+        checks.append(rec)
+        ok = rec["attainment"] >= target
+        best = R if ok else 0
+        while ok and R < r_max:
+            R += 1
+            rec = self.run(R, epoch0 + R, **kw)
+            checks.append(rec)
+            ok = rec["attainment"] >= target
+            if ok:
+                best = R
+        R = checks[0]["robots"]
+        while best == 0 and R > 1:
+            R -= 1
+            rec = self.run(R, epoch0 + R, **kw)
+            checks.append(rec)
+            if rec["attainment"] >= target:
+                best = R
+        return best, checks
+
+
 def serve_main(args):
-    """Co-located serving (pi0-shaped + SmolVLA-shaped models on one GPU):
-    profile every lockstep combination under each CU restriction, build the
-    per-combination restriction table, sweep robot load in simulation on the
-    profiled durations, and check the chosen operating points in real time on
-    the GPU. Prints one JSON line."""
+    """Co-located serving studies (pi0-shaped + SmolVLA-shaped models on one
+    GPU, batch cap --serve-batch, Poisson traffic at the first --serve-rates
+    rate unless stated): every robot count reported is the largest one whose
+    real-time GPU run reaches >= 98 % SLO attainment, searched from the
+    simulated limit on the profiled lockstep durations (the simulated limit is
+    reported beside it). Arms:
+
+    * the paper's execution-mode ablation (Section 5.2, Fig. 7): Monolithic
+      (no stage disaggregation), stage disaggregation only (two streams, no
+      CU restriction), disjoint CU partition (VLM on k CUs, action stage on
+      the other 256 - k, k from a lookup table), and the guarded restriction
+      (VLM on k CUs, action stage on all; the default);
+    * queue policies RR and LQF beside ESF (Section 5.3);
+    * the paper's periodic 2 Hz traffic with per-model SLOs (Section 5.1);
+    * two fine-tuned variants of each architecture co-located (4 models);
+    * per-model GPU robot limits (simulated, each model alone) and the
+      traffic controller's assignment for a two-GPU server (Section 4.2.2).
+
+    Prints one JSON line."""
     import numpy as np
     import torch
     from paper_2609_12075_amd import serve, synth, vla
 
     names = args.serve_models.split(",")
     mb = args.serve_batch
-    cfgs = [synth.CONFIGS[n].with_(max_batch=mb) for n in names]   # workspaces sized for the serving batch
+    cfgs = [synth.CONFIGS[n].with_(max_batch=mb) for n in names]
     slo = [args.slo_ms] * len(cfgs)
     cus = [int(x) for x in args.serve_cus.split(",")]
+    rates = [float(x) for x in args.serve_rates.split(",")]
+    f0 = rates[0]
+    T, E, RM = args.serve_seconds, args.serve_epochs, args.serve_max_robots
     t0 = time.perf_counter()
     models = [vla.Model(c, synth.make_weights(c), device=0) for c in cfgs]
     log(f"[serve] models {names} created in {time.perf_counter() - t0:.1f} s")
@@ -104,117 +198,91 @@ def serve_main(args):
         m.prefill(mb, b["pixels"], b["text_ids"], b["kv0"], state=b.get("state"))
         m.prefill(mb, b["pixels"], b["text_ids"], b["kv1"], state=b.get("state"))
     torch.cuda.synchronize()
-    js = vla.nonblocking_stream(0)      # join stream of every lockstep (profile and executor alike)
+    js = vla.nonblocking_stream(0)
     t0 = time.perf_counter()
     prof = serve.profile_locksteps(models, bufs, mb, cus, reps=3, log=log, join_stream=js)
-    log(f"[serve] profiled {prof.size} lockstep entries in {time.perf_counter() - t0:.1f} s")
+    prof_dj = serve.profile_locksteps(models, bufs, mb, cus, reps=3, log=log, join_stream=js, disjoint=True)
+    log(f"[serve] profiled guarded and disjoint tables in {time.perf_counter() - t0:.1f} s")
     cu_table, dur_lut = serve.best_cu_table(prof, cus)
+    cu_dj, dur_dj = serve.best_cu_table(prof_dj, cus)
     dur_static = {cu: prof[i] for i, cu in enumerate(cus)}
-    rates = [float(x) for x in args.serve_rates.split(",")]
-    robots = list(range(1, args.serve_max_robots + 1))
-    result = {"metric": METRIC, "unit": "action chunks/s", "n_gpus": 1, "dtype": "bf16",
-              "data": "synthetic Poisson robot traffic, seeded (6000 + epoch)",
-              "config": {"workload": "co-located " + " + ".join(f"{n}-shaped" for n in names),
-                         "max_batch": mb, "slo_ms": args.slo_ms, "cu_candidates": cus, "policy": "esf",
-                         "epochs": args.serve_epochs, "trace_s": args.serve_seconds},
-              "rates": {}}
-    for f in rates:
-        rows, best = serve.sweep_robots(dur_lut, slo, mb, robots, f, args.serve_seconds, args.serve_epochs)
-        static = {}
-        for cu, d in dur_static.items():
-            _, b = serve.sweep_robots(d, slo, mb, robots, f, args.serve_seconds, args.serve_epochs)
-            static[str(cu)] = b
-        entry = {"robots_at_98_sim": best, "chunks_per_s_at_98_sim": best * f,
-                 "static_cu_robots_at_98_sim": static, "sweep": rows}
-        if best > 0 and not args.serve_no_validate:
-            for R in sorted({best, best + 1}):
-                s = serve.Scheduler(slo, mb, "esf")
-                s.set_gpu(models, bufs, join_stream=js)
-                s.set_cu(256, cu_table)
-                arr = synth.poisson_arrivals(R, f, args.validate_seconds, epoch=100, n_models=len(cfgs))
-                req, ls = s.run(arr, drain_ns=int(1e9))
-                s.close()
-                entry.setdefault("gpu_validation", []).append(
-                    {"robots": R, "attainment": serve.attainment(req), "p99_ms": serve.p99_ms(req),
-                     "locksteps": int(len(ls)), "requests": int(len(req))})
-                log(f"[serve] f={f} R={R}: GPU attainment {serve.attainment(req):.3f}, p99 {serve.p99_ms(req):.1f} ms")
-        result["rates"][str(f)] = entry
-        log(f"[serve] f={f} Hz: max robots at 98% (sim, CU table) {best}; static {static}")
-    result["cu_table"] = cu_table.tolist()
-    result["lockstep_ms_lut"] = (dur_lut / 1e6).round(3).tolist()
-    best_f = max(rates, key=lambda f: result["rates"][str(f)]["chunks_per_s_at_98_sim"])
-    result["value"] = result["rates"][str(best_f)]["chunks_per_s_at_98_sim"]
+    val = GpuValidator(models, cfgs, slo, f0, args.validate_seconds, js, RM + 2, log_prefix="[serve]")
 
-    # ---- controls and studies on the same profiled durations (simulated)
-    T, E = args.serve_seconds, args.serve_epochs
-    f0 = rates[0]
+    def arm(label, dur, sim_kw, gpu_kw, rate=f0, slo_=None, traffic="poisson", r_max=RM):
+        s = slo if slo_ is None else slo_
+        r_sim, rows = serve.max_robots(dur, s, mb, rate, T, E, traffic=traffic, r_max=r_max, **sim_kw)
+        v = val if rate == f0 else GpuValidator(models, cfgs, s, rate, args.validate_seconds, js, r_max + 2,
+                                                log_prefix="[serve]")
+        best, checks = v.search(r_sim, r_max, mb=mb, traffic=traffic, slo=s, **gpu_kw)
+        log(f"[serve] {label}: {best} robots at >= 98 % on the GPU (simulated {r_sim})")
+        return {"robots_at_98": best, "chunks_per_s": best * rate, "robots_at_98_sim": r_sim,
+                "gpu_validation": checks,
+                "attainment_by_robots_sim": {str(x["robots"]): round(x["attainment"], 4) for x in rows}}
+
     studies = {}
-    for label, d, kw in (("stage_disaggregated_esf", dur_lut, {}),
-                         ("monolithic_esf", dur_static[max(cus)], {"mode": "monolithic"}),
-                         ("stage_disaggregated_rr", dur_lut, {"policy": "rr"}),
-                         ("stage_disaggregated_lqf", dur_lut, {"policy": "lqf"})):
-        b, rows = serve.max_robots(d, slo, mb, f0, T, E, **kw)
-        at = {str(x["robots"]): round(x["attainment"], 4) for x in rows}
-        studies[label] = {"robots_at_98_sim": b, "chunks_per_s": b * f0, "attainment_by_robots": at}
-        log(f"[serve] study {label} @ {f0} Hz Poisson: {b} robots at 98%")
-    # the paper's traffic shape: periodic requests with a random phase per robot
-    # at 2 Hz, per-model SLOs (pi0-shaped 156 ms, SmolVLA-shaped 50 ms)
+    t0 = time.perf_counter()
+    # execution-mode ablation
+    studies["guarded_cu_table"] = arm("guarded (VLM restricted by the table, action stage on all CUs)", dur_lut, {},
+                                      {"cu_table": cu_table})
+    studies["disjoint_cu_table"] = arm("disjoint (VLM on k CUs, action stage on the other 256 - k)", dur_dj, {},
+                                       {"cu_table": cu_dj, "disjoint": True})
+    studies["stage_disaggregation_only"] = arm("stage disaggregation only (no restriction)", dur_static[256], {},
+                                               {"default_cu": 256})
+    studies["monolithic"] = arm("Monolithic", dur_static[256], {"mode": "monolithic"}, {"mode": "monolithic"})
+    # queue policies
+    for pol in ("rr", "lqf"):
+        studies[f"guarded_{pol}"] = arm(f"guarded, {pol.upper()}", dur_lut, {"policy": pol},
+                                        {"cu_table": cu_table, "policy": pol})
+    # the paper's traffic shape: periodic, random phase per robot, 2 Hz, per-model SLOs
     paper_slo = [{"pi0": 156.0, "smolvla": 50.0, "gr00t": 53.0}.get(n, args.slo_ms) for n in names]
-    for label, d, kw in (("periodic_2hz_paper_slo_disaggregated", dur_lut, {}),
-                         ("periodic_2hz_paper_slo_monolithic", dur_static[max(cus)], {"mode": "monolithic"})):
-        b, _ = serve.max_robots(d, paper_slo, mb, 2.0, T, E, traffic="periodic", r_max=512, **kw)
-        studies[label] = {"robots_at_98_sim": b, "chunks_per_s": b * 2.0, "slo_ms": paper_slo}
-        log(f"[serve] study {label}: {b} robots at 98%")
-    # per-model GPU robot limits (each model alone) and the traffic controller
-    # assignment they imply for a two-GPU server hosting both models
+    studies["periodic_2hz_paper_slo_guarded"] = arm("periodic 2 Hz, paper SLOs, guarded", dur_lut, {},
+                                                    {"cu_table": cu_table}, rate=2.0, slo_=paper_slo,
+                                                    traffic="periodic", r_max=4 * RM)
+    studies["periodic_2hz_paper_slo_monolithic"] = arm("periodic 2 Hz, paper SLOs, Monolithic", dur_static[256],
+                                                       {"mode": "monolithic"}, {"mode": "monolithic"}, rate=2.0,
+                                                       slo_=paper_slo, traffic="periodic", r_max=4 * RM)
+    log(f"[serve] studies validated in {time.perf_counter() - t0:.1f} s")
+    # per-model GPU robot limits (simulated, each model alone) and the
+    # traffic controller's assignment they imply for a two-GPU server
     limits = []
     for i, n in enumerate(names):
         c, _ = serve.robot_limit(dur_lut, i, slo[i], mb, f0, T, E)
         limits.append(max(c, 1))
-    # populations shaped like the paper's worked example: 1.5 GPUs' worth of
-    # the first model's robots, half a GPU's worth of the others (sum <= 2)
     pops = [max(1, int(1.5 * limits[0]))] + [max(1, int(0.5 * c / max(1, len(names) - 1))) for c in limits[1:]]
     r, obj, opt = serve.traffic_assign(np.ones((len(names), 2), dtype=int), pops, limits)
-    studies["robot_limits_alone"] = {n: c for n, c in zip(names, limits)}
+    studies["robot_limits_alone_sim"] = {n: c for n, c in zip(names, limits)}
     studies["traffic_controller_2gpu_example"] = {"populations": dict(zip(names, pops)), "assignment": r.tolist(),
                                                   "objective": obj, "optimal": opt}
-    log(f"[serve] robot limits alone {dict(zip(names, limits))}; 2-GPU assignment for {pops}: {r.tolist()} "
-        f"(eq (3) = {obj})")
-    # fine-tuned variants: two variants of each architecture (different
-    # weights, same shapes) co-located on the GPU, robot i -> model i mod 4;
-    # the variants reuse the architectures' profile
+    # fine-tuned variants: nv variants of each architecture (different weights,
+    # same shapes) co-located, robot i -> model i mod (nv * architectures); the
+    # variants reuse their architecture's profile
     nv = args.serve_variants
     if nv > 1:
         arch_of = [i % len(names) for i in range(nv * len(names))]
         vdur, vcu = serve.expand_tables(dur_lut, cu_table, arch_of)
         vslo = [args.slo_ms] * len(arch_of)
-        b, rows = serve.max_robots(vdur, vslo, mb, f0, T, E)
-        entry = {"models": [f"{names[a]}-v{i // len(names)}" for i, a in enumerate(arch_of)],
-                 "robots_at_98_sim": b, "chunks_per_s": b * f0,
-                 "attainment_by_robots": {str(x["robots"]): round(x["attainment"], 4) for x in rows}}
-        log(f"[serve] study {nv} variants per architecture ({len(arch_of)} models) @ {f0} Hz: {b} robots at 98%")
-        if b > 0 and not args.serve_no_validate:
-            vcfgs = [cfgs[a].with_(seed=cfgs[a].seed + 17 * (i // len(names))) for i, a in enumerate(arch_of)]
-            vmodels = [models[a] if i < len(names) else vla.Model(c, synth.make_weights(c), device=0)
-                       for i, (a, c) in enumerate(zip(arch_of, vcfgs))]
-            vbufs = [bufs[a] if i < len(names) else serve.alloc_io([m], mb)[0] for i, (a, m) in enumerate(zip(arch_of, vmodels))]
-            for m, bb in list(zip(vmodels, vbufs))[len(names):]:
-                m.prefill(mb, bb["pixels"], bb["text_ids"], bb["kv0"], state=bb.get("state"))
-                m.prefill(mb, bb["pixels"], bb["text_ids"], bb["kv1"], state=bb.get("state"))
-            torch.cuda.synchronize()
-            sch = serve.Scheduler(vslo, mb, "esf")
-            sch.set_gpu(vmodels, vbufs, join_stream=js)
-            sch.set_cu(256, vcu)
-            arr = synth.poisson_arrivals(b, f0, args.validate_seconds, epoch=100, n_models=len(arch_of))
-            req, ls = sch.run(arr, drain_ns=int(1e9))
-            sch.close()
-            entry["gpu_validation"] = {"robots": b, "attainment": serve.attainment(req), "p99_ms": serve.p99_ms(req),
-                                       "locksteps": int(len(ls)), "requests": int(len(req))}
-            log(f"[serve] variants: GPU attainment {serve.attainment(req):.3f} at {b} robots, p99 {serve.p99_ms(req):.1f} ms")
-            for m in vmodels[len(names):]:
-                m.close()
-        studies["fine_tuned_variants"] = entry
-    result["studies"] = studies
+        vcfgs = [cfgs[a].with_(seed=cfgs[a].seed + 17 * (i // len(names))) for i, a in enumerate(arch_of)]
+        vmodels = [models[a] if i < len(names) else vla.Model(c, synth.make_weights(c), device=0)
+                   for i, (a, c) in enumerate(zip(arch_of, vcfgs))]
+        r_sim, rows = serve.max_robots(vdur, vslo, mb, f0, T, E)
+        vv = GpuValidator(vmodels, vcfgs, vslo, f0, args.validate_seconds, js, RM + 4, log_prefix="[serve]")
+        best, checks = vv.search(r_sim, RM, mb=mb, cu_table=vcu)
+        studies["fine_tuned_variants"] = {"models": [f"{names[a]}-v{i // len(names)}" for i, a in enumerate(arch_of)],
+                                          "robots_at_98": best, "chunks_per_s": best * f0, "robots_at_98_sim": r_sim,
+                                          "gpu_validation": checks}
+        log(f"[serve] {len(arch_of)} co-located variants: {best} robots at >= 98 % on the GPU (simulated {r_sim})")
+        for m in vmodels[len(names):]:
+            m.close()
+    g = studies["guarded_cu_table"]
+    result = {"metric": METRIC, "value": float(g["chunks_per_s"]), "unit": "action chunks/s", "n_gpus": 1,
+              "dtype": "bf16", "data": "synthetic robot traffic, seeded (Poisson 6000 + epoch, periodic 7000 + epoch)",
+              "config": {"workload": "co-located " + " + ".join(f"{n}-shaped" for n in names),
+                         "max_batch": mb, "slo_ms": args.slo_ms, "rate_hz": f0, "cu_candidates": cus,
+                         "validate_s": args.validate_seconds, "sim_epochs": E, "sim_trace_s": T},
+              "cu_table": cu_table.tolist(), "cu_table_disjoint": cu_dj.tolist(),
+              "lockstep_ms_lut": (dur_lut / 1e6).round(3).tolist(), "studies": studies}
+    for m in models:
+        m.close()
     print(json.dumps(result), flush=True)
 
 
@@ -548,63 +616,9 @@ def colocated_main(args):
         f"{mb * 1e3 / ms_per_step:.1f} chunks/s")
 
     # ---- 3. real-time validation on the GPU (online executor, per-robot inputs)
-    sch = serve.Scheduler(slo, mb, "esf")
-    sch.set_gpu_online(models, join_stream=js)
-    sch.set_cu(256, cu_table)
-    n_rob_max = args.serve_max_robots + 2
-    rob_in = []
-    for i, c in enumerate(cfgs):
-        n = (n_rob_max + len(cfgs) - 1 - i) // len(cfgs)
-        inp = synth.make_inputs(c, n, first_row=100)
-        rob_in.append({k: torch.from_numpy(v).to("cuda:0") for k, v in inp.items()})
-
-    def validate(R, epoch):
-        arr = synth.poisson_arrivals(R, f, args.validate_seconds, epoch=epoch, n_models=len(cfgs))
-        outs = [torch.full((int((arr["model"] == i).sum()), c.horizon, c.action_dim), float("nan"), device="cuda:0")
-                for i, c in enumerate(cfgs)]
-        cnt = [0] * len(cfgs)
-        ios = []
-        for j in range(len(arr)):
-            mi, r = int(arr["model"][j]), int(arr["robot"][j]) // len(cfgs)
-            d = rob_in[mi]
-            ios.append(serve.Scheduler.request_io(d["pixels"][r], d["text_ids"][r], d["noise"][r], outs[mi][cnt[mi]],
-                                                  d["state"][r] if "state" in d else None))
-            cnt[mi] += 1
-        torch.cuda.synchronize()
-        req, ls = sch.run(arr, drain_ns=int(1e9), ios=ios)
-        done = req["t_done_ns"] >= 0
-        finite = all(bool(torch.isfinite(o).all()) for o, c in zip(outs, cnt) if c) if done.all() else None
-        dur = (ls["t_end_ns"] - ls["t_start_ns"]) / 1e6
-        rec = {"robots": int(R), "requests": int(len(req)), "attainment": round(serve.attainment(req), 4),
-               "p99_ms": round(serve.p99_ms(req), 2), "locksteps": int(len(ls)),
-               "lockstep_ms_mean": round(float(dur.mean()), 3) if len(dur) else None,
-               "outputs_finite": finite, "seconds": args.validate_seconds}
-        log(f"[bench] GPU R={R}: attainment {rec['attainment']:.4f}, p99 {rec['p99_ms']} ms, "
-            f"{rec['requests']} requests, {rec['locksteps']} locksteps")
-        return rec
-
     t0 = time.perf_counter()
-    checks = []
-    R = max(1, min(r_sim, args.serve_max_robots))
-    rec = validate(R, 100)
-    checks.append(rec)
-    ok = rec["attainment"] >= 0.98
-    best = R if ok else 0
-    while ok and R < args.serve_max_robots:             # one more robot
-        R += 1
-        rec = validate(R, 100 + R)
-        checks.append(rec)
-        ok = rec["attainment"] >= 0.98
-        if ok:
-            best = R
-    R = checks[0]["robots"]
-    while best == 0 and R > 1:                          # or fewer, until one passes
-        R -= 1
-        rec = validate(R, 100 + R)
-        checks.append(rec)
-        if rec["attainment"] >= 0.98:
-            best = R
-    sch.close()
+    val = GpuValidator(models, cfgs, slo, f, args.validate_seconds, js, args.serve_max_robots + 2)
+    best, checks = val.search(r_sim, args.serve_max_robots, mb=mb, cu_table=cu_table)
     value = best * f
     log(f"[bench] GPU-validated: {best} robots at >= 98 % -> {value} action chunks/s "
         f"({time.perf_counter() - t0:.1f} s of validation)")
@@ -726,7 +740,8 @@ def main():
     ap.add_argument("--serve-epochs", type=int, default=5)
     ap.add_argument("--serve-no-validate", action="store_true")
     ap.add_argument("--serve-variants", type=int, default=2, help="fine-tuned variants per architecture in the co-location study")
-    ap.add_argument("--validate-seconds", type=float, default=20.0)
+    ap.add_argument("--validate-seconds", type=float, default=20.0,
+                    help="seconds of real-time traffic per GPU validation run")
     ap.add_argument("--slo-ms", type=float, default=100.0)
     ap.add_argument("--stages", action="store_true", help="stage times per config and batch instead of the lockstep bench")
     ap.add_argument("--stage-configs", default="tiny,smolvla,smolvla_vit,pi0,gr00t")

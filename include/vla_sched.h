@@ -103,6 +103,14 @@ vla_status vla_sched_set_gpu_executor(vla_sched s, const vla_sched_model_io* io,
  * is LOCKSTEP. Monolithic ignores the CU table. */
 vla_status vla_sched_set_mode(vla_sched s, int mode);
 
+/* Partition of the compute units between the two halves of a lockstep: 0
+ * (the default, the paper's guarded restriction) restricts only the VLM half
+ * and lets the action half use every CU; 1 (the disjoint partition the paper
+ * compares against, Section 5.2) also restricts the action half, to the
+ * 256 - k CUs the VLM half may not use (k = the lockstep's VLM restriction;
+ * k = 256 leaves both halves unrestricted). Monolithic mode ignores it. */
+vla_status vla_sched_set_disjoint(vla_sched s, int disjoint);
+
 /* CU restriction of the VLM stream per lockstep: `default_cu` (multiple of 8,
  * 8 .. 256) unless `cu_table` (same indexing as the duration table, entries 0
  * = use default) names another count for the batch combination (the

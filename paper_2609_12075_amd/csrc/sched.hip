@@ -83,6 +83,7 @@ struct vla_sched_s {
   hipStream_t join = nullptr;
   int default_cu = 256;
   std::vector<int> cu_table;
+  int disjoint = 0;                          // action half on the complement of the VLM's CUs
   // serving state
   std::vector<std::deque<Req>> q;
   std::vector<Req> buf;                      // admitted one lockstep ago, waiting for the action stage
@@ -199,6 +200,7 @@ void vla_sched_s::gpu_online_exec(int mv, const std::vector<Req>& vreq, int ma, 
     if (bv > 0) vlm_half(a, slot);
     if (ba > 0) act_half(a, ma, ba, buf_slot);
     a.vlm_cu_count = cu;
+    a.adit_cu_count = disjoint && cu < 256 ? 256 - cu : 0;
     st = vla_step(&a, join);
   }
   if (st != VLA_OK) throw VlaError{(int)st, std::string("lockstep: ") + vla_last_error()};
@@ -297,6 +299,7 @@ void vla_sched_s::lockstep(int64_t now, vla_lockstep_rec& rec, std::vector<Req>*
       a.kv_in = x.kv[buf_slot]; a.noise = x.noise; a.steps = x.steps; a.actions_out = x.actions[buf_slot];
     }
     a.vlm_cu_count = cu;
+    a.adit_cu_count = disjoint && cu < 256 ? 256 - cu : 0;
     vla_status st = vla_step(&a, join);
     if (st != VLA_OK) throw VlaError{(int)st, std::string("lockstep: ") + vla_last_error()};
     VLA_HIP(hipStreamSynchronize(join));
@@ -425,6 +428,13 @@ vla_status vla_sched_set_mode(vla_sched s, int mode) {
     VLA_REQUIRE(s, "null scheduler");
     VLA_REQUIRE(mode == VLA_SCHED_LOCKSTEP || mode == VLA_SCHED_MONOLITHIC, "unknown execution mode");
     s->mode = mode;
+  });
+}
+
+vla_status vla_sched_set_disjoint(vla_sched s, int disjoint) {
+  return guard([&] {
+    VLA_REQUIRE(s, "null scheduler");
+    s->disjoint = disjoint != 0;
   });
 }
 

@@ -57,6 +57,7 @@ def _lib():
         L.vla_sched_run.argtypes = [vp, vp, vp, ci, i64, vp, vp, ci, ctypes.POINTER(ci)]
         L.vla_sched_run.restype = ci
         L.vla_sched_set_gpu_online.argtypes = [vp, vp, vp, vp]; L.vla_sched_set_gpu_online.restype = ci
+        L.vla_sched_set_disjoint.argtypes = [vp, ci]; L.vla_sched_set_disjoint.restype = ci
         L.vla_sched_clock_ns.argtypes = [vp]; L.vla_sched_clock_ns.restype = i64
         L.vla_sched_reset.argtypes = [vp]; L.vla_sched_reset.restype = ci
         L.vla_sched_submit.argtypes = [vp, i64, ci, i64, vp]; L.vla_sched_submit.restype = ci
@@ -144,6 +145,11 @@ class Scheduler:
             io.steps = m.cfg.steps
         self._keep.append((models, bufs))
         vla._check(_lib().vla_sched_set_gpu_executor(self.handle, ctypes.addressof(ios), vla._stream(join_stream)))
+
+    def set_disjoint(self, enabled: bool):
+        """Disjoint CU partition: the action half runs on the CUs the VLM half
+        may not use (the paper's comparison point) instead of on all of them."""
+        vla._check(_lib().vla_sched_set_disjoint(self.handle, int(bool(enabled))))
 
     def set_gpu_online(self, models: Sequence[vla.Model], join_stream=None):
         """Online GPU executor: the library allocates max_batch stage rows per
@@ -243,12 +249,13 @@ def alloc_io(models: Sequence[vla.Model], max_batch: int):
 
 
 def profile_locksteps(models: Sequence[vla.Model], bufs, max_batch: int, cu_counts: Sequence[int],
-                      reps: int = 3, warmup: int = 1, log=None, join_stream=None):
+                      reps: int = 3, warmup: int = 1, log=None, join_stream=None, disjoint: bool = False):
     """Median duration (ns) of one lockstep for every (VLM model, VLM batch,
     action model, action batch) combination and every CU restriction of the
     VLM stream, timed with HIP events on the join stream. Returns
     dur[k_index][mv][bv][ma][ba] (int64; combinations with both halves empty
-    are 0) — the profiling pass behind the restriction lookup table."""
+    are 0) — the profiling pass behind the restriction lookup table. With
+    disjoint=True the action half runs on the complementary 256 - k CUs."""
     import torch
     nm, nb = len(models), n_buckets(max_batch)
     bs = bucket_batches(max_batch)
@@ -272,7 +279,8 @@ def profile_locksteps(models: Sequence[vla.Model], bufs, max_batch: int, cu_coun
                         def one():
                             vla.step(models[mv] if bv else None, bv, xv["pixels"], xv["text_ids"], xv["kv0"],
                                      models[ma] if ba else None, ba, xa["kv1"], xa["noise"], models[ma].cfg.steps,
-                                     xa["act1"], vlm_cu_count=cu, state=xv.get("state"), join_stream=join_stream)
+                                     xa["act1"], vlm_cu_count=cu, state=xv.get("state"), join_stream=join_stream,
+                                     adit_cu_count=256 - cu if disjoint and cu < 256 else 0)
                         for _ in range(warmup):
                             one()
                         ts = []

@@ -87,13 +87,15 @@ def _served_batches(arr, ls, n_models):
     return out
 
 
-def test_online_executor_gathers_and_scatters_per_request():
+@pytest.mark.parametrize("disjoint", [False, True], ids=["guarded", "disjoint"])
+def test_online_executor_gathers_and_scatters_per_request(disjoint):
     """Requests bring their own seeded inputs (row i of the generators for
     request i) and their own output buffers; the library gathers them into
     its stage rows and scatters each chunk back. Every chunk equals a
     standalone run of the batch it was served in (same rows, same order),
     so a wrong gather or scatter row fails; DiT requests alternate between a
-    given state and none (zeros)."""
+    given state and none (zeros). Both CU partitions: the guarded one (only
+    the VLM half restricted) and the disjoint one."""
     import torch
     from paper_2609_12075_amd import serve
     cfgs = [A, B, C]
@@ -102,6 +104,7 @@ def test_online_executor_gathers_and_scatters_per_request():
     s = serve.Scheduler([100.0, 100.0, 100.0], mbatch, "esf")
     s.set_gpu_online(ms)
     s.set_cu(128)
+    s.set_disjoint(disjoint)      # disjoint: the action half on the other 128 CUs
     arr = synth.poisson_arrivals(6, 15.0, 0.8, epoch=3, n_models=3)
     log(f"[serving] online: {len(arr)} requests, 3 models")
     ins, outs, ios, keep = [], [], [], []
