@@ -720,8 +720,12 @@ static void attn_plan(const AttnArgs& a, int& splits, int& kchunk, int& ks) {
   const int rows = (a.Hq / a.Hkv) * a.Lq;
   const long blocks = (long)((rows + BQ - 1) / BQ) * a.Hkv * a.B;
   const int total = a.seg[0].len + a.seg[1].len, ntiles = (total + BKV - 1) / BKV;
-  const bool v2 = a.zeros && (a.hd <= 64 || a.hd > 96);
-  ks = (v2 && a.hd > 32 && blocks < 256) ? 2 : 1;
+  const bool v2 = a.zeros != nullptr;
+  // two key groups per block when the grid leaves CUs free, and always at
+  // head dim 256, where the second group of waves hides the per-tile latency
+  // of the large output accumulators (bidirectional pi0-shaped prefill over
+  // 816 keys: 155 -> 115 us at batch 8)
+  ks = (v2 && a.hd > 32 && (blocks < 256 || a.hd > 128)) ? 2 : 1;
   splits = 1;
   kchunk = ntiles * BKV;
   if (!a.ws || ntiles < 2) return;
@@ -763,10 +767,13 @@ void launch_attention(const AttnArgs& a, hipStream_t s) {
   attn_plan(a, b.splits, b.kchunk, ks);
   const int rows = (a.Hq / a.Hkv) * a.Lq;
   dim3 grid((rows + BQ - 1) / BQ, a.Hkv, a.B * b.splits);
-  // head dims whose rows are a power-of-two number of 16-byte chunks use the
-  // direct-load kernel; 72 (the ViT's, padded to 96) and callers without a
-  // zero buffer use the register-staged one
-  const bool v2 = a.zeros && (a.hd <= 64 || a.hd > 96);
+  // the direct-load kernel serves every head dim (a multiple of 8) with a
+  // zero buffer, padded to the next of 32, 64, 128, 256 (chunks past hd load
+  // zeros and are not stored): the ViT's 72 runs on the 128-wide variant
+  // (54.8 -> 33.4 us per pi0-shaped layer at batch 8 against the
+  // register-staged kernel padded to 96); callers without a zero buffer use
+  // the register-staged one
+  const bool v2 = a.zeros != nullptr;
   if (v2 && a.hd <= 32) hipLaunchKernelGGL((attn_v2_kernel<32, 1>), grid, dim3(256), 0, s, b);
   else if (v2 && a.hd <= 64 && ks == 2) hipLaunchKernelGGL((attn_v2_kernel<64, 2>), grid, dim3(512), 0, s, b);
   else if (v2 && a.hd <= 64) hipLaunchKernelGGL((attn_v2_kernel<64, 1>), grid, dim3(256), 0, s, b);
