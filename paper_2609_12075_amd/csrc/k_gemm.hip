@@ -1114,8 +1114,15 @@ static GemmPlan plan_base(const GemmArgs& a) {
       return p;
     }
     // long-K products with enough 256 x 256 tiles: the large-tile kernel
-    // (measured ahead of the staged tiles from K = 2048 on)
-    if (a.M >= 256 && a.K >= 2048 && blocks(256, 256) >= 160) {
+    // (measured ahead of the staged tiles from K = 2048 on), unless its last
+    // round of tiles leaves the chip mostly idle where the 128 x 128 staged
+    // tiles fill theirs: per K-step of 64, a round of 256 large tiles (one
+    // per CU) measured 2.1 us and a round of 512 staged tiles (two per CU)
+    // 1.2 us (e.g. the 2560-wide QKV projection of 6528 rows: 260 large tiles
+    // in two rounds, 124 us, against 1020 staged tiles in two rounds, 76 us)
+    const long t256 = blocks(256, 256), t128 = blocks(128, 128);
+    if (a.M >= 256 && a.K >= 2048 && t256 >= 160 &&
+        (t256 + 255) / 256 * 2.1 <= (t128 + 511) / 512 * 1.2) {
       p.bn = 256; p.bm = 256; p.kind = 3;
       p.ksplit = nk * BK;
       return p;
@@ -1136,7 +1143,7 @@ static GemmPlan plan_base(const GemmArgs& a) {
     // launches sized for all 256 CUs ran a second round there.
     constexpr long kOneRoundCUs = 192;
     if (a.M <= 1024 && a.K <= 4096 && (a.M > 64 || (a.N < 1536 && a.K >= 2048))) {
-      const long t64 = blocks(64, 64), t128 = blocks(128, 128);
+      const long t64 = blocks(64, 64);
       const int nk128 = (a.K + 127) / 128;
       double best_t = 1e30;
       int best_s = 0;
