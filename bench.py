@@ -315,6 +315,66 @@ def counters_main(args):
     m.close()
 
 
+def sync_costs_main(args):
+    """What a hand-off between dependent phases costs: a kernel boundary inside
+    a replayed graph (empty kernels, and kernels whose blocks each write 4 or
+    16 KiB) against a grid-wide barrier inside one kernel (release add /
+    acquire polls at agent scope), with the same writes before and a read of
+    another block's slice after each barrier. Median of 5 timings of 200
+    boundaries or barriers; one JSON line."""
+    import torch
+    from paper_2609_12075_amd import vla
+    dev = torch.device("cuda:0")
+    ts = vla.nonblocking_stream(0)
+    s = ts
+    n = 200
+    buf = torch.zeros(2 * 256 * 4096, dtype=torch.float32, device=dev)
+    sink = torch.zeros(256 * 256, dtype=torch.float32, device=dev)
+    ctr = torch.zeros(1, dtype=torch.int32, device=dev)
+    err = torch.zeros(1, dtype=torch.int32, device=dev)
+
+    def timed(fn, reps=5):
+        out = []
+        for _ in range(reps):
+            torch.cuda.synchronize()
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(ts)
+            fn()
+            b.record(ts)
+            torch.cuda.synchronize()
+            out.append(a.elapsed_time(b) * 1e3)
+        return sorted(out)[len(out) // 2]
+
+    res = {"metric": "hand-off cost between dependent phases", "unit": "us", "count": n}
+    for grid in (128, 256):
+        for kind, words in ((0, 0), (1, 1024), (1, 4096)):
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.stream(ts):
+                vla.debug_sync_probe(kind, grid, n, words, buf=buf, sink=sink, stream=s)
+                torch.cuda.synchronize()
+                g.capture_begin()
+                vla.debug_sync_probe(kind, grid, n, words, buf=buf, sink=sink, stream=s)
+                g.capture_end()
+            torch.cuda.synchronize()
+            key = f"kernel_boundary_grid{grid}_{words * 4 // 1024}KiB"
+            with torch.cuda.stream(ts):
+                res[key] = round(timed(g.replay) / n, 3)
+            del g
+        for words in (0, 1024, 4096):
+            def run():
+                ctr.zero_()
+                vla.debug_sync_probe(2, grid, n, words, buf=buf, ctr=ctr, err=err, sink=sink, stream=s)
+            err.zero_()
+            with torch.cuda.stream(ts):
+                t = timed(run)
+            res[f"grid_barrier_grid{grid}_{words * 4 // 1024}KiB"] = round(t / n, 3)
+            res[f"grid_barrier_grid{grid}_{words * 4 // 1024}KiB_overruns"] = int(err.item())
+            if int(ctr.item()) != n * grid:
+                raise RuntimeError(f"barrier counter ended at {int(ctr.item())}, expected {n * grid}")
+        log(f"[sync] grid {grid}: " + ", ".join(f"{k}={v}" for k, v in res.items() if f"grid{grid}_" in k))
+    print(json.dumps(res), flush=True)
+
+
 def stage_flops(c) -> tuple:
     """Algorithmic flops per request of the two stages as the library computes
     them (2 M N K per projection, 4 n_q hd Lq Lk per attention; the joint
@@ -743,6 +803,8 @@ def main():
     ap.add_argument("--validate-seconds", type=float, default=20.0,
                     help="seconds of real-time traffic per GPU validation run")
     ap.add_argument("--slo-ms", type=float, default=100.0)
+    ap.add_argument("--sync-costs", action="store_true",
+                    help="kernel-boundary vs in-kernel grid-barrier cost (what fusing dependent phases would trade)")
     ap.add_argument("--stages", action="store_true", help="stage times per config and batch instead of the lockstep bench")
     ap.add_argument("--stage-configs", default="tiny,smolvla,smolvla_vit,pi0,gr00t")
     ap.add_argument("--stage-batches", default="1,4,16")
@@ -763,6 +825,9 @@ def main():
         return
     if args.stages:
         stages_main(args)
+        return
+    if args.sync_costs:
+        sync_costs_main(args)
         return
     if not args.lockstep:
         colocated_main(args)

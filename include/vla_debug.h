@@ -105,6 +105,28 @@ vla_status vla_debug_cu_probe(int device, int cu_count, int from_top, int blocks
                               uint32_t* out, hipStream_t join);
 
 /*
+ * Cost of handing data between workgroups on different XCDs: the kernel
+ * boundary against a grid-wide barrier inside one kernel. kind 0: enqueue
+ * `iters` launches of an empty kernel of `grid` 256-thread blocks; kind 1:
+ * `iters` launches in which every block writes `words` floats of its slice of
+ * buf; kind 2: one launch that runs `iters` grid barriers, each after the
+ * blocks write their slices and followed by every block reading another
+ * block's slice (release add / acquire polls of *ctr at agent scope). For
+ * timing with events around the call (or around a graph that captured it).
+ *  buf  device fp32 [2 * grid * words] (kind 2 alternates halves by round;
+ *       kinds 0 and 1 use the first half; may be NULL when words == 0).
+ *  ctr  device uint32, zero before a kind-2 call; ends at iters * grid.
+ *  err  device int32: kind 2 adds the number of polls that passed spin_limit
+ *       (the block then went on without the barrier; 0 on a correct run).
+ *  sink device fp32 [grid * 256] (the reads' sums, so they are not elided).
+ * grid <= 256 so that every block of the barrier kernel is resident at once on
+ * an otherwise idle GPU; iters <= 1000, words <= 16384, spin_limit in
+ * [1, 1e6] (polls ~64 cycles apart). Status 1 on bad arguments.
+ */
+vla_status vla_debug_sync_probe(int kind, int grid, int iters, int words, int spin_limit, float* buf, unsigned* ctr,
+                                int* err, float* sink, hipStream_t stream);
+
+/*
  * Enqueue `iters` launches of one projection of a model's stage, exactly as
  * the stage launches it (same kernel, shape, epilogue, parameters and
  * workspace buffers), on `stream`, and store the algorithmic flops of one

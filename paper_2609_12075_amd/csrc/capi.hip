@@ -564,6 +564,19 @@ vla_status vla_debug_cu_probe(int device, int cu_count, int from_top, int blocks
   });
 }
 
+vla_status vla_debug_sync_probe(int kind, int grid, int iters, int words, int spin_limit, float* buf, unsigned* ctr,
+                                int* err, float* sink, hipStream_t s) {
+  return guarded([&] {
+    VLA_REQUIRE(kind >= 0 && kind <= 2, "kind must be 0 (empty kernels), 1 (writing kernels) or 2 (grid barriers)");
+    VLA_REQUIRE(grid >= 1 && grid <= 256, "grid must be in [1, 256] (the barrier needs every block resident)");
+    VLA_REQUIRE(iters >= 1 && iters <= 1000 && words >= 0 && words <= 16384, "iters or words out of range");
+    VLA_REQUIRE(spin_limit >= 1 && spin_limit <= 1000000, "spin_limit out of range");
+    VLA_REQUIRE(sink && (words == 0 || buf) && (kind != 2 || (ctr && err)), "missing buffer");
+    launch_sync_probe(kind, grid, iters, words, spin_limit, buf, ctr, err, sink, s);
+    VLA_HIP(hipGetLastError());
+  });
+}
+
 vla_status vla_debug_replay_gemm(vla_model m, int which, int batch, int iters, hipStream_t s, double* flops,
                                  int* plan) {
   return guarded([&] {

@@ -235,6 +235,8 @@ void launch_scale_cols_bf16(void* W, long N, int K, int ldk, const float* g, hip
 // Debug probe: each workgroup writes its hardware placement (XCC id, SE id,
 // CU id) to out[block] as one word: xcc << 16 | se << 8 | cu.
 void launch_cu_probe(uint32_t* out, int blocks, int spin, hipStream_t s);
+void launch_sync_probe(int kind, int grid, int iters, int words, int spin_limit, float* buf, unsigned* ctr, int* err,
+                       float* sink, hipStream_t s);
 // Merge s x s blocks of each image's g x g patch tokens ([n_img][g*g][d],
 // raster order) into [n_img][(g/s)^2][s*s*d]: block (I, J) in raster order,
 // its tokens (s*I + di, s*J + dj) in (di, dj) order, channels innermost.

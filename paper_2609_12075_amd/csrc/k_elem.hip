@@ -297,3 +297,64 @@ void launch_batched_copy(const CopySeg* segs, int n, long long max_bytes, hipStr
 void launch_cu_probe(uint32_t* out, int blocks, int spin, hipStream_t s) {
   hipLaunchKernelGGL(cu_probe_kernel, dim3(blocks), dim3(64), 0, s, out, spin);
 }
+
+// Synchronisation-cost probes. sync_empty_kernel does nothing (a kernel
+// boundary alone); sync_write_kernel has every block write `words` floats of
+// its own slice (a boundary after a tile's worth of stores).
+__global__ void __launch_bounds__(256) sync_empty_kernel(float* sink) {
+  if (sink && threadIdx.x > 1024) sink[0] = 0.f;   // never taken
+}
+
+__global__ void __launch_bounds__(256) sync_write_kernel(float* buf, int words) {
+  float* b = buf + (long)blockIdx.x * words;
+  for (int i = threadIdx.x; i < words; i += 256) b[i] = (float)i;
+}
+
+// `iters` grid-wide barriers inside one kernel. Before each, every block
+// writes `words` floats of its own slice; after it, the block reads the slice
+// of another block (a hand-off between XCDs). Slices alternate between two
+// halves of buf by round, so a block that runs ahead into the next round
+// never overwrites what a slower block still reads. Thread 0 adds to a monotone
+// counter with release semantics at agent scope and polls it with acquire
+// loads until every block of the round has arrived; past `spin_limit` polls
+// it counts an overrun in *err and goes on, so every block always finishes.
+// Needs every block resident at once (grid <= the CUs).
+__global__ void __launch_bounds__(256) sync_barrier_kernel(unsigned* ctr, int iters, int spin_limit, int* err,
+                                                           float* buf, int words, float* sink) {
+  __shared__ int overrun;
+  float acc = 0.f;
+  const unsigned G = gridDim.x;
+  for (int it = 0; it < iters; ++it) {
+    float* half = buf + (long)(it & 1) * G * words;
+    float* mine = half + (long)blockIdx.x * words;
+    for (int i = threadIdx.x; i < words; i += 256) mine[i] = (float)(i + it);
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      overrun = 0;
+      __hip_atomic_fetch_add(ctr, 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+      const unsigned target = (unsigned)(it + 1) * G;
+      int n = 0;
+      while (__hip_atomic_load(ctr, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT) < target) {
+        if (++n > spin_limit) { overrun = 1; break; }
+        __builtin_amdgcn_s_sleep(1);
+      }
+      if (overrun) __hip_atomic_fetch_add(err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    __syncthreads();
+    const float* other = half + (long)((blockIdx.x + 37) % G) * words;
+    for (int i = threadIdx.x; i < words; i += 256) acc += other[i];
+    __syncthreads();
+  }
+  sink[(long)blockIdx.x * 256 + threadIdx.x] = acc;
+}
+
+void launch_sync_probe(int kind, int grid, int iters, int words, int spin_limit, float* buf, unsigned* ctr, int* err,
+                       float* sink, hipStream_t s) {
+  if (kind == 0) {
+    for (int i = 0; i < iters; ++i) hipLaunchKernelGGL(sync_empty_kernel, dim3(grid), dim3(256), 0, s, sink);
+  } else if (kind == 1) {
+    for (int i = 0; i < iters; ++i) hipLaunchKernelGGL(sync_write_kernel, dim3(grid), dim3(256), 0, s, buf, words);
+  } else {
+    hipLaunchKernelGGL(sync_barrier_kernel, dim3(grid), dim3(256), 0, s, ctr, iters, spin_limit, err, buf, words, sink);
+  }
+}

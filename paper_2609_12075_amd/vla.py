@@ -27,7 +27,7 @@ VLA_OK, VLA_EINVAL, VLA_ENOMEM, VLA_EHIP, VLA_EUNSUPPORTED = range(5)
 EXPORTS = ["vla_weight_count", "vla_create_model", "vla_destroy_model", "vla_set_graphs", "vla_kv_bytes",
            "vla_prefill", "vla_prefill_ex", "vla_denoise", "vla_step", "vla_last_error", "vla_shutdown",
            "vla_debug_gemm", "vla_debug_resid_norm", "vla_debug_gemm_rms", "vla_debug_resid_copy", "vla_debug_attention",
-           "vla_debug_cu_probe", "vla_debug_replay_gemm", "vla_gemm_noalloc"]
+           "vla_debug_cu_probe", "vla_debug_replay_gemm", "vla_gemm_noalloc", "vla_debug_sync_probe"]
 
 
 class VlaError(RuntimeError):
@@ -89,6 +89,8 @@ def lib():
         L.vla_debug_attention.argtypes = [ci, ci, ci, ci, ci, ci, vp, vp, vp, ci, vp, vp, ci, vp, vp]
         L.vla_debug_attention.restype = ci
         L.vla_debug_cu_probe.argtypes = [ci, ci, ci, ci, ci, ci, vp, vp]; L.vla_debug_cu_probe.restype = ci
+        L.vla_debug_sync_probe.argtypes = [ci, ci, ci, ci, ci, vp, vp, vp, vp, vp]
+        L.vla_debug_sync_probe.restype = ci
         L.vla_debug_replay_gemm.argtypes = [vp, ci, ci, ci, vp, ctypes.POINTER(ctypes.c_double),
                                             ctypes.POINTER(ctypes.c_int)]
         L.vla_debug_replay_gemm.restype = ci
@@ -353,6 +355,15 @@ def debug_attention(q, k0, v0, k1=None, v1=None, stream=None):
     _check(lib().vla_debug_attention(B, Hq, Hkv, Lq, hd, et, _ptr(q), _ptr(k0), _ptr(v0), len0, _ptr(k1), _ptr(v1),
                                      len1, _ptr(o), _stream(stream)))
     return o
+
+
+def debug_sync_probe(kind: int, grid: int, iters: int, words: int = 0, spin_limit: int = 200000, buf=None, ctr=None,
+                     err=None, sink=None, stream=None):
+    """vla_debug_sync_probe: kind 0 `iters` empty kernels, 1 `iters` kernels
+    writing `words` floats per block, 2 one kernel running `iters` grid
+    barriers (ctr must be zero; err collects spin overruns)."""
+    _check(lib().vla_debug_sync_probe(kind, grid, iters, words, spin_limit, _ptr(buf), _ptr(ctr), _ptr(err), _ptr(sink),
+                                      _stream(stream)))
 
 
 def debug_cu_probe(cu_count: int, blocks: int, spin: int = 200, from_top: bool = False, device: int = 0, stream=None,

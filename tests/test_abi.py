@@ -71,3 +71,21 @@ def test_null_arguments_rejected():
     assert L.vla_kv_bytes(None, 1) == 0
     assert L.vla_step(None, None) == vla.VLA_EINVAL
     assert "null" in L.vla_last_error().decode()
+
+
+@pytest.mark.parametrize("args,msg", [
+    ((3, 64, 10, 0, 100), "kind must be"),
+    ((2, 300, 10, 0, 100), "grid must be"),
+    ((2, 64, 0, 0, 100), "iters or words"),
+    ((1, 64, 10, 20000, 100), "iters or words"),
+    ((2, 64, 10, 0, 0), "spin_limit"),
+])
+def test_sync_probe_rejects_bad_arguments_without_gpu(args, msg):
+    import ctypes
+    from paper_2609_12075_amd import vla
+    L = vla.lib()
+    assert L.vla_debug_sync_probe(*args, None, None, None, ctypes.c_void_p(16), None) == 1
+    assert msg in L.vla_last_error().decode()
+    # a barrier run without its counter is refused before anything launches
+    assert L.vla_debug_sync_probe(2, 64, 10, 0, 100, None, None, None, ctypes.c_void_p(16), None) == 1
+    assert "missing buffer" in L.vla_last_error().decode()

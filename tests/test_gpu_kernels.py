@@ -298,3 +298,26 @@ def test_cu_masked_streams_confine_graph_replays():
         assert len(got) >= k // 2, "a replayed graph spreads over the stream's CUs"
         if len(direct) == k:          # the direct launch reached every CU of the mask
             assert got <= direct
+
+
+def test_sync_probe_barriers_hand_off_data():
+    """The grid-barrier probe: every block arrives at every barrier (the
+    counter ends at iters x grid, no poll overruns) and each block's reads
+    after a barrier see the other block's writes of that round."""
+    import torch
+    from paper_2609_12075_amd import vla
+    grid, iters, words = 64, 12, 1000
+    buf = torch.zeros(2 * grid * words, dtype=torch.float32, device="cuda:0")
+    sink = torch.zeros(grid * 256, dtype=torch.float32, device="cuda:0")
+    ctr = torch.zeros(1, dtype=torch.int32, device="cuda:0")
+    err = torch.zeros(1, dtype=torch.int32, device="cuda:0")
+    log(f"[sync probe] grid={grid} iters={iters} words={words}")
+    vla.debug_sync_probe(2, grid, iters, words, buf=buf, ctr=ctr, err=err, sink=sink)
+    torch.cuda.synchronize()
+    assert int(ctr.item()) == grid * iters
+    assert int(err.item()) == 0
+    # thread t of every block sums (i + it) over its strided i < words, it < iters
+    t = np.arange(256)
+    want = np.array([sum(i + it for it in range(iters) for i in range(tt, words, 256)) for tt in t], dtype=np.float64)
+    got = sink.view(grid, 256).cpu().numpy().astype(np.float64)
+    assert np.array_equal(got, np.broadcast_to(want, got.shape))
