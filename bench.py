@@ -974,7 +974,8 @@ def main():
                 "us_per_launch": round(us, 3), "launches_per_step": per_step[dom]}
 
     out = {
-        "metric": METRIC, "value": round(value, 2), "unit": "action chunks/s", "n_gpus": 1, "steps": K,
+        "metric": "saturated lockstep throughput of one model (not the serving metric)", "value": round(value, 2),
+        "unit": "action chunks/s", "n_gpus": 1, "steps": K,
         "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4), "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": dtype,
         "data": "synthetic (seeded U[0,1) pixels, U[0,1000) text ids, N(0,1) noise; random-init N(0,0.02) weights)",
