@@ -653,9 +653,12 @@ def colocated_main(args):
     nb = serve.n_buckets(mb)
     full = nb - 1                            # bucket of the serving batch
 
-    # ---- timed steps: saturated locksteps alternating the two model pairings
+    # ---- timed steps: saturated locksteps cycling through the model pairings
+    # (model k mod n's VLM stage beside model k + 1 mod n's action stage)
+    n_models = len(models)
+
     def lockstep(k):
-        mv, ma = k % 2, (k + 1) % 2
+        mv, ma = k % n_models, (k + 1) % n_models
         xv, xa = bufs[mv], bufs[ma]
         vla.step(models[mv], mb, xv["pixels"], xv["text_ids"], xv["kv0"], models[ma], mb, xa["kv1"], xa["noise"],
                  cfgs[ma].steps, xa["act1"], vlm_cu_count=int(cu_table[mv, full, ma, full]), state=xv.get("state"),
