@@ -2,9 +2,10 @@
  * vla.h - C ABI of libvla.so: one batched VLA inference step on an MI355X.
  *
  * The paper's VLA models run in two stages (Section 2.1, Fig. 1): a VLM stage
- * turns camera images and a text prompt into intermediate state ("hidden
- * states or a small KV cache"), and an action diffusion transformer (ADiT)
- * runs a fixed number of diffusion steps to produce a chunk of actions. The
+ * encodes the robot's camera frames and its instruction text and hands the
+ * action model either hidden states or a compact per-layer KV cache, and an
+ * action diffusion transformer (ADiT) denoises for a set number of steps into
+ * a chunk of actions. The
  * serving engine (Section 4.1) runs the two stages as separate fixed-size
  * batches on two GPU streams, one lockstep at a time, restricting the compute
  * units the VLM stream may occupy (Section 4.1.2) and ordering requests by

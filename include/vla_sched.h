@@ -2,13 +2,13 @@
  * vla_sched.h - host-side serving scheduler of libvla.so (paper Section 4.1).
  *
  * Requests of co-located models wait in one FIFO queue per model. Work runs
- * in locksteps (Section 4.1.2): at the start of lockstep k the scheduler
+ * in locksteps (Section 4.1.2): when lockstep k begins, the scheduler
  * picks a queue, dequeues a fixed batch of b_k requests for the VLM stage,
  * and the action stage runs the batch that finished the VLM stage in
  * lockstep k-1 (held in a two-slot hand-off buffer, slot = k mod 2). The
  * lockstep ends when both stages have finished. Queue choice (Section 4.1.3):
- * earliest-SLO-first picks the queue whose head request has the least time
- * left before its deadline (SLO minus time already waited); ties go to the
+ * earliest-SLO-first serves the queue whose oldest request is closest to
+ * its deadline (SLO minus time already waited); ties go to the
  * lowest model index. Batch size: the largest power of two not above
  * min(pending requests in that queue, max_batch), so every lockstep replays a
  * pre-captured graph (Section 4.1.2). A request meets its SLO when its

@@ -3,17 +3,17 @@
 Restates the serving rules of the paper for the scheduler tests; it shares
 no code with the library's C++ scheduler.
 
-* Section 4.1.2 (lockstep execution): work advances in locksteps. At the
-  start of lockstep k a fixed batch is admitted to the VLM stage; the action
+* Section 4.1.2 (lockstep execution): work advances in locksteps. When
+  lockstep k begins, a fixed batch is admitted to the VLM stage; the action
   stage runs, in the same lockstep, the batch that finished the VLM stage in
   lockstep k-1 (kept in a small hand-off buffer). The next lockstep starts
   when both stages of this one have finished. When fewer than max_batch
   requests are pending, the admitted batch is a power of two so a
   pre-recorded graph exists for it (reading: the largest power of two not
   above min(pending, max_batch); the printed sentence is garbled).
-* Section 4.1.3 (SLO-aware dual-stream serving): one FIFO queue per model;
-  at each lockstep start the queue whose head request has the least time
-  left before its deadline (SLO minus time already waited) is served
+* Section 4.1.3 (several models on one VLM and one action stream): one FIFO
+  queue per model; when a lockstep begins, the queue whose oldest request is
+  closest to its deadline (SLO minus time already waited) is served
   (reading: ties go to the lowest model index). Round robin and
   largest-queue-first are the comparison policies of Section 5.3.
 * Section 5.1: a request meets its SLO when its end-to-end latency is within

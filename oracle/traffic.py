@@ -2,8 +2,8 @@
 infrastructure; plain Python, tiny instances only).
 
 Section 4.2.2 (adaptive traffic controller): given, for every served model
-i, its robot population N_i and the number of robots C_i one GPU can serve
-for it within the SLO target, and a placement (which GPUs host which
+i, the number N_i of its robots to serve and the number C_i of them that one
+GPU can serve within the SLO target, and a placement (which GPUs host which
 models), choose integer robot counts r[i][j] >= 0 (zero where GPU j does not
 host model i) such that
 

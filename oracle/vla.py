@@ -12,7 +12,8 @@ stated in its docstring):
   (optionally through a pre-LN ViT), text ids are embedded, and the
   concatenated prefix runs through a Gemma-style LLM. Each layer's
   post-RoPE keys and values are the per-layer prefix KV cache handed to the
-  action stage ("hidden states or a small KV cache", Section 2.1).
+  action stage (Section 2.1: the VLM passes either hidden states or a
+  per-layer KV cache to the action model).
 * Action stage (``denoise``): a flow-matching Euler loop of N steps
   (Section 2.1: 5-10 diffusion steps, a chunk of 10-50 actions). For the
   joint action expert every layer's action tokens attend over

@@ -2,8 +2,8 @@
 
 This module holds no arithmetic of the method. It defines
 
-* the model configurations (shapes of the two-stage VLA: a VLM that turns
-  camera images and a text prompt into per-layer prefix state, and an action
+* the model configurations (shapes of the two-stage VLA: a VLM that encodes
+  the camera frames and the instruction text into per-layer prefix state, and an action
   diffusion transformer that runs a few denoising steps, paper Section 2.1),
 * the canonical order and shapes of the parameter tensors, and
 * seeded generators for parameters and request inputs.
