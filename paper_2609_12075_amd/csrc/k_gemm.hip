@@ -924,16 +924,19 @@ gemm_stage_kernel(GemmArgs a) {
 // second K chunk's fragment reads are interleaved with the first chunk's
 // products. The epilogue stages the fp32 tile through LDS in two halves of
 // 128 rows.
-template <int MODE, int NW>
+template <int MODE, int NW, int BM = 256>
 __global__ void __launch_bounds__(NW * 64) gemm_big_kernel(GemmArgs a) {
-  constexpr int BN = 256, BM = 256, BK = 64, ROWB = BK * 2;
+  constexpr int BN = 256, BK = 64, ROWB = BK * 2;
+  static_assert(BM == 256 || BM == 224, "activation tile of 256 or 224 rows");
   constexpr int WGN = NW / 2;                                    // waves along the weight rows
   constexpr int WTN = BN / WGN, WTM = BM / 2;                    // wave tile
   constexpr int TN = WTN / 16, TM = WTM / 16;
-  constexpr int STAGE_BYTES = (BN + BM) * ROWB;                  // 64 KiB
+  constexpr int STAGE_BYTES = (BN + BM) * ROWB;                  // 64 KiB (60 KiB)
   constexpr int LDC = BN + 4;
   constexpr int SMEM = 2 * STAGE_BYTES > 128 * LDC * 4 ? 2 * STAGE_BYTES : 128 * LDC * 4;
-  constexpr int GPW = 32 / NW;                                   // 8-row groups per wave per operand
+  constexpr int GPW = 32 / NW;                                   // 8-row groups per wave of the weight tile
+  constexpr int AG = BM / 8;                                     // 8-row groups of the activation tile
+  constexpr int GPWA = (AG + NW - 1) / NW;                       // ... per wave (the last may be short)
   __shared__ __attribute__((aligned(1024))) char smem[SMEM];
   auto Cs = reinterpret_cast<float (*)[LDC]>(smem);
 
@@ -948,7 +951,9 @@ __global__ void __launch_bounds__(NW * 64) gemm_big_kernel(GemmArgs a) {
   const bf16* A = reinterpret_cast<const bf16*>(a.A);
   const bf16* Z = reinterpret_cast<const bf16*>(a.zeros);
 
-  // 8-row groups: 32 of W and 32 of A per stage
+  // 8-row groups: 32 of W and BM / 8 of A per stage (with 224 rows the
+  // last round of A groups covers half the waves; the count per wave differs,
+  // which the full waits below do not mind)
   const int lrow = lane >> 3, slot = lane & 7;
   auto issue = [&](int kt, int buf) {
     char* st = smem + buf * STAGE_BYTES;
@@ -960,8 +965,9 @@ __global__ void __launch_bounds__(NW * 64) gemm_big_kernel(GemmArgs a) {
       __builtin_amdgcn_global_load_lds(src, st + grp * 8 * ROWB, 16, 0, 0);
     }
 #pragma unroll
-    for (int j = 0; j < GPW; ++j) {
+    for (int j = 0; j < GPWA; ++j) {
       const int grp = j * NW + wave, r = grp * 8 + lrow;
+      if (AG % NW != 0 && grp >= AG) break;
       const int c = slot ^ ((r >> 1) & 7), k = kt * BK + c * 8, m = m_blk + r;
       const bf16* src = (m < a.M && k < K) ? A + (long)m * a.lda + k : Z;
       __builtin_amdgcn_global_load_lds(src, st + BN * ROWB + grp * 8 * ROWB, 16, 0, 0);
@@ -1015,11 +1021,11 @@ __global__ void __launch_bounds__(NW * 64) gemm_big_kernel(GemmArgs a) {
       __builtin_amdgcn_sched_group_barrier(0x008, 2 * NMF - NRD * R, 0);
     }
   }
-  // epilogue in two halves of 128 activation rows (waves with wm0 == 128 h)
+  // epilogue in two halves of BM / 2 activation rows (waves with wm0 == WTM h)
 #pragma unroll 1
   for (int h = 0; h < 2; ++h) {
     __syncthreads();
-    if (wm0 == 128 * h) {
+    if (wm0 == WTM * h) {
 #pragma unroll
       for (int i = 0; i < TN; ++i)
 #pragma unroll
@@ -1028,15 +1034,15 @@ __global__ void __launch_bounds__(NW * 64) gemm_big_kernel(GemmArgs a) {
     }
     __syncthreads();
     if (a.epi_vec) {
-      tile_epilogue<MODE, BN, 128, NW * 64, LDC, 1, 4>(a, &Cs[0][0], m_blk + 128 * h, n_blk, tid);
+      tile_epilogue<MODE, BN, WTM, NW * 64, LDC, 1, 4>(a, &Cs[0][0], m_blk + WTM * h, n_blk, tid);
       continue;
     }
 #pragma unroll 1
-    for (int c = tid; c < 128 * (BN / 4); c += NW * 64) {
+    for (int c = tid; c < WTM * (BN / 4); c += NW * 64) {
       const int mr = c / (BN / 4), nc = (c % (BN / 4)) * 4;
       f32x4 t = *reinterpret_cast<const f32x4*>(&Cs[mr][nc]);
       float v[4] = {t[0], t[1], t[2], t[3]};
-      epilogue4<MODE>(a, m_blk + 128 * h + mr, n_blk + nc, v);
+      epilogue4<MODE>(a, m_blk + WTM * h + mr, n_blk + nc, v);
     }
   }
 }
@@ -1120,10 +1126,17 @@ static GemmPlan plan_base(const GemmArgs& a) {
     // per CU) measured 2.1 us and a round of 512 staged tiles (two per CU)
     // 1.2 us (e.g. the 2560-wide QKV projection of 6528 rows: 260 large tiles
     // in two rounds, 124 us, against 1020 staged tiles in two rounds, 76 us)
-    const long t256 = blocks(256, 256), t128 = blocks(128, 128);
-    if (a.M >= 256 && a.K >= 2048 && t256 >= 160 &&
-        (t256 + 255) / 256 * 2.1 <= (t128 + 511) / 512 * 1.2) {
-      p.bn = 256; p.bm = 256; p.kind = 3;
+    // The large tiles are 256 activation rows high, or 224 when no more
+    // rounds of tiles result: a 224-row tile measured 3-7 % faster than a
+    // 256-row one (not the 12.5 % of its area: each K-step's fixed costs
+    // dominate), e.g. the pi0-shaped MLP down projection at 6528 rows, 240
+    // such tiles in one round, 435 us against 450 us for 208 taller ones. The
+    // accumulation order of every output, and so the result, is the same
+    // for both heights.
+    const long t256 = blocks(256, 256), t224 = blocks(256, 224), t128 = blocks(128, 128);
+    const double c256 = (t256 + 255) / 256 * 2.1, c224 = (t224 + 255) / 256 * 2.1 * 0.95;
+    if (a.M >= 256 && a.K >= 2048 && t256 >= 160 && std::min(c256, c224) <= (t128 + 511) / 512 * 1.2) {
+      p.bn = 256; p.bm = c224 < c256 - 1e-9 ? 224 : 256; p.kind = 3;
       p.ksplit = nk * BK;
       return p;
     }
@@ -1290,9 +1303,14 @@ static void launch_staged128(const GemmArgs& a0, const GemmPlan& p, const NormAr
 }
 
 template <int MODE, int NW = 8>
-static void launch_big(const GemmArgs& a, hipStream_t s) {
+static void launch_big(const GemmArgs& a, int bm, hipStream_t s) {
+  if (bm == 224) {
+    dim3 grid((a.M + 223) / 224, (a.N + 255) / 256, 1);
+    hipLaunchKernelGGL((gemm_big_kernel<MODE, NW, 224>), grid, dim3(NW * 64), 0, s, a);
+    return;
+  }
   dim3 grid((a.M + 255) / 256, (a.N + 255) / 256, 1);
-  hipLaunchKernelGGL((gemm_big_kernel<MODE, NW>), grid, dim3(NW * 64), 0, s, a);
+  hipLaunchKernelGGL((gemm_big_kernel<MODE, NW, 256>), grid, dim3(NW * 64), 0, s, a);
 }
 
 template <int TN, int MODE>
@@ -1341,7 +1359,7 @@ static void launch_mode(const GemmArgs& a, const GemmPlan& p, const NormArgs* fu
     return;
   }
   if (p.kind == 3) {
-    launch_big<MODE>(a, s);
+    launch_big<MODE>(a, p.bm, s);
     return;
   }
   if (p.kind == 4) {

@@ -31,8 +31,10 @@ GEMM_SHAPES = [
     (800, 720, 1920), (600, 1000, 1544),
     # register-pipelined 64 x 32 tiles with K ranges
     (100, 1024, 4096), (200, 720, 1920),
-    # large-tile kernel (256 x 256, K >= 2048), ragged M, N and K
-    (2600, 4100, 2056),
+    # large-tile kernel (K >= 2048): 224-row tiles (2600 rows: 12 row tiles
+    # fill one round as 11 of 256 rows would) with ragged M, N and K, and
+    # 256-row tiles (3584 rows: 224-row tiles would need a second round)
+    (2600, 4100, 2056), (3584, 4600, 2056),
     # staged 64 x 64 tiles (short K, mid-sized M), ragged
     (800, 1600, 720), (431, 2500, 1000),
     # two wave groups per K-step of 128: 128 x 128 tiles, ragged M, N and K;
