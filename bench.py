@@ -99,7 +99,7 @@ class GpuValidator:
             self.rob_in.append({k: torch.from_numpy(v).to("cuda:0") for k, v in inp.items()})
 
     def run(self, R, epoch, mb, cu_table=None, default_cu=256, mode="lockstep", disjoint=False, policy="esf",
-            traffic="poisson", slo=None):
+            traffic="poisson", slo=None, delivery="lockstep"):
         import torch
         from paper_2609_12075_amd import serve, synth
         slo = self.slo if slo is None else slo
@@ -118,16 +118,19 @@ class GpuValidator:
         sch.set_gpu_online(self.models, join_stream=self.js)
         sch.set_cu(default_cu, cu_table)
         sch.set_disjoint(disjoint)
+        sch.set_delivery(delivery)
         torch.cuda.synchronize()
         req, ls = sch.run(arr, drain_ns=int(1e9), ios=ios)
         sch.close()
         done = req["t_done_ns"] >= 0
         finite = all(bool(torch.isfinite(o[:c]).all()) for o, c in zip(outs, cnt) if c) if done.all() else None
         dur = (ls["t_end_ns"] - ls["t_start_ns"]) / 1e6
+        early = (ls["t_end_ns"] - ls["t_chunks_ns"])[ls["adit_batch"] > 0] / 1e6
         rec = {"robots": int(R), "requests": int(len(req)), "attainment": round(serve.attainment(req), 4),
                "p99_ms": round(serve.p99_ms(req), 2), "locksteps": int(len(ls)),
                "lockstep_ms_mean": round(float(dur.mean()), 3) if len(dur) else None,
-               "outputs_finite": finite, "seconds": self.seconds}
+               "chunks_before_lockstep_end_ms_mean": round(float(early.mean()), 3) if len(early) else None,
+               "delivery": delivery, "outputs_finite": finite, "seconds": self.seconds}
         log(f"{self.lp} GPU R={R}: attainment {rec['attainment']:.4f}, p99 {rec['p99_ms']} ms, "
             f"{rec['requests']} requests, {rec['locksteps']} locksteps")
         return rec
@@ -631,25 +634,36 @@ def colocated_main(args):
 
     # ---- 1. lockstep table under each VLM CU restriction, profiled once at the
     # largest batch cap; a smaller cap's table is the leading buckets of it
+    # (and, per combination, when its action half ends: chunks are delivered
+    # then with --delivery adit)
     t0 = time.perf_counter()
-    prof_all = serve.profile_locksteps(models, bufs, mb_prof, cus, reps=3, log=log, join_stream=js)
+    prof_all, adit_all = serve.profile_locksteps(models, bufs, mb_prof, cus, reps=3, log=log, join_stream=js,
+                                                 with_adit=True)
     log(f"[bench] profiled {prof_all.size} lockstep entries in {time.perf_counter() - t0:.1f} s")
+    if args.dump_profile:
+        np.savez(args.dump_profile, prof=prof_all, adit=adit_all, cus=np.asarray(cus), models=np.asarray(names))
 
     # ---- 2. simulated sweep per batch cap (max_batch of the scheduler)
     robots = list(range(1, args.serve_max_robots + 1))
+    early = args.delivery == "adit"
     by_mb = {}
     for mbx in mbs:
         nbx = serve.n_buckets(mbx)
         sub = np.ascontiguousarray(prof_all[:, :, :nbx, :, :nbx])
-        ct, dl = serve.best_cu_table(sub, cus)
-        rows_x, r_x = serve.sweep_robots(dl, slo, mbx, robots, f, args.serve_seconds, args.serve_epochs)
-        by_mb[mbx] = {"robots_at_98_sim": r_x, "cu_table": ct, "dur": dl, "sub": sub, "sweep": rows_x}
+        ct, dl, al = serve.best_cu_table(sub, cus, np.ascontiguousarray(adit_all[:, :, :nbx, :, :nbx]))
+        rows_x, r_x = serve.sweep_robots(dl, slo, mbx, robots, f, args.serve_seconds, args.serve_epochs,
+                                         adit_ns=al if early else None)
+        by_mb[mbx] = {"robots_at_98_sim": r_x, "cu_table": ct, "dur": dl, "adit": al, "sub": sub, "sweep": rows_x}
         log(f"[bench] max_batch {mbx}: simulated {r_x} robots at >= 98 % "
-            f"({args.serve_epochs} x {args.serve_seconds:.0f} s traces)")
+            f"({args.serve_epochs} x {args.serve_seconds:.0f} s traces, delivery {args.delivery})")
     mb = max(mbs, key=lambda x: (by_mb[x]["robots_at_98_sim"], -x))
     prof, cu_table, dur_lut = by_mb[mb]["sub"], by_mb[mb]["cu_table"], by_mb[mb]["dur"]
+    adit_lut = by_mb[mb]["adit"]
     rows, r_sim = by_mb[mb]["sweep"], by_mb[mb]["robots_at_98_sim"]
-    log(f"[bench] serving with max_batch {mb}")
+    # the other delivery point at the chosen cap, simulated, for comparison
+    _, r_other = serve.sweep_robots(dur_lut, slo, mb, robots, f, args.serve_seconds, args.serve_epochs,
+                                    adit_ns=None if early else adit_lut)
+    log(f"[bench] serving with max_batch {mb} (simulated with the other delivery point: {r_other} robots)")
     nb = serve.n_buckets(mb)
     full = nb - 1                            # bucket of the serving batch
 
@@ -681,7 +695,7 @@ def colocated_main(args):
     # ---- 3. real-time validation on the GPU (online executor, per-robot inputs)
     t0 = time.perf_counter()
     val = GpuValidator(models, cfgs, slo, f, args.validate_seconds, js, args.serve_max_robots + 2)
-    best, checks = val.search(r_sim, args.serve_max_robots, mb=mb, cu_table=cu_table)
+    best, checks = val.search(r_sim, args.serve_max_robots, mb=mb, cu_table=cu_table, delivery=args.delivery)
     value = best * f
     log(f"[bench] GPU-validated: {best} robots at >= 98 % -> {value} action chunks/s "
         f"({time.perf_counter() - t0:.1f} s of validation)")
@@ -744,15 +758,19 @@ def colocated_main(args):
         "config": {"workload": "co-located " + " + ".join(f"{n}-shaped" for n in names) +
                                f", Poisson {f:g} Hz per robot, {args.slo_ms:g} ms SLO, robots at >= 98 % attainment",
                    "models": names, "rate_hz": f, "slo_ms": args.slo_ms, "max_batch": mb, "policy": "esf",
+                   "chunk_delivery": ("when the request's action stage ends" if early else
+                                      "at the end of the lockstep that ran its action stage"),
                    "vlm_cu_candidates": cus, "parallelism": "single GPU, two streams (VLM CU-restricted)"},
         "robots_at_98": best, "gpu_validation": checks,
         "robots_at_98_sim": r_sim, "sim": {"epochs": args.serve_epochs, "trace_s": args.serve_seconds,
                                            "sweep": rows},
         "robots_at_98_sim_by_max_batch": {str(x): by_mb[x]["robots_at_98_sim"] for x in mbs},
+        "robots_at_98_sim_other_delivery": {"delivery": "lockstep" if early else "adit", "robots": r_other},
         "saturated_lockstep_chunks_per_s": round(mb * 1e3 / ms_per_step, 2),
         "stages": stages,
         "adit_step_ms": {n: stages[n]["adit_step_ms"] for n in stages},
         "cu_table": cu_table.tolist(), "lockstep_ms_lut": (dur_lut / 1e6).round(3).tolist(),
+        "adit_end_ms_lut": (adit_lut / 1e6).round(3).tolist(),
         "roofline": roofline,
         "kernels": {f"{k[0]}:{GEMM_NAMES[k[1]]}": {"us": round(v["us"], 3), "launches_per_batch": v["launches"],
                                                     "tflops": round(v["flops"] / v["us"] / 1e6, 2),
@@ -806,6 +824,11 @@ def main():
     ap.add_argument("--validate-seconds", type=float, default=20.0,
                     help="seconds of real-time traffic per GPU validation run")
     ap.add_argument("--slo-ms", type=float, default=100.0)
+    ap.add_argument("--delivery", choices=("adit", "lockstep"), default="lockstep",
+                    help="when a request completes: at the end of the lockstep that ran its action stage "
+                         "(default) or when that action stage ends")
+    ap.add_argument("--dump-profile", default="",
+                    help="write the lockstep profile (durations and action-half ends per CU count) to this .npz")
     ap.add_argument("--sync-costs", action="store_true",
                     help="kernel-boundary vs in-kernel grid-barrier cost (what fusing dependent phases would trade)")
     ap.add_argument("--stages", action="store_true", help="stage times per config and batch instead of the lockstep bench")

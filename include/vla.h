@@ -172,7 +172,10 @@ vla_status vla_denoise(vla_model m, int batch, const void* kv, const float* nois
  * `join_stream` is a non-blocking stream (hipStreamNonBlocking) and the action
  * half is unrestricted, the action half runs on `join_stream` itself (faster:
  * no cross-queue wait is pending while its kernels run); otherwise it runs on
- * a pool stream.
+ * a pool stream. `adit_done` (may be NULL) is recorded on the action half's
+ * stream right after its last kernel, when there is an action half: a caller
+ * can wait on it to use the action chunks (copy them out, return them)
+ * before the VLM half ends; the event must belong to the models' device.
  */
 typedef struct {
   vla_model vlm_model;  int vlm_batch;
@@ -182,6 +185,7 @@ typedef struct {
   int vlm_cu_count;
   int adit_cu_count;    /* 0 or 256: unrestricted; else the complement-style
                            disjoint baseline (multiple of 8) */
+  hipEvent_t adit_done; /* NULL, or recorded after the action half */
 } vla_step_args;
 vla_status vla_step(const vla_step_args* args, hipStream_t join_stream);
 

@@ -48,6 +48,7 @@ enum { VLA_SCHED_ESF = 0, VLA_SCHED_RR = 1, VLA_SCHED_LQF = 2 };
  * GPU and completes before the next batch starts (simulated duration: the
  * two stages' stand-alone table entries plus two host overheads). */
 enum { VLA_SCHED_LOCKSTEP = 0, VLA_SCHED_MONOLITHIC = 1 };
+enum { VLA_SCHED_DONE_LOCKSTEP = 0, VLA_SCHED_DONE_ADIT = 1 };
 
 typedef struct {
   int n_models;            /* 1 .. 16 */
@@ -66,12 +67,16 @@ typedef struct {           /* one executed lockstep */
   int adit_model, adit_batch;   /* -1, 0 when the action half is empty */
   int cu_count;                 /* CU restriction applied to the VLM stream */
   int slot;                     /* hand-off slot written by the VLM half (k mod 2) */
+  int64_t t_chunks_ns;          /* when the action half's chunks were delivered
+                                   (t_end_ns without an action half, in Monolithic
+                                   mode, and with delivery at the lockstep end) */
 } vla_lockstep_rec;
 
 typedef struct {           /* outcome of one request */
   int64_t t_arrival_ns;
   int64_t t_vlm_start_ns;       /* start of its VLM lockstep, -1 if never admitted */
-  int64_t t_done_ns;            /* end of its action lockstep, -1 if unfinished */
+  int64_t t_done_ns;            /* delivery of its chunk (see vla_sched_set_delivery),
+                                   -1 if unfinished */
   int model;
   int met_slo;                  /* 1 if t_done - t_arrival <= SLO */
 } vla_request_rec;
@@ -102,6 +107,25 @@ vla_status vla_sched_set_gpu_executor(vla_sched s, const vla_sched_model_io* io,
 /* Execution mode (VLA_SCHED_LOCKSTEP or VLA_SCHED_MONOLITHIC); the default
  * is LOCKSTEP. Monolithic ignores the CU table. */
 vla_status vla_sched_set_mode(vla_sched s, int mode);
+
+/*
+ * When a request completes (lockstep mode). VLA_SCHED_DONE_LOCKSTEP (the
+ * default): at the end of the lockstep in which its action stage ran.
+ * VLA_SCHED_DONE_ADIT: when its action stage ends. The paper's lockstep
+ * starts the next lockstep only once both halves have finished (Section
+ * 4.1.2) and does not say when a finished chunk leaves the server; in this
+ * mode the online GPU executor copies the chunks to the requests' buffers
+ * as soon as the action half is done (on a stream of its own, while the VLM
+ * half may still run), and the completion time is that copy's end, read
+ * from GPU events; the fixed-buffer executor uses the action half's end. The
+ * simulated executor takes it from `adit_ns` (same indexing as the duration
+ * table: time from the lockstep's start to the end of its action half; an
+ * entry above the lockstep's duration counts as the lockstep's end); the
+ * table is copied, and is required before a simulated run in this mode
+ * (NULL keeps the previous one). Monolithic mode always completes a batch at
+ * its end.
+ */
+vla_status vla_sched_set_delivery(vla_sched s, int when, const int64_t* adit_ns);
 
 /* Partition of the compute units between the two halves of a lockstep: 0
  * (the default, the paper's guarded restriction) restricts only the VLM half

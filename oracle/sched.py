@@ -18,6 +18,12 @@ no code with the library's C++ scheduler.
   largest-queue-first are the comparison policies of Section 5.3.
 * Section 5.1: a request meets its SLO when its end-to-end latency is within
   the deadline (network latency taken as zero here).
+* When a request's chunk is delivered (reading; the paper gates only the next
+  lockstep's start on both halves and is silent on when a finished chunk
+  leaves the server): by default at the end of the lockstep that ran its
+  action stage; with delivery "adit", when that action half ends, given by a
+  second table (time from the lockstep's start to its action half's end, same
+  indexing), capped at the lockstep's end.
 * Monolithic, the paper's control system (Section 5): no stage
   disaggregation; the admitted batch runs the VLM stage and then the action
   stage back to back on the whole GPU and completes before the next batch is
@@ -48,12 +54,13 @@ def largest_pow2_at_most(x):
 
 
 def simulate(arrivals, slo_ms, max_batch, dur_ns, policy="esf", drain_ns=10 ** 9, overhead_ns=0,
-             cu_default=256, cu_table=None, mode="lockstep"):
-    """arrivals: list of (t_ns, model) sorted by time. dur_ns: nested lists
-    [mv][bv_bucket][ma][ba_bucket]. Returns (requests, locksteps): requests =
-    list of dicts (t_arrival, t_vlm_start, t_done, model, met), locksteps =
-    list of tuples (t_start, t_end, vlm_model, vlm_batch, adit_model,
-    adit_batch, cu, slot)."""
+             cu_default=256, cu_table=None, mode="lockstep", delivery="lockstep", adit_ns=None):
+    """arrivals: list of (t_ns, model) sorted by time. dur_ns (and adit_ns
+    for delivery "adit"): nested lists [mv][bv_bucket][ma][ba_bucket].
+    Returns (requests, locksteps): requests = list of dicts (t_arrival,
+    t_vlm_start, t_done, model, met), locksteps = list of tuples (t_start,
+    t_end, vlm_model, vlm_batch, adit_model, adit_batch, cu, slot,
+    t_chunks)."""
     n_models = len(slo_ms)
     slo_ns = [int(s * 1e6 + 0.5) for s in slo_ms]
     reqs = [{"t_arrival": t, "t_vlm_start": -1, "t_done": -1, "model": m, "met": 0} for t, m in arrivals]
@@ -92,7 +99,7 @@ def simulate(arrivals, slo_ms, max_batch, dur_ns, policy="esf", drain_ns=10 ** 9
             for r in admitted:
                 reqs[r]["t_vlm_start"] = now
                 reqs[r]["t_done"] = end
-            locksteps.append((now, end, mv, bv, mv, bv, 256, 0))
+            locksteps.append((now, end, mv, bv, mv, bv, 256, 0, end))
             k += 1
             now = end
             continue
@@ -104,11 +111,14 @@ def simulate(arrivals, slo_ms, max_batch, dur_ns, policy="esf", drain_ns=10 ** 9
         if cu_table is not None and cu_table[max(mv, 0)][iv][max(ma, 0)][ia] > 0:
             cu = cu_table[max(mv, 0)][iv][max(ma, 0)][ia]
         end = now + d + overhead_ns
+        chunks = end
+        if delivery == "adit" and handoff:
+            chunks = min(end, now + adit_ns[max(mv, 0)][iv][max(ma, 0)][ia])
         for r in handoff:
-            reqs[r]["t_done"] = end
+            reqs[r]["t_done"] = chunks
         for r in admitted:
             reqs[r]["t_vlm_start"] = now
-        locksteps.append((now, end, mv, bv, ma, ba, cu, slot))
+        locksteps.append((now, end, mv, bv, ma, ba, cu, slot, chunks))
         handoff, handoff_model, handoff_slot = admitted, mv, slot
         k += 1
         now = end

@@ -378,6 +378,7 @@ vla_status vla_step(const vla_step_args* a, hipStream_t join) {
     if (do_v) a->vlm_model->prefill(a->vlm_batch, a->pixels, a->text_ids,
                                     a->vlm_model->cfg.head_kind == VLA_HEAD_DIT ? a->state : nullptr, a->kv_out, vs);
     if (do_a) a->adit_model->denoise(a->adit_batch, a->kv_in, a->noise, a->steps, a->actions_out, as);
+    if (do_a && a->adit_done) VLA_HIP(hipEventRecord(a->adit_done, as));
     if (do_v) { VLA_HIP(hipEventRecord(p.ev_v, vs)); VLA_HIP(hipStreamWaitEvent(join, p.ev_v, 0)); }
     if (do_a && !on_join) { VLA_HIP(hipEventRecord(p.ev_a, as)); VLA_HIP(hipStreamWaitEvent(join, p.ev_a, 0)); }
   });

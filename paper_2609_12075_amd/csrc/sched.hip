@@ -84,6 +84,13 @@ struct vla_sched_s {
   int default_cu = 256;
   std::vector<int> cu_table;
   int disjoint = 0;                          // action half on the complement of the VLM's CUs
+  // chunk delivery: at the lockstep end, or when the action half ends
+  // (GPU executors: events; the online executor copies the chunks out on
+  // its own stream as soon as the action half is done)
+  int deliver = VLA_SCHED_DONE_LOCKSTEP;
+  std::vector<int64_t> adit_ns;              // simulated executor, time to the action half's end
+  hipEvent_t ev_adit = nullptr, ev_scat = nullptr, ev_end = nullptr;
+  hipStream_t scat = nullptr;
   // serving state
   std::vector<std::deque<Req>> q;
   std::vector<Req> buf;                      // admitted one lockstep ago, waiting for the action stage
@@ -116,7 +123,7 @@ struct vla_sched_s {
     return (int)n;
   }
   void free_online() {
-    if (dev_allocs.empty() && !seg_host) return;
+    if (dev_allocs.empty() && !seg_host && !ev_adit) return;
     DeviceGuard g(device);
     (void)hipDeviceSynchronize();
     for (void* p : dev_allocs) (void)hipFree(p);
@@ -124,6 +131,20 @@ struct vla_sched_s {
     if (seg_host) (void)hipHostFree(seg_host);
     seg_host = nullptr; seg_dev = nullptr; seg_cap = 0;
     stage.clear();
+    for (hipEvent_t* e : {&ev_adit, &ev_scat, &ev_end})
+      if (*e) { (void)hipEventDestroy(*e); *e = nullptr; }
+    if (scat) { (void)hipStreamDestroy(scat); scat = nullptr; }
+  }
+  // events and the delivery stream of the GPU executors (on `device`, current)
+  void make_events() {
+    for (hipEvent_t* e : {&ev_adit, &ev_scat, &ev_end}) VLA_HIP(hipEventCreate(e));
+    VLA_HIP(hipStreamCreateWithFlags(&scat, hipStreamNonBlocking));
+  }
+  // GPU milliseconds from event a to event b (both completed)
+  static double gap_ms(hipEvent_t a, hipEvent_t b) {
+    float ms = 0.f;
+    VLA_HIP(hipEventElapsedTime(&ms, a, b));
+    return ms > 0.f ? ms : 0.0;
   }
   void* dalloc(size_t bytes) {
     void* p = nullptr;
@@ -138,10 +159,12 @@ struct vla_sched_s {
   // One lockstep at `now` (a whole batch in Monolithic mode). Appends the
   // admitted requests' indices into their queue order to `admitted`.
   void lockstep(int64_t now, vla_lockstep_rec& rec, std::vector<Req>* admitted);
-  void gpu_online_exec(int mv, const std::vector<Req>& vreq, int ma, int cu, int slot, bool monolithic);
+  // returns, with chunk delivery at the action half's end and an action half,
+  // how long before the lockstep's end the chunks were delivered (ms), else -1
+  double gpu_online_exec(int mv, const std::vector<Req>& vreq, int ma, int cu, int slot, bool monolithic);
 };
 
-void vla_sched_s::gpu_online_exec(int mv, const std::vector<Req>& vreq, int ma, int cu, int slot, bool monolithic) {
+double vla_sched_s::gpu_online_exec(int mv, const std::vector<Req>& vreq, int ma, int cu, int slot, bool monolithic) {
   DeviceGuard g(device);
   const int bv = (int)vreq.size(), ba = monolithic ? bv : (int)buf.size();
   // descriptors: gather (VLM batch inputs), then scatter (finished chunks)
@@ -195,18 +218,32 @@ void vla_sched_s::gpu_online_exec(int mv, const std::vector<Req>& vreq, int ma, 
       d.vlm_cu_count = 256;
       st = vla_step(&d, join);
     }
-  } else {
+  }
+  const bool early = !monolithic && ba > 0 && deliver == VLA_SCHED_DONE_ADIT;
+  if (!monolithic) {
     vla_step_args a{};
     if (bv > 0) vlm_half(a, slot);
     if (ba > 0) act_half(a, ma, ba, buf_slot);
     a.vlm_cu_count = cu;
     a.adit_cu_count = disjoint && cu < 256 ? 256 - cu : 0;
+    a.adit_done = early ? ev_adit : nullptr;
     st = vla_step(&a, join);
   }
   if (st != VLA_OK) throw VlaError{(int)st, std::string("lockstep: ") + vla_last_error()};
-  launch_batched_copy(seg_dev + ng, n - ng, smax, join);
+  if (early) {
+    // the chunks leave as soon as the action half is done; the lockstep
+    // still ends when both halves (and this copy) have finished
+    VLA_HIP(hipStreamWaitEvent(scat, ev_adit, 0));
+    launch_batched_copy(seg_dev + ng, n - ng, smax, scat);
+    VLA_HIP(hipEventRecord(ev_scat, scat));
+    VLA_HIP(hipStreamWaitEvent(join, ev_scat, 0));
+  } else {
+    launch_batched_copy(seg_dev + ng, n - ng, smax, join);
+  }
   VLA_HIP(hipGetLastError());
+  VLA_HIP(hipEventRecord(ev_end, join));
   VLA_HIP(hipStreamSynchronize(join));
+  return early ? gap_ms(ev_scat, ev_end) : -1.0;
 }
 
 void vla_sched_s::lockstep(int64_t now, vla_lockstep_rec& rec, std::vector<Req>* admitted) {
@@ -248,7 +285,7 @@ void vla_sched_s::lockstep(int64_t now, vla_lockstep_rec& rec, std::vector<Req>*
     if (sim()) {
       t_end = now + dur_ns[combo(mv, bv, -1, 0)] + dur_ns[combo(-1, 0, mv, bv)] + 2 * host_overhead_ns;
     } else if (exec_kind == EXEC_GPU_ONLINE) {
-      gpu_online_exec(mv, vreq, -1, 256, 0, true);
+      (void)gpu_online_exec(mv, vreq, -1, 256, 0, true);
       t_end = wall_ns();
     } else {
       const vla_sched_model_io& x = io[mv];
@@ -269,7 +306,7 @@ void vla_sched_s::lockstep(int64_t now, vla_lockstep_rec& rec, std::vector<Req>*
       t_end = wall_ns();
     }
     complete(vreq, t_end);
-    rec = vla_lockstep_rec{now, t_end, mv, bv, mv, bv, 256, 0};
+    rec = vla_lockstep_rec{now, t_end, mv, bv, mv, bv, 256, 0, t_end};
     ++k;
     if (sim()) t_sim = t_end;
     return;
@@ -280,12 +317,15 @@ void vla_sched_s::lockstep(int64_t now, vla_lockstep_rec& rec, std::vector<Req>*
   const size_t ci = combo(mv, bv, ma, ba);
   if (!cu_table.empty() && cu_table[ci] > 0) cu = cu_table[ci];
   // ---- execute the lockstep
-  int64_t t_end;
+  int64_t t_end, t_chunks;
+  const bool early = ba > 0 && deliver == VLA_SCHED_DONE_ADIT;
   if (sim()) {
     t_end = now + dur_ns[ci] + host_overhead_ns;
+    t_chunks = early ? std::min(t_end, now + adit_ns[ci]) : t_end;
   } else if (exec_kind == EXEC_GPU_ONLINE) {
-    gpu_online_exec(mv, vreq, ma, cu, slot, false);
+    const double before_ms = gpu_online_exec(mv, vreq, ma, cu, slot, false);
     t_end = wall_ns();
+    t_chunks = before_ms >= 0.0 ? std::max(now, t_end - (int64_t)(before_ms * 1e6)) : t_end;
   } else {
     vla_step_args a{};
     if (bv > 0) {
@@ -300,13 +340,16 @@ void vla_sched_s::lockstep(int64_t now, vla_lockstep_rec& rec, std::vector<Req>*
     }
     a.vlm_cu_count = cu;
     a.adit_cu_count = disjoint && cu < 256 ? 256 - cu : 0;
+    a.adit_done = early ? ev_adit : nullptr;
     vla_status st = vla_step(&a, join);
     if (st != VLA_OK) throw VlaError{(int)st, std::string("lockstep: ") + vla_last_error()};
+    VLA_HIP(hipEventRecord(ev_end, join));
     VLA_HIP(hipStreamSynchronize(join));
     t_end = wall_ns();
+    t_chunks = early ? std::max(now, t_end - (int64_t)(gap_ms(ev_adit, ev_end) * 1e6)) : t_end;
   }
-  complete(buf, t_end);
-  rec = vla_lockstep_rec{now, t_end, mv, bv, ma, ba, cu, slot};
+  complete(buf, t_chunks);
+  rec = vla_lockstep_rec{now, t_end, mv, bv, ma, ba, cu, slot, t_chunks};
   buf = std::move(vreq);
   buf_model = mv;
   buf_slot = slot;
@@ -369,6 +412,11 @@ vla_status vla_sched_set_gpu_executor(vla_sched s, const vla_sched_model_io* io,
       VLA_REQUIRE(x.steps >= 1 && x.steps <= 1000, "steps must be in [1, 1000]");
     }
     s->free_online();
+    s->device = io[0].model->device;
+    {
+      DeviceGuard g(s->device);
+      s->make_events();
+    }
     s->io.assign(io, io + s->n_models);
     s->join = join;
     s->exec_kind = EXEC_GPU_FIXED;
@@ -413,6 +461,7 @@ vla_status vla_sched_set_gpu_online(vla_sched s, const vla_model* models, const 
       s->seg_cap = 5 * s->max_batch;
       s->seg_dev = (CopySeg*)s->dalloc((size_t)s->seg_cap * sizeof(CopySeg));
       VLA_HIP(hipHostMalloc((void**)&s->seg_host, (size_t)s->seg_cap * sizeof(CopySeg), hipHostMallocDefault));
+      s->make_events();
     } catch (...) {
       s->free_online();
       throw;
@@ -428,6 +477,19 @@ vla_status vla_sched_set_mode(vla_sched s, int mode) {
     VLA_REQUIRE(s, "null scheduler");
     VLA_REQUIRE(mode == VLA_SCHED_LOCKSTEP || mode == VLA_SCHED_MONOLITHIC, "unknown execution mode");
     s->mode = mode;
+  });
+}
+
+vla_status vla_sched_set_delivery(vla_sched s, int when, const int64_t* adit_ns) {
+  return guard([&] {
+    VLA_REQUIRE(s, "null scheduler");
+    VLA_REQUIRE(when == VLA_SCHED_DONE_LOCKSTEP || when == VLA_SCHED_DONE_ADIT, "unknown delivery point");
+    if (adit_ns) {
+      const size_t n = (size_t)s->n_models * s->n_buckets * s->n_models * s->n_buckets;
+      for (size_t i = 0; i < n; ++i) VLA_REQUIRE(adit_ns[i] >= 0, "negative action-half time");
+      s->adit_ns.assign(adit_ns, adit_ns + n);
+    }
+    s->deliver = when;
   });
 }
 
@@ -486,6 +548,8 @@ vla_status vla_sched_run_lockstep(vla_sched s, vla_lockstep_rec* rec, int* ran) 
   return guard([&] {
     VLA_REQUIRE(s && ran, "null scheduler or ran");
     VLA_REQUIRE(s->exec_kind != EXEC_NONE, "no executor set");
+    VLA_REQUIRE(!(s->sim() && s->deliver == VLA_SCHED_DONE_ADIT && s->adit_ns.empty()),
+                "delivery at the action half's end needs its time table for the simulated executor");
     *ran = 0;
     if (s->pending() == 0) return;
     vla_lockstep_rec r{};
@@ -526,6 +590,8 @@ vla_status vla_sched_run_trace(vla_sched s, const int64_t* t_arr, const int32_t*
     VLA_REQUIRE(n >= 0 && ls_cap >= 0 && drain_ns >= 0, "negative size");
     VLA_REQUIRE(s->exec_kind != EXEC_NONE, "no executor set");
     VLA_REQUIRE(s->exec_kind != EXEC_GPU_ONLINE || io, "the online GPU executor needs per-request inputs");
+    VLA_REQUIRE(!(s->sim() && s->deliver == VLA_SCHED_DONE_ADIT && s->adit_ns.empty()),
+                "delivery at the action half's end needs its time table for the simulated executor");
     for (int i = 0; i < n; ++i) {
       VLA_REQUIRE(model[i] >= 0 && model[i] < s->n_models, "request model index out of range");
       VLA_REQUIRE(t_arr[i] >= 0 && (i == 0 || t_arr[i] >= t_arr[i - 1]), "arrivals must be sorted and >= 0");

@@ -16,12 +16,13 @@ from . import synth, vla
 
 POLICIES = {"esf": 0, "rr": 1, "lqf": 2}
 MODES = {"lockstep": 0, "monolithic": 1}
+DELIVERY = {"lockstep": 0, "adit": 1}
 
 REQ_DTYPE = np.dtype([("t_arrival_ns", np.int64), ("t_vlm_start_ns", np.int64), ("t_done_ns", np.int64),
                       ("model", np.int32), ("met_slo", np.int32)])
 LS_DTYPE = np.dtype([("t_start_ns", np.int64), ("t_end_ns", np.int64), ("vlm_model", np.int32),
                      ("vlm_batch", np.int32), ("adit_model", np.int32), ("adit_batch", np.int32),
-                     ("cu_count", np.int32), ("slot", np.int32)])
+                     ("cu_count", np.int32), ("slot", np.int32), ("t_chunks_ns", np.int64)])
 
 
 class _Cfg(ctypes.Structure):
@@ -57,6 +58,7 @@ def _lib():
         L.vla_sched_run.argtypes = [vp, vp, vp, ci, i64, vp, vp, ci, ctypes.POINTER(ci)]
         L.vla_sched_run.restype = ci
         L.vla_sched_set_gpu_online.argtypes = [vp, vp, vp, vp]; L.vla_sched_set_gpu_online.restype = ci
+        L.vla_sched_set_delivery.argtypes = [vp, ci, vp]; L.vla_sched_set_delivery.restype = ci
         L.vla_sched_set_disjoint.argtypes = [vp, ci]; L.vla_sched_set_disjoint.restype = ci
         L.vla_sched_clock_ns.argtypes = [vp]; L.vla_sched_clock_ns.restype = i64
         L.vla_sched_reset.argtypes = [vp]; L.vla_sched_reset.restype = ci
@@ -145,6 +147,18 @@ class Scheduler:
             io.steps = m.cfg.steps
         self._keep.append((models, bufs))
         vla._check(_lib().vla_sched_set_gpu_executor(self.handle, ctypes.addressof(ios), vla._stream(join_stream)))
+
+    def set_delivery(self, when: str = "lockstep", adit_ns: Optional[np.ndarray] = None):
+        """When requests complete: "lockstep" (end of the lockstep that ran
+        their action stage) or "adit" (end of that action half; adit_ns, the
+        simulated executor's table of times from lockstep start to the action
+        half's end, same shape as the duration table)."""
+        ptr = None
+        if adit_ns is not None:
+            t = np.ascontiguousarray(adit_ns, dtype=np.int64)
+            assert t.shape == self.table_shape(), (t.shape, self.table_shape())
+            ptr = t.ctypes.data
+        vla._check(_lib().vla_sched_set_delivery(self.handle, DELIVERY[when], ptr))
 
     def set_disjoint(self, enabled: bool):
         """Disjoint CU partition: the action half runs on the CUs the VLM half
@@ -249,18 +263,25 @@ def alloc_io(models: Sequence[vla.Model], max_batch: int):
 
 
 def profile_locksteps(models: Sequence[vla.Model], bufs, max_batch: int, cu_counts: Sequence[int],
-                      reps: int = 3, warmup: int = 1, log=None, join_stream=None, disjoint: bool = False):
+                      reps: int = 3, warmup: int = 1, log=None, join_stream=None, disjoint: bool = False,
+                      with_adit: bool = False):
     """Median duration (ns) of one lockstep for every (VLM model, VLM batch,
     action model, action batch) combination and every CU restriction of the
     VLM stream, timed with HIP events on the join stream. Returns
     dur[k_index][mv][bv][ma][ba] (int64; combinations with both halves empty
     are 0) — the profiling pass behind the restriction lookup table. With
-    disjoint=True the action half runs on the complementary 256 - k CUs."""
+    disjoint=True the action half runs on the complementary 256 - k CUs. With
+    with_adit=True also returns, same indexing, the median time from the
+    lockstep's start to the end of its action half (the lockstep's duration
+    when it has none): (dur, adit)."""
     import torch
     nm, nb = len(models), n_buckets(max_batch)
     bs = bucket_batches(max_batch)
     out = np.zeros((len(cu_counts), nm, nb, nm, nb), dtype=np.int64)
+    adit = np.zeros_like(out)
     stream = join_stream if join_stream is not None else torch.cuda.current_stream()
+    ev_a = torch.cuda.Event(enable_timing=True)
+    ev_a.record(stream)                      # creates the event before its handle is passed on
     for ki, cu in enumerate(cu_counts):
         for mv in range(nm):
             for iv, bv in enumerate(bs):
@@ -270,9 +291,11 @@ def profile_locksteps(models: Sequence[vla.Model], bufs, max_batch: int, cu_coun
                             continue
                         if bv == 0 and mv > 0:
                             out[ki, mv, iv, ma, ia] = out[ki, 0, iv, ma, ia]   # no VLM half: model irrelevant
+                            adit[ki, mv, iv, ma, ia] = adit[ki, 0, iv, ma, ia]
                             continue
                         if ba == 0 and ma > 0:
                             out[ki, mv, iv, ma, ia] = out[ki, mv, iv, 0, ia]
+                            adit[ki, mv, iv, ma, ia] = adit[ki, mv, iv, 0, ia]
                             continue
                         xv, xa = bufs[mv], bufs[ma]
 
@@ -280,10 +303,11 @@ def profile_locksteps(models: Sequence[vla.Model], bufs, max_batch: int, cu_coun
                             vla.step(models[mv] if bv else None, bv, xv["pixels"], xv["text_ids"], xv["kv0"],
                                      models[ma] if ba else None, ba, xa["kv1"], xa["noise"], models[ma].cfg.steps,
                                      xa["act1"], vlm_cu_count=cu, state=xv.get("state"), join_stream=join_stream,
-                                     adit_cu_count=256 - cu if disjoint and cu < 256 else 0)
+                                     adit_cu_count=256 - cu if disjoint and cu < 256 else 0,
+                                     adit_done=ev_a if (with_adit and ba) else None)
                         for _ in range(warmup):
                             one()
-                        ts = []
+                        ts, ta = [], []
                         for _ in range(reps):
                             e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
                             e0.record(stream)
@@ -291,19 +315,24 @@ def profile_locksteps(models: Sequence[vla.Model], bufs, max_batch: int, cu_coun
                             e1.record(stream)
                             e1.synchronize()
                             ts.append(e0.elapsed_time(e1))
+                            ta.append(e0.elapsed_time(ev_a) if (with_adit and ba) else ts[-1])
                         out[ki, mv, iv, ma, ia] = int(np.median(ts) * 1e6)
+                        adit[ki, mv, iv, ma, ia] = min(int(np.median(ta) * 1e6), out[ki, mv, iv, ma, ia])
         if log:
             log(f"[profile] cu={cu} done")
-    return out
+    return (out, adit) if with_adit else out
 
 
-def best_cu_table(prof: np.ndarray, cu_counts: Sequence[int]):
+def best_cu_table(prof: np.ndarray, cu_counts: Sequence[int], adit: Optional[np.ndarray] = None):
     """Per combination, the CU restriction with the shortest lockstep, and
-    the resulting duration table."""
+    the resulting duration table (and, given the profile's action-half
+    times, those at the chosen restrictions: (table, dur, adit))."""
     best = np.argmin(np.where(prof > 0, prof, np.iinfo(np.int64).max), axis=0)
     table = np.asarray(cu_counts, dtype=np.int32)[best]
     dur = np.take_along_axis(prof, best[None], axis=0)[0]
-    return table, dur
+    if adit is None:
+        return table, dur
+    return table, dur, np.take_along_axis(adit, best[None], axis=0)[0]
 
 
 def expand_tables(dur_ns: np.ndarray, cu_table: np.ndarray, arch_of: Sequence[int]):
@@ -317,9 +346,12 @@ def expand_tables(dur_ns: np.ndarray, cu_table: np.ndarray, arch_of: Sequence[in
 
 def sweep_robots(dur_ns: np.ndarray, slo_ms: Sequence[float], max_batch: int, robots: Sequence[int], rate_hz,
                  duration_s: float, epochs: int, policy: str = "esf", host_overhead_ns: int = 0,
-                 traffic: str = "poisson", target: float = 0.98, mode: str = "lockstep"):
+                 traffic: str = "poisson", target: float = 0.98, mode: str = "lockstep",
+                 adit_ns: Optional[np.ndarray] = None):
     """Simulated robot-load sweep on a lockstep-duration table: for each robot
-    count, the mean SLO attainment over `epochs` seeded traces. Returns
+    count, the mean SLO attainment over `epochs` seeded traces. With adit_ns
+    (time from lockstep start to the action half's end) requests complete
+    when their action half ends, else at their lockstep's end. Returns
     (rows, max robots with attainment >= target)."""
     rows, best = [], 0
     gen = synth.poisson_arrivals if traffic == "poisson" else synth.periodic_arrivals
@@ -329,6 +361,8 @@ def sweep_robots(dur_ns: np.ndarray, slo_ms: Sequence[float], max_batch: int, ro
             arr = gen(R, rate_hz, duration_s, e, n_models=len(slo_ms))
             s = Scheduler(slo_ms, max_batch, policy, mode)
             s.set_sim(dur_ns, host_overhead_ns)
+            if adit_ns is not None:
+                s.set_delivery("adit", adit_ns)
             req, _ = s.run(arr, drain_ns=int(1e9), ls_cap=16)
             s.close()
             att.append(attainment(req))
@@ -342,14 +376,15 @@ def sweep_robots(dur_ns: np.ndarray, slo_ms: Sequence[float], max_batch: int, ro
 
 def max_robots(dur_ns: np.ndarray, slo_ms: Sequence[float], max_batch: int, rate_hz, duration_s: float,
                epochs: int, policy: str = "esf", traffic: str = "poisson", mode: str = "lockstep",
-               target: float = 0.98, r_max: int = 256, patience: int = 3, host_overhead_ns: int = 0):
+               target: float = 0.98, r_max: int = 256, patience: int = 3, host_overhead_ns: int = 0,
+               adit_ns: Optional[np.ndarray] = None):
     """Largest robot count with mean simulated SLO attainment >= target,
     scanning upwards and stopping after `patience` consecutive failures.
     Returns (robots, rows)."""
     rows, best, fails = [], 0, 0
     for R in range(1, r_max + 1):
         r, _ = sweep_robots(dur_ns, slo_ms, max_batch, [R], rate_hz, duration_s, epochs, policy, host_overhead_ns,
-                            traffic, target, mode)
+                            traffic, target, mode, adit_ns)
         rows += r
         if r[0]["attainment"] >= target:
             best, fails = R, 0

@@ -51,7 +51,7 @@ class StepArgsC(ctypes.Structure):
                 ("adit_model", ctypes.c_void_p), ("adit_batch", ctypes.c_int),
                 ("kv_in", ctypes.c_void_p), ("noise", ctypes.c_void_p), ("steps", ctypes.c_int),
                 ("actions_out", ctypes.c_void_p),
-                ("vlm_cu_count", ctypes.c_int), ("adit_cu_count", ctypes.c_int)]
+                ("vlm_cu_count", ctypes.c_int), ("adit_cu_count", ctypes.c_int), ("adit_done", ctypes.c_void_p)]
 
 
 def lib():
@@ -273,9 +273,11 @@ def nonblocking_stream(device: int = 0):
 
 def step(vlm_model: Optional[Model], vlm_batch: int, pixels, text_ids, kv_out,
          adit_model: Optional[Model], adit_batch: int, kv_in, noise, steps: int, actions_out,
-         vlm_cu_count: int = 256, adit_cu_count: int = 0, state=None, join_stream=None):
+         vlm_cu_count: int = 256, adit_cu_count: int = 0, state=None, join_stream=None, adit_done=None):
     """One lockstep: prefill(vlm_batch) on the CU-restricted stream alongside
-    denoise(adit_batch) on the action stream; join_stream waits for both."""
+    denoise(adit_batch) on the action stream; join_stream waits for both.
+    adit_done: a torch.cuda.Event (or raw hipEvent_t) recorded right after the
+    action half."""
     a = StepArgsC()
     a.vlm_model = vlm_model.handle if vlm_model is not None else None
     a.vlm_batch = vlm_batch
@@ -284,6 +286,8 @@ def step(vlm_model: Optional[Model], vlm_batch: int, pixels, text_ids, kv_out,
     a.adit_batch = adit_batch
     a.kv_in, a.noise, a.steps, a.actions_out = _ptr(kv_in), _ptr(noise), steps, _ptr(actions_out)
     a.vlm_cu_count, a.adit_cu_count = vlm_cu_count, adit_cu_count
+    if adit_done is not None:
+        a.adit_done = adit_done.cuda_event if hasattr(adit_done, "cuda_event") else int(adit_done)
     _check(lib().vla_step(ctypes.byref(a), _stream(join_stream)))
 
 

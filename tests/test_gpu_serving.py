@@ -87,15 +87,18 @@ def _served_batches(arr, ls, n_models):
     return out
 
 
-@pytest.mark.parametrize("disjoint", [False, True], ids=["guarded", "disjoint"])
-def test_online_executor_gathers_and_scatters_per_request(disjoint):
+@pytest.mark.parametrize("disjoint,delivery", [(False, "lockstep"), (True, "lockstep"), (False, "adit")],
+                         ids=["guarded", "disjoint", "guarded-early-delivery"])
+def test_online_executor_gathers_and_scatters_per_request(disjoint, delivery):
     """Requests bring their own seeded inputs (row i of the generators for
     request i) and their own output buffers; the library gathers them into
     its stage rows and scatters each chunk back. Every chunk equals a
     standalone run of the batch it was served in (same rows, same order),
     so a wrong gather or scatter row fails; DiT requests alternate between a
     given state and none (zeros). Both CU partitions: the guarded one (only
-    the VLM half restricted) and the disjoint one."""
+    the VLM half restricted) and the disjoint one; and chunks delivered as
+    soon as their action half ends (copied out on the delivery stream while
+    the VLM half may still run), timed inside their lockstep."""
     import torch
     from paper_2609_12075_amd import serve
     cfgs = [A, B, C]
@@ -105,6 +108,7 @@ def test_online_executor_gathers_and_scatters_per_request(disjoint):
     s.set_gpu_online(ms)
     s.set_cu(128)
     s.set_disjoint(disjoint)      # disjoint: the action half on the other 128 CUs
+    s.set_delivery(delivery)
     arr = synth.poisson_arrivals(6, 15.0, 0.8, epoch=3, n_models=3)
     log(f"[serving] online: {len(arr)} requests, 3 models")
     ins, outs, ios, keep = [], [], [], []
@@ -122,6 +126,12 @@ def test_online_executor_gathers_and_scatters_per_request(disjoint):
     s.close()
     assert (req["t_done_ns"] > 0).all(), "every request served"
     log(f"[serving] online: {len(ls)} locksteps, attainment {serve.attainment(req):.3f}")
+    assert ((ls["t_start_ns"] <= ls["t_chunks_ns"]) & (ls["t_chunks_ns"] <= ls["t_end_ns"])).all()
+    if delivery == "lockstep":
+        assert (ls["t_chunks_ns"] == ls["t_end_ns"]).all()
+    # every request completes at its action lockstep's delivery time
+    chunk_times = sorted(int(x["t_chunks_ns"]) for x in ls if x["adit_batch"] > 0)
+    assert set(int(t) for t in req["t_done_ns"]) <= set(chunk_times)
     for m, idx in _served_batches(arr, ls, 3):
         cfg = cfgs[m]
         batch = {k: np.concatenate([ins[i][k] for i in idx]) for k in ("pixels", "text_ids", "noise")}

@@ -143,6 +143,66 @@ def test_matches_reference_scheduler(seed):
                 int(a["met_slo"])) == (b["t_arrival"], b["t_vlm_start"], b["t_done"], b["model"], b["met"])
 
 
+@pytest.mark.parametrize("seed", range(24))
+def test_delivery_at_action_end_matches_reference(seed):
+    """Chunks delivered when their action half ends (a second table, entries
+    below and above the lockstep's duration): requests and lockstep records
+    equal to the reference, field by field."""
+    items, slo, mb, table, policy, overhead = _random_case(seed + 300)
+    rng = np.random.default_rng(seed)
+    adit = (table * rng.uniform(0.2, 1.3, table.shape)).astype(np.int64)
+    s = serve.Scheduler(slo, mb, policy)
+    s.set_sim(table, overhead)
+    s.set_delivery("adit", adit)
+    req, ls = s.run(arr(items), 10 ** 9)
+    s.close()
+    rreq, rls = REF.simulate(items, slo, mb, table.tolist(), policy=policy, overhead_ns=overhead,
+                             delivery="adit", adit_ns=adit.tolist())
+    assert [tuple(int(v) for v in a) for a in ls] == [tuple(b) for b in rls]
+    for a, b in zip(req, rreq):
+        assert (int(a["t_vlm_start_ns"]), int(a["t_done_ns"]), int(a["met_slo"])) == \
+            (b["t_vlm_start"], b["t_done"], b["met"])
+    for x in ls:
+        assert x["t_start_ns"] <= x["t_chunks_ns"] <= x["t_end_ns"]
+
+
+def test_delivery_at_action_end_closed_form():
+    """One model, batch 1: lockstep 0 runs the VLM half of request A (7 ms);
+    lockstep 1 the VLM half of B beside A's action half (9 ms in all, the
+    action half ends after 4 ms); lockstep 2 B's action half (5 ms alone).
+    Delivery at the lockstep end: A at 16 ms, B at 21 ms; at the action
+    half's end: A at 7 + 4 = 11 ms, B at 16 + 5 = 21 ms (its action half is
+    the whole lockstep). An SLO of 12 ms separates the two readings for A."""
+    mb = 1
+    nb = serve.n_buckets(mb)
+    table = np.zeros((1, nb, 1, nb), dtype=np.int64)
+    table[0, 1, 0, 0] = 7 * MS
+    table[0, 0, 0, 1] = 5 * MS
+    table[0, 1, 0, 1] = 9 * MS
+    adit = table.copy()
+    adit[0, 1, 0, 1] = 4 * MS
+    req, ls = run([(0, 0), (0, 0)], [12.0], mb, table)
+    assert req["t_done_ns"].tolist() == [16 * MS, 21 * MS] and req["met_slo"].tolist() == [0, 0]
+    s = serve.Scheduler([12.0], mb)
+    s.set_sim(table, 0)
+    s.set_delivery("adit", adit)
+    req, ls = s.run(arr([(0, 0), (0, 0)]), 10 ** 9)
+    s.close()
+    assert req["t_done_ns"].tolist() == [11 * MS, 21 * MS] and req["met_slo"].tolist() == [1, 0]
+    assert ls["t_chunks_ns"].tolist() == [7 * MS, 11 * MS, 21 * MS]
+
+
+def test_delivery_at_action_end_needs_its_table():
+    s = serve.Scheduler([50.0], 1)
+    s.set_sim(const_table(1, 1, MS), 0)
+    with pytest.raises(vla.VlaError, match="time table"):
+        s.set_delivery("adit")
+        s.run(arr([(0, 0)]), 10 ** 9)
+    with pytest.raises(vla.VlaError, match="unknown delivery"):
+        vla._check(serve._lib().vla_sched_set_delivery(s.handle, 7, None))
+    s.close()
+
+
 @pytest.mark.parametrize("seed", range(12))
 def test_monolithic_matches_reference(seed):
     items, slo, mb, table, policy, overhead = _random_case(seed + 100)
