@@ -1,7 +1,7 @@
 """Full-size parity of the pi0-shaped (27 ViT / 18 LLM / 18 action-expert
 layers) and GR00T-like (27 ViT / 12 LLM / 16 DiT layers) models through the
-C ABI, at batch 1 and at the largest batch (32), against the oracle's values
-for rows 0 and 31 stored under tests/golden/ (written by
+C ABI, at batch 1, at the serving batch cap 8 and at the largest batch (32),
+against the oracle's values for rows 0 and 31 stored under tests/golden/ (written by
 tests/golden/make_fullsize_goldens.py from the oracle alone: a fp64 pass over
 a full pi0-shaped request takes about a minute of CPU).
 
@@ -102,3 +102,17 @@ def test_fullsize_max_batch(full):
     inp, act, kv = _run(cfg, m, B)
     check_chunk(act[rows], g["actions"], inp["noise"][rows], TOL, f"{cfg.name} full B={B} rows {rows}")
     _check_handoff(cfg, g, kv, B, rows, [0, 1])
+
+
+def test_fullsize_serving_batch(full):
+    """Batch 8, the co-located benchmark's batch cap, whose projection plans
+    differ from those at 1 and 32 (pi0-shaped: the 2560-wide QKV on 128 x 128
+    staged tiles, the O and MLP-down projections on 224-row large tiles, the
+    attention's key ranges): row 0 against the oracle (its inputs do not
+    depend on the batch size)."""
+    cfg, g, m = full
+    B = 8
+    inp, act, kv = _run(cfg, m, B)
+    np.testing.assert_array_equal(inp["noise"][0], g["noise"][0])
+    check_chunk(act[:1], g["actions"][:1], inp["noise"][:1], TOL, f"{cfg.name} full B={B} row 0")
+    _check_handoff(cfg, g, kv, B, [0], [0])
