@@ -1111,8 +1111,12 @@ static GemmPlan plan_base(const GemmArgs& a) {
   };
   if (a.a_type == ET_BF16 && a.zeros) {
     // few activation rows and many weight rows: the small-M kernel (one
-    // memory round trip per 1024 of K, no K split)
-    if (a.M <= 64 && a.N >= 1536) {
+    // memory round trip per 1024 of K, no K split); also for 1024-1535
+    // weight rows when K fits one round trip, instead of K ranges and their
+    // reduce (the DiT head's output and cross-attention projections at batch
+    // 1-3: a DiT step at batch 1 1.110 -> 1.054 ms; narrower products such as
+    // the SmolVLA-shaped O projection, 720 x 960, measured slower this way)
+    if (a.M <= 64 && (a.N >= 1536 || (a.N >= 1024 && a.K <= 1024))) {
       p.kind = 2;
       p.bn = a.N >= 6144 ? 32 : 16;
       p.bm = 64;

@@ -25,8 +25,8 @@ GEMM_SHAPES = [
     # 256x128 with ragged M, N and K
     (2048, 4096, 592), (2048, 2048, 4304), (4000, 5000, 200),
     # small-M kernel: one and two weight-row subtiles, K tails, several K
-    # rounds, ragged N
-    (50, 3840, 720), (17, 1600, 1000), (63, 1537, 3000), (64, 8192, 1024),
+    # rounds, ragged N; 1024-1535 weight rows with K <= 1024 (ragged)
+    (50, 3840, 720), (17, 1600, 1000), (63, 1537, 3000), (64, 8192, 1024), (17, 1024, 1024), (60, 1200, 1000),
     # K ranges of the LDS-staged kernel (partial + ordered reduce), ragged
     (800, 720, 1920), (600, 1000, 1544),
     # register-pipelined 64 x 32 tiles with K ranges
@@ -84,7 +84,7 @@ def test_gemm_activations(act, amp):
     np.testing.assert_allclose(got, ref, rtol=2e-4, atol=2e-5 * amp)
 
 
-@pytest.mark.parametrize("M,N,K", [(8, 7, 128), (80, 768, 256), (5, 128, 7), (65, 130, 1024)])
+@pytest.mark.parametrize("M,N,K", [(8, 7, 128), (80, 768, 256), (5, 128, 7), (65, 130, 1024), (17, 1024, 1024)])
 def test_gemm_f32(M, N, K):
     import torch
     from paper_2609_12075_amd import vla
