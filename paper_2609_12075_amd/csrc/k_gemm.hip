@@ -923,17 +923,26 @@ gemm_stage_kernel(GemmArgs a) {
 // 128 x 128 tile. Rows are XOR-swizzled as in the multi-stage kernel; the
 // second K chunk's fragment reads are interleaved with the first chunk's
 // products. The epilogue stages the fp32 tile through LDS in two halves of
-// 128 rows.
-template <int MODE, int NW, int BM = 256>
+// 128 rows; with REG (GeGLU, eight waves) it works from the accumulators
+// instead: a lane's fragment holds four consecutive weight columns, i.e. two
+// whole gate/up pairs, of one activation row, so the activation runs in
+// registers, and the four lanes that share a row trade their packed results
+// (a 4 x 4 transpose of 32-bit words over the wave's four 16-lane rows, two
+// 32-lane and two 16-lane swaps) so that each lane stores 16 contiguous bytes.
+// That takes the LDS round trip and its barriers out of every tile (pi0-shaped
+// gate/up, 6528 x 32768 x 2048: 775 -> 740 us; 3264 rows 407 -> 362 us;
+// results identical).
+template <int MODE, int NW, int BM = 256, bool REG = false>
 __global__ void __launch_bounds__(NW * 64) gemm_big_kernel(GemmArgs a) {
   constexpr int BN = 256, BK = 64, ROWB = BK * 2;
   static_assert(BM == 256 || BM == 224, "activation tile of 256 or 224 rows");
   constexpr int WGN = NW / 2;                                    // waves along the weight rows
   constexpr int WTN = BN / WGN, WTM = BM / 2;                    // wave tile
   constexpr int TN = WTN / 16, TM = WTM / 16;
+  static_assert(!REG || (MODE == EPI_GEGLU && TN == 4), "register epilogue: GeGLU on eight waves");
   constexpr int STAGE_BYTES = (BN + BM) * ROWB;                  // 64 KiB (60 KiB)
   constexpr int LDC = BN + 4;
-  constexpr int SMEM = 2 * STAGE_BYTES > 128 * LDC * 4 ? 2 * STAGE_BYTES : 128 * LDC * 4;
+  constexpr int SMEM = REG || 2 * STAGE_BYTES > 128 * LDC * 4 ? 2 * STAGE_BYTES : 128 * LDC * 4;
   constexpr int GPW = 32 / NW;                                   // 8-row groups per wave of the weight tile
   constexpr int AG = BM / 8;                                     // 8-row groups of the activation tile
   constexpr int GPWA = (AG + NW - 1) / NW;                       // ... per wave (the last may be short)
@@ -1020,6 +1029,40 @@ __global__ void __launch_bounds__(NW * 64) gemm_big_kernel(GemmArgs a) {
       }
       __builtin_amdgcn_sched_group_barrier(0x008, 2 * NMF - NRD * R, 0);
     }
+  }
+  if constexpr (REG) {
+    // fragment (i, j) of lane (lr, lq): weight columns n_blk + wn0 + 16 i +
+    // 4 lq .. + 3 of activation row m_blk + wm0 + 16 j + lr; after the
+    // transpose the lane holds output columns (n_blk + wn0) / 2 + 8 lq .. + 7
+    // (N % 16 == 0, so a 16-column group is wholly inside or outside)
+    typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+    f32x4 bias[TN];
+#pragma unroll
+    for (int i = 0; i < TN; ++i) {
+      const int n0 = n_blk + wn0 + 16 * i + 4 * lq;
+      bias[i] = (a.bias && n0 < a.N) ? *reinterpret_cast<const f32x4*>(a.bias + n0) : f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+    const bool col_ok = n_blk + wn0 + 16 * lq < a.N;
+    bf16* out = reinterpret_cast<bf16*>(a.out) + ((n_blk + wn0) >> 1) + 8 * lq;
+#pragma unroll
+    for (int j = 0; j < TM; ++j) {
+      unsigned p[TN];
+#pragma unroll
+      for (int i = 0; i < TN; ++i) {
+        const f32x4 x = acc[i][j] + bias[i];
+        const bf16x2 h = bf16x2{(bf16)(act_apply(x[0], ACT_GELU) * x[1]), (bf16)(act_apply(x[2], ACT_GELU) * x[3])};
+        p[i] = *reinterpret_cast<const unsigned*>(&h);
+      }
+      // rows 0,1 <-> 2,3 (words 2,3 <-> 0,1), then rows 0 <-> 1 and 2 <-> 3
+      const auto s02 = __builtin_amdgcn_permlane32_swap(p[0], p[2], false, false);
+      const auto s13 = __builtin_amdgcn_permlane32_swap(p[1], p[3], false, false);
+      const auto s01 = __builtin_amdgcn_permlane16_swap(s02[0], s13[0], false, false);
+      const auto s23 = __builtin_amdgcn_permlane16_swap(s02[1], s13[1], false, false);
+      const int m = m_blk + wm0 + 16 * j + lr;
+      if (m < a.M && col_ok)
+        *reinterpret_cast<u32x4*>(out + (long)m * a.ldo) = u32x4{s01[0], s01[1], s23[0], s23[1]};
+    }
+    return;
   }
   // epilogue in two halves of BM / 2 activation rows (waves with wm0 == WTM h)
 #pragma unroll 1
@@ -1306,8 +1349,24 @@ static void launch_staged128(const GemmArgs& a0, const GemmPlan& p, const NormAr
   hipLaunchKernelGGL((gemm_stage_kernel<BT, BT, ST, MODE, 128, 2>), grid, dim3(512), 0, s, a);
 }
 
+// The large-tile GeGLU epilogue from registers needs bf16 output, whole
+// 16-column groups and 16-byte aligned output rows and bias.
+static bool geglu_reg_ok(const GemmArgs& a) {
+  auto al = [](const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; };
+  return a.mode == EPI_GEGLU && a.out_type == ET_BF16 && a.N % 16 == 0 && a.ldo % 8 == 0 && al(a.out) &&
+         (!a.bias || al(a.bias));
+}
+
 template <int MODE, int NW = 8>
 static void launch_big(const GemmArgs& a, int bm, hipStream_t s) {
+  if constexpr (MODE == EPI_GEGLU && NW == 8) {
+    if (geglu_reg_ok(a)) {
+      dim3 grid((a.M + bm - 1) / bm, (a.N + 255) / 256, 1);
+      if (bm == 224) hipLaunchKernelGGL((gemm_big_kernel<MODE, NW, 224, true>), grid, dim3(NW * 64), 0, s, a);
+      else hipLaunchKernelGGL((gemm_big_kernel<MODE, NW, 256, true>), grid, dim3(NW * 64), 0, s, a);
+      return;
+    }
+  }
   if (bm == 224) {
     dim3 grid((a.M + 223) / 224, (a.N + 255) / 256, 1);
     hipLaunchKernelGGL((gemm_big_kernel<MODE, NW, 224>), grid, dim3(NW * 64), 0, s, a);

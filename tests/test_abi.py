@@ -73,6 +73,17 @@ def test_null_arguments_rejected():
     assert "null" in L.vla_last_error().decode()
 
 
+def test_geglu_hook_rejects_bad_shapes_without_gpu():
+    L = vla.lib()
+    buf = (ctypes.c_char * 64)()
+    p = ctypes.cast(buf, ctypes.c_void_p)
+    # odd N (gate/up rows come in pairs), then an output row shorter than N / 2
+    assert L.vla_debug_gemm_geglu(4, 7, 8, p, 8, p, 8, None, p, 8, None) == vla.VLA_EINVAL
+    assert "even" in L.vla_last_error().decode()
+    assert L.vla_debug_gemm_geglu(4, 32, 8, p, 8, p, 8, None, p, 8, None) == vla.VLA_EINVAL
+    assert "leading dimensions" in L.vla_last_error().decode()
+
+
 @pytest.mark.parametrize("args,msg", [
     ((3, 64, 10, 0, 100), "kind must be"),
     ((2, 300, 10, 0, 100), "grid must be"),
