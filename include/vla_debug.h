@@ -30,19 +30,24 @@ vla_status vla_debug_gemm(int M, int N, int K, const void* A, int lda, int a_typ
                           int w_type, const float* bias, int act, float* out, int ldo, hipStream_t stream);
 
 /*
- * Gated-GELU projection (the MLP gate/up of the LLM and of the joint action
- * expert, Section 2.1's VLM and action stages): weight rows interleaved,
- * row 2f the gate and row 2f + 1 the up projection of feature f:
- *   out[m][f] = gelu(D[m][2f] + bias[2f]) * (D[m][2f + 1] + bias[2f + 1]),
- *   D = A Wt^T, tanh-form GELU, bf16 out [M][ldo] (ldo >= N / 2).
- *  A   device bf16 [M][lda]; Wt device bf16 [N][ldw] (K contiguous);
- *  bias device fp32 [N] or NULL. N even; K, lda, ldw multiples of 8.
- * The same plan and kernels as the model's gate/up projection of that shape
- * (the large-tile kernel stores from registers when N % 16 == 0, ldo % 8 ==
- * 0 and out and bias are 16-byte aligned, through LDS otherwise).
+ * Projection with bf16 output, as the model's bf16 layers run it:
+ *  glu = 0: out[m][n] = act(D[m][n] + bias[n])  (act: 0 none, 1 SiLU,
+ *           2 tanh-GELU), out [M][ldo] with ldo >= N;
+ *  glu = 1: the gated-GELU MLP projection (the gate/up of the LLM and of the
+ *           joint action expert, Section 2.1's VLM and action stages): weight
+ *           rows interleaved, row 2f the gate and row 2f + 1 the up projection
+ *           of feature f, out[m][f] = gelu(D[m][2f] + bias[2f]) *
+ *           (D[m][2f + 1] + bias[2f + 1]), out [M][ldo] with ldo >= N / 2,
+ *           N even, act 0;
+ *  D = A Wt^T. A device bf16 [M][lda]; Wt device bf16 [N][ldw] (K
+ *  contiguous); bias device fp32 [N] or NULL. K, lda, ldw multiples of 8.
+ * The same plan and kernels as a model projection of that shape: the
+ * large-tile and 128-column staged kernels store from registers when N % 16
+ * == 0, ldo % 8 == 0 and out and bias are 16-byte aligned, through LDS
+ * otherwise (same results).
  */
-vla_status vla_debug_gemm_geglu(int M, int N, int K, const void* A, int lda, const void* Wt, int ldw, const float* bias,
-                                void* out, int ldo, hipStream_t stream);
+vla_status vla_debug_gemm_bf16(int M, int N, int K, const void* A, int lda, const void* Wt, int ldw, const float* bias,
+                               int glu, int act, void* out, int ldo, hipStream_t stream);
 
 /*
  * vla_debug_gemm without any allocation, for callers that cannot allocate

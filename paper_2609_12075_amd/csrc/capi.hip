@@ -410,16 +410,19 @@ vla_status vla_debug_gemm(int M, int N, int K, const void* A, int lda, int a_typ
   });
 }
 
-vla_status vla_debug_gemm_geglu(int M, int N, int K, const void* A, int lda, const void* Wt, int ldw, const float* bias,
-                                void* out, int ldo, hipStream_t s) {
+vla_status vla_debug_gemm_bf16(int M, int N, int K, const void* A, int lda, const void* Wt, int ldw, const float* bias,
+                               int glu, int act, void* out, int ldo, hipStream_t s) {
   return guarded([&] {
     VLA_REQUIRE(M >= 0 && N >= 0 && K >= 0 && A && Wt && out, "bad gemm arguments");
-    VLA_REQUIRE(N % 2 == 0, "gate/up rows come in pairs: N must be even");
+    VLA_REQUIRE(glu == 0 || glu == 1, "glu must be 0 or 1");
+    VLA_REQUIRE(act >= ACT_NONE && act <= ACT_GELU && !(glu && act), "bad act");
+    VLA_REQUIRE(!glu || N % 2 == 0, "gate/up rows come in pairs: N must be even");
     VLA_REQUIRE(K % 8 == 0 && lda % 8 == 0 && ldw % 8 == 0, "bf16 path needs K, lda, ldw % 8 == 0");
-    VLA_REQUIRE(lda >= K && ldw >= K && ldo >= N / 2, "leading dimensions too small");
+    VLA_REQUIRE(lda >= K && ldw >= K && ldo >= (glu ? N / 2 : N), "leading dimensions too small");
     GemmArgs g{};
     g.M = M; g.N = N; g.K = K; g.A = A; g.lda = lda; g.a_type = ET_BF16; g.W = Wt; g.ldw = ldw; g.w_type = ET_BF16;
-    g.mode = EPI_GEGLU; g.act = ACT_NONE; g.bias = bias; g.tab_period = 1; g.out = out; g.ldo = ldo; g.out_type = ET_BF16;
+    g.mode = glu ? EPI_GEGLU : EPI_STORE; g.act = act; g.bias = bias; g.tab_period = 1; g.out = out; g.ldo = ldo;
+    g.out_type = ET_BF16;
     g.ws = debug_ws(0, vla_model_s::kSplitKFloats); g.ws_floats = vla_model_s::kSplitKFloats;
     g.zeros = debug_ws(2, 64);
     launch_gemm(g, s);

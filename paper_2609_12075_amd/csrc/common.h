@@ -136,6 +136,9 @@ struct GemmArgs {
   // rms_eps) before the epilogue, the sum taken from the bf16 A tiles the
   // product reads (bf16 A and W, no K ranges)
   int rms_in; float rms_eps;
+  // set by the launcher: the tile epilogue runs from the accumulators
+  // (GeGLU or plain bf16 store on the 128-column staged tiles; no LDS pass)
+  int epi_reg;
 };
 
 void launch_gemm(const GemmArgs& a, hipStream_t s);

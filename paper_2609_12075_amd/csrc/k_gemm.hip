@@ -357,6 +357,81 @@ __device__ __forceinline__ void tile_store_partial(const GemmArgs& a, const floa
   }
 }
 
+// ---------------------------------------------------------------- epilogue from registers
+// A wave's four fragments i = 0..3 along the weight rows: lane (lr, lq) of
+// fragment (i, j) holds weight columns nb + 16 i + 4 lq .. + 3 of activation
+// row mb + 16 j + lr (lr = lane % 16, lq = lane / 16). A 4 x 4 transpose of
+// 32-bit words over the four 16-lane rows of the wave (two 32-lane and two
+// 16-lane swaps) hands lane lq the words of fragment i = lq from all four
+// lanes that share its row: 16 consecutive weight columns.
+__device__ __forceinline__ void xpose4x4(unsigned (&p)[4]) {
+  const auto s02 = __builtin_amdgcn_permlane32_swap(p[0], p[2], false, false);   // rows 0,1 <-> 2,3
+  const auto s13 = __builtin_amdgcn_permlane32_swap(p[1], p[3], false, false);
+  const auto s01 = __builtin_amdgcn_permlane16_swap(s02[0], s13[0], false, false);   // rows 0 <-> 1, 2 <-> 3
+  const auto s23 = __builtin_amdgcn_permlane16_swap(s02[1], s13[1], false, false);
+  p[0] = s01[0]; p[1] = s01[1]; p[2] = s23[0]; p[3] = s23[1];
+}
+
+__device__ __forceinline__ unsigned pack_bf16x2(float lo, float hi) {
+  const bf16x2 h = bf16x2{(bf16)lo, (bf16)hi};
+  return *reinterpret_cast<const unsigned*>(&h);
+}
+
+// The GeGLU or plain bf16-store epilogue of such a wave tile, without the LDS
+// round trip: GeGLU (a fragment holds two whole gate/up pairs) leaves one
+// word per fragment and the lane stores 16 bytes (output columns nb / 2 +
+// 8 lq ..); a store leaves two words per fragment (both halves transposed)
+// and the lane stores 32 bytes (columns nb + 16 lq ..). reg_epi_ok states
+// what the caller must hold (N % 16 == 0, so a group of 16 columns is wholly
+// inside or outside; aligned rows; no row table, row groups or copy).
+template <int MODE, int TM>
+__device__ __forceinline__ void reg_epilogue(const GemmArgs& a, const f32x4 (&acc)[4][TM], int nb, int mb, int lane) {
+  static_assert(MODE == EPI_GEGLU || MODE == EPI_STORE, "GeGLU or plain store");
+  typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+  const int lr = lane & 15, lq = lane >> 4;
+  f32x4 bias[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int n0 = nb + 16 * i + 4 * lq;
+    bias[i] = (a.bias && n0 < a.N) ? *reinterpret_cast<const f32x4*>(a.bias + n0) : f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+  const bool col_ok = nb + 16 * lq < a.N;
+  bf16* out = reinterpret_cast<bf16*>(a.out) + (MODE == EPI_GEGLU ? (nb >> 1) + 8 * lq : nb + 16 * lq);
+#pragma unroll
+  for (int j = 0; j < TM; ++j) {
+    const int m = mb + 16 * j + lr;
+    if constexpr (MODE == EPI_GEGLU) {
+      unsigned p[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const f32x4 x = acc[i][j] + bias[i];
+        p[i] = pack_bf16x2(act_apply(x[0], ACT_GELU) * x[1], act_apply(x[2], ACT_GELU) * x[3]);
+      }
+      xpose4x4(p);
+      if (m < a.M && col_ok) *reinterpret_cast<u32x4*>(out + (long)m * a.ldo) = u32x4{p[0], p[1], p[2], p[3]};
+    } else {
+      unsigned lo[4], hi[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        f32x4 x = acc[i][j] + bias[i];
+        if (a.act != ACT_NONE) {
+#pragma unroll
+          for (int e = 0; e < 4; ++e) x[e] = act_apply(x[e], a.act);
+        }
+        lo[i] = pack_bf16x2(x[0], x[1]);
+        hi[i] = pack_bf16x2(x[2], x[3]);
+      }
+      xpose4x4(lo);
+      xpose4x4(hi);
+      if (m < a.M && col_ok) {
+        u32x4* o = reinterpret_cast<u32x4*>(out + (long)m * a.ldo);
+        o[0] = u32x4{lo[0], hi[0], lo[1], hi[1]};
+        o[1] = u32x4{lo[2], hi[2], lo[3], hi[3]};
+      }
+    }
+  }
+}
+
 // ---------------------------------------------------------------- bf16 MFMA kernel
 // Block: 256 threads = 4 waves in a 2 x 2 grid over a BN (weight rows) x BM
 // (activation rows) tile; K advances in steps of 64 through a double-buffered
@@ -872,6 +947,14 @@ gemm_stage_kernel(GemmArgs a) {
         rsq[kg * BM + wm0 + 16 * j + c] = v == 0 ? sq[j][0] : v == 1 ? sq[j][1] : v == 2 ? sq[j][2] : sq[j][3];
     }
   }
+  if constexpr (KG == 1 && !RMS && TN == 4 && (MODE == EPI_GEGLU || MODE == EPI_STORE)) {
+    // GeGLU or a plain bf16 store from the accumulators (the launcher sets
+    // epi_reg when reg_epi_ok holds and K is not split)
+    if (a.epi_reg) {
+      reg_epilogue<MODE, TM>(a, acc, n_blk + wn0, m_blk + wm0, lane);
+      return;
+    }
+  }
   // each wave group's tile to its own fp32 plane; the epilogues add the
   // planes in group order (the row scales, in their own LDS words, are
   // formed while the planes are written)
@@ -923,15 +1006,14 @@ gemm_stage_kernel(GemmArgs a) {
 // 128 x 128 tile. Rows are XOR-swizzled as in the multi-stage kernel; the
 // second K chunk's fragment reads are interleaved with the first chunk's
 // products. The epilogue stages the fp32 tile through LDS in two halves of
-// 128 rows; with REG (GeGLU, eight waves) it works from the accumulators
-// instead: a lane's fragment holds four consecutive weight columns, i.e. two
-// whole gate/up pairs, of one activation row, so the activation runs in
-// registers, and the four lanes that share a row trade their packed results
-// (a 4 x 4 transpose of 32-bit words over the wave's four 16-lane rows, two
-// 32-lane and two 16-lane swaps) so that each lane stores 16 contiguous bytes.
-// That takes the LDS round trip and its barriers out of every tile (pi0-shaped
-// gate/up, 6528 x 32768 x 2048: 775 -> 740 us; 3264 rows 407 -> 362 us;
-// results identical).
+// 128 rows; with REG (GeGLU or a plain bf16 store, eight waves) it works from
+// the accumulators instead (reg_epilogue): a lane's fragment holds four
+// consecutive weight columns of one activation row (for GeGLU two whole
+// gate/up pairs, so the activation runs in registers), and the four lanes
+// that share a row trade their packed results so that each lane stores 16 or
+// 32 contiguous bytes. That takes the LDS round trip and its barriers out of
+// every tile (pi0-shaped gate/up, 6528 x 32768 x 2048: 775 -> 740 us; 3264
+// rows 407 -> 362 us; results identical).
 template <int MODE, int NW, int BM = 256, bool REG = false>
 __global__ void __launch_bounds__(NW * 64) gemm_big_kernel(GemmArgs a) {
   constexpr int BN = 256, BK = 64, ROWB = BK * 2;
@@ -939,7 +1021,7 @@ __global__ void __launch_bounds__(NW * 64) gemm_big_kernel(GemmArgs a) {
   constexpr int WGN = NW / 2;                                    // waves along the weight rows
   constexpr int WTN = BN / WGN, WTM = BM / 2;                    // wave tile
   constexpr int TN = WTN / 16, TM = WTM / 16;
-  static_assert(!REG || (MODE == EPI_GEGLU && TN == 4), "register epilogue: GeGLU on eight waves");
+  static_assert(!REG || ((MODE == EPI_GEGLU || MODE == EPI_STORE) && TN == 4), "register epilogue: eight waves");
   constexpr int STAGE_BYTES = (BN + BM) * ROWB;                  // 64 KiB (60 KiB)
   constexpr int LDC = BN + 4;
   constexpr int SMEM = REG || 2 * STAGE_BYTES > 128 * LDC * 4 ? 2 * STAGE_BYTES : 128 * LDC * 4;
@@ -1031,37 +1113,7 @@ __global__ void __launch_bounds__(NW * 64) gemm_big_kernel(GemmArgs a) {
     }
   }
   if constexpr (REG) {
-    // fragment (i, j) of lane (lr, lq): weight columns n_blk + wn0 + 16 i +
-    // 4 lq .. + 3 of activation row m_blk + wm0 + 16 j + lr; after the
-    // transpose the lane holds output columns (n_blk + wn0) / 2 + 8 lq .. + 7
-    // (N % 16 == 0, so a 16-column group is wholly inside or outside)
-    typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
-    f32x4 bias[TN];
-#pragma unroll
-    for (int i = 0; i < TN; ++i) {
-      const int n0 = n_blk + wn0 + 16 * i + 4 * lq;
-      bias[i] = (a.bias && n0 < a.N) ? *reinterpret_cast<const f32x4*>(a.bias + n0) : f32x4{0.f, 0.f, 0.f, 0.f};
-    }
-    const bool col_ok = n_blk + wn0 + 16 * lq < a.N;
-    bf16* out = reinterpret_cast<bf16*>(a.out) + ((n_blk + wn0) >> 1) + 8 * lq;
-#pragma unroll
-    for (int j = 0; j < TM; ++j) {
-      unsigned p[TN];
-#pragma unroll
-      for (int i = 0; i < TN; ++i) {
-        const f32x4 x = acc[i][j] + bias[i];
-        const bf16x2 h = bf16x2{(bf16)(act_apply(x[0], ACT_GELU) * x[1]), (bf16)(act_apply(x[2], ACT_GELU) * x[3])};
-        p[i] = *reinterpret_cast<const unsigned*>(&h);
-      }
-      // rows 0,1 <-> 2,3 (words 2,3 <-> 0,1), then rows 0 <-> 1 and 2 <-> 3
-      const auto s02 = __builtin_amdgcn_permlane32_swap(p[0], p[2], false, false);
-      const auto s13 = __builtin_amdgcn_permlane32_swap(p[1], p[3], false, false);
-      const auto s01 = __builtin_amdgcn_permlane16_swap(s02[0], s13[0], false, false);
-      const auto s23 = __builtin_amdgcn_permlane16_swap(s02[1], s13[1], false, false);
-      const int m = m_blk + wm0 + 16 * j + lr;
-      if (m < a.M && col_ok)
-        *reinterpret_cast<u32x4*>(out + (long)m * a.ldo) = u32x4{s01[0], s01[1], s23[0], s23[1]};
-    }
+    reg_epilogue<MODE, TM>(a, acc, n_blk + wn0, m_blk + wm0, lane);
     return;
   }
   // epilogue in two halves of BM / 2 activation rows (waves with wm0 == WTM h)
@@ -1290,6 +1342,16 @@ GemmPlan gemm_plan(const GemmArgs& a) {
   return GemmPlan{big ? 128 : 64, big ? 128 : 64, 1, (a.K + 63) / 64 * 64, 1};
 }
 
+// The epilogue from registers (reg_epilogue) needs bf16 output, whole
+// 16-column groups, 16-byte aligned output rows and bias, and for a plain
+// store no row table, row groups or fp32/bf16 copy.
+static bool reg_epi_ok(const GemmArgs& a) {
+  auto al = [](const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; };
+  if (a.out_type != ET_BF16 || a.N % 16 != 0 || a.ldo % 8 != 0 || !al(a.out) || (a.bias && !al(a.bias))) return false;
+  if (a.mode == EPI_GEGLU) return true;
+  return a.mode == EPI_STORE && !a.tab && a.row_group <= 0 && !a.out2;
+}
+
 // Second pass of a split product: the ordered reduce with the epilogue, or
 // for a residual projection with a following row norm, the fused reduce.
 template <int MODE>
@@ -1311,6 +1373,7 @@ static void launch_reduce(const GemmArgs& a, const NormArgs* fuse, hipStream_t s
 template <int BN, int BM, int MODE>
 static void launch_staged(const GemmArgs& a0, const GemmPlan& p, const NormArgs* fuse, hipStream_t s) {
   GemmArgs a = a0;
+  a.epi_reg = 0;
   a.ksplit = p.ksplit;
   a.splits = p.splits;
   dim3 grid((a.M + BM - 1) / BM, (a.N + BN - 1) / BN, a.splits);
@@ -1326,6 +1389,7 @@ static void launch_staged(const GemmArgs& a0, const GemmPlan& p, const NormArgs*
       return;
     }
   }
+  a.epi_reg = BN == 128 && reg_epi_ok(a) ? 1 : 0;
   hipLaunchKernelGGL((gemm_stage_kernel<BN, BM, 2, MODE>), grid, dim3(256), 0, s, a);
 }
 
@@ -1349,18 +1413,11 @@ static void launch_staged128(const GemmArgs& a0, const GemmPlan& p, const NormAr
   hipLaunchKernelGGL((gemm_stage_kernel<BT, BT, ST, MODE, 128, 2>), grid, dim3(512), 0, s, a);
 }
 
-// The large-tile GeGLU epilogue from registers needs bf16 output, whole
-// 16-column groups and 16-byte aligned output rows and bias.
-static bool geglu_reg_ok(const GemmArgs& a) {
-  auto al = [](const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; };
-  return a.mode == EPI_GEGLU && a.out_type == ET_BF16 && a.N % 16 == 0 && a.ldo % 8 == 0 && al(a.out) &&
-         (!a.bias || al(a.bias));
-}
 
 template <int MODE, int NW = 8>
 static void launch_big(const GemmArgs& a, int bm, hipStream_t s) {
-  if constexpr (MODE == EPI_GEGLU && NW == 8) {
-    if (geglu_reg_ok(a)) {
+  if constexpr ((MODE == EPI_GEGLU || MODE == EPI_STORE) && NW == 8) {
+    if (reg_epi_ok(a)) {
       dim3 grid((a.M + bm - 1) / bm, (a.N + 255) / 256, 1);
       if (bm == 224) hipLaunchKernelGGL((gemm_big_kernel<MODE, NW, 224, true>), grid, dim3(NW * 64), 0, s, a);
       else hipLaunchKernelGGL((gemm_big_kernel<MODE, NW, 256, true>), grid, dim3(NW * 64), 0, s, a);

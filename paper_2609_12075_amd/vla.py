@@ -26,7 +26,7 @@ VLA_OK, VLA_EINVAL, VLA_ENOMEM, VLA_EHIP, VLA_EUNSUPPORTED = range(5)
 # every exported symbol declared by include/vla.h and include/vla_debug.h
 EXPORTS = ["vla_weight_count", "vla_create_model", "vla_destroy_model", "vla_set_graphs", "vla_kv_bytes",
            "vla_prefill", "vla_prefill_ex", "vla_denoise", "vla_step", "vla_last_error", "vla_shutdown",
-           "vla_debug_gemm", "vla_debug_gemm_geglu", "vla_debug_resid_norm", "vla_debug_gemm_rms", "vla_debug_resid_copy", "vla_debug_attention",
+           "vla_debug_gemm", "vla_debug_gemm_bf16", "vla_debug_resid_norm", "vla_debug_gemm_rms", "vla_debug_resid_copy", "vla_debug_attention",
            "vla_debug_cu_probe", "vla_debug_replay_gemm", "vla_gemm_noalloc", "vla_debug_sync_probe"]
 
 
@@ -78,8 +78,8 @@ def lib():
         L.vla_last_error.argtypes = []; L.vla_last_error.restype = ctypes.c_char_p
         L.vla_debug_gemm.argtypes = [ci, ci, ci, vp, ci, ci, vp, ci, ci, vp, ci, vp, ci, vp]
         L.vla_debug_gemm.restype = ci
-        L.vla_debug_gemm_geglu.argtypes = [ci, ci, ci, vp, ci, vp, ci, vp, vp, ci, vp]
-        L.vla_debug_gemm_geglu.restype = ci
+        L.vla_debug_gemm_bf16.argtypes = [ci, ci, ci, vp, ci, vp, ci, vp, ci, ci, vp, ci, vp]
+        L.vla_debug_gemm_bf16.restype = ci
         L.vla_gemm_noalloc.argtypes = [ci, ci, ci, vp, ci, ci, vp, ci, ci, vp, ci, vp, ci, vp]
         L.vla_gemm_noalloc.restype = ci
         L.vla_debug_resid_norm.argtypes = [ci, ci, ci, vp, vp, vp, vp, vp, ci, vp, vp, ctypes.c_float, vp, vp]
@@ -321,16 +321,17 @@ def debug_gemm(A, Wt, bias=None, act=0, out=None, M=None, N=None, K=None, stream
     return _gemm_call(lib().vla_debug_gemm, A, Wt, bias, act, out, M, N, K, stream)
 
 
-def debug_gemm_geglu(A, Wt, bias=None, out=None, stream=None):
-    """Gated-GELU projection: out[m][f] = gelu(D[m][2f] + b[2f]) * (D[m][2f+1] + b[2f+1]),
-    D = A Wt^T; bf16 A [M][K], Wt [N][K], out bf16 [M][N/2] (or a given 2-D bf16 view)."""
+def debug_gemm_bf16(A, Wt, bias=None, glu=False, act=0, out=None, stream=None):
+    """Projection with bf16 output: act(A Wt^T + bias) [M][N], or with glu the
+    gated-GELU form gelu(D[:, 2f] + b[2f]) * (D[:, 2f+1] + b[2f+1]) [M][N/2];
+    bf16 A [M][K], Wt [N][K]; out may be a 2-D bf16 view with contiguous rows."""
     import torch
     M, K = A.shape
     N = Wt.shape[0]
     if out is None:
-        out = torch.empty(M, N // 2, dtype=torch.bfloat16, device=A.device)
-    _check(lib().vla_debug_gemm_geglu(M, N, K, _ptr(A), A.stride(0), _ptr(Wt), Wt.stride(0), _ptr(bias),
-                                      _ptr_rows(out), out.stride(0), _stream(stream)))
+        out = torch.empty(M, N // 2 if glu else N, dtype=torch.bfloat16, device=A.device)
+    _check(lib().vla_debug_gemm_bf16(M, N, K, _ptr(A), A.stride(0), _ptr(Wt), Wt.stride(0), _ptr(bias), int(bool(glu)),
+                                     act, _ptr_rows(out), out.stride(0), _stream(stream)))
     return out
 
 

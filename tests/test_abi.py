@@ -73,15 +73,19 @@ def test_null_arguments_rejected():
     assert "null" in L.vla_last_error().decode()
 
 
-def test_geglu_hook_rejects_bad_shapes_without_gpu():
+def test_bf16_gemm_hook_rejects_bad_shapes_without_gpu():
     L = vla.lib()
     buf = (ctypes.c_char * 64)()
     p = ctypes.cast(buf, ctypes.c_void_p)
-    # odd N (gate/up rows come in pairs), then an output row shorter than N / 2
-    assert L.vla_debug_gemm_geglu(4, 7, 8, p, 8, p, 8, None, p, 8, None) == vla.VLA_EINVAL
+    # GeGLU with odd N (gate/up rows come in pairs), an activation on top of
+    # the GeGLU, and an output row shorter than N / 2
+    assert L.vla_debug_gemm_bf16(4, 7, 8, p, 8, p, 8, None, 1, 0, p, 8, None) == vla.VLA_EINVAL
     assert "even" in L.vla_last_error().decode()
-    assert L.vla_debug_gemm_geglu(4, 32, 8, p, 8, p, 8, None, p, 8, None) == vla.VLA_EINVAL
+    assert L.vla_debug_gemm_bf16(4, 8, 8, p, 8, p, 8, None, 1, 2, p, 8, None) == vla.VLA_EINVAL
+    assert "act" in L.vla_last_error().decode()
+    assert L.vla_debug_gemm_bf16(4, 32, 8, p, 8, p, 8, None, 1, 0, p, 8, None) == vla.VLA_EINVAL
     assert "leading dimensions" in L.vla_last_error().decode()
+    assert L.vla_debug_gemm_bf16(4, 32, 8, p, 8, p, 8, None, 0, 0, p, 16, None) == vla.VLA_EINVAL
 
 
 @pytest.mark.parametrize("args,msg", [

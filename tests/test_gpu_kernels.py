@@ -85,36 +85,46 @@ def test_gemm_activations(act, amp):
 
 
 @pytest.mark.parametrize("M,N,K", [
-    # large-tile kernel, GeGLU from registers: 224-row tiles with ragged M, K
-    # and a last weight tile holding one 16-column group; 256-row tiles
+    # large-tile kernel, epilogue from registers: 224-row tiles with ragged M,
+    # K and a last weight tile holding one 16-column group; 256-row tiles
     (2600, 4112, 2056), (3584, 4608, 2048),
-    # large-tile kernel through LDS (N % 16 != 0); the staged and small-M
-    # kernels (the action stage's gate/up shapes)
-    (3584, 4600, 2048), (800, 3840, 720), (50, 8192, 1024),
+    # large-tile kernel through LDS (N % 16 != 0)
+    (3584, 4600, 2048),
+    # staged 128 x 128 and 128 x 64 tiles from registers, ragged N; through LDS
+    (4000, 1616, 640), (1500, 1616, 640), (4000, 1608, 640),
+    # small-M kernel (LDS epilogue)
+    (50, 8192, 1024),
 ])
-def test_gemm_geglu(M, N, K):
-    """Gated-GELU projection (interleaved gate/up rows) against fp64 on sampled
-    rows, and every element of the default output bit-equal to a run whose
-    output rows are only 4-byte aligned (the per-element epilogue)."""
+@pytest.mark.parametrize("glu,act", [(1, 0), (0, 2), (0, 0)])
+def test_gemm_bf16_out(M, N, K, glu, act):
+    """bf16-output projections, gated-GELU (interleaved gate/up rows) or a
+    plain store with or without an activation, against fp64 on sampled rows;
+    every element of the default output bit-equal to a run whose output rows
+    are only 4-byte aligned (the per-element epilogue), and nothing written
+    outside the output view."""
     import torch
     from paper_2609_12075_amd import vla
-    log(f"[gemm geglu] M={M} N={N} K={K}")
+    log(f"[gemm bf16 out] M={M} N={N} K={K} glu={glu} act={act}")
     A = _bf16(RNG.standard_normal((M, K)))
     W = _bf16(RNG.standard_normal((N, K)) * 0.05)
     bias = (RNG.standard_normal(N) * 0.3).astype(np.float32)
     At = torch.from_numpy(A).to(torch.bfloat16).cuda()
     Wt = torch.from_numpy(W).to(torch.bfloat16).cuda()
     bt = torch.from_numpy(bias).cuda()
-    out = vla.debug_gemm_geglu(At, Wt, bt)
-    wide = torch.full((M, N // 2 + 8), float("nan"), dtype=torch.bfloat16, device="cuda")
-    vla.debug_gemm_geglu(At, Wt, bt, out=wide[:, 2:2 + N // 2])
+    No = N // 2 if glu else N
+    out = vla.debug_gemm_bf16(At, Wt, bt, glu=glu, act=act)
+    wide = torch.full((M, No + 8), float("nan"), dtype=torch.bfloat16, device="cuda")
+    vla.debug_gemm_bf16(At, Wt, bt, glu=glu, act=act, out=wide[:, 2:2 + No])
     torch.cuda.synchronize()
     got = out.float().cpu().numpy()
-    assert torch.equal(out.view(torch.int16), wide[:, 2:2 + N // 2].view(torch.int16))
-    assert torch.isnan(wide[:, :2].float()).all() and torch.isnan(wide[:, 2 + N // 2:].float()).all()
+    assert torch.equal(out.view(torch.int16), wide[:, 2:2 + No].view(torch.int16))
+    assert torch.isnan(wide[:, :2].float()).all() and torch.isnan(wide[:, 2 + No:].float()).all()
     rows = np.unique(np.concatenate([np.arange(min(M, 24)), RNG.integers(0, M, 40), np.arange(max(0, M - 24), M)]))
     D = A[rows].astype(np.float64) @ W.astype(np.float64).T + bias
-    ref = O.gelu_tanh(D[:, 0::2]) * D[:, 1::2]
+    if glu:
+        ref = O.gelu_tanh(D[:, 0::2]) * D[:, 1::2]
+    else:
+        ref = O.gelu_tanh(D) if act == 2 else D
     scale = np.abs(ref).max()
     np.testing.assert_allclose(got[rows], ref, rtol=8e-3, atol=2e-3 * scale)
 
