@@ -39,15 +39,18 @@ vla_status vla_debug_gemm(int M, int N, int K, const void* A, int lda, int a_typ
  *           of feature f, out[m][f] = gelu(D[m][2f] + bias[2f]) *
  *           (D[m][2f + 1] + bias[2f + 1]), out [M][ldo] with ldo >= N / 2,
  *           N even, act 0;
- *  D = A Wt^T. A device bf16 [M][lda]; Wt device bf16 [N][ldw] (K
- *  contiguous); bias device fp32 [N] or NULL. K, lda, ldw multiples of 8.
+ *  D = A Wt^T, or with rms = 1 D[m][n] = sum_k A[m][k] Wt[n][k] /
+ *  sqrt(mean_k A[m][k]^2 + eps) (the RMSNorm of the input rows folded into
+ *  the product, as the bf16 action experts run it; K >= 8).
+ *  A device bf16 [M][lda]; Wt device bf16 [N][ldw] (K contiguous); bias
+ *  device fp32 [N] or NULL. K, lda, ldw multiples of 8.
  * The same plan and kernels as a model projection of that shape: the
  * large-tile and 128-column staged kernels store from registers when N % 16
  * == 0, ldo % 8 == 0 and out and bias are 16-byte aligned, through LDS
  * otherwise (same results).
  */
 vla_status vla_debug_gemm_bf16(int M, int N, int K, const void* A, int lda, const void* Wt, int ldw, const float* bias,
-                               int glu, int act, void* out, int ldo, hipStream_t stream);
+                               int glu, int act, int rms, float eps, void* out, int ldo, hipStream_t stream);
 
 /*
  * vla_debug_gemm without any allocation, for callers that cannot allocate

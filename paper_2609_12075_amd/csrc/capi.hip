@@ -411,10 +411,11 @@ vla_status vla_debug_gemm(int M, int N, int K, const void* A, int lda, int a_typ
 }
 
 vla_status vla_debug_gemm_bf16(int M, int N, int K, const void* A, int lda, const void* Wt, int ldw, const float* bias,
-                               int glu, int act, void* out, int ldo, hipStream_t s) {
+                               int glu, int act, int rms, float eps, void* out, int ldo, hipStream_t s) {
   return guarded([&] {
     VLA_REQUIRE(M >= 0 && N >= 0 && K >= 0 && A && Wt && out, "bad gemm arguments");
     VLA_REQUIRE(glu == 0 || glu == 1, "glu must be 0 or 1");
+    VLA_REQUIRE(rms == 0 || (rms == 1 && K >= 8 && eps > 0.f), "rms must be 0, or 1 with K >= 8 and eps > 0");
     VLA_REQUIRE(act >= ACT_NONE && act <= ACT_GELU && !(glu && act), "bad act");
     VLA_REQUIRE(!glu || N % 2 == 0, "gate/up rows come in pairs: N must be even");
     VLA_REQUIRE(K % 8 == 0 && lda % 8 == 0 && ldw % 8 == 0, "bf16 path needs K, lda, ldw % 8 == 0");
@@ -425,6 +426,7 @@ vla_status vla_debug_gemm_bf16(int M, int N, int K, const void* A, int lda, cons
     g.out_type = ET_BF16;
     g.ws = debug_ws(0, vla_model_s::kSplitKFloats); g.ws_floats = vla_model_s::kSplitKFloats;
     g.zeros = debug_ws(2, 64);
+    if (rms) { g.rms_in = K; g.rms_eps = eps; }
     launch_gemm(g, s);
     VLA_HIP(hipGetLastError());
   });

@@ -297,6 +297,14 @@ __device__ __forceinline__ void epi_rows(const GemmArgs& a, const f32x4 (&t)[NIT
   }
 }
 
+// The folded norm's row scale as a multiply of its own, never fused with the
+// bias add that follows, so that every epilogue path (LDS tile, per-element,
+// from registers) rounds alike.
+__device__ __forceinline__ f32x4 row_scale(f32x4 t, float s) {
+#pragma clang fp contract(off)
+  return t * s;
+}
+
 // Thread tid of NT finishes the tile's rows r0 + it * RS of its four columns
 // (see above), GRP rows per memory round trip (GRP bounds the registers the
 // row loads hold); the tile is the sum of NSUM fp32 planes in LDS (plane
@@ -327,7 +335,7 @@ __device__ __forceinline__ void tile_epilogue(const GemmArgs& a, const float* Cs
         t[it] = *reinterpret_cast<const f32x4*>(Cs + mr * LDC + nc);
 #pragma unroll
         for (int z = 1; z < NSUM; ++z) t[it] += *reinterpret_cast<const f32x4*>(Cs + z * ROWS * LDC + mr * LDC + nc);
-        if (rsc) t[it] *= rsc[mr];
+        if (rsc) t[it] = row_scale(t[it], rsc[mr]);
       }
     }
     epi_rows<MODE, G>(a, t, ms, ok, n0);
@@ -774,7 +782,7 @@ __global__ void __launch_bounds__(256) gemm_skinny_kernel(GemmArgs a) {
     const int mr = c / (BN / 4), nc = (c % (BN / 4)) * 4;
     f32x4 t = *reinterpret_cast<const f32x4*>(&red[0][mr][nc]) + *reinterpret_cast<const f32x4*>(&red[1][mr][nc]) +
               *reinterpret_cast<const f32x4*>(&red[2][mr][nc]) + *reinterpret_cast<const f32x4*>(&red[3][mr][nc]);
-    if constexpr (RMS) t *= rsc[mr];
+    if constexpr (RMS) t = row_scale(t, rsc[mr]);
     float v[4] = {t[0], t[1], t[2], t[3]};
     epilogue4<MODE>(a, m0 + mr, n0 + nc, v);
   }
@@ -947,10 +955,22 @@ gemm_stage_kernel(GemmArgs a) {
         rsq[kg * BM + wm0 + 16 * j + c] = v == 0 ? sq[j][0] : v == 1 ? sq[j][1] : v == 2 ? sq[j][2] : sq[j][3];
     }
   }
-  if constexpr (KG == 1 && !RMS && TN == 4 && (MODE == EPI_GEGLU || MODE == EPI_STORE)) {
+  if constexpr (KG == 1 && TN == 4 && (MODE == EPI_GEGLU || MODE == EPI_STORE)) {
     // GeGLU or a plain bf16 store from the accumulators (the launcher sets
-    // epi_reg when reg_epi_ok holds and K is not split)
+    // epi_reg when reg_epi_ok holds and K is not split); RMS: the row scales
+    // meet in LDS as below and each lane scales its rows' fragments
     if (a.epi_reg) {
+      if constexpr (RMS) {
+        __syncthreads();
+        if (tid < BM) rsc[tid] = rsqrtf(rsq[tid] / (float)a.rms_in + a.rms_eps);
+        __syncthreads();
+#pragma unroll
+        for (int j = 0; j < TM; ++j) {
+          const float sc = rsc[wm0 + 16 * j + lr];
+#pragma unroll
+          for (int i = 0; i < TN; ++i) acc[i][j] = row_scale(acc[i][j], sc);
+        }
+      }
       reg_epilogue<MODE, TM>(a, acc, n_blk + wn0, m_blk + wm0, lane);
       return;
     }
@@ -989,7 +1009,7 @@ gemm_stage_kernel(GemmArgs a) {
     f32x4 t = *reinterpret_cast<const f32x4*>(&Cs[mr * LDC + nc]);
 #pragma unroll
     for (int z = 1; z < KG; ++z) t += *reinterpret_cast<const f32x4*>(&Cs[z * BM * LDC + mr * LDC + nc]);
-    if constexpr (RMS) t *= rsc[mr];
+    if constexpr (RMS) t = row_scale(t, rsc[mr]);
     float v[4] = {t[0], t[1], t[2], t[3]};
     epilogue4<MODE>(a, m_blk + mr, n_blk + nc, v);
   }
@@ -1383,13 +1403,13 @@ static void launch_staged(const GemmArgs& a0, const GemmPlan& p, const NormArgs*
     launch_reduce<MODE>(a, fuse, s);
     return;
   }
+  a.epi_reg = BN == 128 && reg_epi_ok(a) ? 1 : 0;
   if constexpr (MODE == EPI_STORE || MODE == EPI_QKV || MODE == EPI_GEGLU || MODE == EPI_EULER) {
     if (a.rms_in) {
       hipLaunchKernelGGL((gemm_stage_kernel<BN, BM, 2, MODE, 64, 1, 1>), grid, dim3(256), 0, s, a);
       return;
     }
   }
-  a.epi_reg = BN == 128 && reg_epi_ok(a) ? 1 : 0;
   hipLaunchKernelGGL((gemm_stage_kernel<BN, BM, 2, MODE>), grid, dim3(256), 0, s, a);
 }
 

@@ -78,7 +78,7 @@ def lib():
         L.vla_last_error.argtypes = []; L.vla_last_error.restype = ctypes.c_char_p
         L.vla_debug_gemm.argtypes = [ci, ci, ci, vp, ci, ci, vp, ci, ci, vp, ci, vp, ci, vp]
         L.vla_debug_gemm.restype = ci
-        L.vla_debug_gemm_bf16.argtypes = [ci, ci, ci, vp, ci, vp, ci, vp, ci, ci, vp, ci, vp]
+        L.vla_debug_gemm_bf16.argtypes = [ci, ci, ci, vp, ci, vp, ci, vp, ci, ci, ci, ctypes.c_float, vp, ci, vp]
         L.vla_debug_gemm_bf16.restype = ci
         L.vla_gemm_noalloc.argtypes = [ci, ci, ci, vp, ci, ci, vp, ci, ci, vp, ci, vp, ci, vp]
         L.vla_gemm_noalloc.restype = ci
@@ -321,9 +321,10 @@ def debug_gemm(A, Wt, bias=None, act=0, out=None, M=None, N=None, K=None, stream
     return _gemm_call(lib().vla_debug_gemm, A, Wt, bias, act, out, M, N, K, stream)
 
 
-def debug_gemm_bf16(A, Wt, bias=None, glu=False, act=0, out=None, stream=None):
-    """Projection with bf16 output: act(A Wt^T + bias) [M][N], or with glu the
+def debug_gemm_bf16(A, Wt, bias=None, glu=False, act=0, rms=False, eps=1e-6, out=None, stream=None):
+    """Projection with bf16 output: act(D + bias) [M][N], or with glu the
     gated-GELU form gelu(D[:, 2f] + b[2f]) * (D[:, 2f+1] + b[2f+1]) [M][N/2];
+    D = A Wt^T, with rms the rows of A RMS-normalised inside the product;
     bf16 A [M][K], Wt [N][K]; out may be a 2-D bf16 view with contiguous rows."""
     import torch
     M, K = A.shape
@@ -331,7 +332,7 @@ def debug_gemm_bf16(A, Wt, bias=None, glu=False, act=0, out=None, stream=None):
     if out is None:
         out = torch.empty(M, N // 2 if glu else N, dtype=torch.bfloat16, device=A.device)
     _check(lib().vla_debug_gemm_bf16(M, N, K, _ptr(A), A.stride(0), _ptr(Wt), Wt.stride(0), _ptr(bias), int(bool(glu)),
-                                     act, _ptr_rows(out), out.stride(0), _stream(stream)))
+                                     act, int(bool(rms)), eps, _ptr_rows(out), out.stride(0), _stream(stream)))
     return out
 
 

@@ -79,13 +79,16 @@ def test_bf16_gemm_hook_rejects_bad_shapes_without_gpu():
     p = ctypes.cast(buf, ctypes.c_void_p)
     # GeGLU with odd N (gate/up rows come in pairs), an activation on top of
     # the GeGLU, and an output row shorter than N / 2
-    assert L.vla_debug_gemm_bf16(4, 7, 8, p, 8, p, 8, None, 1, 0, p, 8, None) == vla.VLA_EINVAL
+    assert L.vla_debug_gemm_bf16(4, 7, 8, p, 8, p, 8, None, 1, 0, 0, 0.0, p, 8, None) == vla.VLA_EINVAL
     assert "even" in L.vla_last_error().decode()
-    assert L.vla_debug_gemm_bf16(4, 8, 8, p, 8, p, 8, None, 1, 2, p, 8, None) == vla.VLA_EINVAL
+    assert L.vla_debug_gemm_bf16(4, 8, 8, p, 8, p, 8, None, 1, 2, 0, 0.0, p, 8, None) == vla.VLA_EINVAL
     assert "act" in L.vla_last_error().decode()
-    assert L.vla_debug_gemm_bf16(4, 32, 8, p, 8, p, 8, None, 1, 0, p, 8, None) == vla.VLA_EINVAL
+    assert L.vla_debug_gemm_bf16(4, 32, 8, p, 8, p, 8, None, 1, 0, 0, 0.0, p, 8, None) == vla.VLA_EINVAL
     assert "leading dimensions" in L.vla_last_error().decode()
-    assert L.vla_debug_gemm_bf16(4, 32, 8, p, 8, p, 8, None, 0, 0, p, 16, None) == vla.VLA_EINVAL
+    assert L.vla_debug_gemm_bf16(4, 32, 8, p, 8, p, 8, None, 0, 0, 0, 0.0, p, 16, None) == vla.VLA_EINVAL
+    # folded norm without a positive eps
+    assert L.vla_debug_gemm_bf16(4, 32, 8, p, 8, p, 8, None, 0, 0, 1, 0.0, p, 32, None) == vla.VLA_EINVAL
+    assert "rms" in L.vla_last_error().decode()
 
 
 @pytest.mark.parametrize("args,msg", [

@@ -102,25 +102,50 @@ def test_gemm_bf16_out(M, N, K, glu, act):
     every element of the default output bit-equal to a run whose output rows
     are only 4-byte aligned (the per-element epilogue), and nothing written
     outside the output view."""
+    _check_bf16_out(M, N, K, glu, act, rms=False)
+
+
+@pytest.mark.parametrize("M,N,K,glu", [
+    # folded RMSNorm: staged 128 x 64 tiles from registers (the action
+    # stage's gate/up at batch 16), ragged N; 64 x 64 tiles with two wave
+    # groups and the small-M kernel through LDS
+    (800, 3840, 720, 1), (1500, 1616, 640, 1), (1500, 1616, 640, 0), (400, 3840, 720, 1), (50, 3840, 720, 1),
+])
+def test_gemm_bf16_out_rms(M, N, K, glu):
+    """The same with the RMSNorm of the input rows folded into the product
+    (rows of different scales and one all-zero row)."""
+    _check_bf16_out(M, N, K, glu, 0, rms=True)
+
+
+def _check_bf16_out(M, N, K, glu, act, rms):
     import torch
     from paper_2609_12075_amd import vla
-    log(f"[gemm bf16 out] M={M} N={N} K={K} glu={glu} act={act}")
-    A = _bf16(RNG.standard_normal((M, K)))
+    log(f"[gemm bf16 out] M={M} N={N} K={K} glu={glu} act={act} rms={rms}")
+    A = RNG.standard_normal((M, K))
+    if rms:
+        A = A * np.exp(RNG.uniform(-2, 2, (M, 1)))
+        A[M // 2] = 0.0
+    A = _bf16(A)
     W = _bf16(RNG.standard_normal((N, K)) * 0.05)
     bias = (RNG.standard_normal(N) * 0.3).astype(np.float32)
     At = torch.from_numpy(A).to(torch.bfloat16).cuda()
     Wt = torch.from_numpy(W).to(torch.bfloat16).cuda()
     bt = torch.from_numpy(bias).cuda()
     No = N // 2 if glu else N
-    out = vla.debug_gemm_bf16(At, Wt, bt, glu=glu, act=act)
+    eps = 1e-6
+    out = vla.debug_gemm_bf16(At, Wt, bt, glu=glu, act=act, rms=rms, eps=eps)
     wide = torch.full((M, No + 8), float("nan"), dtype=torch.bfloat16, device="cuda")
-    vla.debug_gemm_bf16(At, Wt, bt, glu=glu, act=act, out=wide[:, 2:2 + No])
+    vla.debug_gemm_bf16(At, Wt, bt, glu=glu, act=act, rms=rms, eps=eps, out=wide[:, 2:2 + No])
     torch.cuda.synchronize()
     got = out.float().cpu().numpy()
     assert torch.equal(out.view(torch.int16), wide[:, 2:2 + No].view(torch.int16))
     assert torch.isnan(wide[:, :2].float()).all() and torch.isnan(wide[:, 2 + No:].float()).all()
     rows = np.unique(np.concatenate([np.arange(min(M, 24)), RNG.integers(0, M, 40), np.arange(max(0, M - 24), M)]))
-    D = A[rows].astype(np.float64) @ W.astype(np.float64).T + bias
+    A64 = A[rows].astype(np.float64)
+    D = A64 @ W.astype(np.float64).T
+    if rms:
+        D = D / np.sqrt((A64 * A64).mean(axis=1, keepdims=True) + eps)
+    D = D + bias
     if glu:
         ref = O.gelu_tanh(D[:, 0::2]) * D[:, 1::2]
     else:
