@@ -392,17 +392,23 @@ __device__ __forceinline__ unsigned pack_bf16x2(float lo, float hi) {
 // and the lane stores 32 bytes (columns nb + 16 lq ..). reg_epi_ok states
 // what the caller must hold (N % 16 == 0, so a group of 16 columns is wholly
 // inside or outside; aligned rows; no row table, row groups or copy).
-template <int MODE, int TM>
-__device__ __forceinline__ void reg_epilogue(const GemmArgs& a, const f32x4 (&acc)[4][TM], int nb, int mb, int lane) {
-  static_assert(MODE == EPI_GEGLU || MODE == EPI_STORE, "GeGLU or plain store");
-  typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
-  const int lr = lane & 15, lq = lane >> 4;
-  f32x4 bias[4];
+// The bias of the lane's four columns of each fragment (loaded ahead of the
+// K loop where registers allow, so its latency is not paid at the end).
+__device__ __forceinline__ void reg_bias(const GemmArgs& a, int nb, int lane, f32x4 (&bias)[4]) {
+  const int lq = lane >> 4;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int n0 = nb + 16 * i + 4 * lq;
     bias[i] = (a.bias && n0 < a.N) ? *reinterpret_cast<const f32x4*>(a.bias + n0) : f32x4{0.f, 0.f, 0.f, 0.f};
   }
+}
+
+template <int MODE, int TM>
+__device__ __forceinline__ void reg_epilogue(const GemmArgs& a, const f32x4 (&acc)[4][TM], const f32x4 (&bias)[4], int nb,
+                                             int mb, int lane) {
+  static_assert(MODE == EPI_GEGLU || MODE == EPI_STORE, "GeGLU or plain store");
+  typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+  const int lr = lane & 15, lq = lane >> 4;
   const bool col_ok = nb + 16 * lq < a.N;
   bf16* out = reinterpret_cast<bf16*>(a.out) + (MODE == EPI_GEGLU ? (nb >> 1) + 8 * lq : nb + 16 * lq);
 #pragma unroll
@@ -886,6 +892,11 @@ gemm_stage_kernel(GemmArgs a) {
   for (int j = 0; j < TM; ++j) sq[j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   const int lr = lane & 15, lq = lane >> 4;
+  constexpr bool REG_EPI = KG == 1 && TN == 4 && (MODE == EPI_GEGLU || MODE == EPI_STORE);
+  f32x4 rbias[4];
+  if constexpr (REG_EPI) {
+    if (a.epi_reg) reg_bias(a, n_blk + wn0, lane, rbias);
+  }
 #pragma unroll
   for (int s = 0; s < STAGES - 1; ++s)
     if (s < nk) issue(s, s);
@@ -955,7 +966,7 @@ gemm_stage_kernel(GemmArgs a) {
         rsq[kg * BM + wm0 + 16 * j + c] = v == 0 ? sq[j][0] : v == 1 ? sq[j][1] : v == 2 ? sq[j][2] : sq[j][3];
     }
   }
-  if constexpr (KG == 1 && TN == 4 && (MODE == EPI_GEGLU || MODE == EPI_STORE)) {
+  if constexpr (REG_EPI) {
     // GeGLU or a plain bf16 store from the accumulators (the launcher sets
     // epi_reg when reg_epi_ok holds and K is not split); RMS: the row scales
     // meet in LDS as below and each lane scales its rows' fragments
@@ -971,7 +982,7 @@ gemm_stage_kernel(GemmArgs a) {
           for (int i = 0; i < TN; ++i) acc[i][j] = row_scale(acc[i][j], sc);
         }
       }
-      reg_epilogue<MODE, TM>(a, acc, n_blk + wn0, m_blk + wm0, lane);
+      reg_epilogue<MODE, TM>(a, acc, rbias, n_blk + wn0, m_blk + wm0, lane);
       return;
     }
   }
@@ -1133,7 +1144,9 @@ __global__ void __launch_bounds__(NW * 64) gemm_big_kernel(GemmArgs a) {
     }
   }
   if constexpr (REG) {
-    reg_epilogue<MODE, TM>(a, acc, n_blk + wn0, m_blk + wm0, lane);
+    f32x4 bias[4];
+    reg_bias(a, n_blk + wn0, lane, bias);
+    reg_epilogue<MODE, TM>(a, acc, bias, n_blk + wn0, m_blk + wm0, lane);
     return;
   }
   // epilogue in two halves of BM / 2 activation rows (waves with wm0 == WTM h)
