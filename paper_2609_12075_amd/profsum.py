@@ -4,6 +4,7 @@
     python -m paper_2609_12075_amd.profsum trace <kernel_trace.csv> --kernel REGEX [--last N]
     python -m paper_2609_12075_amd.profsum traffic --fetch <pmc.csv> --write <pmc.csv> \
         --kernel REGEX --copy-bytes N [--out traffic.json]
+    python -m paper_2609_12075_amd.profsum mfma <pmc.csv>   (a MfmaUtil + MfmaFlopsBF16 pass)
 
 `traffic` scales the per-dispatch FETCH_SIZE / WRITE_SIZE counters (KiB) of
 the named kernel by what the same counters read for the 256 MiB device copy
@@ -89,6 +90,29 @@ def traffic(fetch_csv: str, write_csv: str, kernel: str, copy_bytes: int) -> dic
             "dispatches": len(f_k)}
 
 
+def mfma(path: str) -> str:
+    """Per kernel of a `--pmc MfmaUtil MfmaFlopsBF16` pass: dispatches, median
+    dispatch duration (counter collection serialises dispatches), counted
+    matrix flops per dispatch / that duration, and the mean MfmaUtil."""
+    disp = collections.defaultdict(dict)
+    for r in csv.DictReader(open(path)):
+        d = disp[r["Dispatch_Id"]]
+        d["name"] = r["Kernel_Name"]
+        d["ns"] = int(r["End_Timestamp"]) - int(r["Start_Timestamp"])
+        d[r["Counter_Name"]] = float(r["Counter_Value"])
+    g = collections.defaultdict(list)
+    for d in disp.values():
+        if "MfmaFlopsBF16" in d and "MfmaUtil" in d:
+            g[d["name"]].append(d)
+    out = [f"{'dispatches':>10} {'median us':>10} {'TFLOP/s':>8} {'MfmaUtil %':>10}  kernel"]
+    for name, ds in sorted(g.items(), key=lambda kv: -sum(x["ns"] for x in kv[1])):
+        med = statistics.median(x["ns"] for x in ds)
+        fl = statistics.median(x["MfmaFlopsBF16"] for x in ds)
+        util = sum(x["MfmaUtil"] for x in ds) / len(ds)
+        out.append(f"{len(ds):10d} {med / 1e3:10.1f} {fl / med / 1e3:8.0f} {util:10.1f}  {name[:110]}")
+    return "\n".join(out)
+
+
 def main(argv=None):
     ap = argparse.ArgumentParser()
     sub = ap.add_subparsers(dest="cmd", required=True)
@@ -99,11 +123,14 @@ def main(argv=None):
     f.add_argument("--fetch", required=True); f.add_argument("--write", required=True)
     f.add_argument("--kernel", required=True); f.add_argument("--copy-bytes", type=int, required=True)
     f.add_argument("--out")
+    mf = sub.add_parser("mfma"); mf.add_argument("csv")
     a = ap.parse_args(argv)
     if a.cmd == "stats":
         print(stats(a.csv, a.top))
     elif a.cmd == "trace":
         print(trace(a.csv, a.kernel, a.last))
+    elif a.cmd == "mfma":
+        print(mfma(a.csv))
     else:
         res = traffic(a.fetch, a.write, a.kernel, a.copy_bytes)
         js = json.dumps(res, indent=1)
