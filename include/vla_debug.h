@@ -97,11 +97,12 @@ vla_status vla_debug_gemm_rms(int M, int N, int K, const void* A, const void* Wt
  * Residual projection that also writes a bf16 copy of the updated rows (the
  * input of a projection with a folded RMSNorm):
  *   x[m][n] += gate[n] * (sum_k A[m][k] Wt[n][k] + bias[n]);  xb[m][n] = bf16(x[m][n])
- * A bf16 [M][K], Wt bf16 [N][K], bias/gate fp32 [N] or NULL, x fp32 [M][N],
- * xb bf16 [M][N]. K % 8 == 0.
+ * A bf16 [M][K], Wt bf16 [N][K], bias/gate fp32 [N] or NULL, x fp32 [M][ldx]
+ * (ldx >= N), xb bf16 [M][ldxb] (ldxb >= N). K % 8 == 0. Rows or strides
+ * that are not 16-byte aligned take the per-element epilogue (same results).
  */
 vla_status vla_debug_resid_copy(int M, int N, int K, const void* A, const void* Wt, const float* bias,
-                                const float* gate, float* x, void* xb, hipStream_t stream);
+                                const float* gate, float* x, int ldx, void* xb, int ldxb, hipStream_t stream);
 
 /*
  * o = softmax(q k^T / sqrt(hd)) v over the keys [k0 ; k1] (segment 1 may be

@@ -511,14 +511,15 @@ vla_status vla_debug_gemm_rms(int M, int N, int K, const void* A, const void* Wt
 }
 
 vla_status vla_debug_resid_copy(int M, int N, int K, const void* A, const void* Wt, const float* bias,
-                                const float* gate, float* x, void* xb, hipStream_t s) {
+                                const float* gate, float* x, int ldx, void* xb, int ldxb, hipStream_t s) {
   return guarded([&] {
     VLA_REQUIRE(M >= 0 && N >= 0 && K >= 8 && A && Wt && x && xb, "bad resid_copy arguments");
     VLA_REQUIRE(K % 8 == 0, "resid_copy needs K % 8 == 0");
+    VLA_REQUIRE(ldx >= N && ldxb >= N, "leading dimensions too small");
     GemmArgs a{};
     a.M = M; a.N = N; a.K = K; a.A = A; a.lda = K; a.a_type = ET_BF16; a.W = Wt; a.ldw = K; a.w_type = ET_BF16;
-    a.mode = EPI_RESID; a.bias = bias; a.gate = gate; a.tab_period = 1; a.out = x; a.ldo = N; a.out_type = ET_F32;
-    a.out2 = xb; a.ldo2 = N;
+    a.mode = EPI_RESID; a.bias = bias; a.gate = gate; a.tab_period = 1; a.out = x; a.ldo = ldx; a.out_type = ET_F32;
+    a.out2 = xb; a.ldo2 = ldxb;
     a.ws = debug_ws(0, vla_model_s::kSplitKFloats); a.ws_floats = vla_model_s::kSplitKFloats;
     a.zeros = debug_ws(2, 64);
     launch_gemm(a, s);

@@ -51,6 +51,16 @@ __device__ __forceinline__ void store_elem(void* base, long idx, int type, float
   else reinterpret_cast<float*>(base)[idx] = v;
 }
 
+// The residual update x + g * (d + b) (g = the gate, or 1) and the Euler
+// update x + dt * (d + b), each one explicit fused multiply-add after the
+// bias add, so that every epilogue path (per-element, vector, from
+// registers, the reduce fused with a row norm) rounds alike.
+__device__ __forceinline__ float upd(float x, float d, float b, float g) { return fmaf(d + b, g, x); }
+__device__ __forceinline__ f32x4 upd(f32x4 x, f32x4 d, f32x4 b, f32x4 g) {
+  return f32x4{upd(x[0], d[0], b[0], g[0]), upd(x[1], d[1], b[1], g[1]), upd(x[2], d[2], b[2], g[2]),
+               upd(x[3], d[3], b[3], g[3])};
+}
+
 // Epilogue for output row m and the four columns n0..n0+3 (n0 % 4 == 0).
 template <int MODE>
 __device__ __forceinline__ void epilogue4(const GemmArgs& a, int m, int n0, float v[4]) {
@@ -97,9 +107,7 @@ __device__ __forceinline__ void epilogue4(const GemmArgs& a, int m, int n0, floa
                                  : (long)m * a.ldo;
       float* o = reinterpret_cast<float*>(a.out) + row + n0;
       for (int j = 0; j < nv; ++j) {
-        float x = v[j] + (a.bias ? a.bias[n0 + j] : 0.0f);
-        if (a.gate) x *= a.gate[n0 + j];
-        o[j] += x;
+        o[j] = upd(o[j], v[j], a.bias ? a.bias[n0 + j] : 0.0f, a.gate ? a.gate[n0 + j] : 1.0f);
         if (a.out2) reinterpret_cast<bf16*>(a.out2)[(long)m * a.ldo2 + n0 + j] = (bf16)o[j];
       }
       break;
@@ -159,7 +167,7 @@ __device__ __forceinline__ void epilogue4(const GemmArgs& a, int m, int n0, floa
     }
     case EPI_EULER: {
       float* o = reinterpret_cast<float*>(a.out) + (long)m * a.ldo + n0;
-      for (int j = 0; j < nv; ++j) o[j] += a.dt * (v[j] + (a.bias ? a.bias[n0 + j] : 0.0f));
+      for (int j = 0; j < nv; ++j) o[j] = upd(o[j], v[j], a.bias ? a.bias[n0 + j] : 0.0f, a.dt);
       break;
     }
   }
@@ -225,8 +233,8 @@ __device__ __forceinline__ void epi_rows(const GemmArgs& a, const f32x4 (&t)[NIT
     for (int it = 0; it < NIT; ++it) {
       if (!ok[it]) continue;
       f32x4 r;
-      if constexpr (MODE == EPI_RESID) r = old[it] + (t[it] + bias) * gate;
-      else r = old[it] + a.dt * (t[it] + bias);
+      if constexpr (MODE == EPI_RESID) r = upd(old[it], t[it], bias, gate);
+      else r = upd(old[it], t[it], bias, f32x4{a.dt, a.dt, a.dt, a.dt});
       *reinterpret_cast<f32x4*>(out + off[it]) = r;
       if (MODE == EPI_RESID && a.out2)
         *reinterpret_cast<bf16x4*>(reinterpret_cast<bf16*>(a.out2) + (long)ms[it] * a.ldo2 + n0) =
@@ -442,6 +450,65 @@ __device__ __forceinline__ void reg_epilogue(const GemmArgs& a, const f32x4 (&ac
         o[0] = u32x4{lo[0], hi[0], lo[1], hi[1]};
         o[1] = u32x4{lo[2], hi[2], lo[3], hi[3]};
       }
+    }
+  }
+}
+
+// The residual update x += gate * (D + bias) of a wave tile from the
+// accumulators (no LDS pass): fragment (i, j) of lane (lr, lq) covers the
+// four fp32 columns nb + 16 i + 4 lq .. + 3 of row mb + 16 j + lr, one
+// 16-byte read and write each (a row's four lanes cover 64 contiguous
+// bytes). The old values, bias and gate are read ahead of the K loop
+// (reg_resid_load): the block alone reads and writes its tile, and the
+// launcher checks that the product's input does not overlap the output.
+__device__ __forceinline__ long resid_row(const GemmArgs& a, int m) {
+  return a.row_group > 0 ? (long)(m / a.row_group) * a.row_group_stride + (long)(m % a.row_group) * a.ldo
+                         : (long)m * a.ldo;
+}
+
+template <int TN, int TM>
+__device__ __forceinline__ void reg_resid_load(const GemmArgs& a, int nb, int mb, int lane, f32x4 (&old)[TN][TM],
+                                               f32x4 (&bias)[TN], f32x4 (&gate)[TN]) {
+  const int lr = lane & 15, lq = lane >> 4;
+  const f32x4 zero = {0.f, 0.f, 0.f, 0.f}, one = {1.f, 1.f, 1.f, 1.f};
+  const float* out = reinterpret_cast<const float*>(a.out);
+#pragma unroll
+  for (int i = 0; i < TN; ++i) {
+    const int n0 = nb + 16 * i + 4 * lq;
+    bias[i] = (a.bias && n0 < a.N) ? *reinterpret_cast<const f32x4*>(a.bias + n0) : zero;
+    gate[i] = (a.gate && n0 < a.N) ? *reinterpret_cast<const f32x4*>(a.gate + n0) : one;
+  }
+#pragma unroll
+  for (int j = 0; j < TM; ++j) {
+    const int m = mb + 16 * j + lr;
+    const long ro = m < a.M ? resid_row(a, m) : 0;
+#pragma unroll
+    for (int i = 0; i < TN; ++i) {
+      const int n0 = nb + 16 * i + 4 * lq;
+      old[i][j] = (m < a.M && n0 < a.N) ? *reinterpret_cast<const f32x4*>(out + ro + n0) : zero;
+    }
+  }
+}
+
+template <int TN, int TM>
+__device__ __forceinline__ void reg_resid(const GemmArgs& a, const f32x4 (&acc)[TN][TM], const f32x4 (&old)[TN][TM],
+                                          const f32x4 (&bias)[TN], const f32x4 (&gate)[TN], int nb, int mb, int lane) {
+  const int lr = lane & 15, lq = lane >> 4;
+  float* out = reinterpret_cast<float*>(a.out);
+#pragma unroll
+  for (int j = 0; j < TM; ++j) {
+    const int m = mb + 16 * j + lr;
+    if (m >= a.M) continue;
+    const long ro = resid_row(a, m);
+#pragma unroll
+    for (int i = 0; i < TN; ++i) {
+      const int n0 = nb + 16 * i + 4 * lq;
+      if (n0 >= a.N) continue;
+      const f32x4 r = upd(old[i][j], acc[i][j], bias[i], gate[i]);
+      *reinterpret_cast<f32x4*>(out + ro + n0) = r;
+      if (a.out2)
+        *reinterpret_cast<bf16x4*>(reinterpret_cast<bf16*>(a.out2) + (long)m * a.ldo2 + n0) =
+            bf16x4{(bf16)r[0], (bf16)r[1], (bf16)r[2], (bf16)r[3]};
     }
   }
 }
@@ -665,8 +732,8 @@ __global__ void __launch_bounds__(256) splitk_reduce_norm_kernel(GemmArgs a, Nor
       v[j] = rownorm::f4{0.f, 0.f, 0.f, 0.f};
       continue;
     }
-    // as the residual epilogue: x += (sum + bias) * gate (gate 1 when absent)
-    v[j] += (t[j] + bs[j]) * gt[j];
+    // as the residual epilogue: x + gate * (sum + bias) (gate 1 when absent)
+    v[j] = upd(v[j], t[j], bs[j], gt[j]);
     *reinterpret_cast<f32x4*>(x + i) = v[j];
   }
   rownorm::store_row<NV>(n, r, v, lane, g, b);
@@ -897,6 +964,18 @@ gemm_stage_kernel(GemmArgs a) {
   if constexpr (REG_EPI) {
     if (a.epi_reg) reg_bias(a, n_blk + wn0, lane, rbias);
   }
+  // residual update from registers with two wave groups (group 1 hands its
+  // tile to group 0 through LDS, group 0 updates the rows: half the LDS
+  // traffic of summing two staged planes; 2-4 % on the action stage's O and
+  // down projections. With one group the LDS-staged update, whose rows are
+  // written whole, measured as fast or faster): old values, bias and gate
+  // read before the first stage's loads
+  constexpr bool REG_RES = MODE == EPI_RESID && !RMS && KG == 2;
+  constexpr int RTN = REG_RES ? TN : 1, RTM = REG_RES ? TM : 1;
+  f32x4 rold[RTN][RTM], rrb[RTN], rrg[RTN];
+  if constexpr (REG_RES) {
+    if (a.epi_reg && kg == 0) reg_resid_load<TN, TM>(a, n_blk + wn0, m_blk + wm0, lane, rold, rrb, rrg);
+  }
 #pragma unroll
   for (int s = 0; s < STAGES - 1; ++s)
     if (s < nk) issue(s, s);
@@ -964,6 +1043,32 @@ gemm_stage_kernel(GemmArgs a) {
 #pragma unroll
       for (int j = 0; j < TM; ++j)
         rsq[kg * BM + wm0 + 16 * j + c] = v == 0 ? sq[j][0] : v == 1 ? sq[j][1] : v == 2 ? sq[j][2] : sq[j][3];
+    }
+  }
+  if constexpr (REG_RES) {
+    if (a.epi_reg) {
+      {
+        // group 1 hands its tile to group 0 through LDS (the stage buffers
+        // are free once every wave has passed the barrier); the sum is in
+        // group order, as in the LDS-staged epilogue
+        __syncthreads();
+        if (kg == 1) {
+#pragma unroll
+          for (int i = 0; i < TN; ++i)
+#pragma unroll
+            for (int j = 0; j < TM; ++j)
+              *reinterpret_cast<f32x4*>(&Cs[(wm0 + 16 * j + lr) * LDC + wn0 + 16 * i + 4 * lq]) = acc[i][j];
+        }
+        __syncthreads();
+        if (kg == 1) return;
+#pragma unroll
+        for (int i = 0; i < TN; ++i)
+#pragma unroll
+          for (int j = 0; j < TM; ++j)
+            acc[i][j] += *reinterpret_cast<const f32x4*>(&Cs[(wm0 + 16 * j + lr) * LDC + wn0 + 16 * i + 4 * lq]);
+      }
+      reg_resid<TN, TM>(a, acc, rold, rrb, rrg, n_blk + wn0, m_blk + wm0, lane);
+      return;
     }
   }
   if constexpr (REG_EPI) {
@@ -1385,6 +1490,22 @@ static bool reg_epi_ok(const GemmArgs& a) {
   return a.mode == EPI_STORE && !a.tab && a.row_group <= 0 && !a.out2;
 }
 
+// The residual update from registers (reg_resid, the two-group staged tiles)
+// needs the vector epilogue's alignment (epi_vec), fp32 output, and a product
+// input that does not overlap the output rows (their old values are read
+// before the K loop).
+static bool reg_res_ok(const GemmArgs& a) {
+  if (a.mode != EPI_RESID || !a.epi_vec || a.out_type != ET_F32 || a.rms_in || a.M <= 0) return false;
+  const size_t esz = a.a_type == ET_BF16 ? 2 : 4;
+  const char* ab = reinterpret_cast<const char*>(a.A);
+  const char* ae = ab + ((size_t)(a.M - 1) * a.lda + a.K) * esz;
+  const long last = a.row_group > 0 ? (long)((a.M - 1) / a.row_group) * a.row_group_stride + (long)(a.row_group - 1) * a.ldo
+                                     : (long)(a.M - 1) * a.ldo;
+  const char* ob = reinterpret_cast<const char*>(a.out);
+  const char* oe = ob + ((size_t)last + a.N) * 4;
+  return ae <= ob || oe <= ab;
+}
+
 // Second pass of a split product: the ordered reduce with the epilogue, or
 // for a residual projection with a following row norm, the fused reduce.
 template <int MODE>
@@ -1429,6 +1550,7 @@ static void launch_staged(const GemmArgs& a0, const GemmPlan& p, const NormArgs*
 template <int BT, int ST, int MODE>
 static void launch_staged128(const GemmArgs& a0, const GemmPlan& p, const NormArgs* fuse, hipStream_t s) {
   GemmArgs a = a0;
+  a.epi_reg = 0;
   a.ksplit = p.ksplit;
   a.splits = p.splits;
   dim3 grid((a.M + BT - 1) / BT, (a.N + BT - 1) / BT, a.splits);
@@ -1437,6 +1559,7 @@ static void launch_staged128(const GemmArgs& a0, const GemmPlan& p, const NormAr
     launch_reduce<MODE>(a, fuse, s);
     return;
   }
+  a.epi_reg = reg_res_ok(a) ? 1 : 0;
   if constexpr (MODE == EPI_STORE || MODE == EPI_QKV || MODE == EPI_GEGLU || MODE == EPI_EULER) {
     if (a.rms_in) {
       hipLaunchKernelGGL((gemm_stage_kernel<BT, BT, ST, MODE, 128, 2, 1>), grid, dim3(512), 0, s, a);

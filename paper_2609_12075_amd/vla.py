@@ -86,7 +86,7 @@ def lib():
         L.vla_debug_resid_norm.restype = ci
         L.vla_debug_gemm_rms.argtypes = [ci, ci, ci, vp, vp, vp, ctypes.c_float, vp, vp]
         L.vla_debug_gemm_rms.restype = ci
-        L.vla_debug_resid_copy.argtypes = [ci, ci, ci, vp, vp, vp, vp, vp, vp, vp]
+        L.vla_debug_resid_copy.argtypes = [ci, ci, ci, vp, vp, vp, vp, vp, ci, vp, ci, vp]
         L.vla_debug_resid_copy.restype = ci
         L.vla_debug_attention.argtypes = [ci, ci, ci, ci, ci, ci, vp, vp, vp, ci, vp, vp, ci, vp, vp]
         L.vla_debug_attention.restype = ci
@@ -364,14 +364,16 @@ def debug_gemm_rms(A, Wt, bias=None, eps=1e-6, stream=None):
     return out
 
 
-def debug_resid_copy(A, Wt, x, bias=None, gate=None, stream=None):
-    """x += gate * (A Wt^T + bias) in place; returns bf16(x)."""
+def debug_resid_copy(A, Wt, x, bias=None, gate=None, xb=None, stream=None):
+    """x += gate * (A Wt^T + bias) in place; returns bf16(x) (in xb when
+    given). x and xb may be 2-D views with contiguous rows."""
     import torch
     M, K = A.shape
     N = Wt.shape[0]
-    xb = torch.empty(M, N, dtype=torch.bfloat16, device=A.device)
-    _check(lib().vla_debug_resid_copy(M, N, K, _ptr(A), _ptr(Wt), _ptr(bias), _ptr(gate), _ptr(x), _ptr(xb),
-                                      _stream(stream)))
+    if xb is None:
+        xb = torch.empty(M, N, dtype=torch.bfloat16, device=A.device)
+    _check(lib().vla_debug_resid_copy(M, N, K, _ptr(A), _ptr(Wt), _ptr(bias), _ptr(gate), _ptr_rows(x), x.stride(0),
+                                      _ptr_rows(xb), xb.stride(0), _stream(stream)))
     return xb
 
 

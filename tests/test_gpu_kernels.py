@@ -235,11 +235,20 @@ def test_gemm_rms(M, N, K):
     np.testing.assert_allclose(out.cpu().numpy(), ref, rtol=1e-4, atol=1e-5 * scale)
 
 
-@pytest.mark.parametrize("M,N,K", [(50, 720, 1920), (800, 720, 1920), (800, 720, 960), (37, 33, 40), (130, 202, 64)])
+@pytest.mark.parametrize("M,N,K", [
+    # register-pipelined kernel; 64 x 64 tiles with two wave groups (the
+    # residual update from registers); ragged, per-element epilogue
+    (50, 720, 1920), (800, 720, 1920), (800, 720, 960), (37, 33, 40), (130, 202, 64),
+    # staged 128 x 64 and 128 x 128 tiles (LDS-staged update), ragged
+    (3840, 960, 960), (2000, 1156, 1000), (4000, 1156, 640),
+    # 128 x 128 tiles with two wave groups and K-steps of 128 (update from registers)
+    (777, 3000, 1000),
+])
 def test_resid_copy(M, N, K):
     """Residual projection with the bf16 copy of the updated rows: x against
-    fp64, the copy bit-identical to x rounded to bf16 (split and unsplit
-    plans, vector and per-element epilogues)."""
+    fp64, the copy bit-identical to x rounded to bf16; x and the copy
+    bit-identical to a run on rows that are not 16-byte aligned (the
+    per-element epilogue), nothing written outside the rows."""
     import torch
     from paper_2609_12075_amd import vla
     log(f"[resid copy] M={M} N={N} K={K}")
@@ -249,12 +258,23 @@ def test_resid_copy(M, N, K):
     bias = RNG.standard_normal(N).astype(np.float32) * 0.1
     gate = (1 + 0.1 * RNG.standard_normal(N)).astype(np.float32)
     x_ref = x0.astype(np.float64) + (A.astype(np.float64) @ W.astype(np.float64).T + bias) * gate
+    At = torch.from_numpy(A).to(torch.bfloat16).cuda()
+    Wt = torch.from_numpy(W).to(torch.bfloat16).cuda()
+    bt, gt = torch.from_numpy(bias).cuda(), torch.from_numpy(gate).cuda()
     x = torch.from_numpy(x0).cuda()
-    xb = vla.debug_resid_copy(torch.from_numpy(A).to(torch.bfloat16).cuda(), torch.from_numpy(W).to(torch.bfloat16).cuda(),
-                              x, bias=torch.from_numpy(bias).cuda(), gate=torch.from_numpy(gate).cuda())
+    xb = vla.debug_resid_copy(At, Wt, x, bias=bt, gate=gt)
+    # the same update on rows 4-byte aligned only (x and its copy)
+    xw = torch.full((M, N + 5), float("nan"), dtype=torch.float32, device="cuda")
+    xw[:, 1:1 + N] = torch.from_numpy(x0).cuda()
+    xbw = torch.full((M, N + 3), float("nan"), dtype=torch.bfloat16, device="cuda")
+    vla.debug_resid_copy(At, Wt, xw[:, 1:1 + N], bias=bt, gate=gt, xb=xbw[:, 1:1 + N])
     torch.cuda.synchronize()
     np.testing.assert_allclose(x.cpu().numpy(), x_ref, rtol=1e-4, atol=1e-4)
     assert torch.equal(xb.cpu(), x.cpu().to(torch.bfloat16))
+    assert torch.equal(x.view(torch.int32), xw[:, 1:1 + N].contiguous().view(torch.int32))
+    assert torch.equal(xb.view(torch.int16), xbw[:, 1:1 + N].contiguous().view(torch.int16))
+    assert torch.isnan(xw[:, 0]).all() and torch.isnan(xw[:, 1 + N:]).all()
+    assert torch.isnan(xbw[:, 0].float()).all() and torch.isnan(xbw[:, 1 + N:].float()).all()
 
 
 ATTN_SHAPES = [
