@@ -1318,6 +1318,16 @@ __global__ void __launch_bounds__(256) gemm_f32_kernel(GemmArgs a) {
   for (int r = 0; r < 4; ++r) epilogue4<MODE>(a, m_blk + tm + r, n_blk + tn, acc[r]);
 }
 
+// The epilogue from registers (reg_epilogue) needs bf16 output, whole
+// 16-column groups, 16-byte aligned output rows and bias, and for a plain
+// store no row table, row groups or fp32/bf16 copy.
+static bool reg_epi_ok(const GemmArgs& a) {
+  auto al = [](const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; };
+  if (a.out_type != ET_BF16 || a.N % 16 != 0 || a.ldo % 8 != 0 || !al(a.out) || (a.bias && !al(a.bias))) return false;
+  if (a.mode == EPI_GEGLU) return true;
+  return a.mode == EPI_STORE && !a.tab && a.row_group <= 0 && !a.out2;
+}
+
 // ---------------------------------------------------------------- dispatch
 // Kernels are specialised on tile shape, activation type and epilogue; fp32
 // activations (the Euler state, conditioning vectors, robot state) only feed
@@ -1370,9 +1380,17 @@ static GemmPlan plan_base(const GemmArgs& a) {
     // such tiles in one round, 435 us against 450 us for 208 taller ones. The
     // accumulation order of every output, and so the result, is the same
     // for both heights.
+    // Below K = 2048 the large tiles' fixed costs weigh more: they are taken
+    // there only for an output stored from registers (reg_epi_ok) and a
+    // margin of 10 % (measured: the SmolVLA-shaped vision encoder's MLP up,
+    // 49152 x 3072 x 768, 270 -> 240 us; the pi0-shaped ViT MLP up at 6144
+    // rows, 73 -> 70 us; half-filled last rounds stay on the staged tiles)
     const long t256 = blocks(256, 256), t224 = blocks(256, 224), t128 = blocks(128, 128);
     const double c256 = (t256 + 255) / 256 * 2.1, c224 = (t224 + 255) / 256 * 2.1 * 0.95;
-    if (a.M >= 256 && a.K >= 2048 && t256 >= 160 && std::min(c256, c224) <= (t128 + 511) / 512 * 1.2) {
+    const double c_big = std::min(c256, c224), c_staged = (t128 + 511) / 512 * 1.2;
+    const bool long_k = a.K >= 2048 && c_big <= c_staged;
+    const bool short_k = a.K >= 512 && a.K < 2048 && reg_epi_ok(a) && c_big <= 0.9 * c_staged;
+    if (a.M >= 256 && t256 >= 160 && (long_k || short_k)) {
       p.bn = 256; p.bm = c224 < c256 - 1e-9 ? 224 : 256; p.kind = 3;
       p.ksplit = nk * BK;
       return p;
@@ -1480,15 +1498,6 @@ GemmPlan gemm_plan(const GemmArgs& a) {
   return GemmPlan{big ? 128 : 64, big ? 128 : 64, 1, (a.K + 63) / 64 * 64, 1};
 }
 
-// The epilogue from registers (reg_epilogue) needs bf16 output, whole
-// 16-column groups, 16-byte aligned output rows and bias, and for a plain
-// store no row table, row groups or fp32/bf16 copy.
-static bool reg_epi_ok(const GemmArgs& a) {
-  auto al = [](const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; };
-  if (a.out_type != ET_BF16 || a.N % 16 != 0 || a.ldo % 8 != 0 || !al(a.out) || (a.bias && !al(a.bias))) return false;
-  if (a.mode == EPI_GEGLU) return true;
-  return a.mode == EPI_STORE && !a.tab && a.row_group <= 0 && !a.out2;
-}
 
 // The residual update from registers (reg_resid, the two-group staged tiles)
 // needs the vector epilogue's alignment (epi_vec), fp32 output, and a product

@@ -90,6 +90,8 @@ def test_gemm_activations(act, amp):
     (2600, 4112, 2056), (3584, 4608, 2048),
     # large-tile kernel through LDS (N % 16 != 0)
     (3584, 4600, 2048),
+    # large tiles below K = 2048 (full rounds of tiles, output from registers)
+    (16384, 3072, 768),
     # staged 128 x 128 and 128 x 64 tiles from registers, ragged N; through LDS
     (4000, 1616, 640), (1500, 1616, 640), (4000, 1608, 640),
     # small-M kernel (LDS epilogue)
