@@ -393,13 +393,6 @@ __device__ __forceinline__ unsigned pack_bf16x2(float lo, float hi) {
   return *reinterpret_cast<const unsigned*>(&h);
 }
 
-// The GeGLU or plain bf16-store epilogue of such a wave tile, without the LDS
-// round trip: GeGLU (a fragment holds two whole gate/up pairs) leaves one
-// word per fragment and the lane stores 16 bytes (output columns nb / 2 +
-// 8 lq ..); a store leaves two words per fragment (both halves transposed)
-// and the lane stores 32 bytes (columns nb + 16 lq ..). reg_epi_ok states
-// what the caller must hold (N % 16 == 0, so a group of 16 columns is wholly
-// inside or outside; aligned rows; no row table, row groups or copy).
 // The bias of the lane's four columns of each fragment (loaded ahead of the
 // K loop where registers allow, so its latency is not paid at the end).
 __device__ __forceinline__ void reg_bias(const GemmArgs& a, int nb, int lane, f32x4 (&bias)[4]) {
@@ -411,6 +404,13 @@ __device__ __forceinline__ void reg_bias(const GemmArgs& a, int nb, int lane, f3
   }
 }
 
+// The GeGLU or plain bf16-store epilogue of such a wave tile, without the LDS
+// round trip: GeGLU (a fragment holds two whole gate/up pairs) leaves one
+// word per fragment and the lane stores 16 bytes (output columns nb / 2 +
+// 8 lq ..); a store leaves two words per fragment (both halves transposed)
+// and the lane stores 32 bytes (columns nb + 16 lq ..). reg_epi_ok states
+// what the caller must hold (N % 16 == 0, so a group of 16 columns is wholly
+// inside or outside; aligned rows; no row table, row groups or copy).
 template <int MODE, int TM>
 __device__ __forceinline__ void reg_epilogue(const GemmArgs& a, const f32x4 (&acc)[4][TM], const f32x4 (&bias)[4], int nb,
                                              int mb, int lane) {
