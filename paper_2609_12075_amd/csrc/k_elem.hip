@@ -1,5 +1,5 @@
 // Row-wise and element-wise kernels of the VLA path on gfx950: RMSNorm /
-// LayerNorm / adaLN modulation (one wavefront per row, wave64 reductions),
+// LayerNorm / adaLN modulation (one to four wavefronts per row, wave64 reductions),
 // patch extraction, token embedding, the flow-time sinusoid, RoPE tables,
 // parameter conversion and a placement probe for CU-masked streams.
 #include "common.h"
@@ -10,25 +10,30 @@ namespace {
 __device__ __forceinline__ float round_bf16(float x) { return (float)(bf16)x; }
 
 // ---------------------------------------------------------------- norms
-// One wavefront per row. The row is read once into registers with 16-byte
-// loads that are all issued before the first reduction (one memory round
-// trip); statistics and output as in rownorm::store_row. Requires d % 4 == 0
-// and d <= 256 * NV.
-template <int NV>
+// A row per WPR wavefronts (rownorm::waves_per_row), each holding NVW
+// 16-byte vectors per lane. The row is read once into registers with loads
+// that are all issued before the first reduction (one memory round trip);
+// statistics and output as in rownorm::store_row. Requires d % 4 == 0 and
+// d <= 256 * NVW * WPR.
+template <int NVW, int WPR>
 __global__ void __launch_bounds__(256) norm_kernel(NormArgs a) {
-  const int lane = threadIdx.x & 63;
-  const int r = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (r >= a.rows) return;
-  const int rin = a.skip > 0 ? r + (r / a.skip_group + 1) * a.skip : r;
+  constexpr int RPB = 4 / WPR;
+  __shared__ float red[4][2];
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6, w = wv % WPR;
+  const int r = blockIdx.x * RPB + wv / WPR;
+  if (WPR == 1 && r >= a.rows) return;              // (no barrier with one wave per row)
+  const bool rok = r < a.rows;
+  const int rr = rok ? r : 0;
+  const int rin = a.skip > 0 ? rr + (rr / a.skip_group + 1) * a.skip : rr;
   const float* x = a.in + (long)rin * a.ld_in;
-  rownorm::f4 v[NV], g[NV], b[NV];
+  rownorm::f4 v[NVW], g[NVW], b[NVW];
 #pragma unroll
-  for (int j = 0; j < NV; ++j) {
-    const int i = (j * 64 + lane) * 4;
+  for (int j = 0; j < NVW; ++j) {
+    const int i = rownorm::col<NVW>(w, j, lane);
     v[j] = i < a.d ? *reinterpret_cast<const rownorm::f4*>(x + i) : rownorm::f4{0.f, 0.f, 0.f, 0.f};
   }
-  rownorm::load_params<NV>(a, lane, g, b);
-  rownorm::store_row<NV>(a, r, v, lane, g, b);
+  rownorm::load_params<NVW>(a, w, lane, g, b);
+  rownorm::store_row<NVW, WPR>(a, r, rok, v, wv, w, lane, g, b, red);
 }
 
 // ---------------------------------------------------------------- staging
@@ -217,14 +222,24 @@ __global__ void __launch_bounds__(256) batched_copy_kernel(const CopySeg* segs) 
   }
 }
 
+// 256-thread blocks of 4 / WPR rows
+template <int NV>
+static void launch_norm_nv(const NormArgs& a, hipStream_t s) {
+  constexpr int W = NV >= 4 ? 4 : NV;
+  if (rownorm::waves_per_row(NV, a.rows) == 1) {
+    hipLaunchKernelGGL((norm_kernel<NV, 1>), dim3((a.rows + 3) / 4), dim3(256), 0, s, a);
+  } else {
+    hipLaunchKernelGGL((norm_kernel<NV / W, W>), dim3((a.rows + 4 / W - 1) / (4 / W)), dim3(256), 0, s, a);
+  }
+}
+
 void launch_norm(const NormArgs& a, hipStream_t s) {
   if (a.rows <= 0) return;
   if (a.d % 4 || a.ld_in % 4 || a.ld_out % 4 || a.d > 2048) throw VlaError{4, "norm: d, ld must be multiples of 4, d <= 2048"};
-  dim3 grid((a.rows + 3) / 4);
-  if (a.d <= 256) hipLaunchKernelGGL(norm_kernel<1>, grid, dim3(256), 0, s, a);
-  else if (a.d <= 512) hipLaunchKernelGGL(norm_kernel<2>, grid, dim3(256), 0, s, a);
-  else if (a.d <= 1024) hipLaunchKernelGGL(norm_kernel<4>, grid, dim3(256), 0, s, a);
-  else hipLaunchKernelGGL(norm_kernel<8>, grid, dim3(256), 0, s, a);
+  if (a.d <= 256) launch_norm_nv<1>(a, s);
+  else if (a.d <= 512) launch_norm_nv<2>(a, s);
+  else if (a.d <= 1024) launch_norm_nv<4>(a, s);
+  else launch_norm_nv<8>(a, s);
 }
 
 void launch_im2col(const float* pix, int n_images, int hw, int p, void* out, int ldo, int out_type, hipStream_t s) {

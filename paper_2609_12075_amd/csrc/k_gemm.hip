@@ -678,46 +678,52 @@ __global__ void __launch_bounds__(256) splitk_reduce_kernel(GemmArgs a) {
 }
 
 // Split-K second pass of a residual projection fused with the row norm that
-// follows it: one wavefront per output row sums the partials in split order,
-// applies the residual epilogue (x += gate * (sum + bias)) exactly as the
-// plain reduce does, writes x, and normalises the new row into n.out (the
-// same arithmetic as the norm kernel). Requires N == n.d <= 256 * NV and
-// contiguous rows (no row groups).
-template <int NV>
+// follows it: the waves of an output row (rownorm::waves_per_row, as in the
+// norm kernel) sum the partials in split order, apply the residual
+// epilogue (x += gate * (sum + bias)) exactly as the plain reduce does,
+// write x, and normalise the new row into n.out (the same arithmetic as the
+// norm kernel). Four waves per row instead of one: 30 % faster at a few
+// thousand rows (1632 x 2048 with two K ranges 16.2 -> 11.1 us). Requires
+// N == n.d <= 256 * NVW * WPR and contiguous rows (no row groups).
+template <int NVW, int WPR>
 __global__ void __launch_bounds__(256) splitk_reduce_norm_kernel(GemmArgs a, NormArgs n) {
-  const int lane = threadIdx.x & 63;
-  const int r = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (r >= a.M) return;
+  constexpr int RPB = 4 / WPR;
+  __shared__ float red[4][2];
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6, w = wv % WPR;
+  const int r = blockIdx.x * RPB + wv / WPR;
+  if (WPR == 1 && r >= a.M) return;                 // (no barrier with one wave per row)
+  const bool rok = r < a.M;
+  const int rr = rok ? r : 0;
   const int ldp = (a.N + 3) & ~3;
   const long stride = (long)a.M * ldp;
-  const float* p = a.ws + (long)r * ldp;
-  float* x = reinterpret_cast<float*>(a.out) + (long)r * a.ldo;
+  const float* p = a.ws + (long)rr * ldp;
+  float* x = reinterpret_cast<float*>(a.out) + (long)rr * a.ldo;
   // every load of the row (partials in split order, old x, the residual's
   // bias and gate, the norm's parameters) before the first store, so they
   // share one memory round trip per four K ranges
-  rownorm::f4 v[NV], g[NV], b[NV];
-  f32x4 t[NV], bs[NV], gt[NV];
+  rownorm::f4 v[NVW], g[NVW], b[NVW];
+  f32x4 t[NVW], bs[NVW], gt[NVW];
   const bool has_bias = a.bias != nullptr, has_gate = a.gate != nullptr;
 #pragma unroll
-  for (int j = 0; j < NV; ++j) {
-    const int i = min((j * 64 + lane) * 4, a.N - 4);
+  for (int j = 0; j < NVW; ++j) {
+    const int i = min(rownorm::col<NVW>(w, j, lane), a.N - 4);
     v[j] = *reinterpret_cast<const f32x4*>(x + i);
     bs[j] = has_bias ? *reinterpret_cast<const f32x4*>(a.bias + i) : f32x4{0.f, 0.f, 0.f, 0.f};
     gt[j] = has_gate ? *reinterpret_cast<const f32x4*>(a.gate + i) : f32x4{1.f, 1.f, 1.f, 1.f};
   }
-  rownorm::load_params<NV>(n, lane, g, b);
+  rownorm::load_params<NVW>(n, w, lane, g, b);
   for (int z0 = 0; z0 < a.splits; z0 += 4) {
-    f32x4 part[NV][4];
+    f32x4 part[NVW][4];
 #pragma unroll
-    for (int j = 0; j < NV; ++j) {
-      const int i = min((j * 64 + lane) * 4, a.N - 4);
+    for (int j = 0; j < NVW; ++j) {
+      const int i = min(rownorm::col<NVW>(w, j, lane), a.N - 4);
 #pragma unroll
       for (int q = 0; q < 4; ++q)
         part[j][q] = z0 + q < a.splits ? *reinterpret_cast<const f32x4*>(p + (z0 + q) * stride + i)
                                        : f32x4{0.f, 0.f, 0.f, 0.f};
     }
 #pragma unroll
-    for (int j = 0; j < NV; ++j) {
+    for (int j = 0; j < NVW; ++j) {
       // partials summed in split order
       if (z0 == 0) t[j] = part[j][0];
       else t[j] += part[j][0];
@@ -726,17 +732,17 @@ __global__ void __launch_bounds__(256) splitk_reduce_norm_kernel(GemmArgs a, Nor
     }
   }
 #pragma unroll
-  for (int j = 0; j < NV; ++j) {
-    const int i = (j * 64 + lane) * 4;
+  for (int j = 0; j < NVW; ++j) {
+    const int i = rownorm::col<NVW>(w, j, lane);
     if (i >= a.N) {
       v[j] = rownorm::f4{0.f, 0.f, 0.f, 0.f};
       continue;
     }
     // as the residual epilogue: x + gate * (sum + bias) (gate 1 when absent)
     v[j] = upd(v[j], t[j], bs[j], gt[j]);
-    *reinterpret_cast<f32x4*>(x + i) = v[j];
+    if (rok) *reinterpret_cast<f32x4*>(x + i) = v[j];
   }
-  rownorm::store_row<NV>(n, r, v, lane, g, b);
+  rownorm::store_row<NVW, WPR>(n, r, rok, v, wv, w, lane, g, b, red);
 }
 
 // ---------------------------------------------------------------- small-M kernel
@@ -1515,17 +1521,29 @@ static bool reg_res_ok(const GemmArgs& a) {
   return ae <= ob || oe <= ab;
 }
 
+// The fused reduce with a row norm over rows of N <= 256 * NV columns: the
+// waves per row of the norm kernel's rule (rownorm::waves_per_row), 256-thread
+// blocks of 4 / WPR rows.
+template <int NV>
+static void launch_reduce_norm(const GemmArgs& a, const NormArgs& n, hipStream_t s) {
+  constexpr int W = NV >= 4 ? 4 : NV;
+  if (rownorm::waves_per_row(NV, a.M) == 1) {
+    hipLaunchKernelGGL((splitk_reduce_norm_kernel<NV, 1>), dim3((a.M + 3) / 4), dim3(256), 0, s, a, n);
+  } else {
+    hipLaunchKernelGGL((splitk_reduce_norm_kernel<NV / W, W>), dim3((a.M + 4 / W - 1) / (4 / W)), dim3(256), 0, s, a, n);
+  }
+}
+
 // Second pass of a split product: the ordered reduce with the epilogue, or
 // for a residual projection with a following row norm, the fused reduce.
 template <int MODE>
 static void launch_reduce(const GemmArgs& a, const NormArgs* fuse, hipStream_t s) {
   if constexpr (MODE == EPI_RESID) {
     if (fuse) {
-      const dim3 grid((a.M + 3) / 4);
-      if (a.N <= 256) hipLaunchKernelGGL(splitk_reduce_norm_kernel<1>, grid, dim3(256), 0, s, a, *fuse);
-      else if (a.N <= 512) hipLaunchKernelGGL(splitk_reduce_norm_kernel<2>, grid, dim3(256), 0, s, a, *fuse);
-      else if (a.N <= 1024) hipLaunchKernelGGL(splitk_reduce_norm_kernel<4>, grid, dim3(256), 0, s, a, *fuse);
-      else hipLaunchKernelGGL(splitk_reduce_norm_kernel<8>, grid, dim3(256), 0, s, a, *fuse);
+      if (a.N <= 256) launch_reduce_norm<1>(a, *fuse, s);
+      else if (a.N <= 512) launch_reduce_norm<2>(a, *fuse, s);
+      else if (a.N <= 1024) launch_reduce_norm<4>(a, *fuse, s);
+      else launch_reduce_norm<8>(a, *fuse, s);
       return;
     }
   }
