@@ -276,44 +276,50 @@ __global__ void __launch_bounds__(256) attn_mfma_kernel(AttnArgs a) {
   }
 }
 
-// Split-KV merge: one wavefront per query row combines the key ranges in
-// order: m = max m_s, l = sum l_s 2^(m_s - m), o = sum o_s 2^(m_s - m) / l.
-// Each lane owns four consecutive dims; all (<= 16) partial loads of a lane
-// are issued before any is used.
+// Split-KV merge: LPR lanes per query row (the fewest of 16, 32, 64 whose
+// four dims each cover the head dim, so 64 / LPR rows share a wavefront)
+// combine the key ranges in order: m = max m_s, l = sum l_s 2^(m_s - m),
+// o = sum o_s 2^(m_s - m) / l. Each lane owns four consecutive dims; its
+// range statistics and all (<= 16) partial loads are issued together before
+// any is used (one memory round trip instead of two: 7.6 -> 6.4 us for the
+// pi0-shaped action attention at batch 8, four ranges).
 constexpr int MAX_SPLITS = 16;
+template <int LPR>
 __global__ void __launch_bounds__(256) attn_combine_kernel(AttnArgs a) {
-  const int lane = threadIdx.x & 63;
-  const long row = blockIdx.x * 4L + (threadIdx.x >> 6);
+  constexpr int RPW = 64 / LPR;
+  const int lane = threadIdx.x & 63, sub = lane % LPR;
+  const long row = (blockIdx.x * 4L + (threadIdx.x >> 6)) * RPW + lane / LPR;
   if (row >= (long)a.B * a.Hq * a.Lq) return;
-  const int S = a.splits, hd = a.hd;
+  const int S = a.splits, hd = a.hd, d = sub * 4;
+  const bool dok = d < hd;
   const float* st = a.ws + (long)a.B * a.Hq * a.Lq * S * hd + row * S * 2;
-  float ms[MAX_SPLITS], w[MAX_SPLITS];
+  const float* po = a.ws + row * S * hd + (dok ? d : 0);
+  float ms[MAX_SPLITS], ls[MAX_SPLITS], w[MAX_SPLITS];
+  f32x4 part[MAX_SPLITS];
 #pragma unroll
-  for (int s = 0; s < MAX_SPLITS; ++s) ms[s] = s < S ? st[2 * s] : -INFINITY;
+  for (int q = 0; q < MAX_SPLITS; ++q) {
+    ms[q] = q < S ? st[2 * q] : -INFINITY;
+    ls[q] = q < S ? st[2 * q + 1] : 0.f;
+    part[q] = (q < S && dok) ? *reinterpret_cast<const f32x4*>(po + (long)q * hd) : f32x4{0.f, 0.f, 0.f, 0.f};
+  }
   float m = -INFINITY;
 #pragma unroll
-  for (int s = 0; s < MAX_SPLITS; ++s) m = fmaxf(m, ms[s]);
+  for (int q = 0; q < MAX_SPLITS; ++q) m = fmaxf(m, ms[q]);
   float l = 0.f;
 #pragma unroll
-  for (int s = 0; s < MAX_SPLITS; ++s) {
-    w[s] = s < S ? exp2f(ms[s] - m) : 0.f;
-    l += s < S ? st[2 * s + 1] * w[s] : 0.f;
+  for (int q = 0; q < MAX_SPLITS; ++q) {
+    w[q] = q < S ? exp2f(ms[q] - m) : 0.f;
+    l += q < S ? ls[q] * w[q] : 0.f;
   }
   const float inv = 1.0f / l;
+  f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int q = 0; q < MAX_SPLITS; ++q) acc += part[q] * w[q];
+  if (!dok) return;
   const int qi = (int)(row % a.Lq), h = (int)((row / a.Lq) % a.Hq), b = (int)(row / ((long)a.Lq * a.Hq));
   bf16* op = reinterpret_cast<bf16*>(a.o) + (long)b * a.o_sb + (long)h * a.o_sh + (long)qi * a.o_si;
-  const float* po = a.ws + row * S * hd;
-  for (int d = lane * 4; d < hd; d += 256) {
-    f32x4 part[MAX_SPLITS];
-#pragma unroll
-    for (int s = 0; s < MAX_SPLITS; ++s)
-      part[s] = s < S ? *reinterpret_cast<const f32x4*>(po + (long)s * hd + d) : f32x4{0.f, 0.f, 0.f, 0.f};
-    f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int s = 0; s < MAX_SPLITS; ++s) acc += part[s] * w[s];
-    *reinterpret_cast<bf16x4*>(op + d) =
-        bf16x4{(bf16)(acc[0] * inv), (bf16)(acc[1] * inv), (bf16)(acc[2] * inv), (bf16)(acc[3] * inv)};
-  }
+  *reinterpret_cast<bf16x4*>(op + d) =
+      bf16x4{(bf16)(acc[0] * inv), (bf16)(acc[1] * inv), (bf16)(acc[2] * inv), (bf16)(acc[3] * inv)};
 }
 
 // fp32 attention: one wave per (query, head, request); keys in chunks of 64
@@ -786,7 +792,11 @@ void launch_attention(const AttnArgs& a, hipStream_t s) {
   else if (a.hd <= 96) hipLaunchKernelGGL(attn_mfma_kernel<96>, grid, dim3(256), 0, s, b);
   else hipLaunchKernelGGL(attn_mfma_kernel<256>, grid, dim3(256), 0, s, b);
   if (b.splits > 1) {
+    // 256-thread blocks of 4 wavefronts x 64 / LPR rows
     const long nrows = (long)a.B * a.Hq * a.Lq;
-    hipLaunchKernelGGL(attn_combine_kernel, dim3((unsigned)((nrows + 3) / 4)), dim3(256), 0, s, b);
+    auto blocks = [&](int lpr) { const long rpb = 4L * (64 / lpr); return dim3((unsigned)((nrows + rpb - 1) / rpb)); };
+    if (a.hd <= 64) hipLaunchKernelGGL(attn_combine_kernel<16>, blocks(16), dim3(256), 0, s, b);
+    else if (a.hd <= 128) hipLaunchKernelGGL(attn_combine_kernel<32>, blocks(32), dim3(256), 0, s, b);
+    else hipLaunchKernelGGL(attn_combine_kernel<64>, blocks(64), dim3(256), 0, s, b);
   }
 }
