@@ -1450,7 +1450,11 @@ static GemmPlan plan_base(const GemmArgs& a) {
     // CU (>= 8 K-steps per range); time = rounds of resident blocks x K-steps
     // per range x step time (0.87 us for 128 x 128, 0.59 us for 128 x 64)
     // + the ordered reduce (its fp32 partial traffic at ~5 TB/s + 3 us).
-    const bool staged = (a.M >= 64 && blocks(128, 64) >= 128) || (a.M >= 512 && nk >= 24 && a.ws);
+    // Also a few hundred rows with K past the two-group kernel's 4096: there
+    // the 64 x 32 register tiles, enough of them to skip K ranges, each ran
+    // the whole K loop alone (the GR00T-like LLM MLP down at batch 1, 296 x
+    // 2048 x 16384: 143 -> 38 us, that prefill 5.89 -> 3.78 ms).
+    const bool staged = (a.M >= 64 && blocks(128, 64) >= 128) || (a.M > 64 && nk >= 24 && a.ws);
     // short K and under ~1.25 128 x 64 tiles per CU (the action stage at
     // batch 8-16): 64 x 64 tiles, up to four blocks per CU (measured 15-25 %
     // faster there)

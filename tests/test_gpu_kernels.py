@@ -40,6 +40,9 @@ GEMM_SHAPES = [
     # two wave groups per K-step of 128: 128 x 128 tiles, ragged M, N and K;
     # 64 x 64 tiles with two and four K ranges (two and three stages), ragged
     (777, 3000, 1000), (390, 1000, 4000), (130, 700, 1800), (300, 700, 1800),
+    # a few hundred rows with K past 4096: LDS-staged tiles with K ranges
+    # (the GR00T-like LLM MLP down and ViT MLP down at batch 1), ragged M
+    (296, 2048, 16384), (256, 1152, 4304), (65, 1000, 8200),
 ]
 
 
@@ -170,7 +173,8 @@ def test_gemm_f32(M, N, K):
 
 @pytest.mark.parametrize("M,N,K,kind", [(50, 720, 960, 0), (50, 720, 1920, 0), (800, 720, 1920, 0),
                                           (17, 1024, 4096, 2), (200, 1024, 2048, 1), (3840, 960, 960, 0),
-                                          (7, 36, 72, 1), (400, 720, 1920, 2)])
+                                          (7, 36, 72, 1), (400, 720, 1920, 2), (296, 2048, 16384, 0),
+                                          (256, 1152, 4304, 1)])
 def test_resid_norm(M, N, K, kind):
     """Residual projection + row norm (fused into the split-K reduce when
     the projection splits K) against fp64."""
