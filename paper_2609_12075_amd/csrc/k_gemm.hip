@@ -1415,8 +1415,13 @@ static GemmPlan plan_base(const GemmArgs& a) {
     // kOneRoundCUs is below the chip's 256 because the action stage shares
     // the GPU with a VLM stage that holds some CUs' LDS: one-block-per-CU
     // launches sized for all 256 CUs ran a second round there.
+    // Up to 36 K-steps (K <= 4608), but past 32 only with K ranges: the ViT
+    // MLP down (K = 4304) with two ranges at 256-768 rows is faster than on
+    // the staged tiles (GR00T-like prefill at batch 1 3.765 -> 3.703 ms, the
+    // pi0-shaped one 7.327 -> 7.278 ms), with one range at 1024 rows slower
+    // (7.38 -> 7.61 ms at batch 4).
     constexpr long kOneRoundCUs = 192;
-    if (a.M <= 1024 && a.K <= 4096 && (a.M > 64 || (a.N < 1536 && a.K >= 2048))) {
+    if (a.M <= 1024 && a.K <= 4608 && (a.M > 64 || (a.N < 1536 && a.K >= 2048))) {
       const long t64 = blocks(64, 64);
       const int nk128 = (a.K + 127) / 128;
       double best_t = 1e30;
@@ -1429,7 +1434,7 @@ static GemmPlan plan_base(const GemmArgs& a) {
         else if (a.norm_follows) t += 4.0;
         if (t < best_t) { best_t = t; best_s = sp; }
       }
-      if (best_s > 0) {
+      if (best_s > 0 && (a.K <= 4096 || best_s > 1)) {
         const int ksteps = (nk128 + best_s - 1) / best_s;
         p.bn = 64; p.bm = 64; p.kind = 4; p.bk = 128; p.kg = 2;
         p.stages = t64 * best_s <= kOneRoundCUs ? 3 : 2;
@@ -1437,7 +1442,7 @@ static GemmPlan plan_base(const GemmArgs& a) {
         p.splits = (nk128 + ksteps - 1) / ksteps;
         return p;
       }
-      if (a.M >= 256 && t128 >= 160 && t128 <= kOneRoundCUs) {
+      if (a.K <= 4096 && a.M >= 256 && t128 >= 160 && t128 <= kOneRoundCUs) {
         p.bn = 128; p.bm = 128; p.kind = 4; p.bk = 128; p.kg = 2; p.stages = 2;
         p.ksplit = nk128 * 128;
         p.splits = 1;

@@ -174,7 +174,7 @@ def test_gemm_f32(M, N, K):
 @pytest.mark.parametrize("M,N,K,kind", [(50, 720, 960, 0), (50, 720, 1920, 0), (800, 720, 1920, 0),
                                           (17, 1024, 4096, 2), (200, 1024, 2048, 1), (3840, 960, 960, 0),
                                           (7, 36, 72, 1), (400, 720, 1920, 2), (296, 2048, 16384, 0),
-                                          (256, 1152, 4304, 1)])
+                                          (256, 1152, 4304, 1), (768, 1152, 4304, 0)])
 def test_resid_norm(M, N, K, kind):
     """Residual projection + row norm (fused into the split-K reduce when
     the projection splits K) against fp64."""
