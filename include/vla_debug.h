@@ -151,6 +151,23 @@ vla_status vla_debug_sync_probe(int kind, int grid, int iters, int words, int sp
                                 int* err, float* sink, hipStream_t stream);
 
 /*
+ * The launch plan of a bf16 projection (bf16 activations and weights, rows of
+ * lengths K, the split-K workspace of a model's stage), as the model's
+ * projections and vla_debug_gemm_bf16 choose it. Host only: no device is
+ * touched, so it also answers on a machine without a GPU.
+ *  mode: 0 store, 1 residual, 2 GeGLU (N even; the output has N / 2
+ *  columns), 3 QKV, 4 Euler; out_bf16: bf16 rather than fp32 output;
+ *  rms != 0: the RMSNorm of the input rows folded in (not with mode 1);
+ *  norm_follows != 0: a row norm of the output follows (residual projections).
+ *  plan: int[8] = weight rows and activation rows per tile, number of K
+ *  ranges, K length per range, kernel kind (0 register-pipelined, 1
+ *  LDS-staged, 2 small-M, 3 large-tile, 4 LDS-staged with K-steps of 128),
+ *  LDS stages, K-step length, wave groups sharing each K-step.
+ * Status 1 (VLA_EINVAL) on bad arguments.
+ */
+vla_status vla_debug_gemm_plan(int M, int N, int K, int mode, int out_bf16, int rms, int norm_follows, int* plan);
+
+/*
  * Enqueue `iters` launches of one projection of a model's stage, exactly as
  * the stage launches it (same kernel, shape, epilogue, parameters and
  * workspace buffers), on `stream`, and store the algorithmic flops of one

@@ -601,6 +601,27 @@ vla_status vla_debug_sync_probe(int kind, int grid, int iters, int words, int sp
   });
 }
 
+vla_status vla_debug_gemm_plan(int M, int N, int K, int mode, int out_bf16, int rms, int norm_follows, int* plan) {
+  return guarded([&] {
+    VLA_REQUIRE(M >= 1 && N >= 1 && K >= 8 && K % 8 == 0 && plan, "bad gemm_plan arguments");
+    VLA_REQUIRE(mode >= EPI_STORE && mode <= EPI_EULER, "bad mode");
+    VLA_REQUIRE(mode != EPI_GEGLU || N % 2 == 0, "GeGLU needs an even N");
+    VLA_REQUIRE(!rms || mode != EPI_RESID, "a folded RMSNorm needs a store, QKV, GeGLU or Euler epilogue");
+    // planning only: nothing below is dereferenced; the addresses are
+    // 256-byte aligned stand-ins for the output, workspace and zero buffer
+    const auto fake = reinterpret_cast<void*>(uintptr_t{256});
+    GemmArgs g{};
+    g.M = M; g.N = N; g.K = K; g.A = fake; g.lda = K; g.a_type = ET_BF16; g.W = fake; g.ldw = K; g.w_type = ET_BF16;
+    g.mode = mode; g.tab_period = 1; g.out = fake; g.out_type = out_bf16 ? ET_BF16 : ET_F32;
+    g.ldo = mode == EPI_GEGLU ? N / 2 : N;
+    g.ws = static_cast<float*>(fake); g.ws_floats = vla_model_s::kSplitKFloats; g.zeros = fake;
+    g.rms_in = rms ? K : 0; g.rms_eps = 1e-6f; g.norm_follows = norm_follows ? 1 : 0;
+    const GemmPlan p = gemm_plan(g);
+    plan[0] = p.bn; plan[1] = p.bm; plan[2] = p.splits; plan[3] = p.ksplit; plan[4] = p.kind;
+    plan[5] = p.stages; plan[6] = p.bk; plan[7] = p.kg;
+  });
+}
+
 vla_status vla_debug_replay_gemm(vla_model m, int which, int batch, int iters, hipStream_t s, double* flops,
                                  int* plan) {
   return guarded([&] {

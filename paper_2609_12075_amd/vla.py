@@ -27,7 +27,8 @@ VLA_OK, VLA_EINVAL, VLA_ENOMEM, VLA_EHIP, VLA_EUNSUPPORTED = range(5)
 EXPORTS = ["vla_weight_count", "vla_create_model", "vla_destroy_model", "vla_set_graphs", "vla_kv_bytes",
            "vla_prefill", "vla_prefill_ex", "vla_denoise", "vla_step", "vla_last_error", "vla_shutdown",
            "vla_debug_gemm", "vla_debug_gemm_bf16", "vla_debug_resid_norm", "vla_debug_gemm_rms", "vla_debug_resid_copy", "vla_debug_attention",
-           "vla_debug_cu_probe", "vla_debug_replay_gemm", "vla_gemm_noalloc", "vla_debug_sync_probe"]
+           "vla_debug_cu_probe", "vla_debug_replay_gemm", "vla_gemm_noalloc", "vla_debug_sync_probe",
+           "vla_debug_gemm_plan"]
 
 
 class VlaError(RuntimeError):
@@ -93,6 +94,8 @@ def lib():
         L.vla_debug_cu_probe.argtypes = [ci, ci, ci, ci, ci, ci, vp, vp]; L.vla_debug_cu_probe.restype = ci
         L.vla_debug_sync_probe.argtypes = [ci, ci, ci, ci, ci, vp, vp, vp, vp, vp]
         L.vla_debug_sync_probe.restype = ci
+        L.vla_debug_gemm_plan.argtypes = [ci, ci, ci, ci, ci, ci, ci, ctypes.POINTER(ci)]
+        L.vla_debug_gemm_plan.restype = ci
         L.vla_debug_replay_gemm.argtypes = [vp, ci, ci, ci, vp, ctypes.POINTER(ctypes.c_double),
                                             ctypes.POINTER(ctypes.c_int)]
         L.vla_debug_replay_gemm.restype = ci
@@ -362,6 +365,14 @@ def debug_gemm_rms(A, Wt, bias=None, eps=1e-6, stream=None):
     _check(lib().vla_debug_gemm_rms(M, N, K, _ptr(A), _ptr(Wt), _ptr(bias), ctypes.c_float(eps), _ptr(out),
                                     _stream(stream)))
     return out
+
+
+def gemm_plan(M, N, K, mode=0, out_bf16=False, rms=False, norm_follows=False):
+    """vla_debug_gemm_plan: the launch plan of a bf16 projection (host only)."""
+    plan = (ctypes.c_int * 8)()
+    _check(lib().vla_debug_gemm_plan(M, N, K, mode, int(bool(out_bf16)), int(bool(rms)), int(bool(norm_follows)), plan))
+    keys = ("tile_n", "tile_m", "splits", "ksplit", "kind", "stages", "bk", "kg")
+    return dict(zip(keys, list(plan)))
 
 
 def debug_resid_copy(A, Wt, x, bias=None, gate=None, xb=None, stream=None):
